@@ -1,0 +1,229 @@
+/*
+ * gpt2.h - C ABI of the MI355X (gfx950) GPT-2 training-step library.
+ *
+ * The library runs one GPU's share of a GPT-2 training step as described in
+ * arXiv 2609.28568: the forward and backward pass of every pre-LayerNorm
+ * block, the LM head tied to the token table (vocabulary padded to a multiple
+ * of 64, softmax over the real tokens only), softmax cross-entropy, global-norm
+ * clipping and an AdamW update of fp32 master weights (section "Model",
+ * Figure 1; section "Optimisation and precision"; section "Batch geometry").
+ * Precision follows the paper's statement: bf16 activations; fp32 master
+ * weights, gradients and optimizer state; fp32 normalisation statistics and
+ * loss.
+ *
+ * Conventions common to every call
+ *  - Plain C types only; nothing here throws. Every call returns a status:
+ *      GPT2_ERR_INVALID_ARG  malformed request (bad config, NULL pointer,
+ *                            shape beyond what was sized); nothing launched;
+ *      GPT2_ERR_STATE        calls out of order (backward without a forward
+ *                            that had targets, accumulate with no gradient,
+ *                            optimizer step with no gradient);
+ *      GPT2_ERR_DEVICE       a HIP runtime or launch error.
+ *    gpt2_last_error() gives a human-readable reason for the last failure.
+ *  - Ownership: the caller allocates every device buffer (sizes from
+ *    gpt2_query_sizes) and owns the HIP stream; the library never allocates
+ *    device memory and owns only the host-side handle. Buffers must outlive
+ *    the handle and must not be used by other work while a call's kernels run.
+ *  - Asynchrony: calls enqueue kernels on the stream given to gpt2_init and
+ *    return without synchronising, except gpt2_loss and gpt2_probe_read.
+ *  - Pointers named d_* are device pointers; others are host pointers.
+ *  - Parameter layout: one flat fp32 buffer grouped by kind, each kind stacked
+ *    over layers: wte [Vp,C], wpe [Tmax,C], ln1w [L,C], ln1b [L,C],
+ *    qkvw [L,3C,C], qkvb [L,3C], attprojw [L,C,C], attprojb [L,C], ln2w [L,C],
+ *    ln2b [L,C], fcw [L,F,C], fcb [L,F], fcprojw [L,C,F], fcprojb [L,C],
+ *    lnfw [C], lnfb [C]. Matrices are row-major [out, in]; q|k|v are stacked in
+ *    that order along qkvw's rows, head h on rows [h*hd, (h+1)*hd) of each.
+ *    Gradients, Adam m and v mirror this layout (fp32); the bf16 weight copy
+ *    mirrors it in bf16.
+ */
+#ifndef GPT2_MI355X_H
+#define GPT2_MI355X_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum gpt2_status {
+  GPT2_OK = 0,
+  GPT2_ERR_INVALID_ARG = 1,
+  GPT2_ERR_STATE = 2,
+  GPT2_ERR_DEVICE = 3
+} gpt2_status;
+
+/* Model, batch and optimiser description ("Model"; "Optimisation and
+ * precision"). Validated by gpt2_query_sizes and gpt2_init:
+ *   n_layer >= 1; d_model % n_head == 0; head_dim in {16, 32, 64, 128};
+ *   d_model and d_ff multiples of 64; vocab_padded >= vocab, a multiple of 64
+ *   and <= 65536; 1 <= T <= max_seq_len; B >= 1; grad_accum >= 1;
+ *   warmup_steps >= 1; total_steps > warmup_steps; 0 <= beta < 1. */
+typedef struct gpt2_config {
+  int32_t n_layer, n_head, d_model, d_ff;
+  int32_t vocab, vocab_padded, max_seq_len;
+  int32_t B, T, grad_accum;
+  float ln_eps;                         /* LayerNorm epsilon (1e-5) */
+  float lr_max, lr_min;                 /* schedule peak and floor */
+  int32_t warmup_steps, total_steps;    /* linear warmup, then cosine */
+  float beta1, beta2, adam_eps, weight_decay, grad_clip;
+} gpt2_config;
+
+/* Byte sizes of the caller-owned buffers, plus the parameter count. */
+typedef struct gpt2_sizes {
+  size_t params_f32, grads_f32, adam_m, adam_v, params_bf16;
+  size_t activations;   /* forward state kept for the backward pass */
+  size_t workspace;     /* backward and optimizer scratch */
+  size_t n_params;      /* number of scalar parameters (padded vocabulary) */
+} gpt2_sizes;
+
+/* Device buffers, each at least the size gpt2_query_sizes reports and
+ * 256-byte aligned. */
+typedef struct gpt2_buffers {
+  void *params_f32, *grads_f32, *adam_m, *adam_v, *params_bf16;
+  void *activations, *workspace;
+} gpt2_buffers;
+
+typedef struct gpt2_model gpt2_model;   /* opaque host-side handle */
+
+/* Sizes for cfg. Returns INVALID_ARG for a config that fails validation. */
+gpt2_status gpt2_query_sizes(const gpt2_config* cfg, gpt2_sizes* out);
+
+/* Number of parameter tensors: 2 + 12*n_layer + 2 (148 for 12 layers, the
+ * count of gradient tensors the paper checks). */
+int32_t gpt2_num_tensors(const gpt2_config* cfg);
+
+/* Describe parameter tensor idx (0 <= idx < gpt2_num_tensors): name in
+ * GPT-2's flat naming (e.g. "h.10.ln_2.weight"), element offset into the flat
+ * buffer, shape (ndim 1 or 2) and whether weight decay applies to it (2-D
+ * weights only, "Optimisation and precision"). name must hold 64 bytes. */
+gpt2_status gpt2_tensor_info(const gpt2_config* cfg, int32_t idx, char* name,
+                             size_t* offset, int32_t* shape, int32_t* ndim,
+                             int32_t* decay);
+
+/* Create a handle over caller-owned buffers. The caller has filled
+ * params_f32 (and zeroed adam_m, adam_v); init enqueues the bf16 weight copy
+ * on hip_stream (a hipStream_t, NULL for the default stream). */
+gpt2_status gpt2_init(const gpt2_config* cfg, const gpt2_buffers* bufs,
+                      void* hip_stream, gpt2_model** out);
+
+/* Refresh the bf16 weight copy after the caller changed params_f32. */
+gpt2_status gpt2_sync_weights(gpt2_model* m);
+
+/* Forward pass (Figure 1): embedding, n_layer blocks, final LayerNorm, tied
+ * LM head over all vocab_padded columns. d_inputs: int32 [B*T] token ids in
+ * [0, vocab), row-major [B, T]. d_targets: int32 [B*T] next-token ids in
+ * [0, vocab), or NULL. With targets the softmax cross-entropy over the first
+ * vocab columns runs too: per-token losses are kept and the logits buffer is
+ * overwritten by dlogits = (softmax - onehot) / (B*T*grad_accum), exactly 0
+ * on padding columns. Without targets the logits are kept. Ids outside
+ * [0, vocab) are a contract violation (not checked on the device). */
+gpt2_status gpt2_forward(gpt2_model* m, const int32_t* d_inputs,
+                         const int32_t* d_targets);
+
+/* Backward pass for the last forward (which must have had targets).
+ * accumulate = 0 overwrites the fp32 gradients, 1 adds to them (micro-steps
+ * of gradient accumulation, "Batch geometry"). */
+gpt2_status gpt2_backward(gpt2_model* m, int32_t accumulate);
+
+/* Optimiser step (0-based step index): global gradient norm over all
+ * tensors, clip coefficient grad_clip/norm when the norm exceeds grad_clip,
+ * then AdamW with bias correction, decay on 2-D weights only and the
+ * scheduled learning rate; the bf16 weight copy is refreshed. *lr_out (host,
+ * optional) receives the rate used; d_grad_norm_out (device fp32, optional)
+ * receives the pre-clip norm. */
+gpt2_status gpt2_adamw_step(gpt2_model* m, int64_t step, float* lr_out,
+                            float* d_grad_norm_out);
+
+/* Mean loss of the last forward with targets, copied to *loss_out (host).
+ * Synchronises the stream. */
+gpt2_status gpt2_loss(gpt2_model* m, float* loss_out);
+
+/* Learning rate at a 0-based step: lr_max*(step+1)/warmup for step < warmup,
+ * then lr_min + (lr_max-lr_min)*(1+cos(pi*f))/2 with f the fraction of the
+ * remaining steps elapsed, clamped to [0,1]. Pure function. */
+float gpt2_lr_at(const gpt2_config* cfg, int64_t step);
+
+void gpt2_destroy(gpt2_model* m);
+const char* gpt2_last_error(const gpt2_model* m);   /* m may be NULL */
+
+/* Saved forward state, for inspection. which: one of gpt2_act; layer selects
+ * the block for per-block entries. Reports the byte offset into the
+ * activations buffer, the element count and the element type (0 = fp32,
+ * 1 = bf16, 2 = int32). */
+typedef enum gpt2_act {
+  GPT2_ACT_RESIDUAL = 0,  /* bf16 [BT,C]: block input (layer 0 = embedding
+                             output; layer n_layer = last block's output) */
+  GPT2_ACT_LN1 = 1,       /* bf16 [BT,C] */
+  GPT2_ACT_LN1_MEAN = 2,  /* fp32 [BT] */
+  GPT2_ACT_LN1_RSTD = 3,  /* fp32 [BT] */
+  GPT2_ACT_QKV = 4,       /* bf16 [BT,3C] */
+  GPT2_ACT_ATT = 5,       /* bf16 [BT,C], heads concatenated */
+  GPT2_ACT_ATT_LSE = 6,   /* fp32 [B,H,T]: log-sum-exp of scaled scores */
+  GPT2_ACT_X_MID = 7,     /* bf16 [BT,C]: residual after attention */
+  GPT2_ACT_LN2 = 8,       /* bf16 [BT,C] */
+  GPT2_ACT_LN2_MEAN = 9,
+  GPT2_ACT_LN2_RSTD = 10,
+  GPT2_ACT_FC = 11,       /* bf16 [BT,F]: MLP pre-activation */
+  GPT2_ACT_GELU = 12,     /* bf16 [BT,F] */
+  GPT2_ACT_LNF = 13,      /* bf16 [BT,C] */
+  GPT2_ACT_LNF_MEAN = 14,
+  GPT2_ACT_LNF_RSTD = 15,
+  GPT2_ACT_LOGITS = 16,   /* bf16 [BT,Vp]: logits, or dlogits after a
+                             forward with targets */
+  GPT2_ACT_LOSSES = 17,   /* fp32 [BT]: per-token loss */
+  GPT2_ACT_COUNT = 18
+} gpt2_act;
+
+gpt2_status gpt2_activation_info(const gpt2_model* m, int32_t which,
+                                 int32_t layer, size_t* offset_bytes,
+                                 size_t* numel, int32_t* dtype);
+
+/* One block in isolation (used to measure and check a single block):
+ * d_x_in bf16 [BT,C] is copied into the residual slot of `layer`, the block
+ * runs, and its output is copied to d_x_out (bf16 [BT,C], optional). The
+ * backward takes the upstream gradient d_dx_out (bf16 [BT,C]), writes the
+ * layer's parameter gradients (overwrite or accumulate) and the gradient
+ * with respect to the block input to d_dx_in (bf16 [BT,C], optional). */
+gpt2_status gpt2_block_forward(gpt2_model* m, int32_t layer,
+                               const void* d_x_in, void* d_x_out);
+gpt2_status gpt2_block_backward(gpt2_model* m, int32_t layer,
+                                const void* d_dx_out, void* d_dx_in,
+                                int32_t accumulate);
+
+/* Embedding backward in isolation (used to check its index handling): the
+ * token-table gradient receives, for each position r, the row d_dx[r] (bf16
+ * [B*T, C]) at row d_ids[r] (int32 [B*T], in [0, vocab)), and the position
+ * table gradient receives the batch sum per position. accumulate = 0 first
+ * clears both gradients; 1 adds to them. Rows of the token table that no id
+ * names are left untouched (exactly 0 after a clear). */
+gpt2_status gpt2_embedding_backward(gpt2_model* m, const int32_t* d_ids,
+                                    const void* d_dx, int32_t accumulate);
+
+/* Kernel timing probes for measurement. Kernels are grouped in classes; for
+ * classes in the enabled mask, every launch is bracketed by HIP events on
+ * the model's stream and its algorithmic work (flops or bytes) is counted.
+ * gpt2_probe_read synchronises and reports totals since the last reset. */
+typedef enum gpt2_kclass {
+  GPT2_K_GEMM_FWD = 0,    /* X W^T (+bias, residual or GELU epilogue) */
+  GPT2_K_GEMM_DX = 1,     /* dY W */
+  GPT2_K_GEMM_DW = 2,     /* dY^T X into fp32 gradients */
+  GPT2_K_ATTN_FWD = 3,
+  GPT2_K_ATTN_BWD = 4,
+  GPT2_K_LAYERNORM = 5,   /* forward and backward */
+  GPT2_K_CROSS_ENTROPY = 6,
+  GPT2_K_OPTIMIZER = 7,   /* norm, clip and AdamW */
+  GPT2_K_OTHER = 8,       /* embedding, reductions, casts */
+  GPT2_K_COUNT = 9
+} gpt2_kclass;
+
+gpt2_status gpt2_probe_enable(gpt2_model* m, uint32_t class_mask);
+gpt2_status gpt2_probe_reset(gpt2_model* m);
+gpt2_status gpt2_probe_read(gpt2_model* m, int32_t kclass, double* total_ms,
+                            int64_t* launches, double* flops, double* bytes);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GPT2_MI355X_H */

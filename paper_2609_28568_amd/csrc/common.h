@@ -1,0 +1,63 @@
+// Device-side helpers shared by the gfx950 kernels: bf16 storage, vector
+// types, MFMA operand types and wavefront reductions.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+typedef uint16_t bf16_t;   // bf16 in memory: raw bits
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+
+#define DEV __device__ __forceinline__
+
+constexpr int WAVE = 64;
+
+// fp32 -> bf16, round to nearest even (NaN stays NaN).
+DEV bf16_t f2bf(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (bf16_t)((u >> 16) | 0x40u);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (bf16_t)(u >> 16);
+}
+DEV float bf2f(bf16_t h) { return __uint_as_float(((uint32_t)h) << 16); }
+
+// two bf16 packed in a 32-bit word (low half = first element)
+DEV uint32_t pack2(float a, float b) { return (uint32_t)f2bf(a) | ((uint32_t)f2bf(b) << 16); }
+DEV float lo_f(uint32_t w) { return __uint_as_float(w << 16); }
+DEV float hi_f(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+
+DEV bf16x8 as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8, v); }
+
+DEV float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, WAVE);
+  return v;
+}
+DEV float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, WAVE));
+  return v;
+}
+
+DEV floatx16 mfma32(bf16x8 a, bf16x8 b, floatx16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+// Transpose two 4-byte words holding (r0c0,r0c1) and (r1c0,r1c1) into
+// (r0c0,r1c0) and (r0c1,r1c1).
+DEV uint32_t lo_pair(uint32_t r0, uint32_t r1) { return (r0 & 0xffffu) | (r1 << 16); }
+DEV uint32_t hi_pair(uint32_t r0, uint32_t r1) { return (r0 >> 16) | (r1 & 0xffff0000u); }
+
+DEV float gelu_tanh(float u) {
+  const float k = 0.7978845608028654f, a = 0.044715f;
+  float t = tanhf(k * (u + a * u * u * u));
+  return 0.5f * u * (1.0f + t);
+}
+DEV float gelu_tanh_grad(float u) {
+  const float k = 0.7978845608028654f, a = 0.044715f;
+  float t = tanhf(k * (u + a * u * u * u));
+  return 0.5f * (1.0f + t) + 0.5f * u * (1.0f - t * t) * k * (1.0f + 3.0f * a * u * u);
+}

@@ -1,0 +1,344 @@
+// Memory-bound kernels of the training step: embedding forward/backward, the
+// fused softmax cross-entropy over the real vocabulary, column sums for bias
+// gradients, slice reductions, the global gradient norm, and the fused AdamW
+// update that also refreshes the bf16 weight copy.
+#include "common.h"
+#include "kernels.h"
+
+namespace {
+
+// ------------------------------------------------------------ reductions
+
+__global__ void reduce_slices_kernel(const float* __restrict__ src, int nslices, long n, float* __restrict__ dst,
+                                     int accumulate) {
+  long i = ((long)blockIdx.x * blockDim.x + threadIdx.x) * 4;
+  if (i >= n) return;
+  float4 acc = accumulate ? *reinterpret_cast<const float4*>(dst + i) : make_float4(0, 0, 0, 0);
+  for (int s = 0; s < nslices; ++s) {
+    float4 v = *reinterpret_cast<const float4*>(src + (size_t)s * n + i);
+    acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
+  }
+  *reinterpret_cast<float4*>(dst + i) = acc;
+}
+
+// parts[p][c] = sum of x[r][c] over the p-th slice of rows; one thread per
+// 4 columns
+__global__ void colsum_kernel(const bf16_t* __restrict__ x, int rows, int N, int rows_per_part,
+                              float* __restrict__ parts) {
+  const int c = (blockIdx.x * blockDim.x + threadIdx.x) * 4;
+  if (c >= N) return;
+  const int r0 = blockIdx.y * rows_per_part, r1 = min(rows, r0 + rows_per_part);
+  float a0 = 0, a1 = 0, a2 = 0, a3 = 0;
+  for (int r = r0; r < r1; ++r) {
+    uint2 u = *reinterpret_cast<const uint2*>(x + (size_t)r * N + c);
+    a0 += lo_f(u.x); a1 += hi_f(u.x); a2 += lo_f(u.y); a3 += hi_f(u.y);
+  }
+  *reinterpret_cast<float4*>(parts + (size_t)blockIdx.y * N + c) = make_float4(a0, a1, a2, a3);
+}
+
+template <int NT>
+DEV float block_sum(float v, float* sh) {
+  v = wave_sum(v);
+  const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
+  __syncthreads();
+  if (l == 0) sh[w] = v;
+  __syncthreads();
+  float t = 0.0f;
+#pragma unroll
+  for (int i = 0; i < NT / 64; ++i) t += sh[i];
+  return t;
+}
+
+template <int NT>
+DEV float block_max(float v, float* sh) {
+  v = wave_max(v);
+  const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
+  __syncthreads();
+  if (l == 0) sh[w] = v;
+  __syncthreads();
+  float t = -INFINITY;
+#pragma unroll
+  for (int i = 0; i < NT / 64; ++i) t = fmaxf(t, sh[i]);
+  return t;
+}
+
+__global__ __launch_bounds__(256) void mean_kernel(const float* __restrict__ x, int n, float* __restrict__ out) {
+  __shared__ float sh[4];
+  float s = 0.0f;
+  for (int i = threadIdx.x; i < n; i += 256) s += x[i];
+  s = block_sum<256>(s, sh);
+  if (threadIdx.x == 0) out[0] = s / n;
+}
+
+// ------------------------------------------------------------ embedding
+
+__global__ void embed_fwd_kernel(const int32_t* __restrict__ ids, const float* __restrict__ wte,
+                                 const float* __restrict__ wpe, bf16_t* __restrict__ x, int BT, int T, int C) {
+  long i = ((long)blockIdx.x * blockDim.x + threadIdx.x) * 4;
+  if (i >= (long)BT * C) return;
+  const int row = i / C, c = i % C, t = row % T;
+  const int id = ids[row];
+  float4 a = *reinterpret_cast<const float4*>(wte + (size_t)id * C + c);
+  float4 p = *reinterpret_cast<const float4*>(wpe + (size_t)t * C + c);
+  *reinterpret_cast<uint2*>(x + i) = make_uint2(pack2(a.x + p.x, a.y + p.y), pack2(a.z + p.z, a.w + p.w));
+}
+
+// token table: scatter-add of each position's gradient into its id's row
+__global__ void embed_bwd_wte_kernel(const int32_t* __restrict__ ids, const bf16_t* __restrict__ dx,
+                                     float* __restrict__ dwte, int BT, int C) {
+  long i = ((long)blockIdx.x * blockDim.x + threadIdx.x) * 4;
+  if (i >= (long)BT * C) return;
+  const int row = i / C, c = i % C;
+  const int id = ids[row];
+  uint2 u = *reinterpret_cast<const uint2*>(dx + i);
+  float* d = dwte + (size_t)id * C + c;
+  atomicAdd(d + 0, lo_f(u.x));
+  atomicAdd(d + 1, hi_f(u.x));
+  atomicAdd(d + 2, lo_f(u.y));
+  atomicAdd(d + 3, hi_f(u.y));
+}
+
+// position table: dwpe[t] = sum over the batch, in batch order; rows t >= T
+// get no gradient
+__global__ void embed_bwd_wpe_kernel(const bf16_t* __restrict__ dx, float* __restrict__ dwpe, int B, int T, int Tmax,
+                                     int C, int accumulate) {
+  long i = ((long)blockIdx.x * blockDim.x + threadIdx.x) * 4;
+  if (i >= (long)Tmax * C) return;
+  const int t = i / C;
+  float4 acc = accumulate ? *reinterpret_cast<const float4*>(dwpe + i) : make_float4(0, 0, 0, 0);
+  if (t < T) {
+    for (int b = 0; b < B; ++b) {
+      uint2 u = *reinterpret_cast<const uint2*>(dx + (size_t)b * T * C + i);
+      acc.x += lo_f(u.x); acc.y += hi_f(u.x); acc.z += lo_f(u.y); acc.w += hi_f(u.y);
+    }
+  }
+  *reinterpret_cast<float4*>(dwpe + i) = acc;
+}
+
+// ------------------------------------------------------------ cross-entropy
+
+// One workgroup per row; the row (Vp bf16) is held in registers as 16-byte
+// chunks, so it is read once and written once.
+template <int NT, int MAXCH>
+__global__ __launch_bounds__(NT) void cross_entropy_kernel(bf16_t* __restrict__ logits,
+                                                           const int32_t* __restrict__ targets,
+                                                           float* __restrict__ losses, int V, int Vp,
+                                                           float grad_scale) {
+  __shared__ float sh[NT / 64];
+  __shared__ float xt;
+  const int row = blockIdx.x;
+  bf16_t* lr = logits + (size_t)row * Vp;
+  const int tgt = targets[row];
+  if (threadIdx.x == 0) xt = bf2f(lr[tgt]);
+  const int nch = Vp / 8;
+  uint4 v[MAXCH];
+  float mx = -INFINITY;
+#pragma unroll
+  for (int i = 0; i < MAXCH; ++i) {
+    int c = threadIdx.x + NT * i;
+    if (c < nch) {
+      v[i] = *reinterpret_cast<const uint4*>(lr + c * 8);
+      const uint32_t w[4] = {v[i].x, v[i].y, v[i].z, v[i].w};
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        float f = (e & 1) ? hi_f(w[e >> 1]) : lo_f(w[e >> 1]);
+        if (c * 8 + e < V) mx = fmaxf(mx, f);
+      }
+    }
+  }
+  mx = block_max<NT>(mx, sh);
+  float se = 0.0f;
+#pragma unroll
+  for (int i = 0; i < MAXCH; ++i) {
+    int c = threadIdx.x + NT * i;
+    if (c < nch) {
+      const uint32_t w[4] = {v[i].x, v[i].y, v[i].z, v[i].w};
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        float f = (e & 1) ? hi_f(w[e >> 1]) : lo_f(w[e >> 1]);
+        if (c * 8 + e < V) se += __expf(f - mx);
+      }
+    }
+  }
+  se = block_sum<NT>(se, sh);
+  const float inv = 1.0f / se;
+#pragma unroll
+  for (int i = 0; i < MAXCH; ++i) {
+    int c = threadIdx.x + NT * i;
+    if (c < nch) {
+      const uint32_t w[4] = {v[i].x, v[i].y, v[i].z, v[i].w};
+      float d[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        int j = c * 8 + e;
+        float f = (e & 1) ? hi_f(w[e >> 1]) : lo_f(w[e >> 1]);
+        float p = j < V ? __expf(f - mx) * inv : 0.0f;
+        if (j == tgt) p -= 1.0f;
+        d[e] = p * grad_scale;
+      }
+      *reinterpret_cast<uint4*>(lr + c * 8) =
+          make_uint4(pack2(d[0], d[1]), pack2(d[2], d[3]), pack2(d[4], d[5]), pack2(d[6], d[7]));
+    }
+  }
+  if (threadIdx.x == 0) losses[row] = mx + logf(se) - xt;
+}
+
+// ------------------------------------------------------------ casts
+
+__global__ void cast_bf16_kernel(const float* __restrict__ src, bf16_t* __restrict__ dst, long n) {
+  long i = ((long)blockIdx.x * blockDim.x + threadIdx.x) * 4;
+  if (i >= n) return;
+  float4 v = *reinterpret_cast<const float4*>(src + i);
+  *reinterpret_cast<uint2*>(dst + i) = make_uint2(pack2(v.x, v.y), pack2(v.z, v.w));
+}
+
+// ------------------------------------------------------------ optimizer
+
+constexpr int SUMSQ_BLOCKS = 1024;
+
+__global__ __launch_bounds__(256) void sumsq_kernel(const float* __restrict__ g, long n, float* __restrict__ parts) {
+  __shared__ float sh[4];
+  float s = 0.0f;
+  for (long i = ((long)blockIdx.x * 256 + threadIdx.x) * 4; i < n; i += (long)gridDim.x * 256 * 4) {
+    float4 v = *reinterpret_cast<const float4*>(g + i);
+    s += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+  }
+  s = block_sum<256>(s, sh);
+  if (threadIdx.x == 0) parts[blockIdx.x] = s;
+}
+
+__global__ __launch_bounds__(256) void clip_coef_kernel(const float* __restrict__ parts, int nparts, float clip,
+                                                        float* __restrict__ norm_coef) {
+  __shared__ float sh[4];
+  float s = 0.0f;
+  for (int i = threadIdx.x; i < nparts; i += 256) s += parts[i];
+  s = block_sum<256>(s, sh);
+  if (threadIdx.x == 0) {
+    float norm = sqrtf(s);
+    norm_coef[0] = norm;
+    norm_coef[1] = norm > clip ? clip / norm : 1.0f;
+  }
+}
+
+__global__ __launch_bounds__(256) void adamw_kernel(AdamArgs a) {
+  const float coef = a.norm_coef[1];
+  for (long i = ((long)blockIdx.x * 256 + threadIdx.x) * 4; i < a.n; i += (long)gridDim.x * 256 * 4) {
+    int sidx = 0;
+    while (sidx < a.seg.count - 1 && i >= a.seg.end[sidx]) ++sidx;
+    const float wd = a.seg.decay[sidx] ? a.weight_decay : 0.0f;
+    float4 p = *reinterpret_cast<const float4*>(a.p + i);
+    float4 g = *reinterpret_cast<const float4*>(a.g + i);
+    float4 m = *reinterpret_cast<const float4*>(a.m + i);
+    float4 v = *reinterpret_cast<const float4*>(a.v + i);
+    float pv[4] = {p.x, p.y, p.z, p.w}, gv[4] = {g.x, g.y, g.z, g.w};
+    float mv[4] = {m.x, m.y, m.z, m.w}, vv[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      float gg = gv[e] * coef;
+      mv[e] = a.beta1 * mv[e] + (1.0f - a.beta1) * gg;
+      vv[e] = a.beta2 * vv[e] + (1.0f - a.beta2) * gg * gg;
+      float mhat = mv[e] / a.bc1, vhat = vv[e] / a.bc2;
+      pv[e] -= a.lr * (mhat / (sqrtf(vhat) + a.eps) + wd * pv[e]);
+    }
+    *reinterpret_cast<float4*>(a.p + i) = make_float4(pv[0], pv[1], pv[2], pv[3]);
+    *reinterpret_cast<float4*>(a.m + i) = make_float4(mv[0], mv[1], mv[2], mv[3]);
+    *reinterpret_cast<float4*>(a.v + i) = make_float4(vv[0], vv[1], vv[2], vv[3]);
+    *reinterpret_cast<uint2*>(a.p_bf16 + i) = make_uint2(pack2(pv[0], pv[1]), pack2(pv[2], pv[3]));
+  }
+}
+
+inline unsigned blocks_for(long n4, int nt) { return (unsigned)((n4 + nt - 1) / nt); }
+
+}  // namespace
+
+hipError_t launch_reduce_slices(const float* src, int nslices, long n, float* dst, int accumulate, hipStream_t s) {
+  if (n % 4) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(reduce_slices_kernel, dim3(blocks_for(n / 4, 256)), dim3(256), 0, s, src, nslices, n, dst,
+                     accumulate);
+  return hipGetLastError();
+}
+
+int colsum_parts(int rows) {
+  int p = rows / 64;
+  return p < 1 ? 1 : (p > 256 ? 256 : p);
+}
+
+hipError_t launch_colsum(const bf16_t* x, int rows, int N, float* parts, hipStream_t s) {
+  if (N % 4) return hipErrorInvalidValue;
+  int np = colsum_parts(rows);
+  int rpp = (rows + np - 1) / np;
+  dim3 grid(blocks_for(N / 4, 64), np);
+  hipLaunchKernelGGL(colsum_kernel, grid, dim3(64), 0, s, x, rows, N, rpp, parts);
+  return hipGetLastError();
+}
+
+hipError_t launch_mean(const float* x, int n, float* out, hipStream_t s) {
+  hipLaunchKernelGGL(mean_kernel, dim3(1), dim3(256), 0, s, x, n, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_embed_fwd(const int32_t* ids, const float* wte, const float* wpe, bf16_t* x, int B, int T, int C,
+                            hipStream_t s) {
+  long n4 = (long)B * T * C / 4;
+  hipLaunchKernelGGL(embed_fwd_kernel, dim3(blocks_for(n4, 256)), dim3(256), 0, s, ids, wte, wpe, x, B * T, T, C);
+  return hipGetLastError();
+}
+
+hipError_t launch_embed_bwd(const int32_t* ids, const bf16_t* dx, float* dwte, int B, int T, int C,
+                            hipStream_t s) {
+  long n4 = (long)B * T * C / 4;
+  hipLaunchKernelGGL(embed_bwd_wte_kernel, dim3(blocks_for(n4, 256)), dim3(256), 0, s, ids, dx, dwte, B * T, C);
+  return hipGetLastError();
+}
+
+hipError_t launch_embed_bwd_pos(const bf16_t* dx, float* dwpe, int B, int T, int Tmax, int C, int accumulate,
+                                hipStream_t s) {
+  long n4 = (long)Tmax * C / 4;
+  hipLaunchKernelGGL(embed_bwd_wpe_kernel, dim3(blocks_for(n4, 256)), dim3(256), 0, s, dx, dwpe, B, T, Tmax, C,
+                     accumulate);
+  return hipGetLastError();
+}
+
+hipError_t launch_cross_entropy(bf16_t* logits, const int32_t* targets, float* losses, int rows, int V, int Vp,
+                                float grad_scale, hipStream_t s) {
+  if (Vp % 8) return hipErrorInvalidValue;
+  int nch = Vp / 8;
+  if (nch <= 256 * 2) {
+    hipLaunchKernelGGL((cross_entropy_kernel<256, 2>), dim3(rows), dim3(256), 0, s, logits, targets, losses, V, Vp,
+                       grad_scale);
+  } else if (nch <= 512 * 16) {
+    hipLaunchKernelGGL((cross_entropy_kernel<512, 16>), dim3(rows), dim3(512), 0, s, logits, targets, losses, V, Vp,
+                       grad_scale);
+  } else {
+    return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_cast_bf16(const float* src, bf16_t* dst, long n, hipStream_t s) {
+  if (n % 4) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(cast_bf16_kernel, dim3(blocks_for(n / 4, 256)), dim3(256), 0, s, src, dst, n);
+  return hipGetLastError();
+}
+
+int sumsq_parts() { return SUMSQ_BLOCKS; }
+
+hipError_t launch_sumsq(const float* g, long n, float* parts, hipStream_t s) {
+  if (n % 4) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(sumsq_kernel, dim3(SUMSQ_BLOCKS), dim3(256), 0, s, g, n, parts);
+  return hipGetLastError();
+}
+
+hipError_t launch_clip_coef(const float* parts, int nparts, float clip, float* norm_coef, hipStream_t s) {
+  hipLaunchKernelGGL(clip_coef_kernel, dim3(1), dim3(256), 0, s, parts, nparts, clip, norm_coef);
+  return hipGetLastError();
+}
+
+hipError_t launch_adamw(const AdamArgs& a, hipStream_t s) {
+  if (a.n % 4) return hipErrorInvalidValue;
+  long n4 = a.n / 4;
+  unsigned blocks = blocks_for(n4, 256);
+  if (blocks > 8192) blocks = 8192;
+  hipLaunchKernelGGL(adamw_kernel, dim3(blocks), dim3(256), 0, s, a);
+  return hipGetLastError();
+}

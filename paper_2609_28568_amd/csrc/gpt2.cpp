@@ -1,0 +1,799 @@
+// Host side of the GPT-2 training-step library: configuration checks, the
+// layout of the caller-owned buffers, and the per-layer launch sequence of the
+// forward pass, the backward pass and the optimizer step. Every launch goes
+// to the stream given at init; nothing here allocates device memory.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "../../include/gpt2.h"
+#include "kernels.h"
+
+namespace {
+
+enum Kind {
+  K_WTE, K_WPE, K_LN1W, K_LN1B, K_QKVW, K_QKVB, K_ATTPROJW, K_ATTPROJB,
+  K_LN2W, K_LN2B, K_FCW, K_FCB, K_FCPROJW, K_FCPROJB, K_LNFW, K_LNFB, K_NKIND
+};
+
+constexpr size_t ALIGN = 256;
+size_t align_up(size_t x) { return (x + ALIGN - 1) / ALIGN * ALIGN; }
+
+struct Dims {
+  int L, H, C, F, V, Vp, Tmax, B, T, hd, accum;
+  long BT;
+};
+
+Dims dims_of(const gpt2_config& c) {
+  Dims d;
+  d.L = c.n_layer; d.H = c.n_head; d.C = c.d_model; d.F = c.d_ff; d.V = c.vocab;
+  d.Vp = c.vocab_padded; d.Tmax = c.max_seq_len; d.B = c.B; d.T = c.T;
+  d.hd = c.n_head > 0 ? c.d_model / c.n_head : 0; d.accum = c.grad_accum;
+  d.BT = (long)c.B * c.T;
+  return d;
+}
+
+const char* validate(const gpt2_config* c) {
+  if (!c) return "config is NULL";
+  if (c->n_layer < 1) return "n_layer must be >= 1";
+  if (c->n_head < 1 || c->d_model % c->n_head) return "d_model must be a multiple of n_head";
+  int hd = c->d_model / c->n_head;
+  if (hd != 16 && hd != 32 && hd != 64 && hd != 128) return "head_dim must be 16, 32, 64 or 128";
+  if (c->d_model % 64 || c->d_model > 2048) return "d_model must be a multiple of 64 and <= 2048";
+  if (c->d_ff % 64 || c->d_ff < 64) return "d_ff must be a positive multiple of 64";
+  if (c->vocab < 1 || c->vocab_padded < c->vocab) return "need 1 <= vocab <= vocab_padded";
+  if (c->vocab_padded % 64 || c->vocab_padded > 65536) return "vocab_padded must be a multiple of 64, <= 65536";
+  if (c->max_seq_len < 1 || c->T < 1 || c->T > c->max_seq_len) return "need 1 <= T <= max_seq_len";
+  if (c->B < 1) return "B must be >= 1";
+  if ((long)c->B * c->T > (1L << 26)) return "B*T too large";
+  if (c->grad_accum < 1) return "grad_accum must be >= 1";
+  if (!(c->ln_eps > 0.0f)) return "ln_eps must be > 0";
+  if (c->warmup_steps < 1 || c->total_steps <= c->warmup_steps) return "need 1 <= warmup_steps < total_steps";
+  if (!(c->beta1 >= 0.0f && c->beta1 < 1.0f && c->beta2 >= 0.0f && c->beta2 < 1.0f)) return "betas must be in [0,1)";
+  if (!(c->adam_eps > 0.0f) || !(c->grad_clip > 0.0f)) return "adam_eps and grad_clip must be > 0";
+  return nullptr;
+}
+
+// element counts of each parameter kind, in flat-buffer order
+void kind_sizes(const Dims& d, size_t n[K_NKIND]) {
+  size_t L = d.L, C = d.C, F = d.F;
+  n[K_WTE] = (size_t)d.Vp * C; n[K_WPE] = (size_t)d.Tmax * C;
+  n[K_LN1W] = n[K_LN1B] = L * C;
+  n[K_QKVW] = L * 3 * C * C; n[K_QKVB] = L * 3 * C;
+  n[K_ATTPROJW] = L * C * C; n[K_ATTPROJB] = L * C;
+  n[K_LN2W] = n[K_LN2B] = L * C;
+  n[K_FCW] = L * F * C; n[K_FCB] = L * F;
+  n[K_FCPROJW] = L * C * F; n[K_FCPROJB] = L * C;
+  n[K_LNFW] = n[K_LNFB] = C;
+}
+const bool kDecay[K_NKIND] = {true, true, false, false, true, false, true, false,
+                              false, false, true, false, true, false, false, false};
+
+// contraction splits for a weight-gradient GEMM with an M x N output
+int dw_splits(const Dims& d, int M, int N) {
+  long tiles = (long)((M + 127) / 128) * ((N + 127) / 128);
+  long want = (512 + tiles - 1) / tiles;
+  long cap = d.BT / 512;
+  if (cap < 1) cap = 1;
+  if (want > cap) want = cap;
+  if (want < 1) want = 1;
+  return gemm_split_plan((int)d.BT, (int)want, nullptr);
+}
+
+int dw_chunk(const Dims& d, int M, int N) {
+  int kc = 0;
+  long tiles = (long)((M + 127) / 128) * ((N + 127) / 128);
+  long want = (512 + tiles - 1) / tiles;
+  long cap = d.BT / 512;
+  if (cap < 1) cap = 1;
+  if (want > cap) want = cap;
+  if (want < 1) want = 1;
+  gemm_split_plan((int)d.BT, (int)want, &kc);
+  return kc;
+}
+
+struct ActLayout {
+  size_t residual, ln1, ln1_mean, ln1_rstd, qkv, att, lse, x_mid, ln2, ln2_mean, ln2_rstd, fc, gelu;
+  size_t lnf, lnf_mean, lnf_rstd, logits, losses, loss_mean, ids, total;
+  // per-layer strides in bytes
+  size_t s_act, s_qkv, s_ff, s_row, s_lse;
+};
+
+struct WsLayout {
+  size_t dres, dh, datt, dbig, dsum, splitk, colsum, lnpart_w, lnpart_b, sumsq, normcoef, total;
+  size_t splitk_elems, colsum_elems;
+};
+
+ActLayout act_layout(const Dims& d) {
+  ActLayout a{};
+  const size_t BT = d.BT, C = d.C, L = d.L;
+  a.s_act = align_up(BT * C * 2);
+  a.s_qkv = align_up(BT * 3 * C * 2);
+  a.s_ff = align_up(BT * d.F * 2);
+  a.s_row = align_up(BT * 4);
+  a.s_lse = align_up((size_t)d.B * d.H * d.T * 4);
+  size_t o = 0;
+  a.residual = o; o += (L + 1) * a.s_act;
+  a.ln1 = o; o += L * a.s_act;
+  a.ln1_mean = o; o += L * a.s_row;
+  a.ln1_rstd = o; o += L * a.s_row;
+  a.qkv = o; o += L * a.s_qkv;
+  a.att = o; o += L * a.s_act;
+  a.lse = o; o += L * a.s_lse;
+  a.x_mid = o; o += L * a.s_act;
+  a.ln2 = o; o += L * a.s_act;
+  a.ln2_mean = o; o += L * a.s_row;
+  a.ln2_rstd = o; o += L * a.s_row;
+  a.fc = o; o += L * a.s_ff;
+  a.gelu = o; o += L * a.s_ff;
+  a.lnf = o; o += a.s_act;
+  a.lnf_mean = o; o += a.s_row;
+  a.lnf_rstd = o; o += a.s_row;
+  a.logits = o; o += align_up(BT * (size_t)d.Vp * 2);
+  a.losses = o; o += a.s_row;
+  a.loss_mean = o; o += ALIGN;
+  a.ids = o; o += a.s_row;
+  a.total = o;
+  return a;
+}
+
+WsLayout ws_layout(const Dims& d) {
+  WsLayout w{};
+  const size_t BT = d.BT, C = d.C, F = d.F;
+  size_t wide = F > 3 * C ? F : 3 * C;
+  size_t sk = 0;
+  auto upd = [&](int M, int N) {
+    int s = dw_splits(d, M, N);
+    if (s > 1) sk = std::max(sk, (size_t)s * M * N);
+  };
+  upd(3 * d.C, d.C); upd(d.C, d.C); upd(d.F, d.C); upd(d.C, d.F); upd(d.Vp, d.C);
+  w.splitk_elems = sk;
+  w.colsum_elems = (size_t)colsum_parts((int)BT) * wide;
+  size_t o = 0;
+  w.dres = o; o += align_up(BT * C * 2);
+  w.dh = o; o += align_up(BT * C * 2);
+  w.datt = o; o += align_up(BT * C * 2);
+  w.dbig = o; o += align_up(BT * wide * 2);
+  w.dsum = o; o += align_up((size_t)d.B * d.H * d.T * 4);
+  w.splitk = o; o += align_up(sk * 4);
+  w.colsum = o; o += align_up(w.colsum_elems * 4);
+  w.lnpart_w = o; o += align_up((size_t)layernorm_bwd_blocks((int)BT) * C * 4);
+  w.lnpart_b = o; o += align_up((size_t)layernorm_bwd_blocks((int)BT) * C * 4);
+  w.sumsq = o; o += align_up((size_t)sumsq_parts() * 4);
+  w.normcoef = o; o += ALIGN;
+  w.total = o;
+  return w;
+}
+
+struct ProbeRec {
+  hipEvent_t a, b;
+  int cls;
+};
+
+}  // namespace
+
+struct gpt2_model {
+  gpt2_config cfg;
+  Dims d;
+  gpt2_buffers buf;
+  hipStream_t stream;
+  size_t kn[K_NKIND], koff[K_NKIND], n_params;
+  ActLayout act;
+  WsLayout ws;
+  bool have_dlogits = false;   // last forward had targets
+  bool have_grads = false;     // gradients hold a backward result
+  bool have_loss = false;
+  std::string err;
+  // probes
+  uint32_t probe_mask = 0;
+  std::vector<ProbeRec> live;
+  std::vector<hipEvent_t> pool;
+  double ms[GPT2_K_COUNT] = {}, flops[GPT2_K_COUNT] = {}, bytes[GPT2_K_COUNT] = {};
+  int64_t launches[GPT2_K_COUNT] = {};
+
+  // typed pointers
+  float* pf(int k) { return static_cast<float*>(buf.params_f32) + koff[k]; }
+  float* gf(int k) { return static_cast<float*>(buf.grads_f32) + koff[k]; }
+  bf16_t* pb(int k) { return static_cast<bf16_t*>(buf.params_bf16) + koff[k]; }
+  char* A(size_t off) { return static_cast<char*>(buf.activations) + off; }
+  char* W(size_t off) { return static_cast<char*>(buf.workspace) + off; }
+  bf16_t* res(int l) { return reinterpret_cast<bf16_t*>(A(act.residual + l * act.s_act)); }
+  bf16_t* ln1(int l) { return reinterpret_cast<bf16_t*>(A(act.ln1 + l * act.s_act)); }
+  float* ln1m(int l) { return reinterpret_cast<float*>(A(act.ln1_mean + l * act.s_row)); }
+  float* ln1r(int l) { return reinterpret_cast<float*>(A(act.ln1_rstd + l * act.s_row)); }
+  bf16_t* qkv(int l) { return reinterpret_cast<bf16_t*>(A(act.qkv + l * act.s_qkv)); }
+  bf16_t* att(int l) { return reinterpret_cast<bf16_t*>(A(act.att + l * act.s_act)); }
+  float* lse(int l) { return reinterpret_cast<float*>(A(act.lse + l * act.s_lse)); }
+  bf16_t* xmid(int l) { return reinterpret_cast<bf16_t*>(A(act.x_mid + l * act.s_act)); }
+  bf16_t* ln2(int l) { return reinterpret_cast<bf16_t*>(A(act.ln2 + l * act.s_act)); }
+  float* ln2m(int l) { return reinterpret_cast<float*>(A(act.ln2_mean + l * act.s_row)); }
+  float* ln2r(int l) { return reinterpret_cast<float*>(A(act.ln2_rstd + l * act.s_row)); }
+  bf16_t* fc(int l) { return reinterpret_cast<bf16_t*>(A(act.fc + l * act.s_ff)); }
+  bf16_t* gelu(int l) { return reinterpret_cast<bf16_t*>(A(act.gelu + l * act.s_ff)); }
+  bf16_t* lnf() { return reinterpret_cast<bf16_t*>(A(act.lnf)); }
+  float* lnfm() { return reinterpret_cast<float*>(A(act.lnf_mean)); }
+  float* lnfr() { return reinterpret_cast<float*>(A(act.lnf_rstd)); }
+  bf16_t* logits() { return reinterpret_cast<bf16_t*>(A(act.logits)); }
+  float* losses() { return reinterpret_cast<float*>(A(act.losses)); }
+  float* loss_mean() { return reinterpret_cast<float*>(A(act.loss_mean)); }
+  int32_t* ids() { return reinterpret_cast<int32_t*>(A(act.ids)); }
+  bf16_t* wsb(size_t off) { return reinterpret_cast<bf16_t*>(W(off)); }
+  float* wsf(size_t off) { return reinterpret_cast<float*>(W(off)); }
+
+  gpt2_status fail(gpt2_status s, const std::string& msg) {
+    err = msg;
+    return s;
+  }
+
+  hipEvent_t get_event() {
+    if (!pool.empty()) {
+      hipEvent_t e = pool.back();
+      pool.pop_back();
+      return e;
+    }
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    return e;
+  }
+
+  // Launch through f(); optionally bracket it with events for the probes.
+  template <class Fn>
+  hipError_t run(int cls, double fl, double by, Fn f) {
+    const bool on = (probe_mask >> cls) & 1u;
+    hipEvent_t e0 = nullptr, e1 = nullptr;
+    if (on) {
+      e0 = get_event();
+      e1 = get_event();
+      if (e0 && e1) (void)hipEventRecord(e0, stream);
+    }
+    hipError_t e = f();
+    if (on && e0 && e1) {
+      (void)hipEventRecord(e1, stream);
+      live.push_back({e0, e1, cls});
+      flops[cls] += fl;
+      bytes[cls] += by;
+      launches[cls] += 1;
+    }
+    return e;
+  }
+};
+
+namespace {
+
+#define TRY(expr)                                                                     \
+  do {                                                                                \
+    hipError_t e_ = (expr);                                                           \
+    if (e_ != hipSuccess)                                                             \
+      return m->fail(GPT2_ERR_DEVICE, std::string("HIP error at ") + #expr + ": " +  \
+                                          hipGetErrorString(e_));                     \
+  } while (0)
+
+using Model = gpt2_model;
+
+hipError_t gemm(Model* m, int cls, int M, int N, int K, const bf16_t* A, int lda, int a_t, const bf16_t* B,
+                int ldb, int b_t, int epi, void* C, int ldc, const float* bias = nullptr,
+                const bf16_t* residual = nullptr, bf16_t* C2 = nullptr, const bf16_t* aux = nullptr,
+                int accumulate = 0, int splits = 1, long split_stride = 0, int k_chunk = 0) {
+  GemmArgs g{};
+  g.A = A; g.B = B; g.M = M; g.N = N; g.K = K; g.lda = lda; g.ldb = ldb;
+  g.C = C; g.ldc = ldc; g.bias = bias; g.residual = residual; g.C2 = C2; g.aux = aux;
+  g.accumulate = accumulate; g.splits = splits; g.split_stride = split_stride; g.k_chunk = k_chunk;
+  double fl = 2.0 * M * N * K;
+  return m->run(cls, fl, 0.0, [&] { return launch_gemm(g, a_t, b_t, epi, m->stream); });
+}
+
+// weight gradient dW[M][N] (=|+=) sum_t A[t][m] * X[t][n] (fp32)
+hipError_t weight_grad(Model* m, int M, int N, const bf16_t* dy, const bf16_t* x, float* dW, int accumulate) {
+  const int BT = (int)m->d.BT;
+  int s = dw_splits(m->d, M, N);
+  if (s <= 1)
+    return gemm(m, GPT2_K_GEMM_DW, M, N, BT, dy, M, 1, x, N, 1, EPI_F32, dW, N, nullptr, nullptr, nullptr, nullptr,
+                accumulate, 1, 0);
+  float* part = m->wsf(m->ws.splitk);
+  hipError_t e = gemm(m, GPT2_K_GEMM_DW, M, N, BT, dy, M, 1, x, N, 1, EPI_F32, part, N, nullptr, nullptr, nullptr,
+                      nullptr, 0, s, (long)M * N, dw_chunk(m->d, M, N));
+  if (e != hipSuccess) return e;
+  return m->run(GPT2_K_OTHER, 0.0, 4.0 * (double)M * N * (s + 1 + accumulate),
+                [&] { return launch_reduce_slices(part, s, (long)M * N, dW, accumulate, m->stream); });
+}
+
+// bias gradient db[N] (=|+=) sum_t dy[t][n]
+hipError_t bias_grad(Model* m, const bf16_t* dy, int N, float* db, int accumulate) {
+  const int BT = (int)m->d.BT;
+  float* parts = m->wsf(m->ws.colsum);
+  int np = colsum_parts(BT);
+  hipError_t e = m->run(GPT2_K_OTHER, 0.0, 2.0 * BT * N + 4.0 * np * N,
+                        [&] { return launch_colsum(dy, BT, N, parts, m->stream); });
+  if (e != hipSuccess) return e;
+  return m->run(GPT2_K_OTHER, 0.0, 4.0 * N * (np + 1 + accumulate),
+                [&] { return launch_reduce_slices(parts, np, N, db, accumulate, m->stream); });
+}
+
+hipError_t ln_fwd(Model* m, const bf16_t* x, const float* w, const float* b, bf16_t* y, float* mean, float* rstd) {
+  const int BT = (int)m->d.BT, C = m->d.C;
+  return m->run(GPT2_K_LAYERNORM, 0.0, 4.0 * BT * C + 8.0 * BT + 8.0 * C,
+                [&] { return launch_layernorm_fwd(x, w, b, y, mean, rstd, BT, C, m->cfg.ln_eps, m->stream); });
+}
+
+hipError_t ln_bwd(Model* m, const bf16_t* dy, const bf16_t* x, const float* mean, const float* rstd, const float* w,
+                  int has_res, float* dw, float* db, int accumulate) {
+  const int BT = (int)m->d.BT, C = m->d.C;
+  float* pw = m->wsf(m->ws.lnpart_w);
+  float* pbias = m->wsf(m->ws.lnpart_b);
+  bf16_t* dres = m->wsb(m->ws.dres);
+  hipError_t e = m->run(GPT2_K_LAYERNORM, 0.0, 2.0 * BT * C * (3 + has_res) + 8.0 * BT, [&] {
+    return launch_layernorm_bwd(dy, x, mean, rstd, w, dres, has_res, pw, pbias, BT, C, m->stream);
+  });
+  if (e != hipSuccess) return e;
+  int nb = layernorm_bwd_blocks(BT);
+  e = m->run(GPT2_K_OTHER, 0.0, 4.0 * C * (nb + 1 + accumulate),
+             [&] { return launch_reduce_slices(pw, nb, C, dw, accumulate, m->stream); });
+  if (e != hipSuccess) return e;
+  return m->run(GPT2_K_OTHER, 0.0, 4.0 * C * (nb + 1 + accumulate),
+                [&] { return launch_reduce_slices(pbias, nb, C, db, accumulate, m->stream); });
+}
+
+AttnArgs attn_args(Model* m, int l) {
+  AttnArgs a{};
+  a.B = m->d.B; a.T = m->d.T; a.H = m->d.H; a.hd = m->d.hd;
+  a.qkv = m->qkv(l); a.out = m->att(l); a.lse = m->lse(l);
+  a.dout = m->wsb(m->ws.datt); a.dsum = m->wsf(m->ws.dsum); a.dqkv = m->wsb(m->ws.dbig);
+  return a;
+}
+
+double attn_fwd_flops(const Dims& d) {
+  // causal: q.k and p.v over the key positions j <= i only
+  return 4.0 * d.B * d.H * d.hd * ((double)d.T * (d.T + 1) / 2.0);
+}
+
+gpt2_status block_fwd(Model* m, int l) {
+  const Dims& d = m->d;
+  const int BT = (int)d.BT, C = d.C, F = d.F;
+  const size_t oC = (size_t)l * C, o3C = (size_t)l * 3 * C, oF = (size_t)l * F;
+  TRY(ln_fwd(m, m->res(l), m->pf(K_LN1W) + oC, m->pf(K_LN1B) + oC, m->ln1(l), m->ln1m(l), m->ln1r(l)));
+  TRY(gemm(m, GPT2_K_GEMM_FWD, BT, 3 * C, C, m->ln1(l), C, 0, m->pb(K_QKVW) + o3C * C, C, 0, EPI_BF16, m->qkv(l),
+           3 * C, m->pf(K_QKVB) + o3C));
+  AttnArgs aa = attn_args(m, l);
+  TRY(m->run(GPT2_K_ATTN_FWD, attn_fwd_flops(d), 0.0, [&] { return launch_attention_fwd(aa, m->stream); }));
+  TRY(gemm(m, GPT2_K_GEMM_FWD, BT, C, C, m->att(l), C, 0, m->pb(K_ATTPROJW) + oC * C, C, 0, EPI_BF16, m->xmid(l), C,
+           m->pf(K_ATTPROJB) + oC, m->res(l)));
+  TRY(ln_fwd(m, m->xmid(l), m->pf(K_LN2W) + oC, m->pf(K_LN2B) + oC, m->ln2(l), m->ln2m(l), m->ln2r(l)));
+  TRY(gemm(m, GPT2_K_GEMM_FWD, BT, F, C, m->ln2(l), C, 0, m->pb(K_FCW) + oF * C, C, 0, EPI_GELU, m->fc(l), F,
+           m->pf(K_FCB) + oF, nullptr, m->gelu(l)));
+  TRY(gemm(m, GPT2_K_GEMM_FWD, BT, C, F, m->gelu(l), F, 0, m->pb(K_FCPROJW) + oC * F, F, 0, EPI_BF16, m->res(l + 1),
+           C, m->pf(K_FCPROJB) + oC, m->xmid(l)));
+  return GPT2_OK;
+}
+
+gpt2_status block_bwd(Model* m, int l, int acc) {
+  const Dims& d = m->d;
+  const int BT = (int)d.BT, C = d.C, F = d.F;
+  const size_t oC = (size_t)l * C, o3C = (size_t)l * 3 * C, oF = (size_t)l * F;
+  bf16_t* dres = m->wsb(m->ws.dres);
+  bf16_t* dh = m->wsb(m->ws.dh);
+  bf16_t* datt = m->wsb(m->ws.datt);
+  bf16_t* dbig = m->wsb(m->ws.dbig);
+  // MLP down projection; GELU backward fused into the input-gradient epilogue
+  TRY(gemm(m, GPT2_K_GEMM_DX, BT, F, C, dres, C, 0, m->pb(K_FCPROJW) + oC * F, F, 1, EPI_GELU_BWD, dbig, F, nullptr,
+           nullptr, nullptr, m->fc(l)));
+  TRY(weight_grad(m, C, F, dres, m->gelu(l), m->gf(K_FCPROJW) + oC * F, acc));
+  TRY(bias_grad(m, dres, C, m->gf(K_FCPROJB) + oC, acc));
+  // MLP up projection
+  TRY(gemm(m, GPT2_K_GEMM_DX, BT, C, F, dbig, F, 0, m->pb(K_FCW) + oF * C, C, 1, EPI_BF16, dh, C));
+  TRY(weight_grad(m, F, C, dbig, m->ln2(l), m->gf(K_FCW) + oF * C, acc));
+  TRY(bias_grad(m, dbig, F, m->gf(K_FCB) + oF, acc));
+  TRY(ln_bwd(m, dh, m->xmid(l), m->ln2m(l), m->ln2r(l), m->pf(K_LN2W) + oC, 1, m->gf(K_LN2W) + oC,
+             m->gf(K_LN2B) + oC, acc));
+  // attention output projection
+  TRY(gemm(m, GPT2_K_GEMM_DX, BT, C, C, dres, C, 0, m->pb(K_ATTPROJW) + oC * C, C, 1, EPI_BF16, datt, C));
+  TRY(weight_grad(m, C, C, dres, m->att(l), m->gf(K_ATTPROJW) + oC * C, acc));
+  TRY(bias_grad(m, dres, C, m->gf(K_ATTPROJB) + oC, acc));
+  // attention
+  AttnArgs aa = attn_args(m, l);
+  TRY(m->run(GPT2_K_ATTN_BWD, 2.0 * attn_fwd_flops(d), 0.0, [&] { return launch_attention_bwd(aa, m->stream); }));
+  // q|k|v projection
+  TRY(gemm(m, GPT2_K_GEMM_DX, BT, C, 3 * C, dbig, 3 * C, 0, m->pb(K_QKVW) + o3C * C, C, 1, EPI_BF16, dh, C));
+  TRY(weight_grad(m, 3 * C, C, dbig, m->ln1(l), m->gf(K_QKVW) + o3C * C, acc));
+  TRY(bias_grad(m, dbig, 3 * C, m->gf(K_QKVB) + o3C, acc));
+  TRY(ln_bwd(m, dh, m->res(l), m->ln1m(l), m->ln1r(l), m->pf(K_LN1W) + oC, 1, m->gf(K_LN1W) + oC,
+             m->gf(K_LN1B) + oC, acc));
+  return GPT2_OK;
+}
+
+double lr_schedule(const gpt2_config& c, int64_t step) {
+  if (step < c.warmup_steps) return (double)c.lr_max * (double)(step + 1) / c.warmup_steps;
+  double frac = (double)(step - c.warmup_steps) / (double)(c.total_steps - c.warmup_steps);
+  if (frac < 0) frac = 0;
+  if (frac > 1) frac = 1;
+  return (double)c.lr_min + 0.5 * (1.0 + std::cos(M_PI * frac)) * ((double)c.lr_max - (double)c.lr_min);
+}
+
+thread_local std::string g_last_error;
+
+}  // namespace
+
+extern "C" {
+
+gpt2_status gpt2_query_sizes(const gpt2_config* cfg, gpt2_sizes* out) {
+  if (const char* why = validate(cfg)) {
+    g_last_error = why;
+    return GPT2_ERR_INVALID_ARG;
+  }
+  if (!out) {
+    g_last_error = "out is NULL";
+    return GPT2_ERR_INVALID_ARG;
+  }
+  Dims d = dims_of(*cfg);
+  size_t kn[K_NKIND];
+  kind_sizes(d, kn);
+  size_t n = 0;
+  for (int k = 0; k < K_NKIND; ++k) n += kn[k];
+  out->n_params = n;
+  out->params_f32 = out->grads_f32 = out->adam_m = out->adam_v = align_up(n * 4);
+  out->params_bf16 = align_up(n * 2);
+  out->activations = act_layout(d).total;
+  out->workspace = ws_layout(d).total;
+  return GPT2_OK;
+}
+
+int32_t gpt2_num_tensors(const gpt2_config* cfg) {
+  if (!cfg || cfg->n_layer < 1) return 0;
+  return 2 + 12 * cfg->n_layer + 2;
+}
+
+gpt2_status gpt2_tensor_info(const gpt2_config* cfg, int32_t idx, char* name, size_t* offset, int32_t* shape,
+                             int32_t* ndim, int32_t* decay) {
+  if (const char* why = validate(cfg)) {
+    g_last_error = why;
+    return GPT2_ERR_INVALID_ARG;
+  }
+  if (!name || !offset || !shape || !ndim || !decay || idx < 0 || idx >= gpt2_num_tensors(cfg)) {
+    g_last_error = "bad tensor_info argument";
+    return GPT2_ERR_INVALID_ARG;
+  }
+  Dims d = dims_of(*cfg);
+  size_t kn[K_NKIND], ko[K_NKIND], o = 0;
+  kind_sizes(d, kn);
+  for (int k = 0; k < K_NKIND; ++k) {
+    ko[k] = o;
+    o += kn[k];
+  }
+  static const char* per_layer[12] = {"ln_1.weight", "ln_1.bias", "attn.c_attn.weight", "attn.c_attn.bias",
+                                      "attn.c_proj.weight", "attn.c_proj.bias", "ln_2.weight", "ln_2.bias",
+                                      "mlp.c_fc.weight", "mlp.c_fc.bias", "mlp.c_proj.weight", "mlp.c_proj.bias"};
+  static const int per_layer_kind[12] = {K_LN1W, K_LN1B, K_QKVW, K_QKVB, K_ATTPROJW, K_ATTPROJB,
+                                         K_LN2W, K_LN2B, K_FCW, K_FCB, K_FCPROJW, K_FCPROJB};
+  const int C = d.C, F = d.F;
+  if (idx == 0) {
+    snprintf(name, 64, "wte");
+    *offset = ko[K_WTE]; shape[0] = d.Vp; shape[1] = C; *ndim = 2; *decay = 1;
+    return GPT2_OK;
+  }
+  if (idx == 1) {
+    snprintf(name, 64, "wpe");
+    *offset = ko[K_WPE]; shape[0] = d.Tmax; shape[1] = C; *ndim = 2; *decay = 1;
+    return GPT2_OK;
+  }
+  int last = gpt2_num_tensors(cfg);
+  if (idx >= last - 2) {
+    bool w = idx == last - 2;
+    snprintf(name, 64, w ? "ln_f.weight" : "ln_f.bias");
+    *offset = ko[w ? K_LNFW : K_LNFB]; shape[0] = C; shape[1] = 0; *ndim = 1; *decay = 0;
+    return GPT2_OK;
+  }
+  int l = (idx - 2) / 12, j = (idx - 2) % 12;
+  int k = per_layer_kind[j];
+  snprintf(name, 64, "h.%d.%s", l, per_layer[j]);
+  size_t per = kn[k] / d.L;
+  *offset = ko[k] + (size_t)l * per;
+  *decay = kDecay[k] ? 1 : 0;
+  switch (k) {
+    case K_QKVW: shape[0] = 3 * C; shape[1] = C; *ndim = 2; break;
+    case K_QKVB: shape[0] = 3 * C; shape[1] = 0; *ndim = 1; break;
+    case K_ATTPROJW: shape[0] = C; shape[1] = C; *ndim = 2; break;
+    case K_FCW: shape[0] = F; shape[1] = C; *ndim = 2; break;
+    case K_FCB: shape[0] = F; shape[1] = 0; *ndim = 1; break;
+    case K_FCPROJW: shape[0] = C; shape[1] = F; *ndim = 2; break;
+    default: shape[0] = C; shape[1] = 0; *ndim = 1; break;
+  }
+  return GPT2_OK;
+}
+
+gpt2_status gpt2_init(const gpt2_config* cfg, const gpt2_buffers* bufs, void* hip_stream, gpt2_model** out) {
+  if (const char* why = validate(cfg)) {
+    g_last_error = why;
+    return GPT2_ERR_INVALID_ARG;
+  }
+  if (!bufs || !out) {
+    g_last_error = "bufs or out is NULL";
+    return GPT2_ERR_INVALID_ARG;
+  }
+  const void* ptrs[7] = {bufs->params_f32, bufs->grads_f32, bufs->adam_m, bufs->adam_v,
+                         bufs->params_bf16, bufs->activations, bufs->workspace};
+  for (const void* p : ptrs) {
+    if (!p || (reinterpret_cast<uintptr_t>(p) % ALIGN)) {
+      g_last_error = "a buffer is NULL or not 256-byte aligned";
+      return GPT2_ERR_INVALID_ARG;
+    }
+  }
+  Model* m = new (std::nothrow) Model();
+  if (!m) {
+    g_last_error = "out of host memory";
+    return GPT2_ERR_INVALID_ARG;
+  }
+  m->cfg = *cfg;
+  m->d = dims_of(*cfg);
+  m->buf = *bufs;
+  m->stream = static_cast<hipStream_t>(hip_stream);
+  kind_sizes(m->d, m->kn);
+  size_t o = 0;
+  for (int k = 0; k < K_NKIND; ++k) {
+    m->koff[k] = o;
+    o += m->kn[k];
+  }
+  m->n_params = o;
+  m->act = act_layout(m->d);
+  m->ws = ws_layout(m->d);
+  gpt2_status st = gpt2_sync_weights(m);
+  if (st != GPT2_OK) {
+    g_last_error = m->err;
+    delete m;
+    return st;
+  }
+  *out = m;
+  return GPT2_OK;
+}
+
+gpt2_status gpt2_sync_weights(gpt2_model* m) {
+  if (!m) return GPT2_ERR_INVALID_ARG;
+  TRY(m->run(GPT2_K_OTHER, 0.0, 6.0 * m->n_params, [&] {
+    return launch_cast_bf16(static_cast<float*>(m->buf.params_f32), static_cast<bf16_t*>(m->buf.params_bf16),
+                            (long)m->n_params, m->stream);
+  }));
+  return GPT2_OK;
+}
+
+gpt2_status gpt2_forward(gpt2_model* m, const int32_t* d_inputs, const int32_t* d_targets) {
+  if (!m) return GPT2_ERR_INVALID_ARG;
+  if (!d_inputs) return m->fail(GPT2_ERR_INVALID_ARG, "inputs is NULL");
+  const Dims& d = m->d;
+  const int BT = (int)d.BT, C = d.C;
+  m->have_dlogits = false;
+  m->have_loss = false;
+  // keep the ids for the embedding backward
+  TRY(hipMemcpyAsync(m->ids(), d_inputs, (size_t)BT * 4, hipMemcpyDeviceToDevice, m->stream));
+  TRY(m->run(GPT2_K_OTHER, 0.0, 4.0 * BT + 8.0 * BT * C + 2.0 * BT * C,
+             [&] { return launch_embed_fwd(d_inputs, m->pf(K_WTE), m->pf(K_WPE), m->res(0), d.B, d.T, C, m->stream); }));
+  for (int l = 0; l < d.L; ++l) {
+    gpt2_status s = block_fwd(m, l);
+    if (s != GPT2_OK) return s;
+  }
+  TRY(ln_fwd(m, m->res(d.L), m->pf(K_LNFW), m->pf(K_LNFB), m->lnf(), m->lnfm(), m->lnfr()));
+  TRY(gemm(m, GPT2_K_GEMM_FWD, BT, d.Vp, C, m->lnf(), C, 0, m->pb(K_WTE), C, 0, EPI_BF16, m->logits(), d.Vp));
+  if (d_targets) {
+    const float scale = (float)(1.0 / ((double)BT * d.accum));
+    TRY(m->run(GPT2_K_CROSS_ENTROPY, 0.0, 4.0 * BT * d.Vp + 8.0 * BT, [&] {
+      return launch_cross_entropy(m->logits(), d_targets, m->losses(), BT, d.V, d.Vp, scale, m->stream);
+    }));
+    TRY(m->run(GPT2_K_OTHER, 0.0, 4.0 * BT, [&] { return launch_mean(m->losses(), BT, m->loss_mean(), m->stream); }));
+    m->have_dlogits = true;
+    m->have_loss = true;
+  }
+  return GPT2_OK;
+}
+
+gpt2_status gpt2_backward(gpt2_model* m, int32_t accumulate) {
+  if (!m) return GPT2_ERR_INVALID_ARG;
+  if (!m->have_dlogits) return m->fail(GPT2_ERR_STATE, "backward needs a forward with targets first");
+  if (accumulate && !m->have_grads) return m->fail(GPT2_ERR_STATE, "accumulate with no gradient to add to");
+  const Dims& d = m->d;
+  const int BT = (int)d.BT, C = d.C;
+  const int acc = accumulate ? 1 : 0;
+  bf16_t* dh = m->wsb(m->ws.dh);
+  bf16_t* dres = m->wsb(m->ws.dres);
+  // tied LM head: input gradient and the head's share of the token-table gradient
+  TRY(gemm(m, GPT2_K_GEMM_DX, BT, C, d.Vp, m->logits(), d.Vp, 0, m->pb(K_WTE), C, 1, EPI_BF16, dh, C));
+  TRY(weight_grad(m, d.Vp, C, m->logits(), m->lnf(), m->gf(K_WTE), acc));
+  TRY(ln_bwd(m, dh, m->res(d.L), m->lnfm(), m->lnfr(), m->pf(K_LNFW), 0, m->gf(K_LNFW), m->gf(K_LNFB), acc));
+  for (int l = d.L - 1; l >= 0; --l) {
+    gpt2_status s = block_bwd(m, l, acc);
+    if (s != GPT2_OK) return s;
+  }
+  // embedding: scatter into the token table (after the head's share), sum into positions
+  TRY(m->run(GPT2_K_OTHER, 0.0, 4.0 * BT + 2.0 * BT * C + 8.0 * BT * C,
+             [&] { return launch_embed_bwd(m->ids(), dres, m->gf(K_WTE), d.B, d.T, C, m->stream); }));
+  TRY(m->run(GPT2_K_OTHER, 0.0, 2.0 * BT * C + 4.0 * d.Tmax * C * (1 + acc),
+             [&] { return launch_embed_bwd_pos(dres, m->gf(K_WPE), d.B, d.T, d.Tmax, C, acc, m->stream); }));
+  m->have_grads = true;
+  return GPT2_OK;
+}
+
+gpt2_status gpt2_adamw_step(gpt2_model* m, int64_t step, float* lr_out, float* d_grad_norm_out) {
+  if (!m) return GPT2_ERR_INVALID_ARG;
+  if (step < 0) return m->fail(GPT2_ERR_INVALID_ARG, "step must be >= 0");
+  if (!m->have_grads) return m->fail(GPT2_ERR_STATE, "optimizer step with no gradient");
+  const gpt2_config& c = m->cfg;
+  const long n = (long)m->n_params;
+  float* grads = static_cast<float*>(m->buf.grads_f32);
+  float* parts = m->wsf(m->ws.sumsq);
+  float* nc = m->wsf(m->ws.normcoef);
+  TRY(m->run(GPT2_K_OPTIMIZER, 0.0, 4.0 * n, [&] { return launch_sumsq(grads, n, parts, m->stream); }));
+  TRY(m->run(GPT2_K_OPTIMIZER, 0.0, 4.0 * sumsq_parts(),
+             [&] { return launch_clip_coef(parts, sumsq_parts(), c.grad_clip, nc, m->stream); }));
+  if (d_grad_norm_out)
+    TRY(hipMemcpyAsync(d_grad_norm_out, nc, sizeof(float), hipMemcpyDeviceToDevice, m->stream));
+  const double lr = lr_schedule(c, step);
+  AdamArgs a{};
+  a.p = static_cast<float*>(m->buf.params_f32);
+  a.g = grads;
+  a.m = static_cast<float*>(m->buf.adam_m);
+  a.v = static_cast<float*>(m->buf.adam_v);
+  a.p_bf16 = static_cast<bf16_t*>(m->buf.params_bf16);
+  a.norm_coef = nc;
+  a.n = n;
+  a.lr = (float)lr;
+  a.beta1 = c.beta1; a.beta2 = c.beta2; a.eps = c.adam_eps; a.weight_decay = c.weight_decay;
+  a.bc1 = (float)(1.0 - std::pow((double)c.beta1, (double)(step + 1)));
+  a.bc2 = (float)(1.0 - std::pow((double)c.beta2, (double)(step + 1)));
+  a.seg.count = K_NKIND;
+  for (int k = 0; k < K_NKIND; ++k) {
+    a.seg.end[k] = (long)(m->koff[k] + m->kn[k]);
+    a.seg.decay[k] = kDecay[k] ? 1 : 0;
+  }
+  TRY(m->run(GPT2_K_OPTIMIZER, 0.0, 30.0 * n, [&] { return launch_adamw(a, m->stream); }));
+  if (lr_out) *lr_out = (float)lr;
+  m->have_grads = false;
+  return GPT2_OK;
+}
+
+gpt2_status gpt2_loss(gpt2_model* m, float* loss_out) {
+  if (!m) return GPT2_ERR_INVALID_ARG;
+  if (!loss_out) return m->fail(GPT2_ERR_INVALID_ARG, "loss_out is NULL");
+  if (!m->have_loss) return m->fail(GPT2_ERR_STATE, "no forward with targets yet");
+  TRY(hipMemcpyAsync(loss_out, m->loss_mean(), sizeof(float), hipMemcpyDeviceToHost, m->stream));
+  TRY(hipStreamSynchronize(m->stream));
+  return GPT2_OK;
+}
+
+float gpt2_lr_at(const gpt2_config* cfg, int64_t step) {
+  if (!cfg || step < 0) return 0.0f;
+  return (float)lr_schedule(*cfg, step);
+}
+
+void gpt2_destroy(gpt2_model* m) {
+  if (!m) return;
+  for (auto& r : m->live) {
+    (void)hipEventSynchronize(r.b);
+    (void)hipEventDestroy(r.a);
+    (void)hipEventDestroy(r.b);
+  }
+  for (hipEvent_t e : m->pool) (void)hipEventDestroy(e);
+  delete m;
+}
+
+const char* gpt2_last_error(const gpt2_model* m) {
+  if (m && !m->err.empty()) return m->err.c_str();
+  return g_last_error.c_str();
+}
+
+gpt2_status gpt2_activation_info(const gpt2_model* mc, int32_t which, int32_t layer, size_t* offset_bytes,
+                                 size_t* numel, int32_t* dtype) {
+  gpt2_model* m = const_cast<gpt2_model*>(mc);
+  if (!m || !offset_bytes || !numel || !dtype) return GPT2_ERR_INVALID_ARG;
+  const Dims& d = m->d;
+  const size_t BT = d.BT, C = d.C;
+  const ActLayout& a = m->act;
+  const bool per_layer = which >= GPT2_ACT_LN1 && which <= GPT2_ACT_GELU;
+  const int lmax = which == GPT2_ACT_RESIDUAL ? d.L : (per_layer ? d.L - 1 : 0);
+  if (layer < 0 || layer > lmax) return m->fail(GPT2_ERR_INVALID_ARG, "layer out of range");
+  const size_t l = layer;
+  switch (which) {
+    case GPT2_ACT_RESIDUAL: *offset_bytes = a.residual + l * a.s_act; *numel = BT * C; *dtype = 1; break;
+    case GPT2_ACT_LN1: *offset_bytes = a.ln1 + l * a.s_act; *numel = BT * C; *dtype = 1; break;
+    case GPT2_ACT_LN1_MEAN: *offset_bytes = a.ln1_mean + l * a.s_row; *numel = BT; *dtype = 0; break;
+    case GPT2_ACT_LN1_RSTD: *offset_bytes = a.ln1_rstd + l * a.s_row; *numel = BT; *dtype = 0; break;
+    case GPT2_ACT_QKV: *offset_bytes = a.qkv + l * a.s_qkv; *numel = BT * 3 * C; *dtype = 1; break;
+    case GPT2_ACT_ATT: *offset_bytes = a.att + l * a.s_act; *numel = BT * C; *dtype = 1; break;
+    case GPT2_ACT_ATT_LSE: *offset_bytes = a.lse + l * a.s_lse; *numel = (size_t)d.B * d.H * d.T; *dtype = 0; break;
+    case GPT2_ACT_X_MID: *offset_bytes = a.x_mid + l * a.s_act; *numel = BT * C; *dtype = 1; break;
+    case GPT2_ACT_LN2: *offset_bytes = a.ln2 + l * a.s_act; *numel = BT * C; *dtype = 1; break;
+    case GPT2_ACT_LN2_MEAN: *offset_bytes = a.ln2_mean + l * a.s_row; *numel = BT; *dtype = 0; break;
+    case GPT2_ACT_LN2_RSTD: *offset_bytes = a.ln2_rstd + l * a.s_row; *numel = BT; *dtype = 0; break;
+    case GPT2_ACT_FC: *offset_bytes = a.fc + l * a.s_ff; *numel = BT * d.F; *dtype = 1; break;
+    case GPT2_ACT_GELU: *offset_bytes = a.gelu + l * a.s_ff; *numel = BT * d.F; *dtype = 1; break;
+    case GPT2_ACT_LNF: *offset_bytes = a.lnf; *numel = BT * C; *dtype = 1; break;
+    case GPT2_ACT_LNF_MEAN: *offset_bytes = a.lnf_mean; *numel = BT; *dtype = 0; break;
+    case GPT2_ACT_LNF_RSTD: *offset_bytes = a.lnf_rstd; *numel = BT; *dtype = 0; break;
+    case GPT2_ACT_LOGITS: *offset_bytes = a.logits; *numel = BT * d.Vp; *dtype = 1; break;
+    case GPT2_ACT_LOSSES: *offset_bytes = a.losses; *numel = BT; *dtype = 0; break;
+    default: return m->fail(GPT2_ERR_INVALID_ARG, "unknown activation");
+  }
+  return GPT2_OK;
+}
+
+gpt2_status gpt2_block_forward(gpt2_model* m, int32_t layer, const void* d_x_in, void* d_x_out) {
+  if (!m) return GPT2_ERR_INVALID_ARG;
+  if (!d_x_in || layer < 0 || layer >= m->d.L) return m->fail(GPT2_ERR_INVALID_ARG, "bad block_forward argument");
+  const size_t bytes = (size_t)m->d.BT * m->d.C * 2;
+  TRY(hipMemcpyAsync(m->res(layer), d_x_in, bytes, hipMemcpyDeviceToDevice, m->stream));
+  gpt2_status s = block_fwd(m, layer);
+  if (s != GPT2_OK) return s;
+  if (d_x_out) TRY(hipMemcpyAsync(d_x_out, m->res(layer + 1), bytes, hipMemcpyDeviceToDevice, m->stream));
+  return GPT2_OK;
+}
+
+gpt2_status gpt2_block_backward(gpt2_model* m, int32_t layer, const void* d_dx_out, void* d_dx_in,
+                                int32_t accumulate) {
+  if (!m) return GPT2_ERR_INVALID_ARG;
+  if (!d_dx_out || layer < 0 || layer >= m->d.L) return m->fail(GPT2_ERR_INVALID_ARG, "bad block_backward argument");
+  const size_t bytes = (size_t)m->d.BT * m->d.C * 2;
+  bf16_t* dres = m->wsb(m->ws.dres);
+  TRY(hipMemcpyAsync(dres, d_dx_out, bytes, hipMemcpyDeviceToDevice, m->stream));
+  gpt2_status s = block_bwd(m, layer, accumulate ? 1 : 0);
+  if (s != GPT2_OK) return s;
+  if (d_dx_in) TRY(hipMemcpyAsync(d_dx_in, dres, bytes, hipMemcpyDeviceToDevice, m->stream));
+  return GPT2_OK;
+}
+
+gpt2_status gpt2_embedding_backward(gpt2_model* m, const int32_t* d_ids, const void* d_dx, int32_t accumulate) {
+  if (!m) return GPT2_ERR_INVALID_ARG;
+  if (!d_ids || !d_dx) return m->fail(GPT2_ERR_INVALID_ARG, "ids or dx is NULL");
+  const Dims& d = m->d;
+  const bf16_t* dx = static_cast<const bf16_t*>(d_dx);
+  const int acc = accumulate ? 1 : 0;
+  if (!acc)  // zero-slice reduction writes zeros
+    TRY(launch_reduce_slices(nullptr, 0, (long)m->kn[K_WTE], m->gf(K_WTE), 0, m->stream));
+  TRY(m->run(GPT2_K_OTHER, 0.0, 4.0 * d.BT + 10.0 * d.BT * d.C,
+             [&] { return launch_embed_bwd(d_ids, dx, m->gf(K_WTE), d.B, d.T, d.C, m->stream); }));
+  TRY(m->run(GPT2_K_OTHER, 0.0, 2.0 * d.BT * d.C + 4.0 * d.Tmax * d.C * (1 + acc),
+             [&] { return launch_embed_bwd_pos(dx, m->gf(K_WPE), d.B, d.T, d.Tmax, d.C, acc, m->stream); }));
+  return GPT2_OK;
+}
+
+gpt2_status gpt2_probe_enable(gpt2_model* m, uint32_t class_mask) {
+  if (!m) return GPT2_ERR_INVALID_ARG;
+  m->probe_mask = class_mask;
+  return GPT2_OK;
+}
+
+gpt2_status gpt2_probe_reset(gpt2_model* m) {
+  if (!m) return GPT2_ERR_INVALID_ARG;
+  for (auto& r : m->live) {
+    if (hipEventSynchronize(r.b) != hipSuccess) return m->fail(GPT2_ERR_DEVICE, "event sync failed");
+    m->pool.push_back(r.a);
+    m->pool.push_back(r.b);
+  }
+  m->live.clear();
+  for (int k = 0; k < GPT2_K_COUNT; ++k) {
+    m->ms[k] = m->flops[k] = m->bytes[k] = 0.0;
+    m->launches[k] = 0;
+  }
+  return GPT2_OK;
+}
+
+gpt2_status gpt2_probe_read(gpt2_model* m, int32_t kclass, double* total_ms, int64_t* launches, double* flops,
+                            double* bytes) {
+  if (!m) return GPT2_ERR_INVALID_ARG;
+  if (kclass < 0 || kclass >= GPT2_K_COUNT) return m->fail(GPT2_ERR_INVALID_ARG, "bad kernel class");
+  for (auto& r : m->live) {
+    if (hipEventSynchronize(r.b) != hipSuccess) return m->fail(GPT2_ERR_DEVICE, "event sync failed");
+    float t = 0.0f;
+    if (hipEventElapsedTime(&t, r.a, r.b) != hipSuccess) return m->fail(GPT2_ERR_DEVICE, "event timing failed");
+    m->ms[r.cls] += t;
+    m->pool.push_back(r.a);
+    m->pool.push_back(r.b);
+  }
+  m->live.clear();
+  if (total_ms) *total_ms = m->ms[kclass];
+  if (launches) *launches = m->launches[kclass];
+  if (flops) *flops = m->flops[kclass];
+  if (bytes) *bytes = m->bytes[kclass];
+  return GPT2_OK;
+}
+
+}  // extern "C"

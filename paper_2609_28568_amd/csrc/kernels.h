@@ -1,0 +1,115 @@
+// Internal launcher interface between the host library and the HIP kernels.
+// Every launcher enqueues on the given stream and returns hipGetLastError().
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+typedef uint16_t bf16_t;
+
+// ---------------------------------------------------------------- GEMM
+enum GemmEpilogue {
+  EPI_BF16 = 0,      // C = bf16(acc + bias? + residual?)
+  EPI_GELU = 1,      // C = bf16(acc + bias) (pre-activation), C2 = bf16(gelu(acc + bias))
+  EPI_GELU_BWD = 2,  // C = bf16(acc * gelu'(aux))
+  EPI_F32 = 3        // C (fp32, one slice per split) = acc (+ C if accumulate)
+};
+
+struct GemmArgs {
+  const bf16_t* A;
+  const bf16_t* B;
+  int M, N, K;
+  int lda, ldb;
+  void* C;
+  int ldc;
+  const float* bias;       // [N] or null
+  const bf16_t* residual;  // [M][ldc] or null
+  bf16_t* C2;              // second output of EPI_GELU
+  const bf16_t* aux;       // pre-activation for EPI_GELU_BWD
+  int accumulate;
+  int splits;              // split of the contraction over grid.z (EPI_F32 only)
+  long split_stride;       // elements between split output slices
+  int k_chunk;             // contraction length per split (from gemm_split_plan)
+};
+
+// Plan a contraction split of K into about `want` pieces: writes the chunk
+// length (a multiple of the 64-wide k tile) and returns the split count.
+int gemm_split_plan(int K, int want, int* k_chunk);
+hipError_t launch_gemm(const GemmArgs& g, int a_t, int b_t, int epi, hipStream_t s);
+
+// ---------------------------------------------------------------- attention
+struct AttnArgs {
+  int B, T, H, hd;
+  const bf16_t* qkv;   // [B*T, 3C]
+  bf16_t* out;         // [B*T, C]
+  float* lse;          // [B, H, T]
+  // backward
+  const bf16_t* dout;  // [B*T, C]
+  float* dsum;         // [B, H, T] rowsum(dout * out)
+  bf16_t* dqkv;        // [B*T, 3C]
+};
+hipError_t launch_attention_fwd(const AttnArgs& a, hipStream_t s);
+hipError_t launch_attention_bwd(const AttnArgs& a, hipStream_t s);
+
+// ---------------------------------------------------------------- layernorm
+hipError_t launch_layernorm_fwd(const bf16_t* x, const float* w, const float* b, bf16_t* y,
+                                float* mean, float* rstd, int rows, int C, float eps, hipStream_t s);
+// dres (in/out, may be null on input when has_res == 0): dres = dres + dx.
+// Per-block partial sums of dy*xhat and dy go to part_w / part_b [nblk][C].
+int layernorm_bwd_blocks(int rows);
+hipError_t launch_layernorm_bwd(const bf16_t* dy, const bf16_t* x, const float* mean,
+                                const float* rstd, const float* w, bf16_t* dres, int has_res,
+                                float* part_w, float* part_b, int rows, int C, hipStream_t s);
+
+// ---------------------------------------------------------------- misc
+// dst[i] (fp32, n elements) = (accumulate ? dst[i] : 0) + sum_s src[s*n + i]
+hipError_t launch_reduce_slices(const float* src, int nslices, long n, float* dst, int accumulate,
+                                hipStream_t s);
+// column sums of bf16 [rows][N] into partials [nparts][N]; returns nparts
+int colsum_parts(int rows);
+hipError_t launch_colsum(const bf16_t* x, int rows, int N, float* parts, hipStream_t s);
+
+hipError_t launch_embed_fwd(const int32_t* ids, const float* wte, const float* wpe, bf16_t* x, int B,
+                            int T, int C, hipStream_t s);
+// dwte[ids[r]] += dx[r] (fp32 atomics; adds to what is there)
+hipError_t launch_embed_bwd(const int32_t* ids, const bf16_t* dx, float* dwte, int B, int T, int C,
+                            hipStream_t s);
+// dwpe[t] = (accumulate ? dwpe[t] : 0) + sum_b dx[b, t] for t < T; rows T..Tmax-1 get 0 added
+hipError_t launch_embed_bwd_pos(const bf16_t* dx, float* dwpe, int B, int T, int Tmax, int C,
+                                int accumulate, hipStream_t s);
+
+// fused softmax cross-entropy over the first V of Vp columns; dlogits
+// (scaled) overwrite the logits; losses fp32 [rows]
+hipError_t launch_cross_entropy(bf16_t* logits, const int32_t* targets, float* losses, int rows,
+                                int V, int Vp, float grad_scale, hipStream_t s);
+// mean of n floats into out[0] (single block, fixed order)
+hipError_t launch_mean(const float* x, int n, float* out, hipStream_t s);
+
+// fp32 -> bf16 copy of n elements (n % 4 == 0)
+hipError_t launch_cast_bf16(const float* src, bf16_t* dst, long n, hipStream_t s);
+
+// ---------------------------------------------------------------- optimizer
+int sumsq_parts();
+hipError_t launch_sumsq(const float* g, long n, float* parts, hipStream_t s);
+// norm = sqrt(sum parts); coef = clip/norm if norm > clip else 1
+hipError_t launch_clip_coef(const float* parts, int nparts, float clip, float* norm_coef,
+                            hipStream_t s);
+
+struct AdamSegments {
+  long end[16];    // exclusive end offset (elements) of each segment
+  int decay[16];   // 1 where weight decay applies
+  int count;
+};
+struct AdamArgs {
+  float* p;
+  const float* g;
+  float* m;
+  float* v;
+  bf16_t* p_bf16;
+  const float* norm_coef;  // [0] norm, [1] clip coefficient
+  long n;
+  float lr, beta1, beta2, eps, weight_decay;
+  float bc1, bc2;          // 1 - beta^t
+  AdamSegments seg;
+};
+hipError_t launch_adamw(const AdamArgs& a, hipStream_t s);

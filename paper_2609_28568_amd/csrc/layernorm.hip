@@ -1,0 +1,166 @@
+// LayerNorm forward and backward over rows of C channels (pre-LN blocks and
+// the final norm, Figure 1). Statistics in fp32, biased variance, eps from the
+// config. One wavefront per row; each lane owns channels {4*(lane + 64*i)..+3},
+// read as 8-byte bf16 chunks.
+#include "common.h"
+#include "kernels.h"
+
+namespace {
+
+constexpr int MAXCH = 8;   // 4-channel chunks per lane: C <= 2048
+
+__global__ __launch_bounds__(256) void ln_fwd_kernel(const bf16_t* __restrict__ x, const float* __restrict__ w,
+                                                     const float* __restrict__ b, bf16_t* __restrict__ y,
+                                                     float* __restrict__ mean_out, float* __restrict__ rstd_out,
+                                                     int rows, int C, float eps) {
+  const int lane = threadIdx.x & 63;
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= rows) return;
+  const bf16_t* xr = x + (size_t)row * C;
+  float v[MAXCH][4];
+  float s = 0.0f;
+#pragma unroll
+  for (int i = 0; i < MAXCH; ++i) {
+    int c = 4 * (lane + 64 * i);
+    if (c < C) {
+      uint2 u = *reinterpret_cast<const uint2*>(xr + c);
+      v[i][0] = lo_f(u.x); v[i][1] = hi_f(u.x); v[i][2] = lo_f(u.y); v[i][3] = hi_f(u.y);
+      s += v[i][0] + v[i][1] + v[i][2] + v[i][3];
+    }
+  }
+  const float mean = wave_sum(s) / C;
+  float q = 0.0f;
+#pragma unroll
+  for (int i = 0; i < MAXCH; ++i) {
+    int c = 4 * (lane + 64 * i);
+    if (c < C)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        float d = v[i][e] - mean;
+        q += d * d;
+      }
+  }
+  const float rstd = 1.0f / sqrtf(wave_sum(q) / C + eps);
+  bf16_t* yr = y + (size_t)row * C;
+#pragma unroll
+  for (int i = 0; i < MAXCH; ++i) {
+    int c = 4 * (lane + 64 * i);
+    if (c < C) {
+      float4 wv = *reinterpret_cast<const float4*>(w + c);
+      float4 bv = *reinterpret_cast<const float4*>(b + c);
+      float o0 = (v[i][0] - mean) * rstd * wv.x + bv.x;
+      float o1 = (v[i][1] - mean) * rstd * wv.y + bv.y;
+      float o2 = (v[i][2] - mean) * rstd * wv.z + bv.z;
+      float o3 = (v[i][3] - mean) * rstd * wv.w + bv.w;
+      *reinterpret_cast<uint2*>(yr + c) = make_uint2(pack2(o0, o1), pack2(o2, o3));
+    }
+  }
+  if (lane == 0) {
+    mean_out[row] = mean;
+    rstd_out[row] = rstd;
+  }
+}
+
+// dx = rstd * (g - mean(g) - xhat * mean(g * xhat)), g = dy * w; the result is
+// added to the residual-stream gradient. Per-block sums of dy*xhat and dy.
+__global__ __launch_bounds__(256) void ln_bwd_kernel(const bf16_t* __restrict__ dy, const bf16_t* __restrict__ x,
+                                                     const float* __restrict__ mean_in,
+                                                     const float* __restrict__ rstd_in, const float* __restrict__ w,
+                                                     bf16_t* __restrict__ dres, int has_res,
+                                                     float* __restrict__ part_w, float* __restrict__ part_b,
+                                                     int rows, int C) {
+  __shared__ float red[4][MAXCH * 4 * 64];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  float aw[MAXCH][4], ab[MAXCH][4], wr[MAXCH][4];
+#pragma unroll
+  for (int i = 0; i < MAXCH; ++i) {
+    int c = 4 * (lane + 64 * i);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) aw[i][e] = ab[i][e] = 0.0f;
+    if (c < C) {
+      float4 wv = *reinterpret_cast<const float4*>(w + c);
+      wr[i][0] = wv.x; wr[i][1] = wv.y; wr[i][2] = wv.z; wr[i][3] = wv.w;
+    }
+  }
+  for (int row = blockIdx.x * 4 + wave; row < rows; row += gridDim.x * 4) {
+    const float mean = mean_in[row], rstd = rstd_in[row];
+    const bf16_t* xr = x + (size_t)row * C;
+    const bf16_t* dr = dy + (size_t)row * C;
+    float xh[MAXCH][4], gg[MAXCH][4];
+    float s1 = 0.0f, s2 = 0.0f;
+#pragma unroll
+    for (int i = 0; i < MAXCH; ++i) {
+      int c = 4 * (lane + 64 * i);
+      if (c < C) {
+        uint2 xu = *reinterpret_cast<const uint2*>(xr + c);
+        uint2 du = *reinterpret_cast<const uint2*>(dr + c);
+        float xv[4] = {lo_f(xu.x), hi_f(xu.x), lo_f(xu.y), hi_f(xu.y)};
+        float dv[4] = {lo_f(du.x), hi_f(du.x), lo_f(du.y), hi_f(du.y)};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          xh[i][e] = (xv[e] - mean) * rstd;
+          gg[i][e] = dv[e] * wr[i][e];
+          s1 += gg[i][e];
+          s2 += gg[i][e] * xh[i][e];
+          aw[i][e] += dv[e] * xh[i][e];
+          ab[i][e] += dv[e];
+        }
+      }
+    }
+    const float gm = wave_sum(s1) / C, gxm = wave_sum(s2) / C;
+    bf16_t* rr = dres + (size_t)row * C;
+#pragma unroll
+    for (int i = 0; i < MAXCH; ++i) {
+      int c = 4 * (lane + 64 * i);
+      if (c < C) {
+        float o[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) o[e] = rstd * (gg[i][e] - gm - xh[i][e] * gxm);
+        if (has_res) {
+          uint2 ru = *reinterpret_cast<const uint2*>(rr + c);
+          o[0] += lo_f(ru.x); o[1] += hi_f(ru.x); o[2] += lo_f(ru.y); o[3] += hi_f(ru.y);
+        }
+        *reinterpret_cast<uint2*>(rr + c) = make_uint2(pack2(o[0], o[1]), pack2(o[2], o[3]));
+      }
+    }
+  }
+  // combine the four waves' partial parameter gradients in a fixed order
+  for (int pass = 0; pass < 2; ++pass) {
+#pragma unroll
+    for (int i = 0; i < MAXCH; ++i)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) red[wave][(i * 64 + lane) * 4 + e] = pass == 0 ? aw[i][e] : ab[i][e];
+    __syncthreads();
+    float* dst = pass == 0 ? part_w : part_b;
+    for (int c = threadIdx.x; c < C; c += 256) {
+      // channel c lives at chunk i = (c/4)/64, lane (c/4)%64, element c%4
+      int cq = c >> 2, i = cq >> 6, l = cq & 63, e = c & 3;
+      int k = (i * 64 + l) * 4 + e;
+      dst[(size_t)blockIdx.x * C + c] = red[0][k] + red[1][k] + red[2][k] + red[3][k];
+    }
+    __syncthreads();
+  }
+}
+
+}  // namespace
+
+hipError_t launch_layernorm_fwd(const bf16_t* x, const float* w, const float* b, bf16_t* y, float* mean,
+                                float* rstd, int rows, int C, float eps, hipStream_t s) {
+  if (C > MAXCH * 256 || C % 4) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(ln_fwd_kernel, dim3((rows + 3) / 4), dim3(256), 0, s, x, w, b, y, mean, rstd, rows, C, eps);
+  return hipGetLastError();
+}
+
+int layernorm_bwd_blocks(int rows) {
+  int n = (rows + 3) / 4;
+  return n < 512 ? n : 512;
+}
+
+hipError_t launch_layernorm_bwd(const bf16_t* dy, const bf16_t* x, const float* mean, const float* rstd,
+                                const float* w, bf16_t* dres, int has_res, float* part_w, float* part_b, int rows,
+                                int C, hipStream_t s) {
+  if (C > MAXCH * 256 || C % 4) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(ln_bwd_kernel, dim3(layernorm_bwd_blocks(rows)), dim3(256), 0, s, dy, x, mean, rstd, w, dres,
+                     has_res, part_w, part_b, rows, C);
+  return hipGetLastError();
+}
