@@ -1,0 +1,213 @@
+"""Throughput of the GPT-2 124M training step on one MI355X.
+
+One step = forward (embedding, 12 blocks, final LN, tied LM head, softmax
+cross-entropy) + backward + global-norm clip + AdamW, on a micro-batch of
+16 x 1024 synthetic Zipf(1.1) tokens already resident in HBM. Prints one JSON
+line with tokens/s, model-FLOPs utilisation against the bf16 MFMA peak, a
+roofline entry for the dominant kernel (its launches timed with HIP events on
+the library's stream during the timed steps) and the CPU oracle timed on a
+bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
+
+
+def flops_per_token(w: dict) -> float:
+    """Algorithmic training FLOPs per token: 6 per matmul parameter (counting
+    the LM head on the real vocabulary) plus causal attention (q.k and p.v
+    over the unmasked half, three times for forward and backward)."""
+    L, C, V, T = w["n_layer"], w["d_model"], w["vocab"], w["T"]
+    n_mm = 12 * L * C * C + C * V
+    return 6.0 * n_mm + 6.0 * L * C * (T + 1)
+
+
+def flops_per_token_palm(w: dict, n_params: int) -> float:
+    return 6.0 * n_params + 12.0 * w["n_layer"] * w["d_model"] * w["T"]
+
+
+def cpu_baseline(w: dict, params, ids, tgt) -> dict:
+    """The oracle's step (fwd + bwd + clip + AdamW) on the first sequence of
+    the batch: 1 x 1024 tokens through the full model."""
+    import numpy as np
+    import oracle
+    from threadpoolctl import threadpool_info
+    ws = dict(w)
+    ws["B"] = 1
+    cfg = oracle.Config.from_dict({**ws, "lr_min": 6e-5})
+    p = {k: v.copy() for k, v in params.items()}
+    m = oracle.zero_grads(p)
+    v = oracle.zero_grads(p)
+    t0 = time.perf_counter()
+    oracle.train_step(p, m, v, 0, [(ids[:1], tgt[:1])], cfg)
+    dt = time.perf_counter() - t0
+    threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    return {"value": round(ws["T"] / dt, 3), "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": f"one optimizer step (fwd+bwd+clip+AdamW) on 1 sequence x {ws['T']} tokens of the same "
+                      f"model and token stream, numpy fp32, {dt:.1f} s"}
+
+
+def traffic_from_profiles(kernel_tag: str, src_hash: str):
+    """HBM bytes per launch from committed rocprofv3 counter summaries, if
+    they were taken on the current kernel source."""
+    path = os.path.join(ROOT, "profiles", f"{kernel_tag}_traffic.json")
+    if not os.path.exists(path):
+        return None
+    d = json.load(open(path))
+    if d.get("source_sha256") != src_hash:
+        return None
+    return d.get("bytes_per_launch")
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2609_28568_amd", "csrc")
+    for f in sorted(os.listdir(csrc)):
+        h.update(open(os.path.join(csrc, f), "rb").read())
+    return h.hexdigest()
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="gpt2_124m")
+    ap.add_argument("--probe", default="gemm_dw", help="kernel class timed for the roofline entry")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--classes", action="store_true", help="also report every kernel class (extra pass)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); this build has no multi-GPU path",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    from paper_2609_28568_amd import binding, synth
+
+    w = dict(synth.WORKLOADS[args.workload])
+    cfg = binding.make_config(w, synth.OPTIM)
+    print(f"bench: {args.workload} B={w['B']} T={w['T']} on {torch.cuda.get_device_name(0)}",
+          file=sys.stderr, flush=True)
+    params = synth.init_params(w)
+    batches = [synth.token_batch(w, micro=i) for i in range(2)]
+    m = binding.GPT2(cfg)
+    m.set_params(params)
+    dev = [(torch.from_numpy(a).cuda(), torch.from_numpy(b).cuda()) for a, b in batches]
+    torch.cuda.synchronize()
+
+    def step(i):
+        ids, tgt = dev[i % len(dev)]
+        m.forward(ids, tgt)
+        m.backward(accumulate=False)
+        m.adamw_step(i)
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    print(f"bench: warmup done, loss {m.loss():.4f}", file=sys.stderr, flush=True)
+
+    m.probe_reset()
+    m.probe_enable([args.probe])
+    stream = torch.cuda.current_stream()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev0.record(stream)
+    for i in range(args.steps):
+        step(args.warmup + i)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    gpu_ms = ev0.elapsed_time(ev1)
+    probe = m.probe_read(args.probe)
+    m.probe_enable([])
+    loss = m.loss()
+    print(f"bench: timed {args.steps} steps, wall {wall:.3f} s, events {gpu_ms / 1e3:.3f} s, loss {loss:.4f}",
+          file=sys.stderr, flush=True)
+
+    tokens = w["B"] * w["T"] * w.get("grad_accum", 1)
+    ms_step = wall * 1e3 / args.steps
+    tok_s = tokens / (wall / args.steps)
+    f_tok = flops_per_token(w)
+    mfu = tok_s * f_tok / (PEAK_BF16_TFLOPS * 1e12)
+
+    extra = {}
+    if args.classes:
+        classes = list(binding.KCLASS)
+        m.probe_reset()
+        m.probe_enable(classes)
+        for i in range(3):
+            step(args.warmup + args.steps + i)
+        torch.cuda.synchronize()
+        for c in classes:
+            r = m.probe_read(c)
+            if r["launches"]:
+                extra[c] = {"ms_per_step": round(r["ms"] / 3, 4), "launches_per_step": r["launches"] // 3,
+                            "tflops": round(r["flops"] / (r["ms"] * 1e-3) / 1e12, 1) if r["flops"] else None,
+                            "gbs": round(r["bytes"] / (r["ms"] * 1e-3) / 1e9, 1) if r["bytes"] else None}
+        m.probe_enable([])
+        print("bench: per-class " + json.dumps(extra), file=sys.stderr, flush=True)
+
+    avg_ms = probe["ms"] / max(probe["launches"], 1)
+    achieved = probe["flops"] / (probe["ms"] * 1e-3) / 1e12 if probe["ms"] else 0.0
+    flops_launch = probe["flops"] / max(probe["launches"], 1)
+    tb = traffic_from_profiles(args.probe, kernel_source_hash())
+    roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": tb,
+                "kernel": args.probe, "launches": probe["launches"], "avg_launch_ms": round(avg_ms, 4),
+                "flops_per_launch": flops_launch}
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        print("bench: timing the CPU oracle on a 1-sequence sample", file=sys.stderr, flush=True)
+        cpu = cpu_baseline(w, params, *batches[0])
+
+    out = {
+        "metric": "training tokens/sec on 1 MI355X at GPT-2 124M; bf16 MFMA model-FLOPs util",
+        "value": round(tok_s, 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"GPT-2 124M training step (fwd+bwd+clip+AdamW), {args.workload}",
+                   "n_layer": w["n_layer"], "d_model": w["d_model"], "n_head": w["n_head"],
+                   "vocab": w["vocab"], "vocab_padded": w["vocab_padded"], "global_batch": w["B"],
+                   "seq_len": w["T"], "grad_accum": w.get("grad_accum", 1), "tokens_per_step": tokens,
+                   "token_dist": "zipf(1.1)", "parallelism": "none"},
+        "mfu": round(mfu, 4),
+        "flops_per_token": f_tok,
+        "flops_per_token_6n_12lct": flops_per_token_palm(w, m.n_params - (w["vocab_padded"] - w["vocab"]) * w["d_model"]),
+        "peak_tflops": PEAK_BF16_TFLOPS,
+        "gpu_event_ms_per_step": round(gpu_ms / args.steps, 3),
+        "final_loss": round(loss, 4),
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+    }
+    if extra:
+        out["classes"] = extra
+    print(json.dumps(out), flush=True)
+    m.close()
+
+
+if __name__ == "__main__":
+    main()

@@ -205,16 +205,18 @@ gpt2_status gpt2_embedding_backward(gpt2_model* m, const int32_t* d_ids,
  * the model's stream and its algorithmic work (flops or bytes) is counted.
  * gpt2_probe_read synchronises and reports totals since the last reset. */
 typedef enum gpt2_kclass {
-  GPT2_K_GEMM_FWD = 0,    /* X W^T (+bias, residual or GELU epilogue) */
-  GPT2_K_GEMM_DX = 1,     /* dY W */
-  GPT2_K_GEMM_DW = 2,     /* dY^T X into fp32 gradients */
-  GPT2_K_ATTN_FWD = 3,
-  GPT2_K_ATTN_BWD = 4,
-  GPT2_K_LAYERNORM = 5,   /* forward and backward */
-  GPT2_K_CROSS_ENTROPY = 6,
-  GPT2_K_OPTIMIZER = 7,   /* norm, clip and AdamW */
-  GPT2_K_OTHER = 8,       /* embedding, reductions, casts */
-  GPT2_K_COUNT = 9
+  GPT2_K_GEMM_FWD = 0,       /* x W^T + bias (+ residual): one kernel */
+  GPT2_K_GEMM_FWD_GELU = 1,  /* x W^T + bias with the GELU epilogue */
+  GPT2_K_GEMM_DX = 2,        /* dY W */
+  GPT2_K_GEMM_DX_GELU = 3,   /* dY W times GELU'(pre-activation) */
+  GPT2_K_GEMM_DW = 4,        /* dY^T X into fp32 gradients (or split slices) */
+  GPT2_K_ATTN_FWD = 5,
+  GPT2_K_ATTN_BWD = 6,       /* D pre-pass, dK/dV and dQ kernels */
+  GPT2_K_LAYERNORM = 7,      /* forward and backward */
+  GPT2_K_CROSS_ENTROPY = 8,
+  GPT2_K_OPTIMIZER = 9,      /* norm, clip coefficient and AdamW */
+  GPT2_K_OTHER = 10,         /* embedding, reductions, casts */
+  GPT2_K_COUNT = 11
 } gpt2_kclass;
 
 gpt2_status gpt2_probe_enable(gpt2_model* m, uint32_t class_mask);

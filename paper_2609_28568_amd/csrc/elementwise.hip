@@ -14,11 +14,44 @@ __global__ void reduce_slices_kernel(const float* __restrict__ src, int nslices,
   long i = ((long)blockIdx.x * blockDim.x + threadIdx.x) * 4;
   if (i >= n) return;
   float4 acc = accumulate ? *reinterpret_cast<const float4*>(dst + i) : make_float4(0, 0, 0, 0);
+#pragma unroll 4
   for (int s = 0; s < nslices; ++s) {
     float4 v = *reinterpret_cast<const float4*>(src + (size_t)s * n + i);
     acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
   }
   *reinterpret_cast<float4*>(dst + i) = acc;
+}
+
+// 16 waves per block, 64 columns per block: wave w sums slices w, w+16, ...
+// with several loads in flight, then the waves are combined in order.
+__global__ __launch_bounds__(1024) void reduce_parts_kernel(const float* __restrict__ part, int S, long stride,
+                                                            int n, int nd, float* __restrict__ d0,
+                                                            float* __restrict__ d1, float* __restrict__ d2,
+                                                            int accumulate) {
+  __shared__ float red[16][64];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int col = blockIdx.x * 64 + lane;
+  const bool ok = col < n * nd;
+  float a = 0.0f;
+  if (ok) {
+    int s = w;
+    for (; s + 48 < S; s += 64) {
+      float v0 = part[(size_t)s * stride + col], v1 = part[(size_t)(s + 16) * stride + col];
+      float v2 = part[(size_t)(s + 32) * stride + col], v3 = part[(size_t)(s + 48) * stride + col];
+      a += v0; a += v1; a += v2; a += v3;
+    }
+    for (; s < S; s += 16) a += part[(size_t)s * stride + col];
+  }
+  red[w][lane] = a;
+  __syncthreads();
+  if (w == 0 && ok) {
+    float t = 0.0f;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) t += red[i][lane];
+    const int j = col / n, c = col % n;
+    float* d = j == 0 ? d0 : (j == 1 ? d1 : d2);
+    if (d) d[c] = (accumulate ? d[c] : 0.0f) + t;
+  }
 }
 
 // parts[p][c] = sum of x[r][c] over the p-th slice of rows; one thread per
@@ -29,6 +62,7 @@ __global__ void colsum_kernel(const bf16_t* __restrict__ x, int rows, int N, int
   if (c >= N) return;
   const int r0 = blockIdx.y * rows_per_part, r1 = min(rows, r0 + rows_per_part);
   float a0 = 0, a1 = 0, a2 = 0, a3 = 0;
+#pragma unroll 8
   for (int r = r0; r < r1; ++r) {
     uint2 u = *reinterpret_cast<const uint2*>(x + (size_t)r * N + c);
     a0 += lo_f(u.x); a1 += hi_f(u.x); a2 += lo_f(u.y); a3 += hi_f(u.y);
@@ -258,9 +292,17 @@ hipError_t launch_reduce_slices(const float* src, int nslices, long n, float* ds
   return hipGetLastError();
 }
 
+hipError_t launch_reduce_parts(const float* part, int S, long stride, int n, int nd, float* d0, float* d1,
+                               float* d2, int accumulate, hipStream_t s) {
+  if (nd < 1 || nd > 3) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(reduce_parts_kernel, dim3((unsigned)((n * nd + 63) / 64)), dim3(1024), 0, s, part, S, stride, n,
+                     nd, d0, d1, d2, accumulate);
+  return hipGetLastError();
+}
+
 int colsum_parts(int rows) {
-  int p = rows / 64;
-  return p < 1 ? 1 : (p > 256 ? 256 : p);
+  int p = rows / 128;
+  return p < 1 ? 1 : (p > 128 ? 128 : p);
 }
 
 hipError_t launch_colsum(const bf16_t* x, int rows, int N, float* parts, hipStream_t s) {

@@ -9,118 +9,187 @@
 //   input    dx[t][i] = sum_o dy[t][o] W[o][i]       A = dy, B = W   (A_T=0, B_T=1)
 //   weight   dW[o][i] = sum_t dy[t][o] x[t][i]       A = dy, B = x   (A_T=1, B_T=1)
 //
-// Tiles of BM x BN x 64 are staged through LDS, double-buffered: the global
-// loads of tile k+1 are in flight while the MFMAs of tile k run. LDS keeps
-// every operand contraction-contiguous ([row][k], padded rows), so each MFMA
-// operand is one 16-byte LDS read. Strided operands are transposed in
-// registers on the way in: a thread loads a 4(k) x 8(row) block with four
-// 16-byte loads and writes eight 8-byte rows.
+// Data movement: operand tiles go from HBM straight into LDS with
+// buffer_load ... lds (no staging registers; the buffer descriptor's range
+// check turns reads past the end of a matrix into zeros), through a ring of
+// NSTAGE stages of 32 contraction steps each, so several tiles are in flight
+// while the MFMAs of the current one run. Each wave waits only for its own
+// loads (vmcnt) before the block barrier that publishes a stage.
 //
-// The MFMA is v_mfma_f32_32x32x16_bf16 with its row index i mapped to n and
-// its column index j to m, so each lane ends up holding four consecutive n
-// of one output row (8-byte bf16 / 16-byte fp32 stores).
+// LDS layouts, both in 16-byte units with an XOR swizzle against bank
+// conflicts:
+//   contraction-contiguous operand: [rows][32] (4 units per row); an MFMA
+//     fragment (8 consecutive k of one row) is one ds_read_b128;
+//   contraction-strided operand: [32][rows], the operand's natural layout;
+//     a fragment is two ds_read_b64_tr_b16, which hand each lane four
+//     consecutive k of one row gathered from four other lanes' reads.
+//
+// MFMA: v_mfma_f32_32x32x16_bf16 with its row index i mapped to n and its
+// column index j to m, so each lane ends up holding four consecutive n of one
+// output row (8-byte bf16 / 16-byte fp32 stores in the epilogue).
 #include "common.h"
 #include "kernels.h"
 
 namespace {
 
-constexpr int BK = 64;
-constexpr int LDK = BK + 8;   // padded LDS row (144 bytes) to spread banks
+constexpr int BK = 32;        // contraction steps per stage
+constexpr int NSTAGE = 4;     // LDS ring depth
 
-template <int R, bool TR, int NT>
-struct TileLoader {
-  // contraction-contiguous: R rows x 64 k as 16-byte chunks
-  static constexpr int CH = TR ? 0 : (R * BK / 8) / NT;
-  // contraction-strided: (64/4) x (R/8) blocks of 4 k x 8 rows
-  static constexpr int UN = TR ? ((BK / 4) * (R / 8)) / NT : 0;
-  static_assert(TR ? (((BK / 4) * (R / 8)) % NT == 0) : ((R * BK / 8) % NT == 0), "tile/threads");
-  static constexpr int NREG = TR ? UN * 4 : CH;
-  uint4 v[NREG];
+#define LDS_AS __attribute__((address_space(3)))
+typedef LDS_AS void lds_void_t;
+typedef LDS_AS char lds_char_t;
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+typedef LDS_AS v4i16 lds_v4i16_t;
+typedef unsigned int v4u32 __attribute__((ext_vector_type(4)));
+typedef LDS_AS v4u32 lds_v4u32_t;
 
-  // rows: [r0, r0+R) of Rtot; contraction: [k0, k0+64) of kend
-  DEV void load(const bf16_t* __restrict__ X, int ld, int r0, int Rtot, int k0, int kend, int tid) {
+typedef int v4i32 __attribute__((ext_vector_type(4)));
+
+// Raw buffer descriptor over [base, base+bytes): stride 0, range checked, so
+// loads past the end return zero.
+DEV v4i32 make_rsrc(const void* base, uint32_t bytes) {
+  const uint64_t a = reinterpret_cast<uint64_t>(base);
+  v4i32 r;
+  r.x = __builtin_amdgcn_readfirstlane((int)(uint32_t)a);
+  r.y = __builtin_amdgcn_readfirstlane((int)(uint32_t)(a >> 32));
+  r.z = __builtin_amdgcn_readfirstlane((int)bytes);
+  r.w = 0x00020000;
+  return r;
+}
+
+// 16 bytes per lane from the buffer at byte offset voff into LDS at
+// lds_base + 16*lane. Issued as inline assembly: the kernel tracks these
+// loads itself (wait_vmcnt before the barrier that publishes a stage), and
+// the compiler's own conservative wait before every LDS read would serialise
+// the ring.
+DEV void dma16(v4i32 rsrc, uint32_t voff, uint32_t lds_base) {
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+               :
+               : "s"(__builtin_amdgcn_readfirstlane(lds_base)), "v"(voff), "s"(rsrc)
+               : "memory", "m0");
+}
+
+// vmcnt-only wait (expcnt and lgkmcnt left at their maxima)
+template <int N>
+DEV void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+
+// workgroup barrier without the memory fence of __syncthreads (which would
+// wait for the prefetches still in flight)
+DEV void block_barrier() { asm volatile("s_barrier" ::: "memory"); }
+
+// Physical 16-byte unit of logical (row, chunk) in a contraction-contiguous
+// tile [R][32]: 4 units per row, chunk XOR (row/4)%4.
+DEV int unit_n(int row, int c) { return row * 4 + (c ^ ((row >> 2) & 3)); }
+// ... in a contraction-strided tile [32][R]: R/8 units per k-row. A
+// transposed fragment read touches 4 consecutive k-rows x 4 units per
+// 32 lanes; the chunk XOR spreads those 16 units over all 64 banks:
+// 4*(k%4) when a row is a multiple of 16 units (256 B), 4*((k/2)%2) for
+// 192-wide tiles (24 units, so consecutive rows already sit 8 units apart).
+// Both stay inside aligned groups of 8 or 16 units, hence inside the row.
+template <int R>
+DEV int unit_t(int k, int c) {
+  if constexpr ((R / 8) % 16 == 0) return k * (R / 8) + (c ^ ((k & 3) << 2));
+  else return k * (R / 8) + (c ^ (((k >> 1) & 1) << 2));
+}
+
+// Issue the direct-to-LDS loads of one operand tile (R rows of the operand,
+// 32 contraction steps starting at k0) into the stage at `dst`. Wave w issues
+// instructions w, w+4, ...; each instruction moves 64 units (1 KB), unit u of
+// the tile going to byte 16*u.
+template <int R, bool TR>
+DEV void issue_tile(v4i32 rs, int ld, int r0, int k0, lds_char_t* dst, int wave, int lane) {
+  constexpr int UNITS = R * BK / 8;
+  constexpr int INSTR = UNITS / 64;
+  static_assert(UNITS % 256 == 0, "tile must split evenly over 4 waves");
+#pragma unroll
+  for (int i = 0; i < INSTR / 4; ++i) {
+    const int ins = wave + 4 * i;
+    const int u = ins * 64 + lane;   // physical unit written by this lane
+    uint32_t off;
     if constexpr (!TR) {
-#pragma unroll
-      for (int i = 0; i < CH; ++i) {
-        int c = tid + NT * i;
-        int row = c >> 3, kc = (c & 7) * 8;
-        int gr = r0 + row, gk = k0 + kc;
-        if (gr < Rtot && gk < kend)
-          v[i] = *reinterpret_cast<const uint4*>(X + (size_t)gr * ld + gk);
-        else
-          v[i] = make_uint4(0, 0, 0, 0);
-      }
+      const int row = u >> 2, p = u & 3;
+      const int c = p ^ ((row >> 2) & 3);
+      off = ((uint32_t)(r0 + row) * (uint32_t)ld + (uint32_t)(k0 + c * 8)) * 2u;
     } else {
-#pragma unroll
-      for (int i = 0; i < UN; ++i) {
-        int u = tid + NT * i;
-        int rc = u % (R / 8), kq = u / (R / 8);
-        int gr = r0 + rc * 8;
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          int gk = k0 + kq * 4 + q;
-          if (gr < Rtot && gk < kend)
-            v[i * 4 + q] = *reinterpret_cast<const uint4*>(X + (size_t)gk * ld + gr);
-          else
-            v[i * 4 + q] = make_uint4(0, 0, 0, 0);
-        }
-      }
+      const int k = u / (R / 8), p = u % (R / 8);
+      const int c = unit_t<R>(k, p) - k * (R / 8);   // the XOR is its own inverse
+      off = ((uint32_t)(k0 + k) * (uint32_t)ld + (uint32_t)(r0 + c * 8)) * 2u;
     }
+    dma16(rs, off, (uint32_t)reinterpret_cast<uintptr_t>(dst + ins * 1024));
   }
+}
 
-  DEV void store(bf16_t* __restrict__ S, int tid) const {
-    if constexpr (!TR) {
-#pragma unroll
-      for (int i = 0; i < CH; ++i) {
-        int c = tid + NT * i;
-        int row = c >> 3, kc = (c & 7) * 8;
-        *reinterpret_cast<uint4*>(S + row * LDK + kc) = v[i];
-      }
-    } else {
-#pragma unroll
-      for (int i = 0; i < UN; ++i) {
-        int u = tid + NT * i;
-        int rc = u % (R / 8), kq = u / (R / 8);
-        const uint4 w0 = v[i * 4 + 0], w1 = v[i * 4 + 1], w2 = v[i * 4 + 2], w3 = v[i * 4 + 3];
-        const uint32_t a0[4] = {w0.x, w0.y, w0.z, w0.w};
-        const uint32_t a1[4] = {w1.x, w1.y, w1.z, w1.w};
-        const uint32_t a2[4] = {w2.x, w2.y, w2.z, w2.w};
-        const uint32_t a3[4] = {w3.x, w3.y, w3.z, w3.w};
-#pragma unroll
-        for (int p = 0; p < 4; ++p) {
-          uint2 even = make_uint2(lo_pair(a0[p], a1[p]), lo_pair(a2[p], a3[p]));
-          uint2 odd = make_uint2(hi_pair(a0[p], a1[p]), hi_pair(a2[p], a3[p]));
-          *reinterpret_cast<uint2*>(S + (rc * 8 + 2 * p) * LDK + kq * 4) = even;
-          *reinterpret_cast<uint2*>(S + (rc * 8 + 2 * p + 1) * LDK + kq * 4) = odd;
-        }
-      }
-    }
+// MFMA fragment: 8 consecutive k (k-step s, lane group lane/32) of row
+// row_base + lane%32 of the tile.
+template <int R, bool TR>
+DEV bf16x8 read_frag(const lds_char_t* stage, int row_base, int s, int lane) {
+  if constexpr (!TR) {
+    const int row = row_base + (lane & 31), c = 2 * s + (lane >> 5);
+    return __builtin_bit_cast(bf16x8, *reinterpret_cast<const lds_v4u32_t*>(stage + unit_n(row, c) * 16));
+  } else {
+    // lane t of each 16-lane group names k-row kb + t/4 and columns
+    // n + 4*(t%4)..+3; it receives column n + t at k-rows kb..kb+3
+    const int t = lane & 15, h = (lane >> 4) & 1, g = lane >> 5;
+    const int n = row_base + 16 * h + 4 * (t & 3);
+    const int kb = 16 * s + 8 * g + (t >> 2);
+    const int c = n >> 3, sub = (n & 7) * 2;   // byte offset 0 or 8 in the unit
+    const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        (lds_v4i16_t*)(stage + unit_t<R>(kb, c) * 16 + sub));
+    const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        (lds_v4i16_t*)(stage + unit_t<R>(kb + 4, c) * 16 + sub));
+    const uint2 a = __builtin_bit_cast(uint2, lo), b = __builtin_bit_cast(uint2, hi);
+    return as_bf16x8(make_uint4(a.x, a.y, b.x, b.y));
   }
-};
+}
 
-template <int BM, int BN, int WGM, int WGN, bool A_T, bool B_T, int EPI>
-__global__ __launch_bounds__(WGM* WGN * 64) void gemm_kernel(GemmArgs g) {
-  constexpr int NT = WGM * WGN * 64;
-  constexpr int WTM = BM / WGM, WTN = BN / WGN;   // wave tile
-  constexpr int TM = WTM / 32, TN = WTN / 32;     // 32x32 MFMA tiles per wave
-  static_assert(WTM % 32 == 0 && WTN % 32 == 0, "wave tile");
+template <int BM, int BN, bool A_T, bool B_T, int EPI>
+__global__ __launch_bounds__(256, 1) void gemm_kernel(GemmArgs g) {
+  constexpr int WTM = BM / 2, WTN = BN / 2;   // 2 x 2 waves
+  constexpr int TM = WTM / 32, TN = WTN / 32;
+  constexpr int A_BYTES = BM * BK * 2, B_BYTES = BN * BK * 2;
+  constexpr int STAGE = A_BYTES + B_BYTES;
+  constexpr int LOADS = (BM + BN) / 64;       // load instructions per wave per stage
+  // one array per ring stage: with the loop unrolled by NSTAGE every LDS read
+  // and every in-flight load names its stage statically, so the compiler
+  // knows the reads of one stage do not wait on the loads into another
+  static_assert(NSTAGE == 4, "ring of four stages");
+  __shared__ __attribute__((aligned(1024))) char st0[STAGE];
+  __shared__ __attribute__((aligned(1024))) char st1[STAGE];
+  __shared__ __attribute__((aligned(1024))) char st2[STAGE];
+  __shared__ __attribute__((aligned(1024))) char st3[STAGE];
+  auto stage = [&](int s) -> lds_char_t* {
+    return (lds_char_t*)(s == 0 ? st0 : (s == 1 ? st1 : (s == 2 ? st2 : st3)));
+  };
 
-  __shared__ __attribute__((aligned(16))) bf16_t smem[2 * (BM + BN) * LDK];
-  constexpr int STAGE = (BM + BN) * LDK;   // one buffer: A rows then B rows
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
 
-  const int tid = threadIdx.x;
-  const int lane = tid & 63, wave = tid >> 6;
-  const int wm = wave / WGN, wn = wave % WGN;
-  const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
+  // Blocks are dealt round-robin to the 8 XCDs; renumber them so each XCD
+  // works through a contiguous run of tiles (n fastest), which keeps the row
+  // panel of A it reads in its own L2.
+  const int ntn = gridDim.x, ntiles = gridDim.x * gridDim.y;
+  int bid = blockIdx.y * gridDim.x + blockIdx.x;
+  if ((ntiles & 7) == 0) bid = (bid & 7) * (ntiles >> 3) + (bid >> 3);
+  const int m0 = (bid / ntn) * BM, n0 = (bid % ntn) * BN;
 
-  // contraction range of this split
-  const int kchunk = g.k_chunk;
-  const int kbeg = blockIdx.z * kchunk;
-  const int kend = min(g.K, kbeg + kchunk);
+  const int kbeg = blockIdx.z * g.k_chunk;
+  const int kend = min(g.K, kbeg + g.k_chunk);
   const int nk = (kend - kbeg + BK - 1) / BK;
 
-  TileLoader<BM, A_T, NT> la;
-  TileLoader<BN, B_T, NT> lb;
+  // buffer ranges: the whole operand matrices; reads past the end return 0
+  const uint32_t a_rows = A_T ? (uint32_t)g.K : (uint32_t)g.M;
+  const uint32_t b_rows = B_T ? (uint32_t)g.K : (uint32_t)g.N;
+  const v4i32 ra = make_rsrc(g.A, a_rows * (uint32_t)g.lda * 2u);
+  const v4i32 rb = make_rsrc(g.B, b_rows * (uint32_t)g.ldb * 2u);
+
+  auto issue = [&](int kt, lds_char_t* st) {
+    const int k0 = kbeg + kt * BK;
+    issue_tile<BM, A_T>(ra, g.lda, m0, k0, st, wave, lane);
+    issue_tile<BN, B_T>(rb, g.ldb, n0, k0, st + A_BYTES, wave, lane);
+  };
 
   floatx16 acc[TM][TN];
 #pragma unroll
@@ -130,43 +199,43 @@ __global__ __launch_bounds__(WGM* WGN * 64) void gemm_kernel(GemmArgs g) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
-  if (nk > 0) {
-    la.load(g.A, g.lda, m0, g.M, kbeg, kend, tid);
-    lb.load(g.B, g.ldb, n0, g.N, kbeg, kend, tid);
-    la.store(smem, tid);
-    lb.store(smem + BM * LDK, tid);
-  }
-  __syncthreads();
+#pragma unroll
+  for (int s = 0; s < NSTAGE - 1; ++s)
+    if (s < nk) issue(s, stage(s));
 
-  const int lrow = lane & 31, lk = (lane >> 5) * 8;
-  for (int kt = 0; kt < nk; ++kt) {
-    const int cur = kt & 1;
-    if (kt + 1 < nk) {
-      la.load(g.A, g.lda, m0, g.M, kbeg + (kt + 1) * BK, kend, tid);
-      lb.load(g.B, g.ldb, n0, g.N, kbeg + (kt + 1) * BK, kend, tid);
+  for (int kt0 = 0; kt0 < nk; kt0 += NSTAGE) {
+#pragma unroll
+    for (int S = 0; S < NSTAGE; ++S) {
+      const int kt = kt0 + S;
+      if (kt < nk) {
+        // tile kt has landed once at most the loads of the tiles issued
+        // after it are outstanding
+        if (kt + NSTAGE - 2 < nk) wait_vmcnt<(NSTAGE - 2) * LOADS>();
+        else wait_vmcnt<0>();
+        block_barrier();
+        // the stage read in the previous step now takes tile kt+NSTAGE-1
+        if (kt + NSTAGE - 1 < nk) issue(kt + NSTAGE - 1, stage((S + NSTAGE - 1) % NSTAGE));
+
+        const lds_char_t* a_s = stage(S);
+        const lds_char_t* b_s = a_s + A_BYTES;
+#pragma unroll
+        for (int s = 0; s < BK / 16; ++s) {
+          bf16x8 fa[TM], fb[TN];
+#pragma unroll
+          for (int i = 0; i < TM; ++i) fa[i] = read_frag<BM, A_T>(a_s, wm * WTM + i * 32, s, lane);
+#pragma unroll
+          for (int j = 0; j < TN; ++j) fb[j] = read_frag<BN, B_T>(b_s, wn * WTN + j * 32, s, lane);
+#pragma unroll
+          for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j) acc[i][j] = mfma32(fb[j], fa[i], acc[i][j]);
+        }
+      }
     }
-    const bf16_t* a_s = smem + cur * STAGE + (wm * WTM + lrow) * LDK + lk;
-    const bf16_t* b_s = smem + cur * STAGE + BM * LDK + (wn * WTN + lrow) * LDK + lk;
-#pragma unroll
-    for (int kk = 0; kk < BK; kk += 16) {
-      uint4 fa[TM], fb[TN];
-#pragma unroll
-      for (int i = 0; i < TM; ++i) fa[i] = *reinterpret_cast<const uint4*>(a_s + i * 32 * LDK + kk);
-#pragma unroll
-      for (int j = 0; j < TN; ++j) fb[j] = *reinterpret_cast<const uint4*>(b_s + j * 32 * LDK + kk);
-#pragma unroll
-      for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j) acc[i][j] = mfma32(as_bf16x8(fb[j]), as_bf16x8(fa[i]), acc[i][j]);
-    }
-    if (kt + 1 < nk) {
-      la.store(smem + (cur ^ 1) * STAGE, tid);
-      lb.store(smem + (cur ^ 1) * STAGE + BM * LDK, tid);
-    }
-    __syncthreads();
   }
 
   // epilogue: lane holds, for output row m, n = nb + 8*(r/4) + (r%4)
+  const int lrow = lane & 31;
 #pragma unroll
   for (int i = 0; i < TM; ++i) {
     const int m = m0 + wm * WTM + i * 32 + lrow;
@@ -215,16 +284,24 @@ __global__ __launch_bounds__(WGM* WGN * 64) void gemm_kernel(GemmArgs g) {
   }
 }
 
-template <int BM, int BN, int WGM, int WGN, bool A_T, bool B_T, int EPI>
+template <int BM, int BN, bool A_T, bool B_T, int EPI>
 hipError_t launch_t(const GemmArgs& g, hipStream_t s) {
   dim3 grid((g.N + BN - 1) / BN, (g.M + BM - 1) / BM, g.splits);
-  hipLaunchKernelGGL((gemm_kernel<BM, BN, WGM, WGN, A_T, B_T, EPI>), grid, dim3(WGM * WGN * 64), 0, s, g);
+  hipLaunchKernelGGL((gemm_kernel<BM, BN, A_T, B_T, EPI>), grid, dim3(256), 0, s, g);
   return hipGetLastError();
 }
 
+// Tile shape per problem: 256 x 192 tiles (4 waves of 128 x 96) when N is a
+// multiple of 192, which holds for every GPT-2 width (768, 2304, 3072 and the
+// padded vocabulary 50304) and makes the 16384-row GEMMs fill the 256 CUs in
+// whole rounds; 256 x 128 otherwise; 128 x 128 for small problems.
 template <bool A_T, bool B_T, int EPI>
 hipError_t launch_shape(const GemmArgs& g, hipStream_t s) {
-  return launch_t<128, 128, 2, 2, A_T, B_T, EPI>(g, s);
+  if (g.M >= 1024 || g.N >= 4096) {
+    if (g.N % 192 == 0) return launch_t<256, 192, A_T, B_T, EPI>(g, s);
+    return launch_t<256, 128, A_T, B_T, EPI>(g, s);
+  }
+  return launch_t<128, 128, A_T, B_T, EPI>(g, s);
 }
 
 }  // namespace
@@ -232,8 +309,8 @@ hipError_t launch_shape(const GemmArgs& g, hipStream_t s) {
 int gemm_split_plan(int K, int want, int* k_chunk) {
   if (want < 1) want = 1;
   int kc = (K + want - 1) / want;
-  kc = (kc + BK - 1) / BK * BK;
-  if (kc < BK) kc = BK;
+  kc = (kc + 63) / 64 * 64;
+  if (kc < 64) kc = 64;
   if (k_chunk) *k_chunk = kc;
   int n = (K + kc - 1) / kc;
   return n < 1 ? 1 : n;
@@ -241,13 +318,18 @@ int gemm_split_plan(int K, int want, int* k_chunk) {
 
 hipError_t launch_gemm(const GemmArgs& g0, int a_t, int b_t, int epi, hipStream_t s) {
   GemmArgs g = g0;
+  // byte offsets are 32-bit: the operand matrices, plus the up to 256 rows a
+  // tile may address past their end, must stay below 4 GiB
+  if ((size_t)((a_t ? g.K : g.M) + 256) * g.lda * 2 >= (1ull << 32) ||
+      (size_t)((b_t ? g.K : g.N) + 256) * g.ldb * 2 >= (1ull << 32))
+    return hipErrorInvalidValue;
   if (g.splits <= 1 || g.k_chunk <= 0) {
     g.splits = 1;
-    g.k_chunk = (g.K + BK - 1) / BK * BK;
-    if (g.k_chunk < BK) g.k_chunk = BK;
+    g.k_chunk = (g.K + 63) / 64 * 64;
+    if (g.k_chunk < 64) g.k_chunk = 64;
   } else {
     // the caller's plan: k_chunk a multiple of 64 and splits = ceil(K / k_chunk)
-    if (g.k_chunk % BK || (long)g.k_chunk * g.splits < g.K || (long)g.k_chunk * (g.splits - 1) >= g.K)
+    if (g.k_chunk % 64 || (long)g.k_chunk * g.splits < g.K || (long)g.k_chunk * (g.splits - 1) >= g.K)
       return hipErrorInvalidValue;
     if (epi != EPI_F32) return hipErrorInvalidValue;
   }

@@ -75,9 +75,20 @@ const bool kDecay[K_NKIND] = {true, true, false, false, true, false, true, false
                               false, false, true, false, true, false, false, false};
 
 // contraction splits for a weight-gradient GEMM with an M x N output
+// output tiles of the weight-gradient GEMM (the tile shape gemm.hip picks)
+long dw_tiles(int M, int N) {
+  if (M >= 1024 || N >= 4096) {
+    int bn = N % 192 == 0 ? 192 : 128;
+    return (long)((M + 255) / 256) * ((N + bn - 1) / bn);
+  }
+  return (long)((M + 127) / 128) * ((N + 127) / 128);
+}
+
+// split the 16384-long contraction so that about one round of blocks (256
+// CUs) is in flight
 int dw_splits(const Dims& d, int M, int N) {
-  long tiles = (long)((M + 127) / 128) * ((N + 127) / 128);
-  long want = (512 + tiles - 1) / tiles;
+  long tiles = dw_tiles(M, N);
+  long want = (256 + tiles - 1) / tiles;
   long cap = d.BT / 512;
   if (cap < 1) cap = 1;
   if (want > cap) want = cap;
@@ -87,8 +98,8 @@ int dw_splits(const Dims& d, int M, int N) {
 
 int dw_chunk(const Dims& d, int M, int N) {
   int kc = 0;
-  long tiles = (long)((M + 127) / 128) * ((N + 127) / 128);
-  long want = (512 + tiles - 1) / tiles;
+  long tiles = dw_tiles(M, N);
+  long want = (256 + tiles - 1) / tiles;
   long cap = d.BT / 512;
   if (cap < 1) cap = 1;
   if (want > cap) want = cap;
@@ -105,7 +116,7 @@ struct ActLayout {
 };
 
 struct WsLayout {
-  size_t dres, dh, datt, dbig, dsum, splitk, colsum, lnpart_w, lnpart_b, sumsq, normcoef, total;
+  size_t dres, dh, datt, dbig, dsum, splitk, colsum, lnpart, sumsq, normcoef, total;
   size_t splitk_elems, colsum_elems;
 };
 
@@ -162,8 +173,7 @@ WsLayout ws_layout(const Dims& d) {
   w.dsum = o; o += align_up((size_t)d.B * d.H * d.T * 4);
   w.splitk = o; o += align_up(sk * 4);
   w.colsum = o; o += align_up(w.colsum_elems * 4);
-  w.lnpart_w = o; o += align_up((size_t)layernorm_bwd_blocks((int)BT) * C * 4);
-  w.lnpart_b = o; o += align_up((size_t)layernorm_bwd_blocks((int)BT) * C * 4);
+  w.lnpart = o; o += align_up((size_t)layernorm_bwd_blocks((int)BT) * 3 * C * 4);
   w.sumsq = o; o += align_up((size_t)sumsq_parts() * 4);
   w.normcoef = o; o += ALIGN;
   w.total = o;
@@ -275,6 +285,12 @@ namespace {
 
 using Model = gpt2_model;
 
+int gemm_class(int a_t, int b_t, int epi) {
+  if (a_t) return GPT2_K_GEMM_DW;
+  if (b_t) return epi == EPI_GELU_BWD ? GPT2_K_GEMM_DX_GELU : GPT2_K_GEMM_DX;
+  return epi == EPI_GELU ? GPT2_K_GEMM_FWD_GELU : GPT2_K_GEMM_FWD;
+}
+
 hipError_t gemm(Model* m, int cls, int M, int N, int K, const bf16_t* A, int lda, int a_t, const bf16_t* B,
                 int ldb, int b_t, int epi, void* C, int ldc, const float* bias = nullptr,
                 const bf16_t* residual = nullptr, bf16_t* C2 = nullptr, const bf16_t* aux = nullptr,
@@ -284,7 +300,8 @@ hipError_t gemm(Model* m, int cls, int M, int N, int K, const bf16_t* A, int lda
   g.C = C; g.ldc = ldc; g.bias = bias; g.residual = residual; g.C2 = C2; g.aux = aux;
   g.accumulate = accumulate; g.splits = splits; g.split_stride = split_stride; g.k_chunk = k_chunk;
   double fl = 2.0 * M * N * K;
-  return m->run(cls, fl, 0.0, [&] { return launch_gemm(g, a_t, b_t, epi, m->stream); });
+  (void)cls;
+  return m->run(gemm_class(a_t, b_t, epi), fl, 0.0, [&] { return launch_gemm(g, a_t, b_t, epi, m->stream); });
 }
 
 // weight gradient dW[M][N] (=|+=) sum_t A[t][m] * X[t][n] (fp32)
@@ -310,8 +327,9 @@ hipError_t bias_grad(Model* m, const bf16_t* dy, int N, float* db, int accumulat
   hipError_t e = m->run(GPT2_K_OTHER, 0.0, 2.0 * BT * N + 4.0 * np * N,
                         [&] { return launch_colsum(dy, BT, N, parts, m->stream); });
   if (e != hipSuccess) return e;
-  return m->run(GPT2_K_OTHER, 0.0, 4.0 * N * (np + 1 + accumulate),
-                [&] { return launch_reduce_slices(parts, np, N, db, accumulate, m->stream); });
+  return m->run(GPT2_K_OTHER, 0.0, 4.0 * N * (np + 1 + accumulate), [&] {
+    return launch_reduce_parts(parts, np, N, N, 1, db, nullptr, nullptr, accumulate, m->stream);
+  });
 }
 
 hipError_t ln_fwd(Model* m, const bf16_t* x, const float* w, const float* b, bf16_t* y, float* mean, float* rstd) {
@@ -320,22 +338,22 @@ hipError_t ln_fwd(Model* m, const bf16_t* x, const float* w, const float* b, bf1
                 [&] { return launch_layernorm_fwd(x, w, b, y, mean, rstd, BT, C, m->cfg.ln_eps, m->stream); });
 }
 
+// LayerNorm backward into the residual-stream gradient; also writes the gain
+// and shift gradients and, when dbias is given, the column sum of the new
+// residual gradient (the bias gradient of the projection that produced it).
 hipError_t ln_bwd(Model* m, const bf16_t* dy, const bf16_t* x, const float* mean, const float* rstd, const float* w,
-                  int has_res, float* dw, float* db, int accumulate) {
+                  int has_res, float* dw, float* db, float* dbias, int accumulate) {
   const int BT = (int)m->d.BT, C = m->d.C;
-  float* pw = m->wsf(m->ws.lnpart_w);
-  float* pbias = m->wsf(m->ws.lnpart_b);
+  float* part = m->wsf(m->ws.lnpart);
   bf16_t* dres = m->wsb(m->ws.dres);
   hipError_t e = m->run(GPT2_K_LAYERNORM, 0.0, 2.0 * BT * C * (3 + has_res) + 8.0 * BT, [&] {
-    return launch_layernorm_bwd(dy, x, mean, rstd, w, dres, has_res, pw, pbias, BT, C, m->stream);
+    return launch_layernorm_bwd(dy, x, mean, rstd, w, dres, has_res, part, BT, C, m->stream);
   });
   if (e != hipSuccess) return e;
   int nb = layernorm_bwd_blocks(BT);
-  e = m->run(GPT2_K_OTHER, 0.0, 4.0 * C * (nb + 1 + accumulate),
-             [&] { return launch_reduce_slices(pw, nb, C, dw, accumulate, m->stream); });
-  if (e != hipSuccess) return e;
-  return m->run(GPT2_K_OTHER, 0.0, 4.0 * C * (nb + 1 + accumulate),
-                [&] { return launch_reduce_slices(pbias, nb, C, db, accumulate, m->stream); });
+  return m->run(GPT2_K_OTHER, 0.0, 4.0 * 3 * C * (nb + 1 + accumulate), [&] {
+    return launch_reduce_parts(part, nb, 3L * C, C, 3, dw, db, dbias, accumulate, m->stream);
+  });
 }
 
 AttnArgs attn_args(Model* m, int l) {
@@ -370,7 +388,12 @@ gpt2_status block_fwd(Model* m, int l) {
   return GPT2_OK;
 }
 
-gpt2_status block_bwd(Model* m, int l, int acc) {
+// Backward of block l. The residual-stream gradient enters in dres. When
+// fcproj_bias_done, the MLP output bias gradient (the column sum of dres) was
+// already produced by the LayerNorm backward that wrote dres. When
+// write_prev_bias, the column sum of the outgoing dres is the MLP output bias
+// gradient of block l-1.
+gpt2_status block_bwd(Model* m, int l, int acc, bool fcproj_bias_done, bool write_prev_bias) {
   const Dims& d = m->d;
   const int BT = (int)d.BT, C = d.C, F = d.F;
   const size_t oC = (size_t)l * C, o3C = (size_t)l * 3 * C, oF = (size_t)l * F;
@@ -382,17 +405,16 @@ gpt2_status block_bwd(Model* m, int l, int acc) {
   TRY(gemm(m, GPT2_K_GEMM_DX, BT, F, C, dres, C, 0, m->pb(K_FCPROJW) + oC * F, F, 1, EPI_GELU_BWD, dbig, F, nullptr,
            nullptr, nullptr, m->fc(l)));
   TRY(weight_grad(m, C, F, dres, m->gelu(l), m->gf(K_FCPROJW) + oC * F, acc));
-  TRY(bias_grad(m, dres, C, m->gf(K_FCPROJB) + oC, acc));
+  if (!fcproj_bias_done) TRY(bias_grad(m, dres, C, m->gf(K_FCPROJB) + oC, acc));
   // MLP up projection
   TRY(gemm(m, GPT2_K_GEMM_DX, BT, C, F, dbig, F, 0, m->pb(K_FCW) + oF * C, C, 1, EPI_BF16, dh, C));
   TRY(weight_grad(m, F, C, dbig, m->ln2(l), m->gf(K_FCW) + oF * C, acc));
   TRY(bias_grad(m, dbig, F, m->gf(K_FCB) + oF, acc));
   TRY(ln_bwd(m, dh, m->xmid(l), m->ln2m(l), m->ln2r(l), m->pf(K_LN2W) + oC, 1, m->gf(K_LN2W) + oC,
-             m->gf(K_LN2B) + oC, acc));
-  // attention output projection
+             m->gf(K_LN2B) + oC, m->gf(K_ATTPROJB) + oC, acc));
+  // attention output projection (its bias gradient came from the LayerNorm above)
   TRY(gemm(m, GPT2_K_GEMM_DX, BT, C, C, dres, C, 0, m->pb(K_ATTPROJW) + oC * C, C, 1, EPI_BF16, datt, C));
   TRY(weight_grad(m, C, C, dres, m->att(l), m->gf(K_ATTPROJW) + oC * C, acc));
-  TRY(bias_grad(m, dres, C, m->gf(K_ATTPROJB) + oC, acc));
   // attention
   AttnArgs aa = attn_args(m, l);
   TRY(m->run(GPT2_K_ATTN_BWD, 2.0 * attn_fwd_flops(d), 0.0, [&] { return launch_attention_bwd(aa, m->stream); }));
@@ -400,8 +422,9 @@ gpt2_status block_bwd(Model* m, int l, int acc) {
   TRY(gemm(m, GPT2_K_GEMM_DX, BT, C, 3 * C, dbig, 3 * C, 0, m->pb(K_QKVW) + o3C * C, C, 1, EPI_BF16, dh, C));
   TRY(weight_grad(m, 3 * C, C, dbig, m->ln1(l), m->gf(K_QKVW) + o3C * C, acc));
   TRY(bias_grad(m, dbig, 3 * C, m->gf(K_QKVB) + o3C, acc));
+  float* prev_bias = (write_prev_bias && l > 0) ? m->gf(K_FCPROJB) + (size_t)(l - 1) * C : nullptr;
   TRY(ln_bwd(m, dh, m->res(l), m->ln1m(l), m->ln1r(l), m->pf(K_LN1W) + oC, 1, m->gf(K_LN1W) + oC,
-             m->gf(K_LN1B) + oC, acc));
+             m->gf(K_LN1B) + oC, prev_bias, acc));
   return GPT2_OK;
 }
 
@@ -599,9 +622,10 @@ gpt2_status gpt2_backward(gpt2_model* m, int32_t accumulate) {
   // tied LM head: input gradient and the head's share of the token-table gradient
   TRY(gemm(m, GPT2_K_GEMM_DX, BT, C, d.Vp, m->logits(), d.Vp, 0, m->pb(K_WTE), C, 1, EPI_BF16, dh, C));
   TRY(weight_grad(m, d.Vp, C, m->logits(), m->lnf(), m->gf(K_WTE), acc));
-  TRY(ln_bwd(m, dh, m->res(d.L), m->lnfm(), m->lnfr(), m->pf(K_LNFW), 0, m->gf(K_LNFW), m->gf(K_LNFB), acc));
+  TRY(ln_bwd(m, dh, m->res(d.L), m->lnfm(), m->lnfr(), m->pf(K_LNFW), 0, m->gf(K_LNFW), m->gf(K_LNFB),
+             m->gf(K_FCPROJB) + (size_t)(d.L - 1) * C, acc));
   for (int l = d.L - 1; l >= 0; --l) {
-    gpt2_status s = block_bwd(m, l, acc);
+    gpt2_status s = block_bwd(m, l, acc, true, true);
     if (s != GPT2_OK) return s;
   }
   // embedding: scatter into the token table (after the head's share), sum into positions
@@ -734,7 +758,7 @@ gpt2_status gpt2_block_backward(gpt2_model* m, int32_t layer, const void* d_dx_o
   const size_t bytes = (size_t)m->d.BT * m->d.C * 2;
   bf16_t* dres = m->wsb(m->ws.dres);
   TRY(hipMemcpyAsync(dres, d_dx_out, bytes, hipMemcpyDeviceToDevice, m->stream));
-  gpt2_status s = block_bwd(m, layer, accumulate ? 1 : 0);
+  gpt2_status s = block_bwd(m, layer, accumulate ? 1 : 0, false, false);
   if (s != GPT2_OK) return s;
   if (d_dx_in) TRY(hipMemcpyAsync(d_dx_in, dres, bytes, hipMemcpyDeviceToDevice, m->stream));
   return GPT2_OK;

@@ -54,17 +54,24 @@ hipError_t launch_attention_bwd(const AttnArgs& a, hipStream_t s);
 // ---------------------------------------------------------------- layernorm
 hipError_t launch_layernorm_fwd(const bf16_t* x, const float* w, const float* b, bf16_t* y,
                                 float* mean, float* rstd, int rows, int C, float eps, hipStream_t s);
-// dres (in/out, may be null on input when has_res == 0): dres = dres + dx.
-// Per-block partial sums of dy*xhat and dy go to part_w / part_b [nblk][C].
+// dres (in/out; only written when has_res == 0): dres = (has_res ? dres : 0) + dx.
+// Each block writes one row of partials part[blk][3][C]: sums over its rows of
+// dy*xhat (gain gradient), dy (shift gradient) and the new dres (the bias
+// gradient of the linear layer whose output gradient dres is).
 int layernorm_bwd_blocks(int rows);
 hipError_t launch_layernorm_bwd(const bf16_t* dy, const bf16_t* x, const float* mean,
                                 const float* rstd, const float* w, bf16_t* dres, int has_res,
-                                float* part_w, float* part_b, int rows, int C, hipStream_t s);
+                                float* part, int rows, int C, hipStream_t s);
 
 // ---------------------------------------------------------------- misc
 // dst[i] (fp32, n elements) = (accumulate ? dst[i] : 0) + sum_s src[s*n + i]
 hipError_t launch_reduce_slices(const float* src, int nslices, long n, float* dst, int accumulate,
                                 hipStream_t s);
+// Sum over S slices of partial rows, for narrow rows and many slices:
+// dst_j[c] (=|+=) sum_s part[s*stride + j*n + c], for j < nd (up to 3
+// destinations, null ones skipped) and c < n. Fixed summation order.
+hipError_t launch_reduce_parts(const float* part, int S, long stride, int n, int nd, float* d0, float* d1,
+                               float* d2, int accumulate, hipStream_t s);
 // column sums of bf16 [rows][N] into partials [nparts][N]; returns nparts
 int colsum_parts(int rows);
 hipError_t launch_colsum(const bf16_t* x, int rows, int N, float* parts, hipStream_t s);

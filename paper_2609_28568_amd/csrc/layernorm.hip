@@ -67,16 +67,15 @@ __global__ __launch_bounds__(256) void ln_bwd_kernel(const bf16_t* __restrict__ 
                                                      const float* __restrict__ mean_in,
                                                      const float* __restrict__ rstd_in, const float* __restrict__ w,
                                                      bf16_t* __restrict__ dres, int has_res,
-                                                     float* __restrict__ part_w, float* __restrict__ part_b,
-                                                     int rows, int C) {
+                                                     float* __restrict__ part, int rows, int C) {
   __shared__ float red[4][MAXCH * 4 * 64];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  float aw[MAXCH][4], ab[MAXCH][4], wr[MAXCH][4];
+  float aw[MAXCH][4], ab[MAXCH][4], ar[MAXCH][4], wr[MAXCH][4];
 #pragma unroll
   for (int i = 0; i < MAXCH; ++i) {
     int c = 4 * (lane + 64 * i);
 #pragma unroll
-    for (int e = 0; e < 4; ++e) aw[i][e] = ab[i][e] = 0.0f;
+    for (int e = 0; e < 4; ++e) aw[i][e] = ab[i][e] = ar[i][e] = 0.0f;
     if (c < C) {
       float4 wv = *reinterpret_cast<const float4*>(w + c);
       wr[i][0] = wv.x; wr[i][1] = wv.y; wr[i][2] = wv.z; wr[i][3] = wv.w;
@@ -120,23 +119,28 @@ __global__ __launch_bounds__(256) void ln_bwd_kernel(const bf16_t* __restrict__ 
           uint2 ru = *reinterpret_cast<const uint2*>(rr + c);
           o[0] += lo_f(ru.x); o[1] += hi_f(ru.x); o[2] += lo_f(ru.y); o[3] += hi_f(ru.y);
         }
-        *reinterpret_cast<uint2*>(rr + c) = make_uint2(pack2(o[0], o[1]), pack2(o[2], o[3]));
+        const uint2 ou = make_uint2(pack2(o[0], o[1]), pack2(o[2], o[3]));
+        *reinterpret_cast<uint2*>(rr + c) = ou;
+        // the stored (rounded) values, so the sum matches what consumers read
+        ar[i][0] += lo_f(ou.x); ar[i][1] += hi_f(ou.x); ar[i][2] += lo_f(ou.y); ar[i][3] += hi_f(ou.y);
       }
     }
   }
-  // combine the four waves' partial parameter gradients in a fixed order
-  for (int pass = 0; pass < 2; ++pass) {
+  // combine the four waves' partial sums in a fixed order; the block's row of
+  // partials is [dw | db | column sum of the residual gradient], 3*C floats
+  for (int pass = 0; pass < 3; ++pass) {
 #pragma unroll
     for (int i = 0; i < MAXCH; ++i)
 #pragma unroll
-      for (int e = 0; e < 4; ++e) red[wave][(i * 64 + lane) * 4 + e] = pass == 0 ? aw[i][e] : ab[i][e];
+      for (int e = 0; e < 4; ++e)
+        red[wave][(i * 64 + lane) * 4 + e] = pass == 0 ? aw[i][e] : (pass == 1 ? ab[i][e] : ar[i][e]);
     __syncthreads();
-    float* dst = pass == 0 ? part_w : part_b;
+    float* dst = part + (size_t)blockIdx.x * 3 * C + pass * C;
     for (int c = threadIdx.x; c < C; c += 256) {
       // channel c lives at chunk i = (c/4)/64, lane (c/4)%64, element c%4
       int cq = c >> 2, i = cq >> 6, l = cq & 63, e = c & 3;
       int k = (i * 64 + l) * 4 + e;
-      dst[(size_t)blockIdx.x * C + c] = red[0][k] + red[1][k] + red[2][k] + red[3][k];
+      dst[c] = red[0][k] + red[1][k] + red[2][k] + red[3][k];
     }
     __syncthreads();
   }
@@ -153,14 +157,14 @@ hipError_t launch_layernorm_fwd(const bf16_t* x, const float* w, const float* b,
 
 int layernorm_bwd_blocks(int rows) {
   int n = (rows + 3) / 4;
-  return n < 512 ? n : 512;
+  return n < 256 ? n : 256;
 }
 
 hipError_t launch_layernorm_bwd(const bf16_t* dy, const bf16_t* x, const float* mean, const float* rstd,
-                                const float* w, bf16_t* dres, int has_res, float* part_w, float* part_b, int rows,
-                                int C, hipStream_t s) {
+                                const float* w, bf16_t* dres, int has_res, float* part, int rows, int C,
+                                hipStream_t s) {
   if (C > MAXCH * 256 || C % 4) return hipErrorInvalidValue;
   hipLaunchKernelGGL(ln_bwd_kernel, dim3(layernorm_bwd_blocks(rows)), dim3(256), 0, s, dy, x, mean, rstd, w, dres,
-                     has_res, part_w, part_b, rows, C);
+                     has_res, part, rows, C);
   return hipGetLastError();
 }
