@@ -1,74 +1,98 @@
-// Causal multi-head attention for gfx950, flash style (online softmax, the
-// score matrix never leaves the chip).
+// Causal multi-head attention for gfx950, flash style: the score matrix never
+// leaves the chip; softmax is computed online in the forward pass and
+// recomputed from the saved log-sum-exp in the backward pass.
 //
 // Layout: q|k|v packed per token [B*T, 3C], head h on channels
 // [h*hd, (h+1)*hd) of each third; output [B*T, C]; log-sum-exp of the scaled
-// scores [B, H, T] in fp32 for the backward pass.
+// scores [B, H, T] in fp32.
 //
-// All products use v_mfma_f32_32x32x16_bf16. Scores are computed transposed
-// (keys along the MFMA row index i, queries along the column index j) so that
-// one lane holds 16 scores of a single query: softmax statistics then need a
-// reduction over the lane's own registers plus one exchange with lane ^ 32.
-// The probabilities feed the next product straight from registers: an MFMA
-// only needs A and B to agree on which contraction index sits in each of the
-// lane's 8 slots, so the value operand is read from LDS in the order the
-// score accumulator already has (two 8-byte reads per operand).
+// Every product is v_mfma_f32_32x32x16_bf16. Tiles of 64 rows x hd move from
+// HBM straight into LDS (buffer_load ... lds, double-buffered: the next tile
+// loads while the current one is used) and stay in their natural row-major
+// layout; operands that need the other orientation are read with
+// ds_read_b64_tr_b16. Scores are arranged so that probabilities (and their
+// gradients) are consumed by the next MFMA straight from the accumulator
+// registers: an MFMA only needs its two operands to agree on which
+// contraction index sits in each of a lane's 8 slots, and the register order
+// of a 32x32 accumulator (rows 8*(r/4) + 4*(lane/32) + r%4) is matched by
+// reading the other operand in that order.
 //
-// Backward: dK/dV by a kernel that owns a key block and walks query tiles,
-// dQ by a kernel that owns a query block and walks key tiles; both recompute
-// P from the saved log-sum-exp and D = rowsum(dO * O) from a small pre-pass.
+//   forward: per 128 queries (4 waves x 32), walk key tiles: S^T = K Q^T
+//            (one query per lane, so the running max and sum are lane-local up
+//            to an exchange with lane^32), O^T += V^T P^T.
+//   dQ:      per 128 queries, walk key tiles: recompute P^T, dP^T = V dO^T,
+//            dS^T = P^T (dP^T - D), dQ^T += K^T dS^T.
+//   dK, dV:  per 128 keys (4 waves x 32), walk query tiles from the diagonal:
+//            S = Q K^T, dP = dO V^T (one key per lane), dV^T += dO^T P,
+//            dK^T += Q^T dS.
+// D = rowsum(dO * O) comes from a small pre-pass.
 #include "common.h"
 #include "kernels.h"
+#include "lds_dma.h"
 
 namespace {
 
-constexpr int BKV = 64;     // keys (or queries) per LDS tile
+constexpr int TILE = 64;    // rows per LDS tile (keys or queries)
+typedef float v4f32 __attribute__((ext_vector_type(4)));
+typedef LDS_AS v4f32 lds_v4f32_t;
 constexpr int BQ = 128;     // rows owned by one workgroup (4 waves x 32)
-constexpr int LDT = BKV + 8;
 constexpr float LOG2E = 1.4426950408889634f;
 constexpr float LN2 = 0.6931471805599453f;
 
-// rows [r0, r0+64) of one head's slice of a q/k/v section -> S[64][HD+8]
+DEV int bitrev3(int x) { return ((x & 1) << 2) | (x & 2) | ((x >> 2) & 1); }
+DEV int bitrev4(int x) { return ((x & 1) << 3) | ((x & 2) << 1) | ((x >> 1) & 2) | ((x >> 3) & 1); }
+
+// Physical 16-byte unit of (row, chunk) in a [64][HD] tile. The XOR keeps
+// both access patterns free of bank conflicts: 32 lanes reading 16 bytes of
+// 32 consecutive rows at one chunk, and 32 lanes of transposed reads covering
+// 4 consecutive rows x 4 chunks.
 template <int HD>
-DEV void load_rows(bf16_t* S, const bf16_t* src, int r0, int T, int ld, int tid) {
-  constexpr int CPR = HD / 8;
-  for (int c = tid; c < BKV * CPR; c += 256) {
-    int r = c / CPR, cc = (c % CPR) * 8;
-    uint4 v = make_uint4(0, 0, 0, 0);
-    if (r0 + r < T) v = *reinterpret_cast<const uint4*>(src + (size_t)(r0 + r) * ld + cc);
-    *reinterpret_cast<uint4*>(S + r * (HD + 8) + cc) = v;
+DEV int unit(int row, int c) {
+  constexpr int U = HD / 8;
+  int f = 0;
+  if constexpr (U == 16) f = bitrev4(row & 15);
+  else if constexpr (U == 8) f = bitrev3((row >> 1) & 7);
+  else if constexpr (U == 4) f = (row >> 2) & 3;
+  return row * U + (c ^ f);
+}
+
+// Load rows [r0, r0+64) of one head's slice (row stride ld elements, buffer
+// over the whole q|k|v or dO matrix) into an LDS tile. Instruction i of the
+// tile goes to bytes [1024 i, 1024 i + 1024); waves take instructions in turn.
+template <int HD>
+DEV void issue_rows(v4i32 rs, const bf16_t* base_of_buffer, const bf16_t* src, int r0, int ld, lds_char_t* dst,
+                    int wave, int lane) {
+  constexpr int U = HD / 8, UNITS = TILE * U, INSTR = (UNITS + 63) / 64;
+  const uint32_t src_off = (uint32_t)((src - base_of_buffer) * 2);
+  for (int ins = wave; ins < INSTR; ins += 4) {
+    const int u = ins * 64 + lane;
+    const int row = u / U, p = u % U;
+    const int c = unit<HD>(row, p) - row * U;   // the XOR is its own inverse
+    const uint32_t off = src_off + ((uint32_t)(r0 + row) * (uint32_t)ld + (uint32_t)(c * 8)) * 2u;
+    if (UNITS % 64 == 0 || u < UNITS) dma16(rs, off, lds_addr(dst + ins * 1024));
   }
 }
 
-// same rows, transposed: St[d][r] (rows of 64+8)
+// 8 contraction values of tile row (row) at chunk c (a natural-layout operand).
 template <int HD>
-DEV void load_rows_t(bf16_t* St, const bf16_t* src, int r0, int T, int ld, int tid) {
-  constexpr int CPR = HD / 8;
-  for (int u = tid; u < (BKV / 4) * CPR; u += 256) {
-    int dc = (u % CPR) * 8, rq = (u / CPR) * 4;
-    uint32_t w[4][4];
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      uint4 v = make_uint4(0, 0, 0, 0);
-      if (r0 + rq + q < T) v = *reinterpret_cast<const uint4*>(src + (size_t)(r0 + rq + q) * ld + dc);
-      w[q][0] = v.x; w[q][1] = v.y; w[q][2] = v.z; w[q][3] = v.w;
-    }
-#pragma unroll
-    for (int p = 0; p < 4; ++p) {
-      *reinterpret_cast<uint2*>(St + (dc + 2 * p) * LDT + rq) =
-          make_uint2(lo_pair(w[0][p], w[1][p]), lo_pair(w[2][p], w[3][p]));
-      *reinterpret_cast<uint2*>(St + (dc + 2 * p + 1) * LDT + rq) =
-          make_uint2(hi_pair(w[0][p], w[1][p]), hi_pair(w[2][p], w[3][p]));
-    }
-  }
+DEV bf16x8 read_row(const lds_char_t* t, int row, int c) {
+  return lds_read16(t + unit<HD>(row, c) * 16);
 }
 
-// Operand read from a transposed tile St[d][r] in the slot order of a
-// 32x32 accumulator: k-step (t, h) covers rows 32t+16h + {4g..4g+3, 8+4g..8+4g+3}.
-DEV bf16x8 read_t_slots(const bf16_t* St, int drow, int t, int h, int g) {
-  const bf16_t* p = St + drow * LDT + 32 * t + 16 * h + 4 * g;
-  uint2 a = *reinterpret_cast<const uint2*>(p);
-  uint2 b = *reinterpret_cast<const uint2*>(p + 8);
+// Transposed operand from a [64][HD] tile: lane gets column n = d0 +
+// lane%32 at tile rows kb + {0..3} (slots 0..3) and kb + 8 + {0..3} (slots
+// 4..7), where kb = rbase + 4*(lane/32) -- the register order of a 32x32
+// accumulator over rows rbase..rbase+15.
+template <int HD>
+DEV bf16x8 read_tr(const lds_char_t* t, int d0, int rbase, int lane) {
+  const int s = lane & 15, h = (lane >> 4) & 1, g = lane >> 5;
+  // for hd 16 the upper 16 output rows of the 32-row MFMA tile are never
+  // stored; their columns are folded back into the tile
+  const int n = (d0 + 16 * h + 4 * (s & 3)) & (HD < 32 ? HD - 1 : 0x7fffffff);
+  const int kb = rbase + 4 * g + (s >> 2);
+  const int c = n >> 3, sub = (n & 7) * 2;
+  const uint2 a = lds_read_tr(t + unit<HD>(kb, c) * 16 + sub);
+  const uint2 b = lds_read_tr(t + unit<HD>(kb + 8, c) * 16 + sub);
   return as_bf16x8(make_uint4(a.x, a.y, b.x, b.y));
 }
 
@@ -78,17 +102,29 @@ DEV bf16x8 acc_slots(const floatx16& x, int h) {
                               pack2(x[8 * h + 4], x[8 * h + 5]), pack2(x[8 * h + 6], x[8 * h + 7])));
 }
 
-// row offset of accumulator register r for lane group g: 8*(r/4) + 4g + r%4
+// accumulator register r of lane group g sits at row 8*(r/4) + 4g + r%4
 DEV int acc_row(int r, int g) { return 8 * (r >> 2) + 4 * g + (r & 3); }
 
-template <int HD>
-__global__ __launch_bounds__(256) void attn_fwd_kernel(AttnArgs a) {
-  constexpr int HDP = HD < 32 ? 32 : HD;
-  constexpr int KS = HD / 16;     // k-steps over the head dimension
-  constexpr int DT = HDP / 32;    // 32-row tiles over the head dimension
-  __shared__ __attribute__((aligned(16))) bf16_t Ks[BKV * (HD + 8)];
-  __shared__ __attribute__((aligned(16))) bf16_t Vt[HDP * LDT];
+DEV void zero(floatx16& x) {
+#pragma unroll
+  for (int r = 0; r < 16; ++r) x[r] = 0.0f;
+}
 
+template <int HD>
+struct Shape {
+  static constexpr int KS = HD / 16;                 // k-steps over the head dim
+  static constexpr int DT = HD < 32 ? 1 : HD / 32;   // 32-row tiles over the head dim
+  static constexpr int TB = TILE * HD * 2;           // bytes of one tile
+  static constexpr int TBA = (TB + 1023) / 1024 * 1024;
+};
+
+// ------------------------------------------------------------------ forward
+
+template <int HD>
+__global__ __launch_bounds__(256, 2) void attn_fwd_kernel(AttnArgs a) {
+  using S = Shape<HD>;
+  __shared__ __attribute__((aligned(1024))) char smem_raw[2 * 2 * S::TBA];   // 2 stages x (K, V)
+  lds_char_t* smem = (lds_char_t*)smem_raw;
   const int T = a.T, H = a.H, C = H * HD, ld = 3 * C;
   const int bh = blockIdx.y, b = bh / H, h = bh % H;
   const int qb = gridDim.x - 1 - blockIdx.x;   // heaviest blocks first
@@ -97,81 +133,85 @@ __global__ __launch_bounds__(256) void attn_fwd_kernel(AttnArgs a) {
   const int q0w = qb * BQ + wave * 32;
   const int q = q0w + lq;
   const bf16_t* base = a.qkv + (size_t)b * T * ld + h * HD;
+  const v4i32 rs = make_rsrc(a.qkv, (uint32_t)((size_t)a.B * T * ld * 2));
 
-  if (HD < 32)
-    for (int i = tid; i < (HDP - HD) * LDT; i += 256) Vt[HD * LDT + i] = 0;
-
-  bf16x8 qf[KS];
+  bf16x8 qf[S::KS];
 #pragma unroll
-  for (int s = 0; s < KS; ++s) {
+  for (int s = 0; s < S::KS; ++s) {
     uint4 v = make_uint4(0, 0, 0, 0);
     if (q < T) v = *reinterpret_cast<const uint4*>(base + (size_t)q * ld + 16 * s + 8 * g);
     qf[s] = as_bf16x8(v);
   }
-
-  floatx16 o[DT];
+  floatx16 o[S::DT];
 #pragma unroll
-  for (int d = 0; d < DT; ++d)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) o[d][r] = 0.0f;
+  for (int d = 0; d < S::DT; ++d) zero(o[d]);
   float m_run = -INFINITY, l_run = 0.0f;
   const float sc = LOG2E / sqrtf((float)HD);
 
   const int kv_end = min(T, qb * BQ + BQ);
-  for (int kv0 = 0; kv0 < kv_end; kv0 += BKV) {
-    __syncthreads();
-    load_rows<HD>(Ks, base + C, kv0, T, ld, tid);
-    load_rows_t<HD>(Vt, base + 2 * C, kv0, T, ld, tid);
-    __syncthreads();
+  const int ntiles = (kv_end + TILE - 1) / TILE;
+  auto issue = [&](int it) {
+    lds_char_t* st = smem + (it & 1) * 2 * S::TBA;
+    issue_rows<HD>(rs, a.qkv, base + C, it * TILE, ld, st, wave, lane);
+    issue_rows<HD>(rs, a.qkv, base + 2 * C, it * TILE, ld, st + S::TBA, wave, lane);
+  };
+  issue(0);
+  for (int it = 0; it < ntiles; ++it) {
+    wait_vmcnt<0>();
+    block_barrier();
+    if (it + 1 < ntiles) issue(it + 1);
+    const int kv0 = it * TILE;
     if (kv0 > q0w + 31) continue;   // every query of this wave precedes the tile
+    const lds_char_t* Ks = smem + (it & 1) * 2 * S::TBA;
+    const lds_char_t* Vs = Ks + S::TBA;
 
     floatx16 s[2];
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
+      zero(s[t]);
 #pragma unroll
-      for (int r = 0; r < 16; ++r) s[t][r] = 0.0f;
-#pragma unroll
-      for (int k = 0; k < KS; ++k) {
-        uint4 kv = *reinterpret_cast<const uint4*>(Ks + (32 * t + lq) * (HD + 8) + 16 * k + 8 * g);
-        s[t] = mfma32(as_bf16x8(kv), qf[k], s[t]);
-      }
+      for (int k = 0; k < S::KS; ++k) s[t] = mfma32(read_row<HD>(Ks, 32 * t + lq, 2 * k + g), qf[k], s[t]);
     }
+    const bool diag = kv0 + TILE - 1 > q0w || kv0 + TILE > T;
     float mt = -INFINITY;
 #pragma unroll
     for (int t = 0; t < 2; ++t)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        int j = kv0 + 32 * t + acc_row(r, g);
-        float x = (j <= q && j < T) ? s[t][r] * sc : -INFINITY;
+        float x = s[t][r] * sc;
+        if (diag) {
+          const int j = kv0 + 32 * t + acc_row(r, g);
+          x = (j <= q && j < T) ? x : -INFINITY;
+        }
         s[t][r] = x;
         mt = fmaxf(mt, x);
       }
     mt = fmaxf(mt, __shfl_xor(mt, 32, WAVE));
     const float m_new = fmaxf(m_run, mt);
     const float alpha = exp2f(m_run - m_new);
-    float rs = 0.0f;
+    float rsum = 0.0f;
 #pragma unroll
     for (int t = 0; t < 2; ++t)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        float p = exp2f(s[t][r] - m_new);
+        const float p = exp2f(s[t][r] - m_new);
         s[t][r] = p;
-        rs += p;
+        rsum += p;
       }
-    rs += __shfl_xor(rs, 32, WAVE);
-    l_run = l_run * alpha + rs;
+    rsum += __shfl_xor(rsum, 32, WAVE);
+    l_run = l_run * alpha + rsum;
     m_run = m_new;
 #pragma unroll
-    for (int d = 0; d < DT; ++d)
+    for (int d = 0; d < S::DT; ++d)
 #pragma unroll
       for (int r = 0; r < 16; ++r) o[d][r] *= alpha;
 #pragma unroll
     for (int t = 0; t < 2; ++t)
 #pragma unroll
       for (int hh = 0; hh < 2; ++hh) {
-        bf16x8 pf = acc_slots(s[t], hh);
+        const bf16x8 pf = acc_slots(s[t], hh);
 #pragma unroll
-        for (int d = 0; d < DT; ++d) o[d] = mfma32(read_t_slots(Vt, 32 * d + lq, t, hh, g), pf, o[d]);
+        for (int d = 0; d < S::DT; ++d) o[d] = mfma32(read_tr<HD>(Vs, 32 * d, 32 * t + 16 * hh, lane), pf, o[d]);
       }
   }
 
@@ -179,18 +219,19 @@ __global__ __launch_bounds__(256) void attn_fwd_kernel(AttnArgs a) {
     const float inv = 1.0f / l_run;
     bf16_t* out = a.out + ((size_t)b * T + q) * C + h * HD;
 #pragma unroll
-    for (int d = 0; d < DT; ++d)
+    for (int d = 0; d < S::DT; ++d)
 #pragma unroll
       for (int c = 0; c < 4; ++c) {
-        int dd = 32 * d + 8 * c + 4 * g;
+        const int dd = 32 * d + 8 * c + 4 * g;
         if (dd < HD)
-          *reinterpret_cast<uint2*>(out + dd) =
-              make_uint2(pack2(o[d][4 * c] * inv, o[d][4 * c + 1] * inv),
-                         pack2(o[d][4 * c + 2] * inv, o[d][4 * c + 3] * inv));
+          *reinterpret_cast<uint2*>(out + dd) = make_uint2(pack2(o[d][4 * c] * inv, o[d][4 * c + 1] * inv),
+                                                           pack2(o[d][4 * c + 2] * inv, o[d][4 * c + 3] * inv));
       }
     if (g == 0) a.lse[(size_t)bh * T + q] = (m_run + log2f(l_run)) * LN2;
   }
 }
+
+// ------------------------------------------------------------------ backward
 
 // D[b,h,t] = sum_d dO * O, one thread per (token, head)
 template <int HD>
@@ -213,36 +254,31 @@ __global__ void attn_dsum_kernel(AttnArgs a) {
   a.dsum[((size_t)b * a.H + h) * a.T + t] = acc;
 }
 
-// dK, dV for a block of 128 keys (4 waves x 32), walking query tiles of 64.
+// dK, dV for 128 keys (4 waves x 32), walking query tiles of 64 from the
+// diagonal to the end.
 template <int HD>
-__global__ __launch_bounds__(256) void attn_bwd_dkdv_kernel(AttnArgs a) {
-  constexpr int HDP = HD < 32 ? 32 : HD;
-  constexpr int KS = HD / 16, DT = HDP / 32;
-  __shared__ __attribute__((aligned(16))) bf16_t Qs[BKV * (HD + 8)];
-  __shared__ __attribute__((aligned(16))) bf16_t Qt[HDP * LDT];
-  __shared__ __attribute__((aligned(16))) bf16_t Ds[BKV * (HD + 8)];
-  __shared__ __attribute__((aligned(16))) bf16_t Dt[HDP * LDT];
-  __shared__ float lse_s[BKV], dsum_s[BKV];
-
+__global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_kernel(AttnArgs a) {
+  using S = Shape<HD>;
+  constexpr int STAGE = 2 * S::TBA + 1024;   // Q tile, dO tile, lse and D rows
+  __shared__ __attribute__((aligned(1024))) char smem_raw[2 * STAGE];
+  lds_char_t* smem = (lds_char_t*)smem_raw;
   const int T = a.T, H = a.H, C = H * HD, ld = 3 * C;
   const int bh = blockIdx.y, b = bh / H, h = bh % H;
   const int kb = blockIdx.x;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int lq = lane & 31, g = lane >> 5;
+  const int lk = lane & 31, g = lane >> 5;
   const int kv0w = kb * BQ + wave * 32;
-  const int kv = kv0w + lq;
+  const int kv = kv0w + lk;
   const bf16_t* base = a.qkv + (size_t)b * T * ld + h * HD;
   const bf16_t* dob = a.dout + (size_t)b * T * C + h * HD;
+  const v4i32 rq = make_rsrc(a.qkv, (uint32_t)((size_t)a.B * T * ld * 2));
+  const v4i32 rd = make_rsrc(a.dout, (uint32_t)((size_t)a.B * T * C * 2));
+  const v4i32 rl = make_rsrc(a.lse, (uint32_t)((size_t)a.B * H * T * 4));
+  const v4i32 rD = make_rsrc(a.dsum, (uint32_t)((size_t)a.B * H * T * 4));
 
-  if (HD < 32)
-    for (int i = tid; i < (HDP - HD) * LDT; i += 256) {
-      Qt[HD * LDT + i] = 0;
-      Dt[HD * LDT + i] = 0;
-    }
-
-  bf16x8 kf[KS], vf[KS];
+  bf16x8 kf[S::KS], vf[S::KS];
 #pragma unroll
-  for (int s = 0; s < KS; ++s) {
+  for (int s = 0; s < S::KS; ++s) {
     uint4 k4 = make_uint4(0, 0, 0, 0), v4 = make_uint4(0, 0, 0, 0);
     if (kv < T) {
       k4 = *reinterpret_cast<const uint4*>(base + (size_t)kv * ld + C + 16 * s + 8 * g);
@@ -251,58 +287,80 @@ __global__ __launch_bounds__(256) void attn_bwd_dkdv_kernel(AttnArgs a) {
     kf[s] = as_bf16x8(k4);
     vf[s] = as_bf16x8(v4);
   }
-  floatx16 dk[DT], dv[DT];
+  floatx16 dk[S::DT], dv[S::DT];
 #pragma unroll
-  for (int d = 0; d < DT; ++d)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) dk[d][r] = dv[d][r] = 0.0f;
+  for (int d = 0; d < S::DT; ++d) {
+    zero(dk[d]);
+    zero(dv[d]);
+  }
   const float scale = 1.0f / sqrtf((float)HD);
   const float sc = scale * LOG2E;
 
-  for (int q0 = kb * BQ; q0 < T; q0 += BKV) {
-    __syncthreads();
-    load_rows<HD>(Qs, base, q0, T, ld, tid);
-    load_rows_t<HD>(Qt, base, q0, T, ld, tid);
-    load_rows<HD>(Ds, dob, q0, T, C, tid);
-    load_rows_t<HD>(Dt, dob, q0, T, C, tid);
-    if (tid < BKV) {
-      int qq = q0 + tid;
-      lse_s[tid] = qq < T ? a.lse[(size_t)bh * T + qq] * LOG2E : 0.0f;
-      dsum_s[tid] = qq < T ? a.dsum[(size_t)bh * T + qq] : 0.0f;
+  const int qstart = kb * BQ;
+  const int ntiles = qstart < T ? (T - qstart + TILE - 1) / TILE : 0;
+  auto issue = [&](int it) {
+    lds_char_t* st = smem + (it & 1) * STAGE;
+    const int q0 = qstart + it * TILE;
+    issue_rows<HD>(rq, a.qkv, base, q0, ld, st, wave, lane);
+    issue_rows<HD>(rd, a.dout, dob, q0, C, st + S::TBA, wave, lane);
+    // the tile's 64 log-sum-exp and D values (256 bytes each): 16 lanes
+    if (wave == 0 && lane < 16) {
+      const uint32_t off = ((uint32_t)bh * (uint32_t)T + (uint32_t)q0) * 4u + 16u * lane;
+      dma16(rl, off, lds_addr(st + 2 * S::TBA));
+      dma16(rD, off, lds_addr(st + 2 * S::TBA + 256));
     }
-    __syncthreads();
-    if (q0 + BKV - 1 < kv0w) continue;   // every query of the tile precedes this wave's keys
+  };
+  if (ntiles > 0) issue(0);
+  for (int it = 0; it < ntiles; ++it) {
+    wait_vmcnt<0>();
+    block_barrier();
+    if (it + 1 < ntiles) issue(it + 1);
+    const int q0 = qstart + it * TILE;
+    if (q0 + TILE - 1 < kv0w) continue;   // every query precedes this wave's keys
+    const lds_char_t* Qs = smem + (it & 1) * STAGE;
+    const lds_char_t* Ds = Qs + S::TBA;
+    const lds_char_t* lr = Qs + 2 * S::TBA;   // lse [64] then D [64], fp32
+    const bool diag = q0 < kv0w + 32 || q0 + TILE > T || kv0w + 32 > T;
 
     floatx16 p[2], ds[2];
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
+      zero(p[t]);
+      zero(ds[t]);
 #pragma unroll
-      for (int r = 0; r < 16; ++r) p[t][r] = ds[t][r] = 0.0f;
-#pragma unroll
-      for (int k = 0; k < KS; ++k) {
-        uint4 qa = *reinterpret_cast<const uint4*>(Qs + (32 * t + lq) * (HD + 8) + 16 * k + 8 * g);
-        uint4 da = *reinterpret_cast<const uint4*>(Ds + (32 * t + lq) * (HD + 8) + 16 * k + 8 * g);
-        p[t] = mfma32(as_bf16x8(qa), kf[k], p[t]);
-        ds[t] = mfma32(as_bf16x8(da), vf[k], ds[t]);
+      for (int k = 0; k < S::KS; ++k) {
+        p[t] = mfma32(read_row<HD>(Qs, 32 * t + lk, 2 * k + g), kf[k], p[t]);
+        ds[t] = mfma32(read_row<HD>(Ds, 32 * t + lk, 2 * k + g), vf[k], ds[t]);
       }
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        int qi = 32 * t + acc_row(r, g);
-        int qq = q0 + qi;
-        float pv = (kv <= qq && qq < T && kv < T) ? exp2f(p[t][r] * sc - lse_s[qi]) : 0.0f;
-        p[t][r] = pv;
-        ds[t][r] = pv * (ds[t][r] - dsum_s[qi]);
+      for (int c4 = 0; c4 < 4; ++c4) {
+        const int qi = 32 * t + 8 * c4 + 4 * g;   // 4 consecutive queries
+        const v4f32 l4 = *reinterpret_cast<const lds_v4f32_t*>(lr + 4 * qi);
+        const v4f32 d4 = *reinterpret_cast<const lds_v4f32_t*>(lr + 256 + 4 * qi);
+        const float lv[4] = {l4.x * LOG2E, l4.y * LOG2E, l4.z * LOG2E, l4.w * LOG2E};
+        const float dvv[4] = {d4.x, d4.y, d4.z, d4.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int r = 4 * c4 + e;
+          float pv = exp2f(p[t][r] * sc - lv[e]);
+          if (diag) {
+            const int qq = q0 + qi + e;
+            pv = (kv <= qq && qq < T && kv < T) ? pv : 0.0f;
+          }
+          p[t][r] = pv;
+          ds[t][r] = pv * (ds[t][r] - dvv[e]);
+        }
       }
     }
 #pragma unroll
     for (int t = 0; t < 2; ++t)
 #pragma unroll
       for (int hh = 0; hh < 2; ++hh) {
-        bf16x8 pf = acc_slots(p[t], hh), sf = acc_slots(ds[t], hh);
+        const bf16x8 pf = acc_slots(p[t], hh), sf = acc_slots(ds[t], hh);
 #pragma unroll
-        for (int d = 0; d < DT; ++d) {
-          dv[d] = mfma32(read_t_slots(Dt, 32 * d + lq, t, hh, g), pf, dv[d]);
-          dk[d] = mfma32(read_t_slots(Qt, 32 * d + lq, t, hh, g), sf, dk[d]);
+        for (int d = 0; d < S::DT; ++d) {
+          dv[d] = mfma32(read_tr<HD>(Ds, 32 * d, 32 * t + 16 * hh, lane), pf, dv[d]);
+          dk[d] = mfma32(read_tr<HD>(Qs, 32 * d, 32 * t + 16 * hh, lane), sf, dk[d]);
         }
       }
   }
@@ -310,10 +368,10 @@ __global__ __launch_bounds__(256) void attn_bwd_dkdv_kernel(AttnArgs a) {
   if (kv < T) {
     bf16_t* dst = a.dqkv + ((size_t)b * T + kv) * ld + h * HD;
 #pragma unroll
-    for (int d = 0; d < DT; ++d)
+    for (int d = 0; d < S::DT; ++d)
 #pragma unroll
       for (int c = 0; c < 4; ++c) {
-        int dd = 32 * d + 8 * c + 4 * g;
+        const int dd = 32 * d + 8 * c + 4 * g;
         if (dd < HD) {
           *reinterpret_cast<uint2*>(dst + C + dd) =
               make_uint2(pack2(dk[d][4 * c] * scale, dk[d][4 * c + 1] * scale),
@@ -325,15 +383,12 @@ __global__ __launch_bounds__(256) void attn_bwd_dkdv_kernel(AttnArgs a) {
   }
 }
 
-// dQ for a block of 128 queries (4 waves x 32), walking key tiles of 64.
+// dQ for 128 queries (4 waves x 32), walking key tiles of 64.
 template <int HD>
-__global__ __launch_bounds__(256) void attn_bwd_dq_kernel(AttnArgs a) {
-  constexpr int HDP = HD < 32 ? 32 : HD;
-  constexpr int KS = HD / 16, DT = HDP / 32;
-  __shared__ __attribute__((aligned(16))) bf16_t Ks[BKV * (HD + 8)];
-  __shared__ __attribute__((aligned(16))) bf16_t Kt[HDP * LDT];
-  __shared__ __attribute__((aligned(16))) bf16_t Vs[BKV * (HD + 8)];
-
+__global__ __launch_bounds__(256, 2) void attn_bwd_dq_kernel(AttnArgs a) {
+  using S = Shape<HD>;
+  __shared__ __attribute__((aligned(1024))) char smem_raw[2 * 2 * S::TBA];   // 2 stages x (K, V)
+  lds_char_t* smem = (lds_char_t*)smem_raw;
   const int T = a.T, H = a.H, C = H * HD, ld = 3 * C;
   const int bh = blockIdx.y, b = bh / H, h = bh % H;
   const int qb = gridDim.x - 1 - blockIdx.x;
@@ -343,13 +398,11 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_kernel(AttnArgs a) {
   const int q = q0w + lq;
   const bf16_t* base = a.qkv + (size_t)b * T * ld + h * HD;
   const bf16_t* dob = a.dout + (size_t)b * T * C + h * HD;
+  const v4i32 rs = make_rsrc(a.qkv, (uint32_t)((size_t)a.B * T * ld * 2));
 
-  if (HD < 32)
-    for (int i = tid; i < (HDP - HD) * LDT; i += 256) Kt[HD * LDT + i] = 0;
-
-  bf16x8 qf[KS], df[KS];
+  bf16x8 qf[S::KS], df[S::KS];
 #pragma unroll
-  for (int s = 0; s < KS; ++s) {
+  for (int s = 0; s < S::KS; ++s) {
     uint4 q4 = make_uint4(0, 0, 0, 0), d4 = make_uint4(0, 0, 0, 0);
     if (q < T) {
       q4 = *reinterpret_cast<const uint4*>(base + (size_t)q * ld + 16 * s + 8 * g);
@@ -360,39 +413,47 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_kernel(AttnArgs a) {
   }
   const float lse2 = q < T ? a.lse[(size_t)bh * T + q] * LOG2E : 0.0f;
   const float dsum = q < T ? a.dsum[(size_t)bh * T + q] : 0.0f;
-  floatx16 dq[DT];
+  floatx16 dq[S::DT];
 #pragma unroll
-  for (int d = 0; d < DT; ++d)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) dq[d][r] = 0.0f;
+  for (int d = 0; d < S::DT; ++d) zero(dq[d]);
   const float scale = 1.0f / sqrtf((float)HD);
   const float sc = scale * LOG2E;
 
   const int kv_end = min(T, qb * BQ + BQ);
-  for (int kv0 = 0; kv0 < kv_end; kv0 += BKV) {
-    __syncthreads();
-    load_rows<HD>(Ks, base + C, kv0, T, ld, tid);
-    load_rows_t<HD>(Kt, base + C, kv0, T, ld, tid);
-    load_rows<HD>(Vs, base + 2 * C, kv0, T, ld, tid);
-    __syncthreads();
+  const int ntiles = (kv_end + TILE - 1) / TILE;
+  auto issue = [&](int it) {
+    lds_char_t* st = smem + (it & 1) * 2 * S::TBA;
+    issue_rows<HD>(rs, a.qkv, base + C, it * TILE, ld, st, wave, lane);
+    issue_rows<HD>(rs, a.qkv, base + 2 * C, it * TILE, ld, st + S::TBA, wave, lane);
+  };
+  issue(0);
+  for (int it = 0; it < ntiles; ++it) {
+    wait_vmcnt<0>();
+    block_barrier();
+    if (it + 1 < ntiles) issue(it + 1);
+    const int kv0 = it * TILE;
     if (kv0 > q0w + 31) continue;
+    const lds_char_t* Ks = smem + (it & 1) * 2 * S::TBA;
+    const lds_char_t* Vs = Ks + S::TBA;
+    const bool diag = kv0 + TILE - 1 > q0w || kv0 + TILE > T || q0w + 32 > T;
 
     floatx16 p[2], ds[2];
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
+      zero(p[t]);
+      zero(ds[t]);
 #pragma unroll
-      for (int r = 0; r < 16; ++r) p[t][r] = ds[t][r] = 0.0f;
-#pragma unroll
-      for (int k = 0; k < KS; ++k) {
-        uint4 ka = *reinterpret_cast<const uint4*>(Ks + (32 * t + lq) * (HD + 8) + 16 * k + 8 * g);
-        uint4 va = *reinterpret_cast<const uint4*>(Vs + (32 * t + lq) * (HD + 8) + 16 * k + 8 * g);
-        p[t] = mfma32(as_bf16x8(ka), qf[k], p[t]);
-        ds[t] = mfma32(as_bf16x8(va), df[k], ds[t]);
+      for (int k = 0; k < S::KS; ++k) {
+        p[t] = mfma32(read_row<HD>(Ks, 32 * t + lq, 2 * k + g), qf[k], p[t]);
+        ds[t] = mfma32(read_row<HD>(Vs, 32 * t + lq, 2 * k + g), df[k], ds[t]);
       }
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        int j = kv0 + 32 * t + acc_row(r, g);
-        float pv = (j <= q && j < T && q < T) ? exp2f(p[t][r] * sc - lse2) : 0.0f;
+        float pv = exp2f(p[t][r] * sc - lse2);
+        if (diag) {
+          const int j = kv0 + 32 * t + acc_row(r, g);
+          pv = (j <= q && j < T && q < T) ? pv : 0.0f;
+        }
         ds[t][r] = pv * (ds[t][r] - dsum);
       }
     }
@@ -400,19 +461,19 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_kernel(AttnArgs a) {
     for (int t = 0; t < 2; ++t)
 #pragma unroll
       for (int hh = 0; hh < 2; ++hh) {
-        bf16x8 sf = acc_slots(ds[t], hh);
+        const bf16x8 sf = acc_slots(ds[t], hh);
 #pragma unroll
-        for (int d = 0; d < DT; ++d) dq[d] = mfma32(read_t_slots(Kt, 32 * d + lq, t, hh, g), sf, dq[d]);
+        for (int d = 0; d < S::DT; ++d) dq[d] = mfma32(read_tr<HD>(Ks, 32 * d, 32 * t + 16 * hh, lane), sf, dq[d]);
       }
   }
 
   if (q < T) {
     bf16_t* dst = a.dqkv + ((size_t)b * T + q) * ld + h * HD;
 #pragma unroll
-    for (int d = 0; d < DT; ++d)
+    for (int d = 0; d < S::DT; ++d)
 #pragma unroll
       for (int c = 0; c < 4; ++c) {
-        int dd = 32 * d + 8 * c + 4 * g;
+        const int dd = 32 * d + 8 * c + 4 * g;
         if (dd < HD)
           *reinterpret_cast<uint2*>(dst + dd) =
               make_uint2(pack2(dq[d][4 * c] * scale, dq[d][4 * c + 1] * scale),
@@ -445,6 +506,7 @@ hipError_t bwd_t(const AttnArgs& a, hipStream_t s) {
 }  // namespace
 
 hipError_t launch_attention_fwd(const AttnArgs& a, hipStream_t s) {
+  if ((size_t)a.B * a.T * 3 * a.H * a.hd * 2 >= (1ull << 32)) return hipErrorInvalidValue;
   switch (a.hd) {
     case 16: return fwd_t<16>(a, s);
     case 32: return fwd_t<32>(a, s);
@@ -455,6 +517,7 @@ hipError_t launch_attention_fwd(const AttnArgs& a, hipStream_t s) {
 }
 
 hipError_t launch_attention_bwd(const AttnArgs& a, hipStream_t s) {
+  if ((size_t)a.B * a.T * 3 * a.H * a.hd * 2 >= (1ull << 32)) return hipErrorInvalidValue;
   switch (a.hd) {
     case 16: return bwd_t<16>(a, s);
     case 32: return bwd_t<32>(a, s);

@@ -51,13 +51,18 @@ DEV floatx16 mfma32(bf16x8 a, bf16x8 b, floatx16 c) {
 DEV uint32_t lo_pair(uint32_t r0, uint32_t r1) { return (r0 & 0xffffu) | (r1 << 16); }
 DEV uint32_t hi_pair(uint32_t r0, uint32_t r1) { return (r0 >> 16) | (r1 & 0xffff0000u); }
 
+// GELU, tanh form: 0.5 u (1 + tanh(y)) with y = sqrt(2/pi) (u + 0.044715 u^3).
+// Evaluated as u * sigmoid(2y) (the same function, since 0.5 (1 + tanh(y)) =
+// 1 / (1 + exp(-2y))) with one exponential and a fast reciprocal.
 DEV float gelu_tanh(float u) {
-  const float k = 0.7978845608028654f, a = 0.044715f;
-  float t = tanhf(k * (u + a * u * u * u));
-  return 0.5f * u * (1.0f + t);
+  const float k2 = 2.0f * 0.7978845608028654f, a = 0.044715f;
+  const float e = __expf(-k2 * (u + a * u * u * u));
+  return __fdividef(u, 1.0f + e);
 }
+// d/du: s + 2 u s (1 - s) sqrt(2/pi) (1 + 3*0.044715 u^2), s = sigmoid(2y)
 DEV float gelu_tanh_grad(float u) {
   const float k = 0.7978845608028654f, a = 0.044715f;
-  float t = tanhf(k * (u + a * u * u * u));
-  return 0.5f * (1.0f + t) + 0.5f * u * (1.0f - t * t) * k * (1.0f + 3.0f * a * u * u);
+  const float e = __expf(-2.0f * k * (u + a * u * u * u));
+  const float s = __fdividef(1.0f, 1.0f + e);
+  return s + 2.0f * u * s * (1.0f - s) * k * (1.0f + 3.0f * a * u * u);
 }

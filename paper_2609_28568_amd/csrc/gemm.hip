@@ -29,56 +29,12 @@
 // output row (8-byte bf16 / 16-byte fp32 stores in the epilogue).
 #include "common.h"
 #include "kernels.h"
+#include "lds_dma.h"
 
 namespace {
 
 constexpr int BK = 32;        // contraction steps per stage
 constexpr int NSTAGE = 4;     // LDS ring depth
-
-#define LDS_AS __attribute__((address_space(3)))
-typedef LDS_AS void lds_void_t;
-typedef LDS_AS char lds_char_t;
-typedef short v4i16 __attribute__((ext_vector_type(4)));
-typedef LDS_AS v4i16 lds_v4i16_t;
-typedef unsigned int v4u32 __attribute__((ext_vector_type(4)));
-typedef LDS_AS v4u32 lds_v4u32_t;
-
-typedef int v4i32 __attribute__((ext_vector_type(4)));
-
-// Raw buffer descriptor over [base, base+bytes): stride 0, range checked, so
-// loads past the end return zero.
-DEV v4i32 make_rsrc(const void* base, uint32_t bytes) {
-  const uint64_t a = reinterpret_cast<uint64_t>(base);
-  v4i32 r;
-  r.x = __builtin_amdgcn_readfirstlane((int)(uint32_t)a);
-  r.y = __builtin_amdgcn_readfirstlane((int)(uint32_t)(a >> 32));
-  r.z = __builtin_amdgcn_readfirstlane((int)bytes);
-  r.w = 0x00020000;
-  return r;
-}
-
-// 16 bytes per lane from the buffer at byte offset voff into LDS at
-// lds_base + 16*lane. Issued as inline assembly: the kernel tracks these
-// loads itself (wait_vmcnt before the barrier that publishes a stage), and
-// the compiler's own conservative wait before every LDS read would serialise
-// the ring.
-DEV void dma16(v4i32 rsrc, uint32_t voff, uint32_t lds_base) {
-  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
-               :
-               : "s"(__builtin_amdgcn_readfirstlane(lds_base)), "v"(voff), "s"(rsrc)
-               : "memory", "m0");
-}
-
-// vmcnt-only wait (expcnt and lgkmcnt left at their maxima)
-template <int N>
-DEV void wait_vmcnt() {
-  static_assert(N >= 0 && N < 64, "vmcnt");
-  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
-}
-
-// workgroup barrier without the memory fence of __syncthreads (which would
-// wait for the prefetches still in flight)
-DEV void block_barrier() { asm volatile("s_barrier" ::: "memory"); }
 
 // Physical 16-byte unit of logical (row, chunk) in a contraction-contiguous
 // tile [R][32]: 4 units per row, chunk XOR (row/4)%4.
@@ -118,7 +74,7 @@ DEV void issue_tile(v4i32 rs, int ld, int r0, int k0, lds_char_t* dst, int wave,
       const int c = unit_t<R>(k, p) - k * (R / 8);   // the XOR is its own inverse
       off = ((uint32_t)(k0 + k) * (uint32_t)ld + (uint32_t)(r0 + c * 8)) * 2u;
     }
-    dma16(rs, off, (uint32_t)reinterpret_cast<uintptr_t>(dst + ins * 1024));
+    dma16(rs, off, lds_addr(dst + ins * 1024));
   }
 }
 
@@ -128,7 +84,7 @@ template <int R, bool TR>
 DEV bf16x8 read_frag(const lds_char_t* stage, int row_base, int s, int lane) {
   if constexpr (!TR) {
     const int row = row_base + (lane & 31), c = 2 * s + (lane >> 5);
-    return __builtin_bit_cast(bf16x8, *reinterpret_cast<const lds_v4u32_t*>(stage + unit_n(row, c) * 16));
+    return lds_read16(stage + unit_n(row, c) * 16);
   } else {
     // lane t of each 16-lane group names k-row kb + t/4 and columns
     // n + 4*(t%4)..+3; it receives column n + t at k-rows kb..kb+3
@@ -136,11 +92,8 @@ DEV bf16x8 read_frag(const lds_char_t* stage, int row_base, int s, int lane) {
     const int n = row_base + 16 * h + 4 * (t & 3);
     const int kb = 16 * s + 8 * g + (t >> 2);
     const int c = n >> 3, sub = (n & 7) * 2;   // byte offset 0 or 8 in the unit
-    const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-        (lds_v4i16_t*)(stage + unit_t<R>(kb, c) * 16 + sub));
-    const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-        (lds_v4i16_t*)(stage + unit_t<R>(kb + 4, c) * 16 + sub));
-    const uint2 a = __builtin_bit_cast(uint2, lo), b = __builtin_bit_cast(uint2, hi);
+    const uint2 a = lds_read_tr(stage + unit_t<R>(kb, c) * 16 + sub);
+    const uint2 b = lds_read_tr(stage + unit_t<R>(kb + 4, c) * 16 + sub);
     return as_bf16x8(make_uint4(a.x, a.y, b.x, b.y));
   }
 }
@@ -291,20 +244,31 @@ hipError_t launch_t(const GemmArgs& g, hipStream_t s) {
   return hipGetLastError();
 }
 
-// Tile shape per problem: 256 x 192 tiles (4 waves of 128 x 96) when N is a
-// multiple of 192, which holds for every GPT-2 width (768, 2304, 3072 and the
-// padded vocabulary 50304) and makes the 16384-row GEMMs fill the 256 CUs in
-// whole rounds; 256 x 128 otherwise; 128 x 128 for small problems.
+// Tile shape per problem (see gemm_tile_shape): 256 x 192 tiles (4 waves of
+// 128 x 96) when N is a multiple of 192, which holds for every GPT-2 width
+// (768, 2304, 3072 and the padded vocabulary 50304) and makes the 16384-row
+// GEMMs fill the 256 CUs in whole rounds; 256 x 128 otherwise; 128 x 128 for
+// small problems.
 template <bool A_T, bool B_T, int EPI>
 hipError_t launch_shape(const GemmArgs& g, hipStream_t s) {
-  if (g.M >= 1024 || g.N >= 4096) {
-    if (g.N % 192 == 0) return launch_t<256, 192, A_T, B_T, EPI>(g, s);
-    return launch_t<256, 128, A_T, B_T, EPI>(g, s);
-  }
+  int bm = 0, bn = 0;
+  gemm_tile_shape(g.M, g.N, &bm, &bn);
+  if (bm == 256 && bn == 192) return launch_t<256, 192, A_T, B_T, EPI>(g, s);
+  if (bm == 256) return launch_t<256, 128, A_T, B_T, EPI>(g, s);
   return launch_t<128, 128, A_T, B_T, EPI>(g, s);
 }
 
 }  // namespace
+
+void gemm_tile_shape(int M, int N, int* bm, int* bn) {
+  if (M >= 256 && N >= 192 && N % 192 == 0) {
+    *bm = 256; *bn = 192;
+  } else if (M >= 256 && N >= 128 && N % 128 == 0) {
+    *bm = 256; *bn = 128;
+  } else {
+    *bm = 128; *bn = 128;
+  }
+}
 
 int gemm_split_plan(int K, int want, int* k_chunk) {
   if (want < 1) want = 1;

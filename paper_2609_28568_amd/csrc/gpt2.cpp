@@ -77,11 +77,9 @@ const bool kDecay[K_NKIND] = {true, true, false, false, true, false, true, false
 // contraction splits for a weight-gradient GEMM with an M x N output
 // output tiles of the weight-gradient GEMM (the tile shape gemm.hip picks)
 long dw_tiles(int M, int N) {
-  if (M >= 1024 || N >= 4096) {
-    int bn = N % 192 == 0 ? 192 : 128;
-    return (long)((M + 255) / 256) * ((N + bn - 1) / bn);
-  }
-  return (long)((M + 127) / 128) * ((N + 127) / 128);
+  int bm = 0, bn = 0;
+  gemm_tile_shape(M, N, &bm, &bn);
+  return (long)((M + bm - 1) / bm) * ((N + bn - 1) / bn);
 }
 
 // split the 16384-long contraction so that about one round of blocks (256

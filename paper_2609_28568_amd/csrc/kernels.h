@@ -32,6 +32,8 @@ struct GemmArgs {
   int k_chunk;             // contraction length per split (from gemm_split_plan)
 };
 
+// Output tile (bm x bn) the GEMM uses for an M x N product.
+void gemm_tile_shape(int M, int N, int* bm, int* bn);
 // Plan a contraction split of K into about `want` pieces: writes the chunk
 // length (a multiple of the 64-wide k tile) and returns the split count.
 int gemm_split_plan(int K, int want, int* k_chunk);
