@@ -12,34 +12,46 @@
 // Data movement: operand tiles go from HBM straight into LDS with
 // buffer_load ... lds (no staging registers; the buffer descriptor's range
 // check turns reads past the end of a matrix into zeros), through a ring of
-// NSTAGE stages of 32 contraction steps each, so several tiles are in flight
-// while the MFMAs of the current one run. Each wave waits only for its own
-// loads (vmcnt) before the block barrier that publishes a stage.
+// NS stages of BK contraction steps each, so later tiles are in flight while
+// the MFMAs of the current one run. Each wave waits only for its own loads
+// (vmcnt) before the block barrier that publishes a stage. With BK = 64 a
+// contraction-contiguous operand is fetched in whole 128-byte row segments.
 //
 // LDS layouts, both in 16-byte units with an XOR swizzle against bank
 // conflicts:
-//   contraction-contiguous operand: [rows][32] (4 units per row); an MFMA
-//     fragment (8 consecutive k of one row) is one ds_read_b128;
-//   contraction-strided operand: [32][rows], the operand's natural layout;
+//   contraction-contiguous operand: [rows][BK]; an MFMA fragment (8
+//     consecutive k of one row) is one ds_read_b128;
+//   contraction-strided operand: [BK][rows], the operand's natural layout;
 //     a fragment is two ds_read_b64_tr_b16, which hand each lane four
 //     consecutive k of one row gathered from four other lanes' reads.
+// The fragments of the next k-step are read while the MFMAs of the current
+// one run.
 //
 // MFMA: v_mfma_f32_32x32x16_bf16 with its row index i mapped to n and its
-// column index j to m, so each lane ends up holding four consecutive n of one
-// output row (8-byte bf16 / 16-byte fp32 stores in the epilogue).
+// column index j to m. The epilogue goes through LDS so that every output row
+// segment of a wave is written (and any residual or pre-activation read) as
+// one contiguous run instead of 16-byte pieces of 32 rows.
 #include "common.h"
 #include "kernels.h"
 #include "lds_dma.h"
 
 namespace {
 
-constexpr int BK = 32;        // contraction steps per stage
-constexpr int NSTAGE = 4;     // LDS ring depth
+typedef float v4f32_t __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) v4f32_t lds_v4f32_t;
+typedef __attribute__((address_space(3))) float lds_f32_t;
+
+DEV int bitrev3(int x) { return ((x & 1) << 2) | (x & 2) | ((x >> 2) & 1); }
 
 // Physical 16-byte unit of logical (row, chunk) in a contraction-contiguous
-// tile [R][32]: 4 units per row, chunk XOR (row/4)%4.
-DEV int unit_n(int row, int c) { return row * 4 + (c ^ ((row >> 2) & 3)); }
-// ... in a contraction-strided tile [32][R]: R/8 units per k-row. A
+// tile [R][BK]. 32 lanes read 32 consecutive rows at one chunk; the XOR
+// spreads them over all 64 banks.
+template <int BK>
+DEV int unit_n(int row, int c) {
+  if constexpr (BK == 32) return row * 4 + (c ^ ((row >> 2) & 3));
+  else return row * 8 + (c ^ bitrev3((row >> 1) & 7));
+}
+// ... in a contraction-strided tile [BK][R]: R/8 units per k-row. A
 // transposed fragment read touches 4 consecutive k-rows x 4 units per
 // 32 lanes; the chunk XOR spreads those 16 units over all 64 banks:
 // 4*(k%4) when a row is a multiple of 16 units (256 B), 4*((k/2)%2) for
@@ -52,10 +64,10 @@ DEV int unit_t(int k, int c) {
 }
 
 // Issue the direct-to-LDS loads of one operand tile (R rows of the operand,
-// 32 contraction steps starting at k0) into the stage at `dst`. Wave w issues
+// BK contraction steps starting at k0) into the stage at `dst`. Wave w issues
 // instructions w, w+4, ...; each instruction moves 64 units (1 KB), unit u of
 // the tile going to byte 16*u.
-template <int R, bool TR>
+template <int R, int BK, bool TR>
 DEV void issue_tile(v4i32 rs, int ld, int r0, int k0, lds_char_t* dst, int wave, int lane) {
   constexpr int UNITS = R * BK / 8;
   constexpr int INSTR = UNITS / 64;
@@ -66,12 +78,13 @@ DEV void issue_tile(v4i32 rs, int ld, int r0, int k0, lds_char_t* dst, int wave,
     const int u = ins * 64 + lane;   // physical unit written by this lane
     uint32_t off;
     if constexpr (!TR) {
-      const int row = u >> 2, p = u & 3;
-      const int c = p ^ ((row >> 2) & 3);
+      constexpr int U = BK / 8;
+      const int row = u / U, p = u % U;
+      const int c = unit_n<BK>(row, p) - row * U;   // the XOR is its own inverse
       off = ((uint32_t)(r0 + row) * (uint32_t)ld + (uint32_t)(k0 + c * 8)) * 2u;
     } else {
       const int k = u / (R / 8), p = u % (R / 8);
-      const int c = unit_t<R>(k, p) - k * (R / 8);   // the XOR is its own inverse
+      const int c = unit_t<R>(k, p) - k * (R / 8);
       off = ((uint32_t)(k0 + k) * (uint32_t)ld + (uint32_t)(r0 + c * 8)) * 2u;
     }
     dma16(rs, off, lds_addr(dst + ins * 1024));
@@ -80,11 +93,11 @@ DEV void issue_tile(v4i32 rs, int ld, int r0, int k0, lds_char_t* dst, int wave,
 
 // MFMA fragment: 8 consecutive k (k-step s, lane group lane/32) of row
 // row_base + lane%32 of the tile.
-template <int R, bool TR>
+template <int R, int BK, bool TR>
 DEV bf16x8 read_frag(const lds_char_t* stage, int row_base, int s, int lane) {
   if constexpr (!TR) {
     const int row = row_base + (lane & 31), c = 2 * s + (lane >> 5);
-    return lds_read16(stage + unit_n(row, c) * 16);
+    return lds_read16(stage + unit_n<BK>(row, c) * 16);
   } else {
     // lane t of each 16-lane group names k-row kb + t/4 and columns
     // n + 4*(t%4)..+3; it receives column n + t at k-rows kb..kb+3
@@ -98,24 +111,22 @@ DEV bf16x8 read_frag(const lds_char_t* stage, int row_base, int s, int lane) {
   }
 }
 
-template <int BM, int BN, bool A_T, bool B_T, int EPI>
-__global__ __launch_bounds__(256, 1) void gemm_kernel(GemmArgs g) {
+template <int BM, int BN, int BK, int NS, bool A_T, bool B_T, int EPI>
+__global__ __launch_bounds__(256, (NS <= 2 ? 2 : 1)) void gemm_kernel(GemmArgs g) {
   constexpr int WTM = BM / 2, WTN = BN / 2;   // 2 x 2 waves
   constexpr int TM = WTM / 32, TN = WTN / 32;
+  constexpr int KSTEPS = BK / 16;
   constexpr int A_BYTES = BM * BK * 2, B_BYTES = BN * BK * 2;
   constexpr int STAGE = A_BYTES + B_BYTES;
-  constexpr int LOADS = (BM + BN) / 64;       // load instructions per wave per stage
-  // one array per ring stage: with the loop unrolled by NSTAGE every LDS read
-  // and every in-flight load names its stage statically, so the compiler
-  // knows the reads of one stage do not wait on the loads into another
-  static_assert(NSTAGE == 4, "ring of four stages");
-  __shared__ __attribute__((aligned(1024))) char st0[STAGE];
-  __shared__ __attribute__((aligned(1024))) char st1[STAGE];
-  __shared__ __attribute__((aligned(1024))) char st2[STAGE];
-  __shared__ __attribute__((aligned(1024))) char st3[STAGE];
-  auto stage = [&](int s) -> lds_char_t* {
-    return (lds_char_t*)(s == 0 ? st0 : (s == 1 ? st1 : (s == 2 ? st2 : st3)));
-  };
+  constexpr int LOADS = (BM + BN) * BK / 2048;   // load instructions per wave per stage
+  // epilogue staging: per wave 32 rows x WTN fp32 (row stride padded by 4)
+  constexpr int EP_LD = WTN + 4;
+  constexpr int EP_BYTES = 4 * 32 * EP_LD * 4;
+  constexpr int SMEM = NS * STAGE > EP_BYTES ? NS * STAGE : EP_BYTES;
+  static_assert(KSTEPS % 2 == 0, "fragment double buffer alternates per k-step");
+  static_assert(NS >= 2 && NS - 2 <= 3 && (NS - 2) * LOADS < 64, "ring depth / vmcnt range");
+  __shared__ __attribute__((aligned(1024))) char smem_raw[SMEM];
+  lds_char_t* smem = (lds_char_t*)smem_raw;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
@@ -123,12 +134,22 @@ __global__ __launch_bounds__(256, 1) void gemm_kernel(GemmArgs g) {
   // Blocks are dealt round-robin to the 8 XCDs; renumber them so each XCD
   // works through a contiguous run of tiles (n fastest), which keeps the row
   // panel of A it reads in its own L2.
-  const int ntn = gridDim.x, ntiles = gridDim.x * gridDim.y;
-  int bid = blockIdx.y * gridDim.x + blockIdx.x;
-  if ((ntiles & 7) == 0) bid = (bid & 7) * (ntiles >> 3) + (bid >> 3);
+  // With a contraction split over 8k blocks the grid is 1-D: block b works on
+  // split b % splits... arranged so that split z always lands on XCD z % 8 and
+  // each XCD's L2 serves one contraction range for all of its tiles.
+  const int ntn = (g.N + BN - 1) / BN, ntiles = ntn * ((g.M + BM - 1) / BM);
+  int bid, split;
+  if (g.splits > 1) {
+    split = blockIdx.x % g.splits;
+    bid = blockIdx.x / g.splits;
+  } else {
+    split = 0;
+    bid = blockIdx.y * gridDim.x + blockIdx.x;
+    if ((ntiles & 7) == 0) bid = (bid & 7) * (ntiles >> 3) + (bid >> 3);
+  }
   const int m0 = (bid / ntn) * BM, n0 = (bid % ntn) * BN;
 
-  const int kbeg = blockIdx.z * g.k_chunk;
+  const int kbeg = split * g.k_chunk;
   const int kend = min(g.K, kbeg + g.k_chunk);
   const int nk = (kend - kbeg + BK - 1) / BK;
 
@@ -138,10 +159,19 @@ __global__ __launch_bounds__(256, 1) void gemm_kernel(GemmArgs g) {
   const v4i32 ra = make_rsrc(g.A, a_rows * (uint32_t)g.lda * 2u);
   const v4i32 rb = make_rsrc(g.B, b_rows * (uint32_t)g.ldb * 2u);
 
-  auto issue = [&](int kt, lds_char_t* st) {
+  auto stage = [&](int kt) { return smem + (kt % NS) * STAGE; };
+  auto issue = [&](int kt) {
+    lds_char_t* st = stage(kt);
     const int k0 = kbeg + kt * BK;
-    issue_tile<BM, A_T>(ra, g.lda, m0, k0, st, wave, lane);
-    issue_tile<BN, B_T>(rb, g.ldb, n0, k0, st + A_BYTES, wave, lane);
+    issue_tile<BM, BK, A_T>(ra, g.lda, m0, k0, st, wave, lane);
+    issue_tile<BN, BK, B_T>(rb, g.ldb, n0, k0, st + A_BYTES, wave, lane);
+  };
+  auto load = [&](bf16x8* fa, bf16x8* fb, int kt, int s) {
+    const lds_char_t* st = stage(kt);
+#pragma unroll
+    for (int i = 0; i < TM; ++i) fa[i] = read_frag<BM, BK, A_T>(st, wm * WTM + i * 32, s, lane);
+#pragma unroll
+    for (int j = 0; j < TN; ++j) fb[j] = read_frag<BN, BK, B_T>(st + A_BYTES, wn * WTN + j * 32, s, lane);
   };
 
   floatx16 acc[TM][TN];
@@ -151,96 +181,116 @@ __global__ __launch_bounds__(256, 1) void gemm_kernel(GemmArgs g) {
     for (int j = 0; j < TN; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+  auto mma = [&](const bf16x8* fa, const bf16x8* fb) {
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j) acc[i][j] = mfma32(fb[j], fa[i], acc[i][j]);
+  };
+  // a tile has landed once at most the loads of the `later` tiles issued
+  // after it are outstanding (loads complete in issue order)
+  auto wait_later = [&](int later) {
+    constexpr int L3 = NS - 2 >= 3 ? 3 : 0, L2 = NS - 2 >= 2 ? 2 : 0;
+    if (L3 && later >= 3) wait_vmcnt<L3 * LOADS>();
+    else if (L2 && later >= 2) wait_vmcnt<L2 * LOADS>();
+    else if (later >= 1) wait_vmcnt<LOADS>();
+    else wait_vmcnt<0>();
+  };
 
+  // Tile kt: wait for it, publish it with the barrier (which also frees the
+  // stage of tile kt-1 for tile kt+NS-1), then walk its k-steps reading the
+  // fragments of step s+1 while the MFMAs of step s run.
+  bf16x8 fa[2][TM], fb[2][TN];
 #pragma unroll
-  for (int s = 0; s < NSTAGE - 1; ++s)
-    if (s < nk) issue(s, stage(s));
-
-  for (int kt0 = 0; kt0 < nk; kt0 += NSTAGE) {
+  for (int s = 0; s < NS - 1; ++s)
+    if (s < nk) issue(s);
+  for (int kt = 0; kt < nk; ++kt) {
+    // issued so far: tiles up to kt + NS - 2
+    wait_later(min(NS - 2, nk - 1 - kt));
+    block_barrier();
+    if (kt + NS - 1 < nk) issue(kt + NS - 1);
+    load(fa[0], fb[0], kt, 0);
 #pragma unroll
-    for (int S = 0; S < NSTAGE; ++S) {
-      const int kt = kt0 + S;
-      if (kt < nk) {
-        // tile kt has landed once at most the loads of the tiles issued
-        // after it are outstanding
-        if (kt + NSTAGE - 2 < nk) wait_vmcnt<(NSTAGE - 2) * LOADS>();
-        else wait_vmcnt<0>();
-        block_barrier();
-        // the stage read in the previous step now takes tile kt+NSTAGE-1
-        if (kt + NSTAGE - 1 < nk) issue(kt + NSTAGE - 1, stage((S + NSTAGE - 1) % NSTAGE));
-
-        const lds_char_t* a_s = stage(S);
-        const lds_char_t* b_s = a_s + A_BYTES;
-#pragma unroll
-        for (int s = 0; s < BK / 16; ++s) {
-          bf16x8 fa[TM], fb[TN];
-#pragma unroll
-          for (int i = 0; i < TM; ++i) fa[i] = read_frag<BM, A_T>(a_s, wm * WTM + i * 32, s, lane);
-#pragma unroll
-          for (int j = 0; j < TN; ++j) fb[j] = read_frag<BN, B_T>(b_s, wn * WTN + j * 32, s, lane);
-#pragma unroll
-          for (int i = 0; i < TM; ++i)
-#pragma unroll
-            for (int j = 0; j < TN; ++j) acc[i][j] = mfma32(fb[j], fa[i], acc[i][j]);
-        }
-      }
+    for (int s = 0; s < KSTEPS; ++s) {
+      if (s + 1 < KSTEPS) load(fa[(s + 1) & 1], fb[(s + 1) & 1], kt, s + 1);
+      mma(fa[s & 1], fb[s & 1]);
     }
   }
 
-  // epilogue: lane holds, for output row m, n = nb + 8*(r/4) + (r%4)
-  const int lrow = lane & 31;
+  // ---------------------------------------------------------------- epilogue
+  // every wave is done with the ring before it is reused for staging
+  block_barrier();
+  lds_f32_t* ep = (lds_f32_t*)smem_raw + wave * 32 * EP_LD;
+  const int lrow = lane & 31, lg = lane >> 5;
+  constexpr int CPR = WTN / 4;                 // 4-column chunks per row
+  constexpr int CHUNKS = 32 * CPR / 64;        // chunks per lane per 32-row block
+  static_assert((32 * CPR) % 64 == 0, "epilogue chunking");
+  float* Cf = static_cast<float*>(g.C) + (size_t)split * g.split_stride;
+  bf16_t* Cb = static_cast<bf16_t*>(g.C);
 #pragma unroll
   for (int i = 0; i < TM; ++i) {
-    const int m = m0 + wm * WTM + i * 32 + lrow;
-    if (m >= g.M) continue;
+    // lane holds, for row lrow of this 32-row block, columns
+    // 32j + 8q + 4*lg .. +3 of the wave's WTN columns
 #pragma unroll
-    for (int j = 0; j < TN; ++j) {
+    for (int j = 0; j < TN; ++j)
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        const int n = n0 + wn * WTN + j * 32 + q * 8 + (lane >> 5) * 4;
-        if (n >= g.N) continue;
-        float v0 = acc[i][j][q * 4 + 0], v1 = acc[i][j][q * 4 + 1];
-        float v2 = acc[i][j][q * 4 + 2], v3 = acc[i][j][q * 4 + 3];
-        const size_t off = (size_t)m * g.ldc + n;
-        if constexpr (EPI == EPI_F32) {
-          float* C = static_cast<float*>(g.C) + (size_t)blockIdx.z * g.split_stride;
-          float4* p = reinterpret_cast<float4*>(C + off);
-          if (g.accumulate) {
-            float4 o = *p;
-            v0 += o.x; v1 += o.y; v2 += o.z; v3 += o.w;
-          }
-          *p = make_float4(v0, v1, v2, v3);
-        } else if constexpr (EPI == EPI_GELU_BWD) {
-          uint2 u = *reinterpret_cast<const uint2*>(g.aux + off);
-          v0 *= gelu_tanh_grad(lo_f(u.x)); v1 *= gelu_tanh_grad(hi_f(u.x));
-          v2 *= gelu_tanh_grad(lo_f(u.y)); v3 *= gelu_tanh_grad(hi_f(u.y));
-          *reinterpret_cast<uint2*>(static_cast<bf16_t*>(g.C) + off) = make_uint2(pack2(v0, v1), pack2(v2, v3));
+        const int col = 32 * j + 8 * q + 4 * lg;
+        const v4f32_t v = {acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
+        *reinterpret_cast<lds_v4f32_t*>(ep + lrow * EP_LD + col) = v;
+      }
+    __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0): this wave's LDS writes are done
+    __builtin_amdgcn_wave_barrier();
+#pragma unroll
+    for (int cc = 0; cc < CHUNKS; ++cc) {
+      const int idx = lane + 64 * cc;
+      const int row = idx / CPR, c4 = (idx % CPR) * 4;
+      const v4f32_t v = *reinterpret_cast<const lds_v4f32_t*>(ep + row * EP_LD + c4);
+      const int m = m0 + wm * WTM + i * 32 + row;
+      const int n = n0 + wn * WTN + c4;
+      if (m >= g.M || n >= g.N) continue;
+      float v0 = v.x, v1 = v.y, v2 = v.z, v3 = v.w;
+      const size_t off = (size_t)m * g.ldc + n;
+      if constexpr (EPI == EPI_F32) {
+        float4* p = reinterpret_cast<float4*>(Cf + off);
+        if (g.accumulate) {
+          const float4 o = *p;
+          v0 += o.x; v1 += o.y; v2 += o.z; v3 += o.w;
+        }
+        *p = make_float4(v0, v1, v2, v3);
+      } else if constexpr (EPI == EPI_GELU_BWD) {
+        const uint2 u = *reinterpret_cast<const uint2*>(g.aux + off);
+        v0 *= gelu_tanh_grad(lo_f(u.x)); v1 *= gelu_tanh_grad(hi_f(u.x));
+        v2 *= gelu_tanh_grad(lo_f(u.y)); v3 *= gelu_tanh_grad(hi_f(u.y));
+        *reinterpret_cast<uint2*>(Cb + off) = make_uint2(pack2(v0, v1), pack2(v2, v3));
+      } else {
+        if (g.bias) {
+          const float4 b = *reinterpret_cast<const float4*>(g.bias + n);
+          v0 += b.x; v1 += b.y; v2 += b.z; v3 += b.w;
+        }
+        if constexpr (EPI == EPI_GELU) {
+          *reinterpret_cast<uint2*>(Cb + off) = make_uint2(pack2(v0, v1), pack2(v2, v3));
+          *reinterpret_cast<uint2*>(g.C2 + off) =
+              make_uint2(pack2(gelu_tanh(v0), gelu_tanh(v1)), pack2(gelu_tanh(v2), gelu_tanh(v3)));
         } else {
-          if (g.bias) {
-            float4 b = *reinterpret_cast<const float4*>(g.bias + n);
-            v0 += b.x; v1 += b.y; v2 += b.z; v3 += b.w;
+          if (g.residual) {
+            const uint2 r = *reinterpret_cast<const uint2*>(g.residual + off);
+            v0 += lo_f(r.x); v1 += hi_f(r.x); v2 += lo_f(r.y); v3 += hi_f(r.y);
           }
-          if constexpr (EPI == EPI_GELU) {
-            *reinterpret_cast<uint2*>(static_cast<bf16_t*>(g.C) + off) = make_uint2(pack2(v0, v1), pack2(v2, v3));
-            *reinterpret_cast<uint2*>(g.C2 + off) =
-                make_uint2(pack2(gelu_tanh(v0), gelu_tanh(v1)), pack2(gelu_tanh(v2), gelu_tanh(v3)));
-          } else {
-            if (g.residual) {
-              uint2 r = *reinterpret_cast<const uint2*>(g.residual + off);
-              v0 += lo_f(r.x); v1 += hi_f(r.x); v2 += lo_f(r.y); v3 += hi_f(r.y);
-            }
-            *reinterpret_cast<uint2*>(static_cast<bf16_t*>(g.C) + off) = make_uint2(pack2(v0, v1), pack2(v2, v3));
-          }
+          *reinterpret_cast<uint2*>(Cb + off) = make_uint2(pack2(v0, v1), pack2(v2, v3));
         }
       }
     }
+    __builtin_amdgcn_s_waitcnt(0xC07F);   // reads done before the next block overwrites
+    __builtin_amdgcn_wave_barrier();
   }
 }
 
-template <int BM, int BN, bool A_T, bool B_T, int EPI>
+template <int BM, int BN, int BK, int NS, bool A_T, bool B_T, int EPI>
 hipError_t launch_t(const GemmArgs& g, hipStream_t s) {
-  dim3 grid((g.N + BN - 1) / BN, (g.M + BM - 1) / BM, g.splits);
-  hipLaunchKernelGGL((gemm_kernel<BM, BN, A_T, B_T, EPI>), grid, dim3(256), 0, s, g);
+  const unsigned tn = (g.N + BN - 1) / BN, tm = (g.M + BM - 1) / BM;
+  dim3 grid = g.splits > 1 ? dim3(tn * tm * g.splits) : dim3(tn, tm);
+  hipLaunchKernelGGL((gemm_kernel<BM, BN, BK, NS, A_T, B_T, EPI>), grid, dim3(256), 0, s, g);
   return hipGetLastError();
 }
 
@@ -253,9 +303,14 @@ template <bool A_T, bool B_T, int EPI>
 hipError_t launch_shape(const GemmArgs& g, hipStream_t s) {
   int bm = 0, bn = 0;
   gemm_tile_shape(g.M, g.N, &bm, &bn);
-  if (bm == 256 && bn == 192) return launch_t<256, 192, A_T, B_T, EPI>(g, s);
-  if (bm == 256) return launch_t<256, 128, A_T, B_T, EPI>(g, s);
-  return launch_t<128, 128, A_T, B_T, EPI>(g, s);
+  // short contractions: two 2-stage blocks per CU, so one block's prologue
+  // and epilogue overlap the other's MFMAs; long ones: one 5-stage block
+  const bool short_k = g.k_chunk <= 4096;
+  if (bm == 256 && bn == 192)
+    return short_k ? launch_t<256, 192, 32, 2, A_T, B_T, EPI>(g, s) : launch_t<256, 192, 32, 5, A_T, B_T, EPI>(g, s);
+  if (bm == 256)
+    return short_k ? launch_t<256, 128, 32, 2, A_T, B_T, EPI>(g, s) : launch_t<256, 128, 32, 5, A_T, B_T, EPI>(g, s);
+  return launch_t<128, 128, 32, 2, A_T, B_T, EPI>(g, s);
 }
 
 }  // namespace

@@ -82,27 +82,24 @@ long dw_tiles(int M, int N) {
   return (long)((M + bm - 1) / bm) * ((N + bn - 1) / bn);
 }
 
-// split the 16384-long contraction so that about one round of blocks (256
-// CUs) is in flight
+// Split the token contraction of a weight gradient when its tiles alone
+// would leave CUs idle: 8 splits (one per XCD) or 16, each at least 512
+// tokens long.
+int dw_want(const Dims& d, int M, int N) {
+  const long tiles = dw_tiles(M, N);
+  if (tiles >= 256) return 1;
+  int want = tiles * 8 >= 256 ? 8 : 16;
+  while (want > 1 && d.BT / want < 512) want /= 2;
+  return want;
+}
+
 int dw_splits(const Dims& d, int M, int N) {
-  long tiles = dw_tiles(M, N);
-  long want = (256 + tiles - 1) / tiles;
-  long cap = d.BT / 512;
-  if (cap < 1) cap = 1;
-  if (want > cap) want = cap;
-  if (want < 1) want = 1;
-  return gemm_split_plan((int)d.BT, (int)want, nullptr);
+  return gemm_split_plan((int)d.BT, dw_want(d, M, N), nullptr);
 }
 
 int dw_chunk(const Dims& d, int M, int N) {
   int kc = 0;
-  long tiles = dw_tiles(M, N);
-  long want = (256 + tiles - 1) / tiles;
-  long cap = d.BT / 512;
-  if (cap < 1) cap = 1;
-  if (want > cap) want = cap;
-  if (want < 1) want = 1;
-  gemm_split_plan((int)d.BT, (int)want, &kc);
+  gemm_split_plan((int)d.BT, dw_want(d, M, N), &kc);
   return kc;
 }
 
