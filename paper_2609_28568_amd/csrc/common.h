@@ -15,17 +15,19 @@ typedef float floatx4 __attribute__((ext_vector_type(4)));
 
 constexpr int WAVE = 64;
 
-// fp32 -> bf16, round to nearest even (NaN stays NaN).
-DEV bf16_t f2bf(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return (bf16_t)((u >> 16) | 0x40u);
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return (bf16_t)(u >> 16);
-}
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float floatx2 __attribute__((ext_vector_type(2)));
+
+// fp32 -> bf16, round to nearest even (NaN stays NaN): gfx950 converts in
+// hardware (v_cvt_pk_bf16_f32, one instruction for a pair).
+DEV bf16_t f2bf(float f) { return __builtin_bit_cast(bf16_t, (__bf16)f); }
 DEV float bf2f(bf16_t h) { return __uint_as_float(((uint32_t)h) << 16); }
 
 // two bf16 packed in a 32-bit word (low half = first element)
-DEV uint32_t pack2(float a, float b) { return (uint32_t)f2bf(a) | ((uint32_t)f2bf(b) << 16); }
+DEV uint32_t pack2(float a, float b) {
+  floatx2 v = {a, b};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
+}
 DEV float lo_f(uint32_t w) { return __uint_as_float(w << 16); }
 DEV float hi_f(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 

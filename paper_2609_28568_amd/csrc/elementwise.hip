@@ -348,8 +348,8 @@ hipError_t launch_cross_entropy(bf16_t* logits, const int32_t* targets, float* l
   if (nch <= 256 * 2) {
     hipLaunchKernelGGL((cross_entropy_kernel<256, 2>), dim3(rows), dim3(256), 0, s, logits, targets, losses, V, Vp,
                        grad_scale);
-  } else if (nch <= 512 * 16) {
-    hipLaunchKernelGGL((cross_entropy_kernel<512, 16>), dim3(rows), dim3(512), 0, s, logits, targets, losses, V, Vp,
+  } else if (nch <= 1024 * 8) {
+    hipLaunchKernelGGL((cross_entropy_kernel<1024, 8>), dim3(rows), dim3(1024), 0, s, logits, targets, losses, V, Vp,
                        grad_scale);
   } else {
     return hipErrorInvalidValue;

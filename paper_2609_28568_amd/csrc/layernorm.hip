@@ -7,8 +7,8 @@
 
 namespace {
 
-constexpr int MAXCH = 8;   // 4-channel chunks per lane: C <= 2048
-
+// MAXCH: 4-channel chunks per lane, C <= 256*MAXCH
+template <int MAXCH>
 __global__ __launch_bounds__(256) void ln_fwd_kernel(const bf16_t* __restrict__ x, const float* __restrict__ w,
                                                      const float* __restrict__ b, bf16_t* __restrict__ y,
                                                      float* __restrict__ mean_out, float* __restrict__ rstd_out,
@@ -63,6 +63,7 @@ __global__ __launch_bounds__(256) void ln_fwd_kernel(const bf16_t* __restrict__ 
 
 // dx = rstd * (g - mean(g) - xhat * mean(g * xhat)), g = dy * w; the result is
 // added to the residual-stream gradient. Per-block sums of dy*xhat and dy.
+template <int MAXCH>
 __global__ __launch_bounds__(256) void ln_bwd_kernel(const bf16_t* __restrict__ dy, const bf16_t* __restrict__ x,
                                                      const float* __restrict__ mean_in,
                                                      const float* __restrict__ rstd_in, const float* __restrict__ w,
@@ -146,25 +147,49 @@ __global__ __launch_bounds__(256) void ln_bwd_kernel(const bf16_t* __restrict__ 
   }
 }
 
+template <int MAXCH>
+hipError_t fwd_t(const bf16_t* x, const float* w, const float* b, bf16_t* y, float* mean, float* rstd, int rows,
+                 int C, float eps, hipStream_t s) {
+  hipLaunchKernelGGL(ln_fwd_kernel<MAXCH>, dim3((rows + 3) / 4), dim3(256), 0, s, x, w, b, y, mean, rstd, rows, C, eps);
+  return hipGetLastError();
+}
+
+template <int MAXCH>
+hipError_t bwd_t(const bf16_t* dy, const bf16_t* x, const float* mean, const float* rstd, const float* w,
+                 bf16_t* dres, int has_res, float* part, int rows, int C, hipStream_t s) {
+  hipLaunchKernelGGL(ln_bwd_kernel<MAXCH>, dim3(layernorm_bwd_blocks(rows)), dim3(256), 0, s, dy, x, mean, rstd, w,
+                     dres, has_res, part, rows, C);
+  return hipGetLastError();
+}
+
 }  // namespace
 
 hipError_t launch_layernorm_fwd(const bf16_t* x, const float* w, const float* b, bf16_t* y, float* mean,
                                 float* rstd, int rows, int C, float eps, hipStream_t s) {
-  if (C > MAXCH * 256 || C % 4) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(ln_fwd_kernel, dim3((rows + 3) / 4), dim3(256), 0, s, x, w, b, y, mean, rstd, rows, C, eps);
-  return hipGetLastError();
+  if (C % 4) return hipErrorInvalidValue;
+  if (C <= 256) return fwd_t<1>(x, w, b, y, mean, rstd, rows, C, eps, s);
+  if (C <= 512) return fwd_t<2>(x, w, b, y, mean, rstd, rows, C, eps, s);
+  if (C <= 768) return fwd_t<3>(x, w, b, y, mean, rstd, rows, C, eps, s);
+  if (C <= 1024) return fwd_t<4>(x, w, b, y, mean, rstd, rows, C, eps, s);
+  if (C <= 2048) return fwd_t<8>(x, w, b, y, mean, rstd, rows, C, eps, s);
+  return hipErrorInvalidValue;
 }
 
+// 4 rows per wave, 4 waves per block: enough blocks to fill the chip, each
+// writing one row of partial sums
 int layernorm_bwd_blocks(int rows) {
-  int n = (rows + 3) / 4;
-  return n < 256 ? n : 256;
+  int n = (rows + 15) / 16;
+  return n < 1024 ? (n < 1 ? 1 : n) : 1024;
 }
 
 hipError_t launch_layernorm_bwd(const bf16_t* dy, const bf16_t* x, const float* mean, const float* rstd,
                                 const float* w, bf16_t* dres, int has_res, float* part, int rows, int C,
                                 hipStream_t s) {
-  if (C > MAXCH * 256 || C % 4) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(ln_bwd_kernel, dim3(layernorm_bwd_blocks(rows)), dim3(256), 0, s, dy, x, mean, rstd, w, dres,
-                     has_res, part, rows, C);
-  return hipGetLastError();
+  if (C % 4) return hipErrorInvalidValue;
+  if (C <= 256) return bwd_t<1>(dy, x, mean, rstd, w, dres, has_res, part, rows, C, s);
+  if (C <= 512) return bwd_t<2>(dy, x, mean, rstd, w, dres, has_res, part, rows, C, s);
+  if (C <= 768) return bwd_t<3>(dy, x, mean, rstd, w, dres, has_res, part, rows, C, s);
+  if (C <= 1024) return bwd_t<4>(dy, x, mean, rstd, w, dres, has_res, part, rows, C, s);
+  if (C <= 2048) return bwd_t<8>(dy, x, mean, rstd, w, dres, has_res, part, rows, C, s);
+  return hipErrorInvalidValue;
 }

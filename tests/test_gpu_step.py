@@ -285,3 +285,29 @@ def test_call_order_errors():
     m.backward()
     m.adamw_step(0)
     m.close()
+
+
+def test_bf16_copy_rounds_to_nearest_even_exactly():
+    """The bf16 weight copy is the round-to-nearest-even image of the fp32
+    master, bit for bit: exact ties both ways, values just beside a tie,
+    subnormals, the largest finite values (which round to infinity) and
+    infinities."""
+    w = workload("tiny")
+    m = _model(w)
+    n = m.n_params
+    g = np.random.default_rng(77)
+    hi = g.integers(0, 1 << 16, n, dtype=np.uint32) << 16
+    lo = g.choice(np.array([0x8000, 0x7FFF, 0x8001, 0x0000, 0xFFFF], np.uint32), n)
+    bits = hi | lo
+    bits[:13] = [0x00008000, 0x00018000, 0x7F7F8000, 0x7F7FFFFF, 0xFF7F7FFF, 0x7F800000, 0xFF800000,
+                 0x00000001, 0x807FFFFF, 0x3F808000, 0x3F818000, 0xBF808000, 0x3F80FFFF]
+    nan = ((bits & 0x7F800000) == 0x7F800000) & ((bits & 0x007FFFFF) != 0)
+    bits[nan] = 0
+    vals = bits.view(np.float32)
+    m.flat("params").copy_(torch.from_numpy(vals.copy()))
+    assert m.L.gpt2_sync_weights(m.handle) == 0
+    torch.cuda.synchronize()
+    got = m.flat_bf16().view(torch.int16).cpu().numpy().view(np.uint16)
+    want = (synth.round_to_bf16(vals).view(np.uint32) >> 16).astype(np.uint16)
+    assert np.array_equal(got, want), np.flatnonzero(got != want)[:8]
+    m.close()
