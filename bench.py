@@ -59,24 +59,72 @@ def cpu_baseline(w: dict, params, ids, tgt) -> dict:
                       f"model and token stream, numpy fp32, {dt:.1f} s"}
 
 
-def traffic_from_profiles(kernel_tag: str, src_hash: str):
-    """HBM bytes per launch from committed rocprofv3 counter summaries, if
-    they were taken on the current kernel source."""
-    path = os.path.join(ROOT, "profiles", f"{kernel_tag}_traffic.json")
-    if not os.path.exists(path):
+# Kernel class -> (sources its code comes from, rocprofv3 kernel-name pattern)
+KERNEL_CLASSES = {
+    "gemm_fwd": (("gemm.hip", "common.h", "lds_dma.h", "kernels.h"),
+                 r"gemm_kernel<\d+, \d+, \d+, \d+, false, false, 0>"),
+    "gemm_dw": (("gemm.hip", "common.h", "lds_dma.h", "kernels.h"),
+                r"gemm_kernel<\d+, \d+, \d+, \d+, true, true, 3>"),
+    "attn_bwd": (("attention.hip", "common.h", "lds_dma.h", "kernels.h"), r"attn_(bwd|dsum)"),
+}
+CALIBRATION_BYTES = 1 << 30
+
+
+def kernel_source_hash(kernel_tag: str) -> str:
+    """Hash of the sources the kernel class is built from, so that stored
+    counter readings go stale when its code changes."""
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2609_28568_amd", "csrc")
+    for f in KERNEL_CLASSES[kernel_tag][0]:
+        h.update(open(os.path.join(csrc, f), "rb").read())
+    return h.hexdigest()
+
+
+def traffic_path(kernel_tag: str, workload: str) -> str:
+    return os.path.join(ROOT, "profiles", f"{kernel_tag}_{workload}_traffic.json")
+
+
+def traffic_from_profiles(kernel_tag: str, workload: str):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, if
+    it was taken on the kernel's current source."""
+    path = traffic_path(kernel_tag, workload)
+    if kernel_tag not in KERNEL_CLASSES or not os.path.exists(path):
         return None
     d = json.load(open(path))
-    if d.get("source_sha256") != src_hash:
+    if d.get("source_sha256") != kernel_source_hash(kernel_tag):
         return None
     return d.get("bytes_per_launch")
 
 
-def kernel_source_hash() -> str:
-    h = hashlib.sha256()
-    csrc = os.path.join(ROOT, "paper_2609_28568_amd", "csrc")
-    for f in sorted(os.listdir(csrc)):
-        h.update(open(os.path.join(csrc, f), "rb").read())
-    return h.hexdigest()
+def pmc_summary(kernel_tag: str, fetch_csv: str, write_csv: str, command: str) -> dict:
+    """Turn two rocprofv3 counter passes (FETCH_SIZE, WRITE_SIZE; KiB per
+    dispatch) into HBM bytes per launch of one kernel class, each counter
+    scaled by its reading on a device-to-device copy of CALIBRATION_BYTES."""
+    import csv
+    import re
+    pat = re.compile(KERNEL_CLASSES[kernel_tag][1])
+
+    def read(path, counter):
+        kern, copy = [], []
+        for r in csv.DictReader(open(path)):
+            if r["Counter_Name"] != counter:
+                continue
+            v = float(r["Counter_Value"]) * 1024.0
+            if pat.search(r["Kernel_Name"]):
+                kern.append(v)
+            elif "copyBuffer" in r["Kernel_Name"] and int(r["Grid_Size"]) >= 1 << 16:
+                copy.append(v)
+        if not kern or not copy:
+            raise SystemExit(f"{path}: no {counter} rows for {kernel_tag} or for the calibration copy")
+        return sum(kern) / len(kern), max(copy), len(kern)
+
+    fk, fc, n = read(fetch_csv, "FETCH_SIZE")
+    wk, wc, _ = read(write_csv, "WRITE_SIZE")
+    f_scale, w_scale = CALIBRATION_BYTES / fc, CALIBRATION_BYTES / wc
+    return {"kernel": kernel_tag, "dispatches": n, "fetch_bytes_raw": fk, "write_bytes_raw": wk,
+            "copy_fetch_bytes_raw": fc, "copy_write_bytes_raw": wc, "fetch_scale": f_scale,
+            "write_scale": w_scale, "bytes_per_launch": fk * f_scale + wk * w_scale,
+            "source_sha256": kernel_source_hash(kernel_tag), "command": command}
 
 
 def main():
@@ -85,10 +133,22 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="gpt2_124m")
-    ap.add_argument("--probe", default="gemm_dw", help="kernel class timed for the roofline entry")
+    ap.add_argument("--probe", default="gemm_fwd", help="kernel class timed for the roofline entry")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--classes", action="store_true", help="also report every kernel class (extra pass)")
+    ap.add_argument("--calibration-copy", action="store_true",
+                    help="after the timed steps, copy 1 GiB device-to-device (counter calibration)")
+    ap.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="write profiles/<probe>_<workload>_traffic.json from two rocprofv3 counter passes and exit")
+    ap.add_argument("--pmc-command", default="", help="the profiling command, recorded with --pmc-summary")
     args = ap.parse_args()
+    if args.pmc_summary:
+        d = pmc_summary(args.probe, *args.pmc_summary, args.pmc_command)
+        d["workload"] = args.workload
+        with open(traffic_path(args.probe, args.workload), "w") as f:
+            json.dump(d, f, indent=1)
+        print(json.dumps(d, indent=1))
+        return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); this build has no multi-GPU path",
               file=sys.stderr)
@@ -165,11 +225,18 @@ def main():
     avg_ms = probe["ms"] / max(probe["launches"], 1)
     achieved = probe["flops"] / (probe["ms"] * 1e-3) / 1e12 if probe["ms"] else 0.0
     flops_launch = probe["flops"] / max(probe["launches"], 1)
-    tb = traffic_from_profiles(args.probe, kernel_source_hash())
+    tb = traffic_from_profiles(args.probe, args.workload)
     roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                 "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": tb,
                 "kernel": args.probe, "launches": probe["launches"], "avg_launch_ms": round(avg_ms, 4),
                 "flops_per_launch": flops_launch}
+
+    if args.calibration_copy:
+        src = torch.empty(CALIBRATION_BYTES, dtype=torch.uint8, device="cuda").fill_(1)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     cpu = None
     if not args.no_cpu_baseline:

@@ -289,26 +289,30 @@ int gemm_class(int a_t, int b_t, int epi) {
 hipError_t gemm(Model* m, int cls, int M, int N, int K, const bf16_t* A, int lda, int a_t, const bf16_t* B,
                 int ldb, int b_t, int epi, void* C, int ldc, const float* bias = nullptr,
                 const bf16_t* residual = nullptr, bf16_t* C2 = nullptr, const bf16_t* aux = nullptr,
-                int accumulate = 0, int splits = 1, long split_stride = 0, int k_chunk = 0) {
+                int accumulate = 0, int splits = 1, long split_stride = 0, int k_chunk = 0, double alg_flops = 0.0) {
   GemmArgs g{};
   g.A = A; g.B = B; g.M = M; g.N = N; g.K = K; g.lda = lda; g.ldb = ldb;
   g.C = C; g.ldc = ldc; g.bias = bias; g.residual = residual; g.C2 = C2; g.aux = aux;
   g.accumulate = accumulate; g.splits = splits; g.split_stride = split_stride; g.k_chunk = k_chunk;
-  double fl = 2.0 * M * N * K;
+  // algorithmic FLOPs: the tied head passes its count over the real vocabulary
+  // only (the padded columns are computed but carry no probability)
+  const double fl = alg_flops > 0.0 ? alg_flops : 2.0 * M * N * K;
   (void)cls;
   return m->run(gemm_class(a_t, b_t, epi), fl, 0.0, [&] { return launch_gemm(g, a_t, b_t, epi, m->stream); });
 }
 
 // weight gradient dW[M][N] (=|+=) sum_t A[t][m] * X[t][n] (fp32)
-hipError_t weight_grad(Model* m, int M, int N, const bf16_t* dy, const bf16_t* x, float* dW, int accumulate) {
+hipError_t weight_grad(Model* m, int M, int N, const bf16_t* dy, const bf16_t* x, float* dW, int accumulate,
+                       int m_real = 0) {
   const int BT = (int)m->d.BT;
+  const double fl = 2.0 * (m_real ? m_real : M) * (double)N * BT;
   int s = dw_splits(m->d, M, N);
   if (s <= 1)
     return gemm(m, GPT2_K_GEMM_DW, M, N, BT, dy, M, 1, x, N, 1, EPI_F32, dW, N, nullptr, nullptr, nullptr, nullptr,
-                accumulate, 1, 0);
+                accumulate, 1, 0, 0, fl);
   float* part = m->wsf(m->ws.splitk);
   hipError_t e = gemm(m, GPT2_K_GEMM_DW, M, N, BT, dy, M, 1, x, N, 1, EPI_F32, part, N, nullptr, nullptr, nullptr,
-                      nullptr, 0, s, (long)M * N, dw_chunk(m->d, M, N));
+                      nullptr, 0, s, (long)M * N, dw_chunk(m->d, M, N), fl);
   if (e != hipSuccess) return e;
   return m->run(GPT2_K_OTHER, 0.0, 4.0 * (double)M * N * (s + 1 + accumulate),
                 [&] { return launch_reduce_slices(part, s, (long)M * N, dW, accumulate, m->stream); });
@@ -592,7 +596,8 @@ gpt2_status gpt2_forward(gpt2_model* m, const int32_t* d_inputs, const int32_t* 
     if (s != GPT2_OK) return s;
   }
   TRY(ln_fwd(m, m->res(d.L), m->pf(K_LNFW), m->pf(K_LNFB), m->lnf(), m->lnfm(), m->lnfr()));
-  TRY(gemm(m, GPT2_K_GEMM_FWD, BT, d.Vp, C, m->lnf(), C, 0, m->pb(K_WTE), C, 0, EPI_BF16, m->logits(), d.Vp));
+  TRY(gemm(m, GPT2_K_GEMM_FWD, BT, d.Vp, C, m->lnf(), C, 0, m->pb(K_WTE), C, 0, EPI_BF16, m->logits(), d.Vp,
+           nullptr, nullptr, nullptr, nullptr, 0, 1, 0, 0, 2.0 * BT * (double)d.V * C));
   if (d_targets) {
     const float scale = (float)(1.0 / ((double)BT * d.accum));
     TRY(m->run(GPT2_K_CROSS_ENTROPY, 0.0, 4.0 * BT * d.Vp + 8.0 * BT, [&] {
@@ -615,8 +620,9 @@ gpt2_status gpt2_backward(gpt2_model* m, int32_t accumulate) {
   bf16_t* dh = m->wsb(m->ws.dh);
   bf16_t* dres = m->wsb(m->ws.dres);
   // tied LM head: input gradient and the head's share of the token-table gradient
-  TRY(gemm(m, GPT2_K_GEMM_DX, BT, C, d.Vp, m->logits(), d.Vp, 0, m->pb(K_WTE), C, 1, EPI_BF16, dh, C));
-  TRY(weight_grad(m, d.Vp, C, m->logits(), m->lnf(), m->gf(K_WTE), acc));
+  TRY(gemm(m, GPT2_K_GEMM_DX, BT, C, d.Vp, m->logits(), d.Vp, 0, m->pb(K_WTE), C, 1, EPI_BF16, dh, C, nullptr,
+           nullptr, nullptr, nullptr, 0, 1, 0, 0, 2.0 * BT * (double)d.V * C));
+  TRY(weight_grad(m, d.Vp, C, m->logits(), m->lnf(), m->gf(K_WTE), acc, d.V));
   TRY(ln_bwd(m, dh, m->res(d.L), m->lnfm(), m->lnfr(), m->pf(K_LNFW), 0, m->gf(K_LNFW), m->gf(K_LNFB),
              m->gf(K_FCPROJB) + (size_t)(d.L - 1) * C, acc));
   for (int l = d.L - 1; l >= 0; --l) {
