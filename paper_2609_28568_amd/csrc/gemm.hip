@@ -294,35 +294,41 @@ hipError_t launch_t(const GemmArgs& g, hipStream_t s) {
   return hipGetLastError();
 }
 
-// Tile shape per problem (see gemm_tile_shape): 256 x 192 tiles (4 waves of
-// 128 x 96) when N is a multiple of 192, which holds for every GPT-2 width
-// (768, 2304, 3072 and the padded vocabulary 50304) and makes the 16384-row
-// GEMMs fill the 256 CUs in whole rounds; 256 x 128 otherwise; 128 x 128 for
-// small problems.
-template <bool A_T, bool B_T, int EPI>
-hipError_t launch_shape(const GemmArgs& g, hipStream_t s) {
-  int bm = 0, bn = 0;
-  gemm_tile_shape(g.M, g.N, &bm, &bn);
-  // short contractions: two 2-stage blocks per CU, so one block's prologue
-  // and epilogue overlap the other's MFMAs; long ones: one 5-stage block
-  const bool short_k = g.k_chunk <= 4096;
-  if (bm == 256 && bn == 192)
-    return short_k ? launch_t<256, 192, 32, 2, A_T, B_T, EPI>(g, s) : launch_t<256, 192, 32, 5, A_T, B_T, EPI>(g, s);
-  if (bm == 256)
-    return short_k ? launch_t<256, 128, 32, 2, A_T, B_T, EPI>(g, s) : launch_t<256, 128, 32, 5, A_T, B_T, EPI>(g, s);
-  return launch_t<128, 128, 32, 2, A_T, B_T, EPI>(g, s);
+template <int BM, int BN, int BK>
+hipError_t launch_cfg(const GemmArgs& g, int a_t, int b_t, int epi, hipStream_t s) {
+  if (!a_t && !b_t && epi == EPI_BF16) return launch_t<BM, BN, BK, 2, false, false, EPI_BF16>(g, s);
+  if (!a_t && !b_t && epi == EPI_GELU) return launch_t<BM, BN, BK, 2, false, false, EPI_GELU>(g, s);
+  if (!a_t && b_t && epi == EPI_BF16) return launch_t<BM, BN, BK, 2, false, true, EPI_BF16>(g, s);
+  if (!a_t && b_t && epi == EPI_GELU_BWD) return launch_t<BM, BN, BK, 2, false, true, EPI_GELU_BWD>(g, s);
+  if (a_t && b_t && epi == EPI_F32) return launch_t<BM, BN, BK, 2, true, true, EPI_F32>(g, s);
+  return hipErrorInvalidValue;
 }
 
 }  // namespace
 
-void gemm_tile_shape(int M, int N, int* bm, int* bn) {
-  if (M >= 256 && N >= 192 && N % 192 == 0) {
-    *bm = 256; *bn = 192;
-  } else if (M >= 256 && N >= 128 && N % 128 == 0) {
-    *bm = 256; *bn = 128;
-  } else {
-    *bm = 128; *bn = 128;
+// Tile configuration per product, chosen from timings of every GPT-2 124M
+// product on the MI355X (all with two blocks per CU and a 2-stage ring):
+//   weight gradients: 192 x 192 tiles, 32-deep stages;
+//   forward MLP-up with GELU, and products with at least 8192 such tiles
+//   (the tied head): 256 x 192 x 32, whose rounds of 512 tiles fill the chip;
+//   other forward and input-gradient products: 128 x 192, 64-deep stages
+//   (32-deep when the epilogue applies the GELU derivative).
+// Widths that are not multiples of 192 (small test models) take 256 x 128 or
+// 128 x 128 tiles.
+GemmConfig gemm_config(int M, int N, int a_t, int b_t, int epi) {
+  (void)b_t;
+  if (N >= 192 && N % 192 == 0) {
+    if (a_t) {
+      if (M >= 192 && M % 192 == 0) return {192, 192, 32};
+      if (M >= 128) return {128, 192, 32};
+    } else {
+      const long tiles256 = (long)((M + 255) / 256) * (N / 192);
+      if (M >= 256 && (epi == EPI_GELU || tiles256 >= 8192)) return {256, 192, 32};
+      if (M >= 128) return {128, 192, epi == EPI_GELU_BWD ? 32 : 64};
+    }
   }
+  if (M >= 256 && N >= 128 && N % 128 == 0) return {256, 128, 32};
+  return {128, 128, 32};
 }
 
 int gemm_split_plan(int K, int want, int* k_chunk) {
@@ -352,20 +358,14 @@ hipError_t launch_gemm(const GemmArgs& g0, int a_t, int b_t, int epi, hipStream_
       return hipErrorInvalidValue;
     if (epi != EPI_F32) return hipErrorInvalidValue;
   }
-  if (!a_t && !b_t) {
-    switch (epi) {
-      case EPI_BF16: return launch_shape<false, false, EPI_BF16>(g, s);
-      case EPI_GELU: return launch_shape<false, false, EPI_GELU>(g, s);
-      default: break;
-    }
-  } else if (!a_t && b_t) {
-    switch (epi) {
-      case EPI_BF16: return launch_shape<false, true, EPI_BF16>(g, s);
-      case EPI_GELU_BWD: return launch_shape<false, true, EPI_GELU_BWD>(g, s);
-      default: break;
-    }
-  } else if (a_t && b_t) {
-    if (epi == EPI_F32) return launch_shape<true, true, EPI_F32>(g, s);
+  const GemmConfig c = gemm_config(g.M, g.N, a_t, b_t, epi);
+  if (c.bm == 192) return launch_cfg<192, 192, 32>(g, a_t, b_t, epi, s);
+  if (c.bm == 256 && c.bn == 192) return launch_cfg<256, 192, 32>(g, a_t, b_t, epi, s);
+  if (c.bm == 128 && c.bn == 192) {
+    if (c.bk == 64) return launch_cfg<128, 192, 64>(g, a_t, b_t, epi, s);
+    return launch_cfg<128, 192, 32>(g, a_t, b_t, epi, s);
   }
-  return hipErrorInvalidValue;
+  if (c.bm == 256) return launch_cfg<256, 128, 32>(g, a_t, b_t, epi, s);
+  return launch_cfg<128, 128, 32>(g, a_t, b_t, epi, s);
 }
+

@@ -77,9 +77,8 @@ const bool kDecay[K_NKIND] = {true, true, false, false, true, false, true, false
 // contraction splits for a weight-gradient GEMM with an M x N output
 // output tiles of the weight-gradient GEMM (the tile shape gemm.hip picks)
 long dw_tiles(int M, int N) {
-  int bm = 0, bn = 0;
-  gemm_tile_shape(M, N, &bm, &bn);
-  return (long)((M + bm - 1) / bm) * ((N + bn - 1) / bn);
+  const GemmConfig c = gemm_config(M, N, 1, 1, EPI_F32);
+  return (long)((M + c.bm - 1) / c.bm) * ((N + c.bn - 1) / c.bn);
 }
 
 // Split the token contraction of a weight gradient when its tiles alone

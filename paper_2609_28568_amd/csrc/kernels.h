@@ -32,8 +32,10 @@ struct GemmArgs {
   int k_chunk;             // contraction length per split (from gemm_split_plan)
 };
 
-// Output tile (bm x bn) the GEMM uses for an M x N product.
-void gemm_tile_shape(int M, int N, int* bm, int* bn);
+// Block tile (bm x bn, contraction depth bk per stage) the GEMM uses for an
+// M x N product with the given operand orientation and epilogue.
+struct GemmConfig { int bm, bn, bk; };
+GemmConfig gemm_config(int M, int N, int a_t, int b_t, int epi);
 // Plan a contraction split of K into about `want` pieces: writes the chunk
 // length (a multiple of the 64-wide k tile) and returns the split count.
 int gemm_split_plan(int K, int want, int* k_chunk);
