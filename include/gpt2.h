@@ -58,7 +58,10 @@ typedef enum gpt2_status {
  *   n_layer >= 1; d_model % n_head == 0; head_dim in {16, 32, 64, 128};
  *   d_model and d_ff multiples of 64; vocab_padded >= vocab, a multiple of 64
  *   and <= 65536; 1 <= T <= max_seq_len; B >= 1; grad_accum >= 1;
- *   warmup_steps >= 1; total_steps > warmup_steps; 0 <= beta < 1. */
+ *   warmup_steps >= 1; total_steps > warmup_steps; 0 <= beta < 1;
+ *   (B*T + 256) * max(vocab_padded, 3*d_model, d_ff) * 2 < 2^32, since the
+ *   kernels address each token-major bf16 operand with 32-bit byte offsets
+ *   (at vocab_padded 50304 that is B*T <= 42436). */
 typedef struct gpt2_config {
   int32_t n_layer, n_head, d_model, d_ff;
   int32_t vocab, vocab_padded, max_seq_len;

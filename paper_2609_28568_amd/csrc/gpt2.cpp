@@ -8,6 +8,7 @@
 #include <cstdio>
 #include <cstring>
 #include <new>
+#include <algorithm>
 #include <string>
 #include <vector>
 
@@ -51,6 +52,13 @@ const char* validate(const gpt2_config* c) {
   if (c->max_seq_len < 1 || c->T < 1 || c->T > c->max_seq_len) return "need 1 <= T <= max_seq_len";
   if (c->B < 1) return "B must be >= 1";
   if ((long)c->B * c->T > (1L << 26)) return "B*T too large";
+  {
+    // kernels address each [B*T, width] operand (plus up to 256 rows of tile
+    // overhang) with 32-bit byte offsets
+    const long wide = std::max({(long)c->vocab_padded, 3L * c->d_model, (long)c->d_ff});
+    if (((long)c->B * c->T + 256) * wide * 2 >= (1L << 32))
+      return "B*T too large: a [B*T, max(vocab_padded, 3*d_model, d_ff)] bf16 operand must stay below 4 GiB";
+  }
   if (c->grad_accum < 1) return "grad_accum must be >= 1";
   if (!(c->ln_eps > 0.0f)) return "ln_eps must be > 0";
   if (c->warmup_steps < 1 || c->total_steps <= c->warmup_steps) return "need 1 <= warmup_steps < total_steps";

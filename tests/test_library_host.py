@@ -60,6 +60,8 @@ def test_paper_parameter_count_through_the_abi():
 @pytest.mark.parametrize("over", [
     dict(n_head=5), dict(d_model=96, n_head=2), dict(vocab_padded=500), dict(vocab=600),
     dict(T=64, max_seq_len=32), dict(B=0), dict(d_ff=100), dict(vocab_padded=70000, vocab=512),
+    # 42,496 tokens x 50,304 padded vocabulary: the logits exceed 32-bit offsets
+    dict(B=83, T=512, max_seq_len=512, vocab=50257, vocab_padded=50304),
 ])
 def test_invalid_configs_are_rejected(over):
     w = workload("tiny", **over)
