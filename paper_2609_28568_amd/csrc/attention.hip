@@ -26,6 +26,8 @@
 //            S = Q K^T, dP = dO V^T (one key per lane), dV^T += dO^T P,
 //            dK^T += Q^T dS.
 // D = rowsum(dO * O) comes from a small pre-pass.
+#include <type_traits>
+
 #include "common.h"
 #include "kernels.h"
 #include "lds_dma.h"
@@ -38,6 +40,10 @@ typedef LDS_AS v4f32 lds_v4f32_t;
 constexpr int BQ = 128;     // rows owned by one workgroup (4 waves x 32)
 constexpr float LOG2E = 1.4426950408889634f;
 constexpr float LN2 = 0.6931471805599453f;
+
+// 2^x with the bare hardware instruction: softmax arguments are <= 0 and
+// results below 2^-126 are negligible against the row maximum's 1
+DEV float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
 DEV int bitrev3(int x) { return ((x & 1) << 2) | (x & 2) | ((x >> 2) & 1); }
 DEV int bitrev4(int x) { return ((x & 1) << 3) | ((x & 2) << 1) | ((x >> 1) & 2) | ((x >> 3) & 1); }
@@ -128,7 +134,9 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(AttnArgs a) {
   const int T = a.T, H = a.H, C = H * HD, ld = 3 * C;
   const int bh = blockIdx.y, b = bh / H, h = bh % H;
   const int qb = gridDim.x - 1 - blockIdx.x;   // heaviest blocks first
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // the wave index is uniform across the wave: say so, so that per-wave
+  // conditions compile to scalar branches
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int lq = lane & 31, g = lane >> 5;
   const int q0w = qb * BQ + wave * 32;
   const int q = q0w + lq;
@@ -172,29 +180,32 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(AttnArgs a) {
 #pragma unroll
       for (int k = 0; k < S::KS; ++k) s[t] = mfma32(read_row<HD>(Ks, 32 * t + lq, 2 * k + g), qf[k], s[t]);
     }
+    // only tiles that straddle the diagonal or the sequence end are masked
     const bool diag = kv0 + TILE - 1 > q0w || kv0 + TILE > T;
     float mt = -INFINITY;
+    auto scale_mask = [&](auto masked) {
+      const int jmax = min(q, T - 1) - kv0 - 4 * g;   // key j = kv0 + 4g + offset is kept if offset <= jmax
 #pragma unroll
-    for (int t = 0; t < 2; ++t)
+      for (int t = 0; t < 2; ++t)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        float x = s[t][r] * sc;
-        if (diag) {
-          const int j = kv0 + 32 * t + acc_row(r, g);
-          x = (j <= q && j < T) ? x : -INFINITY;
+        for (int r = 0; r < 16; ++r) {
+          float x = s[t][r] * sc;
+          if constexpr (decltype(masked)::value) x = (32 * t + acc_row(r, 0) <= jmax) ? x : -INFINITY;
+          s[t][r] = x;
+          mt = fmaxf(mt, x);
         }
-        s[t][r] = x;
-        mt = fmaxf(mt, x);
-      }
+    };
+    if (diag) scale_mask(std::true_type{});
+    else scale_mask(std::false_type{});
     mt = fmaxf(mt, __shfl_xor(mt, 32, WAVE));
     const float m_new = fmaxf(m_run, mt);
-    const float alpha = exp2f(m_run - m_new);
+    const float alpha = fast_exp2(m_run - m_new);
     float rsum = 0.0f;
 #pragma unroll
     for (int t = 0; t < 2; ++t)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const float p = exp2f(s[t][r] - m_new);
+        const float p = fast_exp2(s[t][r] - m_new);
         s[t][r] = p;
         rsum += p;
       }
@@ -265,7 +276,9 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_kernel(AttnArgs a) {
   const int T = a.T, H = a.H, C = H * HD, ld = 3 * C;
   const int bh = blockIdx.y, b = bh / H, h = bh % H;
   const int kb = blockIdx.x;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // the wave index is uniform across the wave: say so, so that per-wave
+  // conditions compile to scalar branches
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int lk = lane & 31, g = lane >> 5;
   const int kv0w = kb * BQ + wave * 32;
   const int kv = kv0w + lk;
@@ -339,17 +352,20 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_kernel(AttnArgs a) {
         const v4f32 d4 = *reinterpret_cast<const lds_v4f32_t*>(lr + 256 + 4 * qi);
         const float lv[4] = {l4.x * LOG2E, l4.y * LOG2E, l4.z * LOG2E, l4.w * LOG2E};
         const float dvv[4] = {d4.x, d4.y, d4.z, d4.w};
+        auto probs = [&](auto masked) {
+          // query qq = q0 + qi + e sees key kv if kv <= qq < T (and kv < T)
+          const int qlo = kv - q0 - qi, qhi = T - q0 - qi;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int r = 4 * c4 + e;
-          float pv = exp2f(p[t][r] * sc - lv[e]);
-          if (diag) {
-            const int qq = q0 + qi + e;
-            pv = (kv <= qq && qq < T && kv < T) ? pv : 0.0f;
+          for (int e = 0; e < 4; ++e) {
+            const int r = 4 * c4 + e;
+            float pv = fast_exp2(p[t][r] * sc - lv[e]);
+            if constexpr (decltype(masked)::value) pv = (e >= qlo && e < qhi && kv < T) ? pv : 0.0f;
+            p[t][r] = pv;
+            ds[t][r] = pv * (ds[t][r] - dvv[e]);
           }
-          p[t][r] = pv;
-          ds[t][r] = pv * (ds[t][r] - dvv[e]);
-        }
+        };
+        if (diag) probs(std::true_type{});
+        else probs(std::false_type{});
       }
     }
 #pragma unroll
@@ -392,7 +408,9 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_kernel(AttnArgs a) {
   const int T = a.T, H = a.H, C = H * HD, ld = 3 * C;
   const int bh = blockIdx.y, b = bh / H, h = bh % H;
   const int qb = gridDim.x - 1 - blockIdx.x;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // the wave index is uniform across the wave: say so, so that per-wave
+  // conditions compile to scalar branches
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int lq = lane & 31, g = lane >> 5;
   const int q0w = qb * BQ + wave * 32;
   const int q = q0w + lq;
@@ -447,15 +465,18 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_kernel(AttnArgs a) {
         p[t] = mfma32(read_row<HD>(Ks, 32 * t + lq, 2 * k + g), qf[k], p[t]);
         ds[t] = mfma32(read_row<HD>(Vs, 32 * t + lq, 2 * k + g), df[k], ds[t]);
       }
+      auto probs = [&](auto masked) {
+        // key j = kv0 + 32t + 4g + offset is seen if j <= q, j < T, and q < T
+        const int jmax = (q < T ? min(q, T - 1) : -1) - kv0 - 32 * t - 4 * g;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        float pv = exp2f(p[t][r] * sc - lse2);
-        if (diag) {
-          const int j = kv0 + 32 * t + acc_row(r, g);
-          pv = (j <= q && j < T && q < T) ? pv : 0.0f;
+        for (int r = 0; r < 16; ++r) {
+          float pv = fast_exp2(p[t][r] * sc - lse2);
+          if constexpr (decltype(masked)::value) pv = (acc_row(r, 0) <= jmax) ? pv : 0.0f;
+          ds[t][r] = pv * (ds[t][r] - dsum);
         }
-        ds[t][r] = pv * (ds[t][r] - dsum);
-      }
+      };
+      if (diag) probs(std::true_type{});
+      else probs(std::false_type{});
     }
 #pragma unroll
     for (int t = 0; t < 2; ++t)
