@@ -31,6 +31,8 @@
 // column index j to m. The epilogue goes through LDS so that every output row
 // segment of a wave is written (and any residual or pre-activation read) as
 // one contiguous run instead of 16-byte pieces of 32 rows.
+#include <type_traits>
+
 #include "common.h"
 #include "kernels.h"
 #include "lds_dma.h"
@@ -40,6 +42,12 @@ namespace {
 typedef float v4f32_t __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) v4f32_t lds_v4f32_t;
 typedef __attribute__((address_space(3))) float lds_f32_t;
+
+// Epilogues of the kernel: the four of GemmEpilogue, plus the two variants
+// that read global memory (residual add; fp32 accumulation), kept separate so
+// the others do not reserve registers for those reads.
+constexpr int EPI_BF16_RES = 4;
+constexpr int EPI_F32_ACC = 5;
 
 DEV int bitrev3(int x) { return ((x & 1) << 2) | (x & 2) | ((x >> 2) & 1); }
 
@@ -218,17 +226,56 @@ __global__ __launch_bounds__(256, (NS <= 2 ? 2 : 1)) void gemm_kernel(GemmArgs g
   }
 
   // ---------------------------------------------------------------- epilogue
-  // every wave is done with the ring before it is reused for staging
-  block_barrier();
-  lds_f32_t* ep = (lds_f32_t*)smem_raw + wave * 32 * EP_LD;
-  const int lrow = lane & 31, lg = lane >> 5;
+  // Each wave writes its tile 32 rows at a time: accumulators go to LDS, come
+  // back as whole row segments, and are stored with the bias, residual,
+  // GELU, GELU derivative or fp32 accumulation applied. Every global read an
+  // output block needs (residual, pre-activation, previous fp32 value) is
+  // issued before its LDS round trip, so its latency is paid once per block
+  // of 32 rows instead of once per chunk.
   constexpr int CPR = WTN / 4;                 // 4-column chunks per row
   constexpr int CHUNKS = 32 * CPR / 64;        // chunks per lane per 32-row block
   static_assert((32 * CPR) % 64 == 0, "epilogue chunking");
+  // a lane's chunk cc sits at column ((lane + 64 cc) % CPR) * 4, which takes
+  // NB = CPR / gcd(64, CPR) distinct values, repeating with period NB in cc
+  constexpr int G64 = (CPR % 64 == 0) ? 64 : (CPR % 32 == 0) ? 32 : (CPR % 16 == 0) ? 16 : (CPR % 8 == 0) ? 8
+                    : (CPR % 4 == 0) ? 4 : (CPR % 2 == 0) ? 2 : 1;
+  constexpr int NB = CPR / G64;
+  const int lrow = lane & 31, lg = lane >> 5;
   float* Cf = static_cast<float*>(g.C) + (size_t)split * g.split_stride;
   bf16_t* Cb = static_cast<bf16_t*>(g.C);
+  const int ncol0 = n0 + wn * WTN;
+  float4 bias4[NB];
+  if constexpr (EPI == EPI_BF16 || EPI == EPI_BF16_RES || EPI == EPI_GELU) {
+#pragma unroll
+    for (int q = 0; q < NB; ++q) {
+      const int n = ncol0 + ((lane + 64 * q) % CPR) * 4;
+      bias4[q] = (g.bias && n < g.N) ? *reinterpret_cast<const float4*>(g.bias + n) : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+  }
+
+  // every wave is done with the ring before it is reused for staging
+  block_barrier();
+  lds_f32_t* ep = (lds_f32_t*)smem_raw + wave * 32 * EP_LD;
+  constexpr int CG = 4;   // chunks per group read back from LDS together
+  static_assert(CHUNKS % CG == 0, "epilogue groups");
+  // bf16 inputs of a chunk (residual or pre-activation) are read for the
+  // whole 32-row block before its LDS round trip; fp32 values to accumulate
+  // onto, four times larger, a group at a time
+  constexpr bool RD16 = EPI == EPI_BF16_RES || EPI == EPI_GELU_BWD;
+  const bf16_t* rd_src = EPI == EPI_GELU_BWD ? g.aux : g.residual;
 #pragma unroll
   for (int i = 0; i < TM; ++i) {
+    const int mrow0 = m0 + wm * WTM + i * 32;
+    uint2 rd[RD16 ? CHUNKS : 1];
+    if constexpr (RD16) {
+#pragma unroll
+      for (int cc = 0; cc < CHUNKS; ++cc) {
+        const int idx = lane + 64 * cc;
+        const int m = mrow0 + idx / CPR, n = ncol0 + (idx % CPR) * 4;
+        rd[cc] = (m < g.M && n < g.N) ? *reinterpret_cast<const uint2*>(rd_src + (size_t)m * g.ldc + n)
+                                      : make_uint2(0, 0);
+      }
+    }
     // lane holds, for row lrow of this 32-row block, columns
     // 32j + 8q + 4*lg .. +3 of the wave's WTN columns
 #pragma unroll
@@ -241,43 +288,50 @@ __global__ __launch_bounds__(256, (NS <= 2 ? 2 : 1)) void gemm_kernel(GemmArgs g
       }
     __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0): this wave's LDS writes are done
     __builtin_amdgcn_wave_barrier();
+    // read back row segments a group at a time, apply and store
 #pragma unroll
-    for (int cc = 0; cc < CHUNKS; ++cc) {
-      const int idx = lane + 64 * cc;
-      const int row = idx / CPR, c4 = (idx % CPR) * 4;
-      const v4f32_t v = *reinterpret_cast<const lds_v4f32_t*>(ep + row * EP_LD + c4);
-      const int m = m0 + wm * WTM + i * 32 + row;
-      const int n = n0 + wn * WTN + c4;
-      if (m >= g.M || n >= g.N) continue;
-      float v0 = v.x, v1 = v.y, v2 = v.z, v3 = v.w;
-      const size_t off = (size_t)m * g.ldc + n;
-      if constexpr (EPI == EPI_F32) {
-        float4* p = reinterpret_cast<float4*>(Cf + off);
-        if (g.accumulate) {
-          const float4 o = *p;
-          v0 += o.x; v1 += o.y; v2 += o.z; v3 += o.w;
+    for (int c0 = 0; c0 < CHUNKS; c0 += CG) {
+      v4f32_t vals[CG];
+      float4 prev[EPI == EPI_F32_ACC ? CG : 1];
+#pragma unroll
+      for (int c = 0; c < CG; ++c) {
+        const int idx = lane + 64 * (c0 + c);
+        if constexpr (EPI == EPI_F32_ACC) {
+          const int m = mrow0 + idx / CPR, n = ncol0 + (idx % CPR) * 4;
+          prev[c] = (m < g.M && n < g.N) ? *reinterpret_cast<const float4*>(Cf + (size_t)m * g.ldc + n)
+                                         : make_float4(0.f, 0.f, 0.f, 0.f);
         }
-        *p = make_float4(v0, v1, v2, v3);
-      } else if constexpr (EPI == EPI_GELU_BWD) {
-        const uint2 u = *reinterpret_cast<const uint2*>(g.aux + off);
-        v0 *= gelu_tanh_grad(lo_f(u.x)); v1 *= gelu_tanh_grad(hi_f(u.x));
-        v2 *= gelu_tanh_grad(lo_f(u.y)); v3 *= gelu_tanh_grad(hi_f(u.y));
-        *reinterpret_cast<uint2*>(Cb + off) = make_uint2(pack2(v0, v1), pack2(v2, v3));
-      } else {
-        if (g.bias) {
-          const float4 b = *reinterpret_cast<const float4*>(g.bias + n);
-          v0 += b.x; v1 += b.y; v2 += b.z; v3 += b.w;
-        }
-        if constexpr (EPI == EPI_GELU) {
-          *reinterpret_cast<uint2*>(Cb + off) = make_uint2(pack2(v0, v1), pack2(v2, v3));
-          *reinterpret_cast<uint2*>(g.C2 + off) =
-              make_uint2(pack2(gelu_tanh(v0), gelu_tanh(v1)), pack2(gelu_tanh(v2), gelu_tanh(v3)));
-        } else {
-          if (g.residual) {
-            const uint2 r = *reinterpret_cast<const uint2*>(g.residual + off);
-            v0 += lo_f(r.x); v1 += hi_f(r.x); v2 += lo_f(r.y); v3 += hi_f(r.y);
+        vals[c] = *reinterpret_cast<const lds_v4f32_t*>(ep + (idx / CPR) * EP_LD + (idx % CPR) * 4);
+      }
+#pragma unroll
+      for (int c = 0; c < CG; ++c) {
+        const int cc = c0 + c, idx = lane + 64 * cc;
+        const int m = mrow0 + idx / CPR, n = ncol0 + (idx % CPR) * 4;
+        if (m >= g.M || n >= g.N) continue;
+        float v0 = vals[c].x, v1 = vals[c].y, v2 = vals[c].z, v3 = vals[c].w;
+        const size_t off = (size_t)m * g.ldc + n;
+        if constexpr (EPI == EPI_F32 || EPI == EPI_F32_ACC) {
+          if constexpr (EPI == EPI_F32_ACC) {
+            v0 += prev[c].x; v1 += prev[c].y; v2 += prev[c].z; v3 += prev[c].w;
           }
+          *reinterpret_cast<float4*>(Cf + off) = make_float4(v0, v1, v2, v3);
+        } else if constexpr (EPI == EPI_GELU_BWD) {
+          v0 *= gelu_tanh_grad(lo_f(rd[cc].x)); v1 *= gelu_tanh_grad(hi_f(rd[cc].x));
+          v2 *= gelu_tanh_grad(lo_f(rd[cc].y)); v3 *= gelu_tanh_grad(hi_f(rd[cc].y));
           *reinterpret_cast<uint2*>(Cb + off) = make_uint2(pack2(v0, v1), pack2(v2, v3));
+        } else {
+          const float4 bb = bias4[cc % NB];
+          v0 += bb.x; v1 += bb.y; v2 += bb.z; v3 += bb.w;
+          if constexpr (EPI == EPI_GELU) {
+            *reinterpret_cast<uint2*>(Cb + off) = make_uint2(pack2(v0, v1), pack2(v2, v3));
+            *reinterpret_cast<uint2*>(g.C2 + off) =
+                make_uint2(pack2(gelu_tanh(v0), gelu_tanh(v1)), pack2(gelu_tanh(v2), gelu_tanh(v3)));
+          } else {
+            if constexpr (EPI == EPI_BF16_RES) {
+              v0 += lo_f(rd[cc].x); v1 += hi_f(rd[cc].x); v2 += lo_f(rd[cc].y); v3 += hi_f(rd[cc].y);
+            }
+            *reinterpret_cast<uint2*>(Cb + off) = make_uint2(pack2(v0, v1), pack2(v2, v3));
+          }
         }
       }
     }
@@ -296,11 +350,17 @@ hipError_t launch_t(const GemmArgs& g, hipStream_t s) {
 
 template <int BM, int BN, int BK>
 hipError_t launch_cfg(const GemmArgs& g, int a_t, int b_t, int epi, hipStream_t s) {
-  if (!a_t && !b_t && epi == EPI_BF16) return launch_t<BM, BN, BK, 2, false, false, EPI_BF16>(g, s);
+  if (!a_t && !b_t && epi == EPI_BF16)
+    return g.residual ? launch_t<BM, BN, BK, 2, false, false, EPI_BF16_RES>(g, s)
+                      : launch_t<BM, BN, BK, 2, false, false, EPI_BF16>(g, s);
   if (!a_t && !b_t && epi == EPI_GELU) return launch_t<BM, BN, BK, 2, false, false, EPI_GELU>(g, s);
-  if (!a_t && b_t && epi == EPI_BF16) return launch_t<BM, BN, BK, 2, false, true, EPI_BF16>(g, s);
+  if (!a_t && b_t && epi == EPI_BF16)
+    return g.residual ? launch_t<BM, BN, BK, 2, false, true, EPI_BF16_RES>(g, s)
+                      : launch_t<BM, BN, BK, 2, false, true, EPI_BF16>(g, s);
   if (!a_t && b_t && epi == EPI_GELU_BWD) return launch_t<BM, BN, BK, 2, false, true, EPI_GELU_BWD>(g, s);
-  if (a_t && b_t && epi == EPI_F32) return launch_t<BM, BN, BK, 2, true, true, EPI_F32>(g, s);
+  if (a_t && b_t && epi == EPI_F32)
+    return g.accumulate ? launch_t<BM, BN, BK, 2, true, true, EPI_F32_ACC>(g, s)
+                        : launch_t<BM, BN, BK, 2, true, true, EPI_F32>(g, s);
   return hipErrorInvalidValue;
 }
 
