@@ -117,19 +117,74 @@ __global__ void embed_fwd_kernel(const int32_t* __restrict__ ids, const float* _
   *reinterpret_cast<uint2*>(x + i) = make_uint2(pack2(a.x + p.x, a.y + p.y), pack2(a.z + p.z, a.w + p.w));
 }
 
-// token table: scatter-add of each position's gradient into its id's row
-__global__ void embed_bwd_wte_kernel(const int32_t* __restrict__ ids, const bf16_t* __restrict__ dx,
-                                     float* __restrict__ dwte, int BT, int C) {
-  long i = ((long)blockIdx.x * blockDim.x + threadIdx.x) * 4;
-  if (i >= (long)BT * C) return;
-  const int row = i / C, c = i % C;
-  const int id = ids[row];
-  uint2 u = *reinterpret_cast<const uint2*>(dx + i);
-  float* d = dwte + (size_t)id * C + c;
-  atomicAdd(d + 0, lo_f(u.x));
-  atomicAdd(d + 1, hi_f(u.x));
-  atomicAdd(d + 2, lo_f(u.y));
-  atomicAdd(d + 3, hi_f(u.y));
+// token table: scatter-add of each position's gradient into its id's row.
+// A workgroup takes EMB_P consecutive positions and one 256-column slice of
+// the row; it sorts the positions by (id, position) in LDS, and each wave
+// walks 64 of the sorted positions, summing runs of equal ids in registers
+// and adding each run once with fp32 atomics. Frequent ids (the token
+// distribution is Zipf-like) then cost one atomic per workgroup instead of
+// one per occurrence.
+constexpr int EMB_P = 256;
+__global__ __launch_bounds__(256) void embed_bwd_wte_kernel(const int32_t* __restrict__ ids,
+                                                            const bf16_t* __restrict__ dx, float* __restrict__ dwte,
+                                                            int BT, int C) {
+  __shared__ unsigned long long key[EMB_P];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int p0 = blockIdx.x * EMB_P;
+  const int c = blockIdx.y * 256 + 4 * lane;
+  {
+    const int p = p0 + tid;
+    key[tid] = p < BT ? ((unsigned long long)(uint32_t)ids[p] << 32) | (uint32_t)p : ~0ull;
+  }
+  __syncthreads();
+  // bitonic sort of the EMB_P keys, one per thread
+  for (int k = 2; k <= EMB_P; k <<= 1)
+    for (int j = k >> 1; j > 0; j >>= 1) {
+      const int x = tid ^ j;
+      if (x > tid) {
+        const unsigned long long a = key[tid], b = key[x];
+        const bool up = (tid & k) == 0;
+        if ((a > b) == up) {
+          key[tid] = b;
+          key[x] = a;
+        }
+      }
+      __syncthreads();
+    }
+  const bool col_ok = c < C;
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+  constexpr int BATCH = 8;
+  for (int k0 = 0; k0 < 64; k0 += BATCH) {
+    unsigned long long kk[BATCH];
+    uint2 u[BATCH];
+#pragma unroll
+    for (int q = 0; q < BATCH; ++q) {
+      kk[q] = key[64 * w + k0 + q];
+      u[q] = make_uint2(0, 0);
+      if (kk[q] != ~0ull && col_ok) {
+        const uint32_t pos = (uint32_t)kk[q];
+        u[q] = *reinterpret_cast<const uint2*>(dx + (size_t)pos * C + c);
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < BATCH; ++q) {
+      if (kk[q] == ~0ull) continue;
+      acc.x += lo_f(u[q].x); acc.y += hi_f(u[q].x); acc.z += lo_f(u[q].y); acc.w += hi_f(u[q].y);
+      const int kn = k0 + q + 1;
+      const unsigned long long nxt = kn < 64 ? key[64 * w + kn] : ~0ull;
+      const uint32_t id = (uint32_t)(kk[q] >> 32);
+      if ((uint32_t)(nxt >> 32) != id || nxt == ~0ull) {
+        if (col_ok) {
+          float* d = dwte + (size_t)id * C + c;
+          atomicAdd(d + 0, acc.x);
+          atomicAdd(d + 1, acc.y);
+          atomicAdd(d + 2, acc.z);
+          atomicAdd(d + 3, acc.w);
+        }
+        acc = make_float4(0.f, 0.f, 0.f, 0.f);
+      }
+    }
+  }
 }
 
 // position table: dwpe[t] = sum over the batch, in batch order; rows t >= T
@@ -152,61 +207,90 @@ __global__ void embed_bwd_wpe_kernel(const bf16_t* __restrict__ dx, float* __res
 // ------------------------------------------------------------ cross-entropy
 
 // One workgroup per row; the row (Vp bf16) is held in registers as 16-byte
-// chunks, so it is read once and written once.
+// chunks, so it is read once and written once. Workgroups are small enough
+// (a few hundred threads) that several rows are in flight per CU, so one
+// row's loads overlap another's stores. Each thread first finds its own
+// maximum and its sum of exponentials relative to it; the pairs are then
+// combined across the workgroup in one pass: M = max m_i, S = sum s_i
+// exp(m_i - M).
 template <int NT, int MAXCH>
 __global__ __launch_bounds__(NT) void cross_entropy_kernel(bf16_t* __restrict__ logits,
                                                            const int32_t* __restrict__ targets,
                                                            float* __restrict__ losses, int V, int Vp,
                                                            float grad_scale) {
-  __shared__ float sh[NT / 64];
+  constexpr int NW = NT / 64;
+  __shared__ float shm[NW], shs[NW];
   __shared__ float xt;
-  const int row = blockIdx.x;
+  const int row = blockIdx.x, tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   bf16_t* lr = logits + (size_t)row * Vp;
   const int tgt = targets[row];
-  if (threadIdx.x == 0) xt = bf2f(lr[tgt]);
+  if (tid == 0) xt = bf2f(lr[tgt]);
   const int nch = Vp / 8;
   uint4 v[MAXCH];
-  float mx = -INFINITY;
 #pragma unroll
   for (int i = 0; i < MAXCH; ++i) {
-    int c = threadIdx.x + NT * i;
-    if (c < nch) {
-      v[i] = *reinterpret_cast<const uint4*>(lr + c * 8);
-      const uint32_t w[4] = {v[i].x, v[i].y, v[i].z, v[i].w};
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        float f = (e & 1) ? hi_f(w[e >> 1]) : lo_f(w[e >> 1]);
-        if (c * 8 + e < V) mx = fmaxf(mx, f);
-      }
-    }
+    const int c = tid + NT * i;
+    v[i] = c < nch ? *reinterpret_cast<const uint4*>(lr + c * 8) : make_uint4(0, 0, 0, 0);
   }
-  mx = block_max<NT>(mx, sh);
+  // element j of chunk c counts if j < V (the padding columns carry no
+  // probability)
+  auto elem = [&](const uint4& q, int e) {
+    const uint32_t wd = e < 2 ? q.x : e < 4 ? q.y : e < 6 ? q.z : q.w;
+    return (e & 1) ? hi_f(wd) : lo_f(wd);
+  };
+  float m = -INFINITY;
+#pragma unroll
+  for (int i = 0; i < MAXCH; ++i) {
+    const int c = tid + NT * i;
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+      if (c * 8 + e < V) m = fmaxf(m, elem(v[i], e));
+  }
+  // the packed row is all that stays live between passes (otherwise the
+  // compiler keeps every unpacked fp32 value in registers)
+  auto opaque = [&]() {
+#pragma unroll
+    for (int i = 0; i < MAXCH; ++i) asm volatile("" : "+v"(v[i].x), "+v"(v[i].y), "+v"(v[i].z), "+v"(v[i].w));
+  };
+  opaque();
   float se = 0.0f;
 #pragma unroll
   for (int i = 0; i < MAXCH; ++i) {
-    int c = threadIdx.x + NT * i;
-    if (c < nch) {
-      const uint32_t w[4] = {v[i].x, v[i].y, v[i].z, v[i].w};
+    const int c = tid + NT * i;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        float f = (e & 1) ? hi_f(w[e >> 1]) : lo_f(w[e >> 1]);
-        if (c * 8 + e < V) se += __expf(f - mx);
-      }
-    }
+    for (int e = 0; e < 8; ++e)
+      if (c * 8 + e < V) se += __expf(elem(v[i], e) - m);
   }
-  se = block_sum<NT>(se, sh);
-  const float inv = 1.0f / se;
+  opaque();
+  // combine (m, se) over the wave, then over the waves
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) {
+    const float m2 = __shfl_xor(m, o, WAVE), s2 = __shfl_xor(se, o, WAVE);
+    const float mn = fmaxf(m, m2);
+    se = (m == -INFINITY ? 0.0f : se * __expf(m - mn)) + (m2 == -INFINITY ? 0.0f : s2 * __expf(m2 - mn));
+    m = mn;
+  }
+  if (lane == 0) {
+    shm[w] = m;
+    shs[w] = se;
+  }
+  __syncthreads();
+  float mx = shm[0];
+#pragma unroll
+  for (int k = 1; k < NW; ++k) mx = fmaxf(mx, shm[k]);
+  float sum = 0.0f;
+#pragma unroll
+  for (int k = 0; k < NW; ++k) sum += shm[k] == -INFINITY ? 0.0f : shs[k] * __expf(shm[k] - mx);
+  const float inv = 1.0f / sum;
 #pragma unroll
   for (int i = 0; i < MAXCH; ++i) {
-    int c = threadIdx.x + NT * i;
+    const int c = tid + NT * i;
     if (c < nch) {
-      const uint32_t w[4] = {v[i].x, v[i].y, v[i].z, v[i].w};
       float d[8];
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        int j = c * 8 + e;
-        float f = (e & 1) ? hi_f(w[e >> 1]) : lo_f(w[e >> 1]);
-        float p = j < V ? __expf(f - mx) * inv : 0.0f;
+        const int j = c * 8 + e;
+        float p = j < V ? __expf(elem(v[i], e) - mx) * inv : 0.0f;
         if (j == tgt) p -= 1.0f;
         d[e] = p * grad_scale;
       }
@@ -214,7 +298,7 @@ __global__ __launch_bounds__(NT) void cross_entropy_kernel(bf16_t* __restrict__ 
           make_uint4(pack2(d[0], d[1]), pack2(d[2], d[3]), pack2(d[4], d[5]), pack2(d[6], d[7]));
     }
   }
-  if (threadIdx.x == 0) losses[row] = mx + logf(se) - xt;
+  if (tid == 0) losses[row] = mx + logf(sum) - xt;
 }
 
 // ------------------------------------------------------------ casts
@@ -328,8 +412,10 @@ hipError_t launch_embed_fwd(const int32_t* ids, const float* wte, const float* w
 
 hipError_t launch_embed_bwd(const int32_t* ids, const bf16_t* dx, float* dwte, int B, int T, int C,
                             hipStream_t s) {
-  long n4 = (long)B * T * C / 4;
-  hipLaunchKernelGGL(embed_bwd_wte_kernel, dim3(blocks_for(n4, 256)), dim3(256), 0, s, ids, dx, dwte, B * T, C);
+  if (C % 4) return hipErrorInvalidValue;
+  const int BT = B * T;
+  dim3 grid((BT + EMB_P - 1) / EMB_P, (C + 255) / 256);
+  hipLaunchKernelGGL(embed_bwd_wte_kernel, grid, dim3(256), 0, s, ids, dx, dwte, BT, C);
   return hipGetLastError();
 }
 
@@ -344,9 +430,12 @@ hipError_t launch_embed_bwd_pos(const bf16_t* dx, float* dwpe, int B, int T, int
 hipError_t launch_cross_entropy(bf16_t* logits, const int32_t* targets, float* losses, int rows, int V, int Vp,
                                 float grad_scale, hipStream_t s) {
   if (Vp % 8) return hipErrorInvalidValue;
-  int nch = Vp / 8;
+  const int nch = Vp / 8;
   if (nch <= 256 * 2) {
     hipLaunchKernelGGL((cross_entropy_kernel<256, 2>), dim3(rows), dim3(256), 0, s, logits, targets, losses, V, Vp,
+                       grad_scale);
+  } else if (nch <= 512 * 13) {
+    hipLaunchKernelGGL((cross_entropy_kernel<512, 13>), dim3(rows), dim3(512), 0, s, logits, targets, losses, V, Vp,
                        grad_scale);
   } else if (nch <= 1024 * 8) {
     hipLaunchKernelGGL((cross_entropy_kernel<1024, 8>), dim3(rows), dim3(1024), 0, s, logits, targets, losses, V, Vp,
