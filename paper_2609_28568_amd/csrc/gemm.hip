@@ -262,20 +262,32 @@ __global__ __launch_bounds__(256, (NS <= 2 ? 2 : 1)) void gemm_kernel(GemmArgs g
   // whole 32-row block before its LDS round trip; fp32 values to accumulate
   // onto, four times larger, a group at a time
   constexpr bool RD16 = EPI == EPI_BF16_RES || EPI == EPI_GELU_BWD;
+  // with at most two 32-row blocks per wave the bf16 inputs of the whole tile
+  // are read up front; otherwise block by block
+  constexpr int RD_AHEAD = TM <= 2 ? TM : 1;
   const bf16_t* rd_src = EPI == EPI_GELU_BWD ? g.aux : g.residual;
+  uint2 rd_all[RD16 ? TM : 1][RD16 ? CHUNKS : 1];
+  auto read_block = [&](int i) {
+    const int mrow0 = m0 + wm * WTM + i * 32;
+#pragma unroll
+    for (int cc = 0; cc < CHUNKS; ++cc) {
+      const int idx = lane + 64 * cc;
+      const int m = mrow0 + idx / CPR, n = ncol0 + (idx % CPR) * 4;
+      rd_all[i][cc] = (m < g.M && n < g.N) ? *reinterpret_cast<const uint2*>(rd_src + (size_t)m * g.ldc + n)
+                                           : make_uint2(0, 0);
+    }
+  };
+  if constexpr (RD16) {
+#pragma unroll
+    for (int i = 0; i < RD_AHEAD; ++i) read_block(i);
+  }
 #pragma unroll
   for (int i = 0; i < TM; ++i) {
     const int mrow0 = m0 + wm * WTM + i * 32;
-    uint2 rd[RD16 ? CHUNKS : 1];
     if constexpr (RD16) {
-#pragma unroll
-      for (int cc = 0; cc < CHUNKS; ++cc) {
-        const int idx = lane + 64 * cc;
-        const int m = mrow0 + idx / CPR, n = ncol0 + (idx % CPR) * 4;
-        rd[cc] = (m < g.M && n < g.N) ? *reinterpret_cast<const uint2*>(rd_src + (size_t)m * g.ldc + n)
-                                      : make_uint2(0, 0);
-      }
+      if (i >= RD_AHEAD) read_block(i);
     }
+    uint2 (&rd)[RD16 ? CHUNKS : 1] = rd_all[RD16 ? i : 0];
     // lane holds, for row lrow of this 32-row block, columns
     // 32j + 8q + 4*lg .. +3 of the wave's WTN columns
 #pragma unroll
@@ -288,6 +300,9 @@ __global__ __launch_bounds__(256, (NS <= 2 ? 2 : 1)) void gemm_kernel(GemmArgs g
       }
     __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0): this wave's LDS writes are done
     __builtin_amdgcn_wave_barrier();
+    // the bias and bf16 inputs read above have landed: one explicit wait here
+    // (otherwise the compiler waits before every store that follows a read)
+    if (i == 0 || (RD16 && i >= RD_AHEAD)) wait_vmcnt<0>();
     // read back row segments a group at a time, apply and store
 #pragma unroll
     for (int c0 = 0; c0 < CHUNKS; c0 += CG) {
