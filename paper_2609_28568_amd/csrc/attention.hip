@@ -345,14 +345,22 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_kernel(AttnArgs a) {
         p[t] = mfma32(read_row<HD>(Qs, 32 * t + lk, 2 * k + g), kf[k], p[t]);
         ds[t] = mfma32(read_row<HD>(Ds, 32 * t + lk, 2 * k + g), vf[k], ds[t]);
       }
+    }
+    // probabilities and their score gradients for the whole tile, masked only
+    // on tiles that straddle the diagonal or the sequence end
+    auto probs = [&](auto masked) {
 #pragma unroll
-      for (int c4 = 0; c4 < 4; ++c4) {
-        const int qi = 32 * t + 8 * c4 + 4 * g;   // 4 consecutive queries
-        const v4f32 l4 = *reinterpret_cast<const lds_v4f32_t*>(lr + 4 * qi);
-        const v4f32 d4 = *reinterpret_cast<const lds_v4f32_t*>(lr + 256 + 4 * qi);
-        const float lv[4] = {l4.x * LOG2E, l4.y * LOG2E, l4.z * LOG2E, l4.w * LOG2E};
-        const float dvv[4] = {d4.x, d4.y, d4.z, d4.w};
-        auto probs = [&](auto masked) {
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int c4 = 0; c4 < 4; ++c4) {
+          // keep the per-group reads of lse and D next to their use (hoisting
+          // them all would run out of registers)
+          __builtin_amdgcn_sched_barrier(0);
+          const int qi = 32 * t + 8 * c4 + 4 * g;   // 4 consecutive queries
+          const v4f32 l4 = *reinterpret_cast<const lds_v4f32_t*>(lr + 4 * qi);
+          const v4f32 d4 = *reinterpret_cast<const lds_v4f32_t*>(lr + 256 + 4 * qi);
+          const float lv[4] = {l4.x * LOG2E, l4.y * LOG2E, l4.z * LOG2E, l4.w * LOG2E};
+          const float dvv[4] = {d4.x, d4.y, d4.z, d4.w};
           // query qq = q0 + qi + e sees key kv if kv <= qq < T (and kv < T)
           const int qlo = kv - q0 - qi, qhi = T - q0 - qi;
 #pragma unroll
@@ -363,11 +371,10 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_kernel(AttnArgs a) {
             p[t][r] = pv;
             ds[t][r] = pv * (ds[t][r] - dvv[e]);
           }
-        };
-        if (diag) probs(std::true_type{});
-        else probs(std::false_type{});
-      }
-    }
+        }
+    };
+    if (diag) probs(std::true_type{});
+    else probs(std::false_type{});
 #pragma unroll
     for (int t = 0; t < 2; ++t)
 #pragma unroll
