@@ -133,7 +133,7 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="gpt2_124m")
-    ap.add_argument("--probe", default="gemm_fwd", help="kernel class timed for the roofline entry")
+    ap.add_argument("--probe", default="gemm_dw", help="kernel class timed for the roofline entry")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--classes", action="store_true", help="also report every kernel class (extra pass)")
     ap.add_argument("--calibration-copy", action="store_true",
