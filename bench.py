@@ -203,6 +203,19 @@ def main():
     print(f"bench: timed {args.steps} steps, wall {wall:.3f} s, events {gpu_ms / 1e3:.3f} s, loss {loss:.4f}",
           file=sys.stderr, flush=True)
 
+    # forward-only evaluation of the same batch (held-out loss path)
+    ev_ids, ev_tgt = dev[0]
+    for _ in range(2):
+        m.evaluate(ev_ids, ev_tgt)
+    n_eval = 10
+    t_ev = time.perf_counter()
+    for _ in range(n_eval):
+        m.evaluate(ev_ids, ev_tgt)
+    ev_ms = (time.perf_counter() - t_ev) * 1e3 / n_eval
+    eval_out = {"tokens_per_s": round(w["B"] * w["T"] / (ev_ms * 1e-3), 1), "ms_per_pass": round(ev_ms, 3),
+                "passes": n_eval, "note": "forward only, one block's activations kept, no dlogits; each pass "
+                                          "synchronises to return its loss"}
+
     tokens = w["B"] * w["T"] * w.get("grad_accum", 1)
     ms_step = wall * 1e3 / args.steps
     tok_s = tokens / (wall / args.steps)
@@ -273,6 +286,7 @@ def main():
         "final_loss": round(loss, 4),
         "roofline": roofline,
         "cpu_baseline": cpu,
+        "eval": eval_out,
     }
     if extra:
         out["classes"] = extra

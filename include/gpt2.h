@@ -142,6 +142,19 @@ gpt2_status gpt2_adamw_step(gpt2_model* m, int64_t step, float* lr_out,
  * Synchronises the stream. */
 gpt2_status gpt2_loss(gpt2_model* m, float* loss_out);
 
+/* Forward-only evaluation of held-out tokens (the held-out loss of section
+ * "Batch geometry" and the evaluation cadence of "Method"): the same forward
+ * as gpt2_forward, with the same kernels and the same per-token losses, but
+ * keeping one block's activations at a time and not writing dlogits.
+ * d_inputs, d_targets: int32 [B*T] as for gpt2_forward (targets required).
+ * *loss_out (host) receives the mean loss; d_token_losses (device fp32
+ * [B*T], optional) the per-token losses. It reuses the activation buffer, so
+ * a following gpt2_backward needs a new gpt2_forward first (GPT2_ERR_STATE
+ * otherwise); gradients and optimiser state are untouched. Synchronises the
+ * stream. */
+gpt2_status gpt2_evaluate(gpt2_model* m, const int32_t* d_inputs, const int32_t* d_targets, float* loss_out,
+                          float* d_token_losses);
+
 /* Learning rate at a 0-based step: lr_max*(step+1)/warmup for step < warmup,
  * then lr_min + (lr_max-lr_min)*(1+cos(pi*f))/2 with f the fraction of the
  * remaining steps elapsed, clamped to [0,1]. Pure function. */

@@ -76,6 +76,7 @@ def lib():
         "gpt2_backward": (I32, [P, I32]),
         "gpt2_adamw_step": (I32, [P, I64, ctypes.POINTER(F32), P]),
         "gpt2_loss": (I32, [P, ctypes.POINTER(F32)]),
+        "gpt2_evaluate": (I32, [P, P, P, ctypes.POINTER(F32), P]),
         "gpt2_lr_at": (F32, [cfgp, I64]),
         "gpt2_destroy": (None, [P]),
         "gpt2_last_error": (ctypes.c_char_p, [P]),
@@ -246,6 +247,18 @@ class GPT2:
     def loss(self) -> float:
         out = ctypes.c_float()
         _check(self.L.gpt2_loss(self.handle, ctypes.byref(out)), self.handle)
+        return out.value
+
+    def evaluate(self, ids, targets, token_losses=None) -> float:
+        """Forward-only loss of held-out tokens (no activations kept, no
+        dlogits); optionally fills a device fp32 [B*T] tensor of per-token
+        losses."""
+        ids = ids.to(self.device, self.torch.int32).contiguous()
+        tgt = targets.to(self.device, self.torch.int32).contiguous()
+        out = ctypes.c_float()
+        tl = ctypes.c_void_p(token_losses.data_ptr()) if token_losses is not None else ctypes.c_void_p(0)
+        _check(self.L.gpt2_evaluate(self.handle, ctypes.c_void_p(ids.data_ptr()), ctypes.c_void_p(tgt.data_ptr()),
+                                    ctypes.byref(out), tl), self.handle)
         return out.value
 
     def lr_at(self, step: int) -> float:

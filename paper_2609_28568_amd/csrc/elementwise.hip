@@ -213,7 +213,7 @@ __global__ void embed_bwd_wpe_kernel(const bf16_t* __restrict__ dx, float* __res
 // maximum and its sum of exponentials relative to it; the pairs are then
 // combined across the workgroup in one pass: M = max m_i, S = sum s_i
 // exp(m_i - M).
-template <int NT, int MAXCH>
+template <int NT, int MAXCH, bool GRAD>
 __global__ __launch_bounds__(NT) void cross_entropy_kernel(bf16_t* __restrict__ logits,
                                                            const int32_t* __restrict__ targets,
                                                            float* __restrict__ losses, int V, int Vp,
@@ -285,7 +285,7 @@ __global__ __launch_bounds__(NT) void cross_entropy_kernel(bf16_t* __restrict__ 
 #pragma unroll
   for (int i = 0; i < MAXCH; ++i) {
     const int c = tid + NT * i;
-    if (c < nch) {
+    if (GRAD && c < nch) {
       float d[8];
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
@@ -427,22 +427,25 @@ hipError_t launch_embed_bwd_pos(const bf16_t* dx, float* dwpe, int B, int T, int
   return hipGetLastError();
 }
 
+template <int NT, int MAXCH>
+void ce_launch(bf16_t* logits, const int32_t* targets, float* losses, int rows, int V, int Vp, float grad_scale,
+               int write_grad, hipStream_t s) {
+  if (write_grad)
+    hipLaunchKernelGGL((cross_entropy_kernel<NT, MAXCH, true>), dim3(rows), dim3(NT), 0, s, logits, targets, losses, V,
+                       Vp, grad_scale);
+  else
+    hipLaunchKernelGGL((cross_entropy_kernel<NT, MAXCH, false>), dim3(rows), dim3(NT), 0, s, logits, targets, losses,
+                       V, Vp, grad_scale);
+}
+
 hipError_t launch_cross_entropy(bf16_t* logits, const int32_t* targets, float* losses, int rows, int V, int Vp,
-                                float grad_scale, hipStream_t s) {
+                                float grad_scale, int write_grad, hipStream_t s) {
   if (Vp % 8) return hipErrorInvalidValue;
   const int nch = Vp / 8;
-  if (nch <= 256 * 2) {
-    hipLaunchKernelGGL((cross_entropy_kernel<256, 2>), dim3(rows), dim3(256), 0, s, logits, targets, losses, V, Vp,
-                       grad_scale);
-  } else if (nch <= 512 * 13) {
-    hipLaunchKernelGGL((cross_entropy_kernel<512, 13>), dim3(rows), dim3(512), 0, s, logits, targets, losses, V, Vp,
-                       grad_scale);
-  } else if (nch <= 1024 * 8) {
-    hipLaunchKernelGGL((cross_entropy_kernel<1024, 8>), dim3(rows), dim3(1024), 0, s, logits, targets, losses, V, Vp,
-                       grad_scale);
-  } else {
-    return hipErrorInvalidValue;
-  }
+  if (nch <= 256 * 2) ce_launch<256, 2>(logits, targets, losses, rows, V, Vp, grad_scale, write_grad, s);
+  else if (nch <= 512 * 13) ce_launch<512, 13>(logits, targets, losses, rows, V, Vp, grad_scale, write_grad, s);
+  else if (nch <= 1024 * 8) ce_launch<1024, 8>(logits, targets, losses, rows, V, Vp, grad_scale, write_grad, s);
+  else return hipErrorInvalidValue;
   return hipGetLastError();
 }
 

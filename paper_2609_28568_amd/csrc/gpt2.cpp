@@ -362,10 +362,10 @@ hipError_t ln_bwd(Model* m, const bf16_t* dy, const bf16_t* x, const float* mean
   });
 }
 
-AttnArgs attn_args(Model* m, int l) {
+AttnArgs attn_args(Model* m, int slot) {
   AttnArgs a{};
   a.B = m->d.B; a.T = m->d.T; a.H = m->d.H; a.hd = m->d.hd;
-  a.qkv = m->qkv(l); a.out = m->att(l); a.lse = m->lse(l);
+  a.qkv = m->qkv(slot); a.out = m->att(slot); a.lse = m->lse(slot);
   a.dout = m->wsb(m->ws.datt); a.dsum = m->wsf(m->ws.dsum); a.dqkv = m->wsb(m->ws.dbig);
   return a;
 }
@@ -375,22 +375,26 @@ double attn_fwd_flops(const Dims& d) {
   return 4.0 * d.B * d.H * d.hd * ((double)d.T * (d.T + 1) / 2.0);
 }
 
-gpt2_status block_fwd(Model* m, int l) {
+// Forward of block l (its weights) from residual slot `in` to slot `out`,
+// keeping the block's activations in activation slot `a`. Training uses
+// in = a = l, out = l + 1 (everything kept for the backward); evaluation
+// reuses slot 0 and two residual slots.
+gpt2_status block_fwd(Model* m, int l, int in, int out, int a) {
   const Dims& d = m->d;
   const int BT = (int)d.BT, C = d.C, F = d.F;
   const size_t oC = (size_t)l * C, o3C = (size_t)l * 3 * C, oF = (size_t)l * F;
-  TRY(ln_fwd(m, m->res(l), m->pf(K_LN1W) + oC, m->pf(K_LN1B) + oC, m->ln1(l), m->ln1m(l), m->ln1r(l)));
-  TRY(gemm(m, GPT2_K_GEMM_FWD, BT, 3 * C, C, m->ln1(l), C, 0, m->pb(K_QKVW) + o3C * C, C, 0, EPI_BF16, m->qkv(l),
+  TRY(ln_fwd(m, m->res(in), m->pf(K_LN1W) + oC, m->pf(K_LN1B) + oC, m->ln1(a), m->ln1m(a), m->ln1r(a)));
+  TRY(gemm(m, GPT2_K_GEMM_FWD, BT, 3 * C, C, m->ln1(a), C, 0, m->pb(K_QKVW) + o3C * C, C, 0, EPI_BF16, m->qkv(a),
            3 * C, m->pf(K_QKVB) + o3C));
-  AttnArgs aa = attn_args(m, l);
+  AttnArgs aa = attn_args(m, a);
   TRY(m->run(GPT2_K_ATTN_FWD, attn_fwd_flops(d), 0.0, [&] { return launch_attention_fwd(aa, m->stream); }));
-  TRY(gemm(m, GPT2_K_GEMM_FWD, BT, C, C, m->att(l), C, 0, m->pb(K_ATTPROJW) + oC * C, C, 0, EPI_BF16, m->xmid(l), C,
-           m->pf(K_ATTPROJB) + oC, m->res(l)));
-  TRY(ln_fwd(m, m->xmid(l), m->pf(K_LN2W) + oC, m->pf(K_LN2B) + oC, m->ln2(l), m->ln2m(l), m->ln2r(l)));
-  TRY(gemm(m, GPT2_K_GEMM_FWD, BT, F, C, m->ln2(l), C, 0, m->pb(K_FCW) + oF * C, C, 0, EPI_GELU, m->fc(l), F,
-           m->pf(K_FCB) + oF, nullptr, m->gelu(l)));
-  TRY(gemm(m, GPT2_K_GEMM_FWD, BT, C, F, m->gelu(l), F, 0, m->pb(K_FCPROJW) + oC * F, F, 0, EPI_BF16, m->res(l + 1),
-           C, m->pf(K_FCPROJB) + oC, m->xmid(l)));
+  TRY(gemm(m, GPT2_K_GEMM_FWD, BT, C, C, m->att(a), C, 0, m->pb(K_ATTPROJW) + oC * C, C, 0, EPI_BF16, m->xmid(a), C,
+           m->pf(K_ATTPROJB) + oC, m->res(in)));
+  TRY(ln_fwd(m, m->xmid(a), m->pf(K_LN2W) + oC, m->pf(K_LN2B) + oC, m->ln2(a), m->ln2m(a), m->ln2r(a)));
+  TRY(gemm(m, GPT2_K_GEMM_FWD, BT, F, C, m->ln2(a), C, 0, m->pb(K_FCW) + oF * C, C, 0, EPI_GELU, m->fc(a), F,
+           m->pf(K_FCB) + oF, nullptr, m->gelu(a)));
+  TRY(gemm(m, GPT2_K_GEMM_FWD, BT, C, F, m->gelu(a), F, 0, m->pb(K_FCPROJW) + oC * F, F, 0, EPI_BF16, m->res(out),
+           C, m->pf(K_FCPROJB) + oC, m->xmid(a)));
   return GPT2_OK;
 }
 
@@ -599,7 +603,7 @@ gpt2_status gpt2_forward(gpt2_model* m, const int32_t* d_inputs, const int32_t* 
   TRY(m->run(GPT2_K_OTHER, 0.0, 4.0 * BT + 8.0 * BT * C + 2.0 * BT * C,
              [&] { return launch_embed_fwd(d_inputs, m->pf(K_WTE), m->pf(K_WPE), m->res(0), d.B, d.T, C, m->stream); }));
   for (int l = 0; l < d.L; ++l) {
-    gpt2_status s = block_fwd(m, l);
+    gpt2_status s = block_fwd(m, l, l, l + 1, l);
     if (s != GPT2_OK) return s;
   }
   TRY(ln_fwd(m, m->res(d.L), m->pf(K_LNFW), m->pf(K_LNFB), m->lnf(), m->lnfm(), m->lnfr()));
@@ -608,12 +612,41 @@ gpt2_status gpt2_forward(gpt2_model* m, const int32_t* d_inputs, const int32_t* 
   if (d_targets) {
     const float scale = (float)(1.0 / ((double)BT * d.accum));
     TRY(m->run(GPT2_K_CROSS_ENTROPY, 0.0, 4.0 * BT * d.Vp + 8.0 * BT, [&] {
-      return launch_cross_entropy(m->logits(), d_targets, m->losses(), BT, d.V, d.Vp, scale, m->stream);
+      return launch_cross_entropy(m->logits(), d_targets, m->losses(), BT, d.V, d.Vp, scale, 1, m->stream);
     }));
     TRY(m->run(GPT2_K_OTHER, 0.0, 4.0 * BT, [&] { return launch_mean(m->losses(), BT, m->loss_mean(), m->stream); }));
     m->have_dlogits = true;
     m->have_loss = true;
   }
+  return GPT2_OK;
+}
+
+gpt2_status gpt2_evaluate(gpt2_model* m, const int32_t* d_inputs, const int32_t* d_targets, float* loss_out,
+                          float* d_token_losses) {
+  if (!m) return GPT2_ERR_INVALID_ARG;
+  if (!d_inputs || !d_targets || !loss_out) return m->fail(GPT2_ERR_INVALID_ARG, "inputs, targets or loss_out is NULL");
+  const Dims& d = m->d;
+  const int BT = (int)d.BT, C = d.C;
+  // the activation buffer is reused: the last training forward is gone
+  m->have_dlogits = false;
+  m->have_loss = false;
+  TRY(m->run(GPT2_K_OTHER, 0.0, 4.0 * BT + 8.0 * BT * C + 2.0 * BT * C,
+             [&] { return launch_embed_fwd(d_inputs, m->pf(K_WTE), m->pf(K_WPE), m->res(0), d.B, d.T, C, m->stream); }));
+  for (int l = 0; l < d.L; ++l) {
+    gpt2_status s = block_fwd(m, l, l & 1, (l + 1) & 1, 0);
+    if (s != GPT2_OK) return s;
+  }
+  TRY(ln_fwd(m, m->res(d.L & 1), m->pf(K_LNFW), m->pf(K_LNFB), m->lnf(), m->lnfm(), m->lnfr()));
+  TRY(gemm(m, GPT2_K_GEMM_FWD, BT, d.Vp, C, m->lnf(), C, 0, m->pb(K_WTE), C, 0, EPI_BF16, m->logits(), d.Vp,
+           nullptr, nullptr, nullptr, nullptr, 0, 1, 0, 0, 2.0 * BT * (double)d.V * C));
+  TRY(m->run(GPT2_K_CROSS_ENTROPY, 0.0, 2.0 * BT * d.Vp + 8.0 * BT, [&] {
+    return launch_cross_entropy(m->logits(), d_targets, m->losses(), BT, d.V, d.Vp, 0.0f, 0, m->stream);
+  }));
+  TRY(m->run(GPT2_K_OTHER, 0.0, 4.0 * BT, [&] { return launch_mean(m->losses(), BT, m->loss_mean(), m->stream); }));
+  if (d_token_losses)
+    TRY(hipMemcpyAsync(d_token_losses, m->losses(), (size_t)BT * 4, hipMemcpyDeviceToDevice, m->stream));
+  TRY(hipMemcpyAsync(loss_out, m->loss_mean(), sizeof(float), hipMemcpyDeviceToHost, m->stream));
+  TRY(hipStreamSynchronize(m->stream));
   return GPT2_OK;
 }
 
@@ -753,7 +786,7 @@ gpt2_status gpt2_block_forward(gpt2_model* m, int32_t layer, const void* d_x_in,
   if (!d_x_in || layer < 0 || layer >= m->d.L) return m->fail(GPT2_ERR_INVALID_ARG, "bad block_forward argument");
   const size_t bytes = (size_t)m->d.BT * m->d.C * 2;
   TRY(hipMemcpyAsync(m->res(layer), d_x_in, bytes, hipMemcpyDeviceToDevice, m->stream));
-  gpt2_status s = block_fwd(m, layer);
+  gpt2_status s = block_fwd(m, layer, layer, layer + 1, layer);
   if (s != GPT2_OK) return s;
   if (d_x_out) TRY(hipMemcpyAsync(d_x_out, m->res(layer + 1), bytes, hipMemcpyDeviceToDevice, m->stream));
   return GPT2_OK;

@@ -91,8 +91,9 @@ hipError_t launch_embed_bwd_pos(const bf16_t* dx, float* dwpe, int B, int T, int
 
 // fused softmax cross-entropy over the first V of Vp columns; dlogits
 // (scaled) overwrite the logits; losses fp32 [rows]
-hipError_t launch_cross_entropy(bf16_t* logits, const int32_t* targets, float* losses, int rows,
-                                int V, int Vp, float grad_scale, hipStream_t s);
+// write_grad: overwrite the logits with dlogits (training) or leave them
+hipError_t launch_cross_entropy(bf16_t* logits, const int32_t* targets, float* losses, int rows, int V, int Vp,
+                                float grad_scale, int write_grad, hipStream_t s);
 // mean of n floats into out[0] (single block, fixed order)
 hipError_t launch_mean(const float* x, int n, float* out, hipStream_t s);
 

@@ -125,3 +125,20 @@ def test_gpt2_124m_gradients_replicated_batch(full_setup):
             worst = max(worst, e)
             assert e < REL_L2, (k, i, e)
     print(f"  worst tensor rel_l2 {worst:.2e}")
+
+
+def test_gpt2_124m_evaluate_equals_forward(full_setup):
+    """Forward-only evaluation at full size reuses one block's activation
+    slots: its per-token losses equal the training forward's exactly."""
+    w, p, ids, tgt = full_setup
+    m = _model(w)
+    m.set_params(p)
+    m.forward(torch.from_numpy(ids), torch.from_numpy(tgt))
+    loss = m.loss()
+    ref = _np(m.activation("losses")).copy()
+    tl = torch.zeros(w["B"] * w["T"], device="cuda")
+    ev = m.evaluate(torch.from_numpy(ids), torch.from_numpy(tgt), tl)
+    got = tl.cpu().numpy()
+    m.close()
+    assert np.array_equal(got, ref)
+    assert ev == loss

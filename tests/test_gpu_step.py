@@ -177,6 +177,33 @@ def test_per_token_losses_at_their_positions():
     m.close()
 
 
+@pytest.mark.parametrize("case", list(CASES))
+def test_evaluate_equals_the_training_forward(case):
+    """The forward-only evaluation runs the same kernels on the same inputs:
+    per-token losses equal the training forward's bit for bit (so they match
+    the oracle as that forward does), and it leaves no state to backward
+    from."""
+    w = workload("tiny", **CASES[case])
+    p = synth.perturb_params(synth.init_params(w, seed=41), seed=42)
+    ids, tgt = synth.token_batch(w, seed=43)
+    m = _model(w)
+    m.set_params(p)
+    m.forward(torch.from_numpy(ids), torch.from_numpy(tgt))
+    loss = m.loss()
+    ref = _np(m.activation("losses")).copy()
+    tl = torch.zeros(w["B"] * w["T"], device="cuda")
+    ev = m.evaluate(torch.from_numpy(ids), torch.from_numpy(tgt), tl)
+    got = tl.cpu().numpy()
+    assert np.array_equal(got, ref)
+    assert ev == loss
+    cache = oracle.forward(p, ids, tgt, oracle_config(w))
+    assert abs(ev - float(cache["loss"])) < LOSS_ATOL
+    from paper_2609_28568_amd import binding
+    with pytest.raises(binding.LibError):
+        m.backward()
+    m.close()
+
+
 def test_zero_table_loss_is_ln_vocab():
     w = workload("tiny", vocab=500, vocab_padded=512)
     p = synth.init_params(w)
