@@ -169,10 +169,15 @@ def main():
     dev = [(torch.from_numpy(a).cuda(), torch.from_numpy(b).cuda()) for a, b in batches]
     torch.cuda.synchronize()
 
+    accum = w.get("grad_accum", 1)
+
     def step(i):
-        ids, tgt = dev[i % len(dev)]
-        m.forward(ids, tgt)
-        m.backward(accumulate=False)
+        # one optimizer step: grad_accum micro-batches (forward + backward
+        # accumulating into the gradients), then clip + AdamW
+        for k in range(accum):
+            ids, tgt = dev[(i * accum + k) % len(dev)]
+            m.forward(ids, tgt)
+            m.backward(accumulate=k > 0)
         m.adamw_step(i)
 
     for i in range(args.warmup):
