@@ -110,6 +110,38 @@ int dw_chunk(const Dims& d, int M, int N) {
   return kc;
 }
 
+// An unsplit weight gradient runs in rounds of 512 tiles (two workgroups per
+// CU). When its last round would be at most half full, only the whole rounds
+// (the first m_main rows) run unsplit, and the remaining rows take a
+// contraction split sized to fill the chip, reduced afterwards. Used only
+// when the remaining rows are a whole number of their own tiles, so no
+// operand read leaves the matrices.
+struct DwTail {
+  int m_main;   // rows computed unsplit (M when there is no tail split)
+  int splits;   // contraction splits of rows [m_main, M)
+  int chunk;    // tokens per split
+};
+
+DwTail dw_tail(const Dims& d, int M, int N) {
+  DwTail t{M, 1, 0};
+  constexpr long ROUND = 512;
+  const GemmConfig c = gemm_config(M, N, 1, 1, EPI_F32);
+  const long tm = (M + c.bm - 1) / c.bm, tn = (N + c.bn - 1) / c.bn, tiles = tm * tn;
+  if (tiles < ROUND || tiles % ROUND == 0 || tiles % ROUND > ROUND / 2 || ROUND % tn != 0) return t;
+  if (M % c.bm != 0 || N % c.bn != 0) return t;
+  const int m_main = (int)(tiles / ROUND * ROUND / tn) * c.bm;
+  const int m_rest = M - m_main;
+  const GemmConfig cr = gemm_config(m_rest, N, 1, 1, EPI_F32);
+  if (m_rest % cr.bm != 0 || N % cr.bn != 0) return t;
+  const long rest_tiles = (long)(m_rest / cr.bm) * (N / cr.bn);
+  int want = (int)(ROUND / rest_tiles);
+  while (want > 1 && d.BT / want < 512) --want;
+  if (want < 2) return t;
+  t.m_main = m_main;
+  t.splits = gemm_split_plan((int)d.BT, want, &t.chunk);
+  return t;
+}
+
 struct ActLayout {
   size_t residual, ln1, ln1_mean, ln1_rstd, qkv, att, lse, x_mid, ln2, ln2_mean, ln2_rstd, fc, gelu;
   size_t lnf, lnf_mean, lnf_rstd, logits, losses, loss_mean, ids, total;
@@ -163,6 +195,8 @@ WsLayout ws_layout(const Dims& d) {
   auto upd = [&](int M, int N) {
     int s = dw_splits(d, M, N);
     if (s > 1) sk = std::max(sk, (size_t)s * M * N);
+    const DwTail t = dw_tail(d, M, N);
+    if (t.splits > 1) sk = std::max(sk, (size_t)t.splits * (M - t.m_main) * N);
   };
   upd(3 * d.C, d.C); upd(d.C, d.C); upd(d.F, d.C); upd(d.C, d.F); upd(d.Vp, d.C);
   w.splitk_elems = sk;
@@ -312,11 +346,28 @@ hipError_t gemm(Model* m, int cls, int M, int N, int K, const bf16_t* A, int lda
 hipError_t weight_grad(Model* m, int M, int N, const bf16_t* dy, const bf16_t* x, float* dW, int accumulate,
                        int m_real = 0) {
   const int BT = (int)m->d.BT;
-  const double fl = 2.0 * (m_real ? m_real : M) * (double)N * BT;
+  const int mr = m_real ? m_real : M;
+  const double fl = 2.0 * mr * (double)N * BT;
   int s = dw_splits(m->d, M, N);
-  if (s <= 1)
-    return gemm(m, GPT2_K_GEMM_DW, M, N, BT, dy, M, 1, x, N, 1, EPI_F32, dW, N, nullptr, nullptr, nullptr, nullptr,
-                accumulate, 1, 0, 0, fl);
+  if (s <= 1) {
+    const DwTail t = dw_tail(m->d, M, N);
+    if (t.splits <= 1)
+      return gemm(m, GPT2_K_GEMM_DW, M, N, BT, dy, M, 1, x, N, 1, EPI_F32, dW, N, nullptr, nullptr, nullptr, nullptr,
+                  accumulate, 1, 0, 0, fl);
+    // whole rounds unsplit, the rest split over tokens and reduced
+    const int m0 = t.m_main, m1 = M - t.m_main;
+    const double fl0 = 2.0 * std::min(mr, m0) * (double)N * BT, fl1 = fl - fl0;
+    hipError_t e = gemm(m, GPT2_K_GEMM_DW, m0, N, BT, dy, M, 1, x, N, 1, EPI_F32, dW, N, nullptr, nullptr, nullptr,
+                        nullptr, accumulate, 1, 0, 0, fl0);
+    if (e != hipSuccess) return e;
+    float* part = m->wsf(m->ws.splitk);
+    e = gemm(m, GPT2_K_GEMM_DW, m1, N, BT, dy + m0, M, 1, x, N, 1, EPI_F32, part, N, nullptr, nullptr, nullptr,
+             nullptr, 0, t.splits, (long)m1 * N, t.chunk, fl1);
+    if (e != hipSuccess) return e;
+    float* dW1 = dW + (size_t)m0 * N;
+    return m->run(GPT2_K_OTHER, 0.0, 4.0 * (double)m1 * N * (t.splits + 1 + accumulate),
+                  [&] { return launch_reduce_slices(part, t.splits, (long)m1 * N, dW1, accumulate, m->stream); });
+  }
   float* part = m->wsf(m->ws.splitk);
   hipError_t e = gemm(m, GPT2_K_GEMM_DW, M, N, BT, dy, M, 1, x, N, 1, EPI_F32, part, N, nullptr, nullptr, nullptr,
                       nullptr, 0, s, (long)M * N, dw_chunk(m->d, M, N), fl);
