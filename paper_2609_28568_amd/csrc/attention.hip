@@ -132,8 +132,14 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(AttnArgs a) {
   __shared__ __attribute__((aligned(1024))) char smem_raw[2 * 2 * S::TBA];   // 2 stages x (K, V)
   lds_char_t* smem = (lds_char_t*)smem_raw;
   const int T = a.T, H = a.H, C = H * HD, ld = 3 * C;
-  const int bh = blockIdx.y, b = bh / H, h = bh % H;
-  const int qb = gridDim.x - 1 - blockIdx.x;   // heaviest blocks first
+  // 1-D grid, head fastest: every head's heaviest (last) query block is
+  // dispatched first, then the next heaviest of every head, and so on, so the
+  // causal imbalance leaves no long blocks for the end; and with B*H a
+  // multiple of 8 all blocks of a head land on one XCD (blocks are dealt to
+  // the 8 XCDs round-robin)
+  const int BH = a.B * H, nqb = (T + BQ - 1) / BQ;
+  const int bh = blockIdx.x % BH, b = bh / H, h = bh % H;
+  const int qb = nqb - 1 - (int)(blockIdx.x / BH);
   // the wave index is uniform across the wave: say so, so that per-wave
   // conditions compile to scalar branches
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -274,8 +280,11 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_kernel(AttnArgs a) {
   __shared__ __attribute__((aligned(1024))) char smem_raw[2 * STAGE];
   lds_char_t* smem = (lds_char_t*)smem_raw;
   const int T = a.T, H = a.H, C = H * HD, ld = 3 * C;
-  const int bh = blockIdx.y, b = bh / H, h = bh % H;
-  const int kb = blockIdx.x;
+  // 1-D grid, head fastest: the heaviest (first) key blocks of every head are
+  // dispatched first (see the forward kernel)
+  const int BH = a.B * H;
+  const int bh = blockIdx.x % BH, b = bh / H, h = bh % H;
+  const int kb = (int)(blockIdx.x / BH);
   // the wave index is uniform across the wave: say so, so that per-wave
   // conditions compile to scalar branches
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -413,8 +422,11 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_kernel(AttnArgs a) {
   __shared__ __attribute__((aligned(1024))) char smem_raw[2 * 2 * S::TBA];   // 2 stages x (K, V)
   lds_char_t* smem = (lds_char_t*)smem_raw;
   const int T = a.T, H = a.H, C = H * HD, ld = 3 * C;
-  const int bh = blockIdx.y, b = bh / H, h = bh % H;
-  const int qb = gridDim.x - 1 - blockIdx.x;
+  // 1-D grid, head fastest, heaviest (last) query blocks first, as in the
+  // forward pass
+  const int BH = a.B * H, nqb = (T + BQ - 1) / BQ;
+  const int bh = blockIdx.x % BH, b = bh / H, h = bh % H;
+  const int qb = nqb - 1 - (int)(blockIdx.x / BH);
   // the wave index is uniform across the wave: say so, so that per-wave
   // conditions compile to scalar branches
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -512,7 +524,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_kernel(AttnArgs a) {
 
 template <int HD>
 hipError_t fwd_t(const AttnArgs& a, hipStream_t s) {
-  dim3 grid((a.T + BQ - 1) / BQ, a.B * a.H);
+  dim3 grid(((a.T + BQ - 1) / BQ) * a.B * a.H);
   hipLaunchKernelGGL(attn_fwd_kernel<HD>, grid, dim3(256), 0, s, a);
   return hipGetLastError();
 }
@@ -523,7 +535,7 @@ hipError_t bwd_t(const AttnArgs& a, hipStream_t s) {
   hipLaunchKernelGGL(attn_dsum_kernel<HD>, dim3((n + 255) / 256), dim3(256), 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  dim3 grid((a.T + BQ - 1) / BQ, a.B * a.H);
+  dim3 grid(((a.T + BQ - 1) / BQ) * a.B * a.H);
   hipLaunchKernelGGL(attn_bwd_dkdv_kernel<HD>, grid, dim3(256), 0, s, a);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
