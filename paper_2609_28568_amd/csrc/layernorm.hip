@@ -82,20 +82,43 @@ __global__ __launch_bounds__(256) void ln_bwd_kernel(const bf16_t* __restrict__ 
       wr[i][0] = wv.x; wr[i][1] = wv.y; wr[i][2] = wv.z; wr[i][3] = wv.w;
     }
   }
-  for (int row = blockIdx.x * 4 + wave; row < rows; row += gridDim.x * 4) {
-    const float mean = mean_in[row], rstd = rstd_in[row];
+  // Rows are software-pipelined: the next row's inputs (x, dy, the residual
+  // gradient, mean, rstd) are loaded while the current row is reduced and
+  // written, so each row costs one memory round trip, not two.
+  uint2 xu[MAXCH], du[MAXCH], ru[MAXCH];
+  float mean = 0.0f, rstd = 0.0f;
+  auto load_row = [&](int row, uint2 (&xl)[MAXCH], uint2 (&dl)[MAXCH], uint2 (&rl)[MAXCH], float& ml, float& sl) {
+    ml = mean_in[row];
+    sl = rstd_in[row];
     const bf16_t* xr = x + (size_t)row * C;
     const bf16_t* dr = dy + (size_t)row * C;
+    const bf16_t* rr = dres + (size_t)row * C;
+#pragma unroll
+    for (int i = 0; i < MAXCH; ++i) {
+      const int c = 4 * (lane + 64 * i);
+      xl[i] = dl[i] = rl[i] = make_uint2(0, 0);
+      if (c < C) {
+        xl[i] = *reinterpret_cast<const uint2*>(xr + c);
+        dl[i] = *reinterpret_cast<const uint2*>(dr + c);
+        if (has_res) rl[i] = *reinterpret_cast<const uint2*>(rr + c);
+      }
+    }
+  };
+  const int stride = gridDim.x * 4;
+  int row = blockIdx.x * 4 + wave;
+  if (row < rows) load_row(row, xu, du, ru, mean, rstd);
+  for (; row < rows; row += stride) {
+    uint2 xn[MAXCH], dn[MAXCH], rn[MAXCH];
+    float mean_n = 0.0f, rstd_n = 0.0f;
+    if (row + stride < rows) load_row(row + stride, xn, dn, rn, mean_n, rstd_n);
     float xh[MAXCH][4], gg[MAXCH][4];
     float s1 = 0.0f, s2 = 0.0f;
 #pragma unroll
     for (int i = 0; i < MAXCH; ++i) {
       int c = 4 * (lane + 64 * i);
       if (c < C) {
-        uint2 xu = *reinterpret_cast<const uint2*>(xr + c);
-        uint2 du = *reinterpret_cast<const uint2*>(dr + c);
-        float xv[4] = {lo_f(xu.x), hi_f(xu.x), lo_f(xu.y), hi_f(xu.y)};
-        float dv[4] = {lo_f(du.x), hi_f(du.x), lo_f(du.y), hi_f(du.y)};
+        float xv[4] = {lo_f(xu[i].x), hi_f(xu[i].x), lo_f(xu[i].y), hi_f(xu[i].y)};
+        float dv[4] = {lo_f(du[i].x), hi_f(du[i].x), lo_f(du[i].y), hi_f(du[i].y)};
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           xh[i][e] = (xv[e] - mean) * rstd;
@@ -117,8 +140,7 @@ __global__ __launch_bounds__(256) void ln_bwd_kernel(const bf16_t* __restrict__ 
 #pragma unroll
         for (int e = 0; e < 4; ++e) o[e] = rstd * (gg[i][e] - gm - xh[i][e] * gxm);
         if (has_res) {
-          uint2 ru = *reinterpret_cast<const uint2*>(rr + c);
-          o[0] += lo_f(ru.x); o[1] += hi_f(ru.x); o[2] += lo_f(ru.y); o[3] += hi_f(ru.y);
+          o[0] += lo_f(ru[i].x); o[1] += hi_f(ru[i].x); o[2] += lo_f(ru[i].y); o[3] += hi_f(ru[i].y);
         }
         const uint2 ou = make_uint2(pack2(o[0], o[1]), pack2(o[2], o[3]));
         *reinterpret_cast<uint2*>(rr + c) = ou;
@@ -126,6 +148,14 @@ __global__ __launch_bounds__(256) void ln_bwd_kernel(const bf16_t* __restrict__ 
         ar[i][0] += lo_f(ou.x); ar[i][1] += hi_f(ou.x); ar[i][2] += lo_f(ou.y); ar[i][3] += hi_f(ou.y);
       }
     }
+#pragma unroll
+    for (int i = 0; i < MAXCH; ++i) {
+      xu[i] = xn[i];
+      du[i] = dn[i];
+      ru[i] = rn[i];
+    }
+    mean = mean_n;
+    rstd = rstd_n;
   }
   // combine the four waves' partial sums in a fixed order; the block's row of
   // partials is [dw | db | column sum of the residual gradient], 3*C floats
@@ -175,11 +205,13 @@ hipError_t launch_layernorm_fwd(const bf16_t* x, const float* w, const float* b,
   return hipErrorInvalidValue;
 }
 
-// 4 rows per wave, 4 waves per block: enough blocks to fill the chip, each
-// writing one row of partial sums
+// At least 4 rows per wave, 4 waves per block, each block writing one row of
+// partial sums; at most 768 blocks, three per CU, which is what the
+// backward's registers (two rows' inputs in flight per wave) let stay
+// resident at once
 int layernorm_bwd_blocks(int rows) {
   int n = (rows + 15) / 16;
-  return n < 1024 ? (n < 1 ? 1 : n) : 1024;
+  return n < 768 ? (n < 1 ? 1 : n) : 768;
 }
 
 hipError_t launch_layernorm_bwd(const bf16_t* dy, const bf16_t* x, const float* mean, const float* rstd,
