@@ -17,23 +17,34 @@ __global__ __launch_bounds__(256) void ln_fwd_kernel(const bf16_t* __restrict__ 
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (row >= rows) return;
   const bf16_t* xr = x + (size_t)row * C;
+  // Every lane issues all its loads at once: chunks past C read the row's
+  // last chunk (an in-range address) and are masked out of the arithmetic,
+  // so no load waits behind a branch.
+  uint2 xu[MAXCH];
+  float4 wv[MAXCH], bv[MAXCH];
+#pragma unroll
+  for (int i = 0; i < MAXCH; ++i) {
+    const int c = min(4 * (lane + 64 * i), C - 4);
+    xu[i] = *reinterpret_cast<const uint2*>(xr + c);
+    wv[i] = *reinterpret_cast<const float4*>(w + c);
+    bv[i] = *reinterpret_cast<const float4*>(b + c);
+  }
   float v[MAXCH][4];
   float s = 0.0f;
 #pragma unroll
   for (int i = 0; i < MAXCH; ++i) {
-    int c = 4 * (lane + 64 * i);
-    if (c < C) {
-      uint2 u = *reinterpret_cast<const uint2*>(xr + c);
-      v[i][0] = lo_f(u.x); v[i][1] = hi_f(u.x); v[i][2] = lo_f(u.y); v[i][3] = hi_f(u.y);
-      s += v[i][0] + v[i][1] + v[i][2] + v[i][3];
-    }
+    const bool in = 4 * (lane + 64 * i) < C;
+    v[i][0] = in ? lo_f(xu[i].x) : 0.0f;
+    v[i][1] = in ? hi_f(xu[i].x) : 0.0f;
+    v[i][2] = in ? lo_f(xu[i].y) : 0.0f;
+    v[i][3] = in ? hi_f(xu[i].y) : 0.0f;
+    s += v[i][0] + v[i][1] + v[i][2] + v[i][3];
   }
   const float mean = wave_sum(s) / C;
   float q = 0.0f;
 #pragma unroll
   for (int i = 0; i < MAXCH; ++i) {
-    int c = 4 * (lane + 64 * i);
-    if (c < C)
+    if (4 * (lane + 64 * i) < C)
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         float d = v[i][e] - mean;
@@ -46,12 +57,10 @@ __global__ __launch_bounds__(256) void ln_fwd_kernel(const bf16_t* __restrict__ 
   for (int i = 0; i < MAXCH; ++i) {
     int c = 4 * (lane + 64 * i);
     if (c < C) {
-      float4 wv = *reinterpret_cast<const float4*>(w + c);
-      float4 bv = *reinterpret_cast<const float4*>(b + c);
-      float o0 = (v[i][0] - mean) * rstd * wv.x + bv.x;
-      float o1 = (v[i][1] - mean) * rstd * wv.y + bv.y;
-      float o2 = (v[i][2] - mean) * rstd * wv.z + bv.z;
-      float o3 = (v[i][3] - mean) * rstd * wv.w + bv.w;
+      float o0 = (v[i][0] - mean) * rstd * wv[i].x + bv[i].x;
+      float o1 = (v[i][1] - mean) * rstd * wv[i].y + bv[i].y;
+      float o2 = (v[i][2] - mean) * rstd * wv[i].z + bv[i].z;
+      float o3 = (v[i][3] - mean) * rstd * wv[i].w + bv[i].w;
       *reinterpret_cast<uint2*>(yr + c) = make_uint2(pack2(o0, o1), pack2(o2, o3));
     }
   }
@@ -74,13 +83,12 @@ __global__ __launch_bounds__(256) void ln_bwd_kernel(const bf16_t* __restrict__ 
   float aw[MAXCH][4], ab[MAXCH][4], ar[MAXCH][4], wr[MAXCH][4];
 #pragma unroll
   for (int i = 0; i < MAXCH; ++i) {
-    int c = 4 * (lane + 64 * i);
+    // chunks past C read an in-range address; their values are never used
+    const int c = min(4 * (lane + 64 * i), C - 4);
 #pragma unroll
     for (int e = 0; e < 4; ++e) aw[i][e] = ab[i][e] = ar[i][e] = 0.0f;
-    if (c < C) {
-      float4 wv = *reinterpret_cast<const float4*>(w + c);
-      wr[i][0] = wv.x; wr[i][1] = wv.y; wr[i][2] = wv.z; wr[i][3] = wv.w;
-    }
+    const float4 wv = *reinterpret_cast<const float4*>(w + c);
+    wr[i][0] = wv.x; wr[i][1] = wv.y; wr[i][2] = wv.z; wr[i][3] = wv.w;
   }
   // Rows are software-pipelined: the next row's inputs (x, dy, the residual
   // gradient, mean, rstd) are loaded while the current row is reduced and
@@ -93,15 +101,14 @@ __global__ __launch_bounds__(256) void ln_bwd_kernel(const bf16_t* __restrict__ 
     const bf16_t* xr = x + (size_t)row * C;
     const bf16_t* dr = dy + (size_t)row * C;
     const bf16_t* rr = dres + (size_t)row * C;
+    // all loads issued at once (no branch per chunk): chunks past C read the
+    // row's last chunk and are never used
 #pragma unroll
     for (int i = 0; i < MAXCH; ++i) {
-      const int c = 4 * (lane + 64 * i);
-      xl[i] = dl[i] = rl[i] = make_uint2(0, 0);
-      if (c < C) {
-        xl[i] = *reinterpret_cast<const uint2*>(xr + c);
-        dl[i] = *reinterpret_cast<const uint2*>(dr + c);
-        if (has_res) rl[i] = *reinterpret_cast<const uint2*>(rr + c);
-      }
+      const int c = min(4 * (lane + 64 * i), C - 4);
+      xl[i] = *reinterpret_cast<const uint2*>(xr + c);
+      dl[i] = *reinterpret_cast<const uint2*>(dr + c);
+      rl[i] = has_res ? *reinterpret_cast<const uint2*>(rr + c) : make_uint2(0, 0);
     }
   };
   const int stride = gridDim.x * 4;
