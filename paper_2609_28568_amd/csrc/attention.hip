@@ -21,11 +21,11 @@
 //            (one query per lane, so the running max and sum are lane-local up
 //            to an exchange with lane^32), O^T += V^T P^T.
 //   dQ:      per 128 queries, walk key tiles: recompute P^T, dP^T = V dO^T,
-//            dS^T = P^T (dP^T - D), dQ^T += K^T dS^T.
+//            dS^T = P^T (dP^T - D), dQ^T += K^T dS^T. D = rowsum(dO * O) is
+//            computed here from the query's dO and O rows and stored.
 //   dK, dV:  per 128 keys (4 waves x 32), walk query tiles from the diagonal:
 //            S = Q K^T, dP = dO V^T (one key per lane), dV^T += dO^T P,
-//            dK^T += Q^T dS.
-// D = rowsum(dO * O) comes from a small pre-pass.
+//            dK^T += Q^T dS; runs after dQ, reading the stored D.
 #include <type_traits>
 
 #include "common.h"
@@ -251,26 +251,6 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(AttnArgs a) {
 // ------------------------------------------------------------------ backward
 
 // D[b,h,t] = sum_d dO * O, one thread per (token, head)
-template <int HD>
-__global__ void attn_dsum_kernel(AttnArgs a) {
-  const int C = a.H * HD;
-  const long idx = (long)blockIdx.x * blockDim.x + threadIdx.x;
-  if (idx >= (long)a.B * a.T * a.H) return;
-  const int h = idx % a.H;
-  const long tok = idx / a.H;
-  const int b = tok / a.T, t = tok % a.T;
-  const bf16_t* o = a.out + tok * C + h * HD;
-  const bf16_t* d = a.dout + tok * C + h * HD;
-  float acc = 0.0f;
-#pragma unroll
-  for (int i = 0; i < HD; i += 8) {
-    uint4 x = *reinterpret_cast<const uint4*>(o + i), y = *reinterpret_cast<const uint4*>(d + i);
-    acc += lo_f(x.x) * lo_f(y.x) + hi_f(x.x) * hi_f(y.x) + lo_f(x.y) * lo_f(y.y) + hi_f(x.y) * hi_f(y.y);
-    acc += lo_f(x.z) * lo_f(y.z) + hi_f(x.z) * hi_f(y.z) + lo_f(x.w) * lo_f(y.w) + hi_f(x.w) * hi_f(y.w);
-  }
-  a.dsum[((size_t)b * a.H + h) * a.T + t] = acc;
-}
-
 // dK, dV for 128 keys (4 waves x 32), walking query tiles of 64 from the
 // diagonal to the end.
 template <int HD>
@@ -437,19 +417,27 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_kernel(AttnArgs a) {
   const bf16_t* dob = a.dout + (size_t)b * T * C + h * HD;
   const v4i32 rs = make_rsrc(a.qkv, (uint32_t)((size_t)a.B * T * ld * 2));
 
+  const bf16_t* ob = a.out + (size_t)b * T * C + h * HD;
   bf16x8 qf[S::KS], df[S::KS];
+  float dpart = 0.0f;
 #pragma unroll
   for (int s = 0; s < S::KS; ++s) {
-    uint4 q4 = make_uint4(0, 0, 0, 0), d4 = make_uint4(0, 0, 0, 0);
+    uint4 q4 = make_uint4(0, 0, 0, 0), d4 = make_uint4(0, 0, 0, 0), o4 = make_uint4(0, 0, 0, 0);
     if (q < T) {
       q4 = *reinterpret_cast<const uint4*>(base + (size_t)q * ld + 16 * s + 8 * g);
       d4 = *reinterpret_cast<const uint4*>(dob + (size_t)q * C + 16 * s + 8 * g);
+      o4 = *reinterpret_cast<const uint4*>(ob + (size_t)q * C + 16 * s + 8 * g);
     }
     qf[s] = as_bf16x8(q4);
     df[s] = as_bf16x8(d4);
+    dpart += lo_f(d4.x) * lo_f(o4.x) + hi_f(d4.x) * hi_f(o4.x) + lo_f(d4.y) * lo_f(o4.y) + hi_f(d4.y) * hi_f(o4.y);
+    dpart += lo_f(d4.z) * lo_f(o4.z) + hi_f(d4.z) * hi_f(o4.z) + lo_f(d4.w) * lo_f(o4.w) + hi_f(d4.w) * hi_f(o4.w);
   }
   const float lse2 = q < T ? a.lse[(size_t)bh * T + q] * LOG2E : 0.0f;
-  const float dsum = q < T ? a.dsum[(size_t)bh * T + q] : 0.0f;
+  // D = rowsum(dO * O) of query q: lanes lq and lq + 32 hold the two halves of
+  // its row. Stored for the dK/dV kernel, which runs after this one.
+  const float dsum = dpart + __shfl_xor(dpart, 32);
+  if (g == 0 && q < T) a.dsum[(size_t)bh * T + q] = dsum;
   floatx16 dq[S::DT];
 #pragma unroll
   for (int d = 0; d < S::DT; ++d) zero(dq[d]);
@@ -531,15 +519,12 @@ hipError_t fwd_t(const AttnArgs& a, hipStream_t s) {
 
 template <int HD>
 hipError_t bwd_t(const AttnArgs& a, hipStream_t s) {
-  long n = (long)a.B * a.T * a.H;
-  hipLaunchKernelGGL(attn_dsum_kernel<HD>, dim3((n + 255) / 256), dim3(256), 0, s, a);
+  // dQ first: it also computes D = rowsum(dO * O), which dK/dV reads
+  dim3 grid(((a.T + BQ - 1) / BQ) * a.B * a.H);
+  hipLaunchKernelGGL(attn_bwd_dq_kernel<HD>, grid, dim3(256), 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  dim3 grid(((a.T + BQ - 1) / BQ) * a.B * a.H);
   hipLaunchKernelGGL(attn_bwd_dkdv_kernel<HD>, grid, dim3(256), 0, s, a);
-  e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(attn_bwd_dq_kernel<HD>, grid, dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
