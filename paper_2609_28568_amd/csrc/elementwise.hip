@@ -220,17 +220,22 @@ __global__ __launch_bounds__(NT) void cross_entropy_kernel(bf16_t* __restrict__ 
                                                            float grad_scale) {
   constexpr int NW = NT / 64;
   __shared__ float shm[NW], shs[NW];
-  __shared__ float xt;
   const int row = blockIdx.x, tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   bf16_t* lr = logits + (size_t)row * Vp;
   const int tgt = targets[row];
-  if (tid == 0) xt = bf2f(lr[tgt]);
+  // the target's logit, read before the row is overwritten (by every thread,
+  // one broadcast address, so the load needs no branch; thread 0 uses it)
+  const bf16_t xt_raw = lr[tgt];
   const int nch = Vp / 8;
+  // Every thread issues all its row loads at once: chunks past the row end
+  // read its last chunk (an in-range address) and are excluded below by the
+  // column test (their columns would be >= Vp >= V), so no load waits behind
+  // a per-chunk branch.
   uint4 v[MAXCH];
 #pragma unroll
   for (int i = 0; i < MAXCH; ++i) {
-    const int c = tid + NT * i;
-    v[i] = c < nch ? *reinterpret_cast<const uint4*>(lr + c * 8) : make_uint4(0, 0, 0, 0);
+    const int c = min(tid + NT * i, nch - 1);
+    v[i] = *reinterpret_cast<const uint4*>(lr + c * 8);
   }
   // element j of chunk c counts if j < V (the padding columns carry no
   // probability)
@@ -298,7 +303,7 @@ __global__ __launch_bounds__(NT) void cross_entropy_kernel(bf16_t* __restrict__ 
           make_uint4(pack2(d[0], d[1]), pack2(d[2], d[3]), pack2(d[4], d[5]), pack2(d[6], d[7]));
     }
   }
-  if (tid == 0) losses[row] = mx + logf(sum) - xt;
+  if (tid == 0) losses[row] = mx + logf(sum) - bf2f(xt_raw);
 }
 
 // ------------------------------------------------------------ casts
