@@ -23,7 +23,7 @@ __global__ void reduce_slices_kernel(const float* __restrict__ src, int nslices,
 }
 
 // 16 waves per block, 64 columns per block: wave w sums slices w, w+16, ...
-// with several loads in flight, then the waves are combined in order.
+// sixteen loads at a time, then the waves are combined in order.
 __global__ __launch_bounds__(1024) void reduce_parts_kernel(const float* __restrict__ part, int S, long stride,
                                                             int n, int nd, float* __restrict__ d0,
                                                             float* __restrict__ d1, float* __restrict__ d2,
@@ -34,11 +34,15 @@ __global__ __launch_bounds__(1024) void reduce_parts_kernel(const float* __restr
   const bool ok = col < n * nd;
   float a = 0.0f;
   if (ok) {
+    // 16 loads in flight per wave (slices s, s+16, ..., s+240), then summed
+    // in slice order
     int s = w;
-    for (; s + 48 < S; s += 64) {
-      float v0 = part[(size_t)s * stride + col], v1 = part[(size_t)(s + 16) * stride + col];
-      float v2 = part[(size_t)(s + 32) * stride + col], v3 = part[(size_t)(s + 48) * stride + col];
-      a += v0; a += v1; a += v2; a += v3;
+    for (; s + 240 < S; s += 256) {
+      float v[16];
+#pragma unroll
+      for (int k = 0; k < 16; ++k) v[k] = part[(size_t)(s + 16 * k) * stride + col];
+#pragma unroll
+      for (int k = 0; k < 16; ++k) a += v[k];
     }
     for (; s < S; s += 16) a += part[(size_t)s * stride + col];
   }
@@ -96,11 +100,20 @@ DEV float block_max(float v, float* sh) {
   return t;
 }
 
-__global__ __launch_bounds__(256) void mean_kernel(const float* __restrict__ x, int n, float* __restrict__ out) {
-  __shared__ float sh[4];
+// one block of 1024 threads, each with up to 16 loads in flight at a time
+__global__ __launch_bounds__(1024) void mean_kernel(const float* __restrict__ x, int n, float* __restrict__ out) {
+  __shared__ float sh[16];
   float s = 0.0f;
-  for (int i = threadIdx.x; i < n; i += 256) s += x[i];
-  s = block_sum<256>(s, sh);
+  int i = threadIdx.x;
+  for (; i + 15 * 1024 < n; i += 16 * 1024) {
+    float v[16];
+#pragma unroll
+    for (int k = 0; k < 16; ++k) v[k] = x[i + 1024 * k];
+#pragma unroll
+    for (int k = 0; k < 16; ++k) s += v[k];
+  }
+  for (; i < n; i += 1024) s += x[i];
+  s = block_sum<1024>(s, sh);
   if (threadIdx.x == 0) out[0] = s / n;
 }
 
@@ -404,7 +417,7 @@ hipError_t launch_colsum(const bf16_t* x, int rows, int N, float* parts, hipStre
 }
 
 hipError_t launch_mean(const float* x, int n, float* out, hipStream_t s) {
-  hipLaunchKernelGGL(mean_kernel, dim3(1), dim3(256), 0, s, x, n, out);
+  hipLaunchKernelGGL(mean_kernel, dim3(1), dim3(1024), 0, s, x, n, out);
   return hipGetLastError();
 }
 
