@@ -60,12 +60,15 @@ def cpu_baseline(w: dict, params, ids, tgt) -> dict:
 
 
 # Kernel class -> (sources its code comes from, rocprofv3 kernel-name pattern)
+# Each class: the sources its launches depend on (the kernels, and gpt2.cpp,
+# which plans the launches: shapes, splits, tile configurations) and the
+# pattern of its kernel names in rocprofv3 output.
 KERNEL_CLASSES = {
-    "gemm_fwd": (("gemm.hip", "common.h", "lds_dma.h", "kernels.h"),
+    "gemm_fwd": (("gemm.hip", "common.h", "lds_dma.h", "kernels.h", "gpt2.cpp"),
                  r"gemm_kernel<\d+, \d+, \d+, \d+, false, false, 0>"),
-    "gemm_dw": (("gemm.hip", "common.h", "lds_dma.h", "kernels.h"),
+    "gemm_dw": (("gemm.hip", "common.h", "lds_dma.h", "kernels.h", "gpt2.cpp"),
                 r"gemm_kernel<\d+, \d+, \d+, \d+, true, true, 3>"),
-    "attn_bwd": (("attention.hip", "common.h", "lds_dma.h", "kernels.h"), r"attn_(bwd|dsum)"),
+    "attn_bwd": (("attention.hip", "common.h", "lds_dma.h", "kernels.h", "gpt2.cpp"), r"attn_bwd"),
 }
 CALIBRATION_BYTES = 1 << 30
 
