@@ -14,12 +14,33 @@ __global__ void reduce_slices_kernel(const float* __restrict__ src, int nslices,
   long i = ((long)blockIdx.x * blockDim.x + threadIdx.x) * 4;
   if (i >= n) return;
   float4 acc = accumulate ? *reinterpret_cast<const float4*>(dst + i) : make_float4(0, 0, 0, 0);
-#pragma unroll 4
+  // up to 16 slices' loads in flight before their sums
+#pragma unroll 16
   for (int s = 0; s < nslices; ++s) {
     float4 v = *reinterpret_cast<const float4*>(src + (size_t)s * n + i);
     acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
   }
   *reinterpret_cast<float4*>(dst + i) = acc;
+}
+
+// Two independent reductions in one launch; blockIdx.y picks the segment.
+__global__ void reduce_slices2_kernel(const float* __restrict__ src, int nslices, long n, float* __restrict__ dst,
+                                      const float* __restrict__ src2, int nslices2, long n2,
+                                      float* __restrict__ dst2, int accumulate) {
+  const bool second = blockIdx.y == 1;
+  const float* sp = second ? src2 : src;
+  const int ns = second ? nslices2 : nslices;
+  const long nn = second ? n2 : n;
+  float* dp = second ? dst2 : dst;
+  long i = ((long)blockIdx.x * blockDim.x + threadIdx.x) * 4;
+  if (i >= nn) return;
+  float4 acc = accumulate ? *reinterpret_cast<const float4*>(dp + i) : make_float4(0, 0, 0, 0);
+#pragma unroll 16
+  for (int k = 0; k < ns; ++k) {
+    float4 v = *reinterpret_cast<const float4*>(sp + (size_t)k * nn + i);
+    acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
+  }
+  *reinterpret_cast<float4*>(dp + i) = acc;
 }
 
 // 16 waves per block, 64 columns per block: wave w sums slices w, w+16, ...
@@ -56,22 +77,6 @@ __global__ __launch_bounds__(1024) void reduce_parts_kernel(const float* __restr
     float* d = j == 0 ? d0 : (j == 1 ? d1 : d2);
     if (d) d[c] = (accumulate ? d[c] : 0.0f) + t;
   }
-}
-
-// parts[p][c] = sum of x[r][c] over the p-th slice of rows; one thread per
-// 4 columns
-__global__ void colsum_kernel(const bf16_t* __restrict__ x, int rows, int N, int rows_per_part,
-                              float* __restrict__ parts) {
-  const int c = (blockIdx.x * blockDim.x + threadIdx.x) * 4;
-  if (c >= N) return;
-  const int r0 = blockIdx.y * rows_per_part, r1 = min(rows, r0 + rows_per_part);
-  float a0 = 0, a1 = 0, a2 = 0, a3 = 0;
-#pragma unroll 8
-  for (int r = r0; r < r1; ++r) {
-    uint2 u = *reinterpret_cast<const uint2*>(x + (size_t)r * N + c);
-    a0 += lo_f(u.x); a1 += hi_f(u.x); a2 += lo_f(u.y); a3 += hi_f(u.y);
-  }
-  *reinterpret_cast<float4*>(parts + (size_t)blockIdx.y * N + c) = make_float4(a0, a1, a2, a3);
 }
 
 template <int NT>
@@ -394,25 +399,20 @@ hipError_t launch_reduce_slices(const float* src, int nslices, long n, float* ds
   return hipGetLastError();
 }
 
+hipError_t launch_reduce_slices2(const float* src, int nslices, long n, float* dst, const float* src2,
+                                 int nslices2, long n2, float* dst2, int accumulate, hipStream_t s) {
+  if (n % 4 || n2 % 4) return hipErrorInvalidValue;
+  const long nmax = n > n2 ? n : n2;
+  hipLaunchKernelGGL(reduce_slices2_kernel, dim3(blocks_for(nmax / 4, 256), 2), dim3(256), 0, s, src, nslices, n, dst,
+                     src2, nslices2, n2, dst2, accumulate);
+  return hipGetLastError();
+}
+
 hipError_t launch_reduce_parts(const float* part, int S, long stride, int n, int nd, float* d0, float* d1,
                                float* d2, int accumulate, hipStream_t s) {
   if (nd < 1 || nd > 3) return hipErrorInvalidValue;
   hipLaunchKernelGGL(reduce_parts_kernel, dim3((unsigned)((n * nd + 63) / 64)), dim3(1024), 0, s, part, S, stride, n,
                      nd, d0, d1, d2, accumulate);
-  return hipGetLastError();
-}
-
-int colsum_parts(int rows) {
-  int p = rows / 128;
-  return p < 1 ? 1 : (p > 128 ? 128 : p);
-}
-
-hipError_t launch_colsum(const bf16_t* x, int rows, int N, float* parts, hipStream_t s) {
-  if (N % 4) return hipErrorInvalidValue;
-  int np = colsum_parts(rows);
-  int rpp = (rows + np - 1) / np;
-  dim3 grid(blocks_for(N / 4, 64), np);
-  hipLaunchKernelGGL(colsum_kernel, grid, dim3(64), 0, s, x, rows, N, rpp, parts);
   return hipGetLastError();
 }
 

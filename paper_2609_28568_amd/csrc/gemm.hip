@@ -205,6 +205,26 @@ __global__ __launch_bounds__(256, (NS <= 2 ? 2 : 1)) void gemm_kernel(GemmArgs g
     else wait_vmcnt<0>();
   };
 
+  // Bias-gradient partial sums of a weight gradient: row m of A (dY^T) summed
+  // over this workgroup's share of the contraction, from the A fragments the
+  // MFMAs consume. The ntn workgroups of a row of tiles take alternate
+  // k-tiles, and the two waves reading the same A fragments alternate
+  // k-steps, so each wave adds up 1/(2 ntn) of its fragments. Lane l holds
+  // row l%32 of each 32-row fragment at k-slots 8*(l/32)..+7.
+  constexpr bool BSUM = A_T && (EPI == EPI_F32 || EPI == EPI_F32_ACC);
+  const bool bsum_on = BSUM && g.bsum != nullptr;
+  const int tn = n0 / BN;
+  float bs[BSUM ? TM : 1];
+#pragma unroll
+  for (int i = 0; i < (BSUM ? TM : 1); ++i) bs[i] = 0.0f;
+  auto bias_sums = [&](const bf16x8* f) {
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+      const uint4 u = __builtin_bit_cast(uint4, f[i]);
+      bs[i] += ((lo_f(u.x) + hi_f(u.x)) + (lo_f(u.y) + hi_f(u.y))) + ((lo_f(u.z) + hi_f(u.z)) + (lo_f(u.w) + hi_f(u.w)));
+    }
+  };
+
   // Tile kt: wait for it, publish it with the barrier (which also frees the
   // stage of tile kt-1 for tile kt+NS-1), then walk its k-steps reading the
   // fragments of step s+1 while the MFMAs of step s run.
@@ -222,6 +242,22 @@ __global__ __launch_bounds__(256, (NS <= 2 ? 2 : 1)) void gemm_kernel(GemmArgs g
     for (int s = 0; s < KSTEPS; ++s) {
       if (s + 1 < KSTEPS) load(fa[(s + 1) & 1], fb[(s + 1) & 1], kt, s + 1);
       mma(fa[s & 1], fb[s & 1]);
+      if constexpr (BSUM) {
+        if (bsum_on && (s & 1) == wn && kt % ntn == tn) bias_sums(fa[s & 1]);
+      }
+    }
+  }
+  if constexpr (BSUM) {
+    // lanes l and l+32 hold the two k-halves of row l; each wave writes its
+    // own partial row, slot (split, tile column, wave column)
+    if (bsum_on) {
+      const size_t slot = ((size_t)split * ntn + tn) * 2 + wn;
+#pragma unroll
+      for (int i = 0; i < TM; ++i) {
+        const float v = bs[i] + __shfl_xor(bs[i], 32);
+        const int m = m0 + wm * WTM + 32 * i + (lane & 31);
+        if (lane < 32 && m < g.M) g.bsum[slot * g.M + m] = v;
+      }
     }
   }
 
@@ -404,6 +440,11 @@ GemmConfig gemm_config(int M, int N, int a_t, int b_t, int epi) {
   }
   if (M >= 256 && N >= 128 && N % 128 == 0) return {256, 128, 32};
   return {128, 128, 32};
+}
+
+int gemm_bias_parts(int M, int N, int splits) {
+  const GemmConfig c = gemm_config(M, N, 1, 1, EPI_F32);
+  return (splits < 1 ? 1 : splits) * ((N + c.bn - 1) / c.bn) * 2;
 }
 
 int gemm_split_plan(int K, int want, int* k_chunk) {

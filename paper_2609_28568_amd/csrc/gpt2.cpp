@@ -150,8 +150,8 @@ struct ActLayout {
 };
 
 struct WsLayout {
-  size_t dres, dh, datt, dbig, dsum, splitk, colsum, lnpart, sumsq, normcoef, total;
-  size_t splitk_elems, colsum_elems;
+  size_t dres, dh, datt, dbig, dsum, splitk, bsum, lnpart, sumsq, normcoef, total;
+  size_t splitk_elems, bsum_elems;
 };
 
 ActLayout act_layout(const Dims& d) {
@@ -200,7 +200,14 @@ WsLayout ws_layout(const Dims& d) {
   };
   upd(3 * d.C, d.C); upd(d.C, d.C); upd(d.F, d.C); upd(d.C, d.F); upd(d.Vp, d.C);
   w.splitk_elems = sk;
-  w.colsum_elems = (size_t)colsum_parts((int)BT) * wide;
+  // bias partial sums of the weight gradients that carry a bias gradient
+  size_t bs = 0;
+  auto bupd = [&](int M, int N) {
+    const int s = dw_splits(d, M, N);
+    bs = std::max(bs, (size_t)gemm_bias_parts(M, N, s) * M);
+  };
+  bupd(3 * d.C, d.C); bupd(d.F, d.C); bupd(d.C, d.F);
+  w.bsum_elems = bs;
   size_t o = 0;
   w.dres = o; o += align_up(BT * C * 2);
   w.dh = o; o += align_up(BT * C * 2);
@@ -208,7 +215,7 @@ WsLayout ws_layout(const Dims& d) {
   w.dbig = o; o += align_up(BT * wide * 2);
   w.dsum = o; o += align_up((size_t)d.B * d.H * d.T * 4);
   w.splitk = o; o += align_up(sk * 4);
-  w.colsum = o; o += align_up(w.colsum_elems * 4);
+  w.bsum = o; o += align_up(w.bsum_elems * 4);
   w.lnpart = o; o += align_up((size_t)layernorm_bwd_blocks((int)BT) * 3 * C * 4);
   w.sumsq = o; o += align_up((size_t)sumsq_parts() * 4);
   w.normcoef = o; o += ALIGN;
@@ -330,11 +337,13 @@ int gemm_class(int a_t, int b_t, int epi) {
 hipError_t gemm(Model* m, int cls, int M, int N, int K, const bf16_t* A, int lda, int a_t, const bf16_t* B,
                 int ldb, int b_t, int epi, void* C, int ldc, const float* bias = nullptr,
                 const bf16_t* residual = nullptr, bf16_t* C2 = nullptr, const bf16_t* aux = nullptr,
-                int accumulate = 0, int splits = 1, long split_stride = 0, int k_chunk = 0, double alg_flops = 0.0) {
+                int accumulate = 0, int splits = 1, long split_stride = 0, int k_chunk = 0, double alg_flops = 0.0,
+                float* bsum = nullptr) {
   GemmArgs g{};
   g.A = A; g.B = B; g.M = M; g.N = N; g.K = K; g.lda = lda; g.ldb = ldb;
   g.C = C; g.ldc = ldc; g.bias = bias; g.residual = residual; g.C2 = C2; g.aux = aux;
   g.accumulate = accumulate; g.splits = splits; g.split_stride = split_stride; g.k_chunk = k_chunk;
+  g.bsum = bsum;
   // algorithmic FLOPs: the tied head passes its count over the real vocabulary
   // only (the padded columns are computed but carry no probability)
   const double fl = alg_flops > 0.0 ? alg_flops : 2.0 * M * N * K;
@@ -342,18 +351,26 @@ hipError_t gemm(Model* m, int cls, int M, int N, int K, const bf16_t* A, int lda
   return m->run(gemm_class(a_t, b_t, epi), fl, 0.0, [&] { return launch_gemm(g, a_t, b_t, epi, m->stream); });
 }
 
-// weight gradient dW[M][N] (=|+=) sum_t A[t][m] * X[t][n] (fp32)
+// weight gradient dW[M][N] (=|+=) sum_t A[t][m] * X[t][n] (fp32); with db,
+// also the bias gradient db[M] (=|+=) sum_t A[t][m], summed by the GEMM from
+// the A fragments it reads and reduced together with its contraction split
 hipError_t weight_grad(Model* m, int M, int N, const bf16_t* dy, const bf16_t* x, float* dW, int accumulate,
-                       int m_real = 0) {
+                       int m_real = 0, float* db = nullptr) {
   const int BT = (int)m->d.BT;
   const int mr = m_real ? m_real : M;
   const double fl = 2.0 * mr * (double)N * BT;
   int s = dw_splits(m->d, M, N);
+  float* bp = db ? m->wsf(m->ws.bsum) : nullptr;
   if (s <= 1) {
     const DwTail t = dw_tail(m->d, M, N);
-    if (t.splits <= 1)
-      return gemm(m, GPT2_K_GEMM_DW, M, N, BT, dy, M, 1, x, N, 1, EPI_F32, dW, N, nullptr, nullptr, nullptr, nullptr,
-                  accumulate, 1, 0, 0, fl);
+    if (t.splits <= 1 || db) {
+      hipError_t e = gemm(m, GPT2_K_GEMM_DW, M, N, BT, dy, M, 1, x, N, 1, EPI_F32, dW, N, nullptr, nullptr, nullptr,
+                          nullptr, accumulate, 1, 0, 0, fl, bp);
+      if (e != hipSuccess || !db) return e;
+      const int np = gemm_bias_parts(M, N, 1);
+      return m->run(GPT2_K_OTHER, 0.0, 4.0 * (double)M * (np + 1 + accumulate),
+                    [&] { return launch_reduce_slices(bp, np, M, db, accumulate, m->stream); });
+    }
     // whole rounds unsplit, the rest split over tokens and reduced
     const int m0 = t.m_main, m1 = M - t.m_main;
     const double fl0 = 2.0 * std::min(mr, m0) * (double)N * BT, fl1 = fl - fl0;
@@ -370,23 +387,16 @@ hipError_t weight_grad(Model* m, int M, int N, const bf16_t* dy, const bf16_t* x
   }
   float* part = m->wsf(m->ws.splitk);
   hipError_t e = gemm(m, GPT2_K_GEMM_DW, M, N, BT, dy, M, 1, x, N, 1, EPI_F32, part, N, nullptr, nullptr, nullptr,
-                      nullptr, 0, s, (long)M * N, dw_chunk(m->d, M, N), fl);
+                      nullptr, 0, s, (long)M * N, dw_chunk(m->d, M, N), fl, bp);
   if (e != hipSuccess) return e;
-  return m->run(GPT2_K_OTHER, 0.0, 4.0 * (double)M * N * (s + 1 + accumulate),
-                [&] { return launch_reduce_slices(part, s, (long)M * N, dW, accumulate, m->stream); });
-}
-
-// bias gradient db[N] (=|+=) sum_t dy[t][n]
-hipError_t bias_grad(Model* m, const bf16_t* dy, int N, float* db, int accumulate) {
-  const int BT = (int)m->d.BT;
-  float* parts = m->wsf(m->ws.colsum);
-  int np = colsum_parts(BT);
-  hipError_t e = m->run(GPT2_K_OTHER, 0.0, 2.0 * BT * N + 4.0 * np * N,
-                        [&] { return launch_colsum(dy, BT, N, parts, m->stream); });
-  if (e != hipSuccess) return e;
-  return m->run(GPT2_K_OTHER, 0.0, 4.0 * N * (np + 1 + accumulate), [&] {
-    return launch_reduce_parts(parts, np, N, N, 1, db, nullptr, nullptr, accumulate, m->stream);
-  });
+  if (!db)
+    return m->run(GPT2_K_OTHER, 0.0, 4.0 * (double)M * N * (s + 1 + accumulate),
+                  [&] { return launch_reduce_slices(part, s, (long)M * N, dW, accumulate, m->stream); });
+  const int np = gemm_bias_parts(M, N, s);
+  return m->run(GPT2_K_OTHER, 0.0, 4.0 * ((double)M * N * (s + 1 + accumulate) + (double)M * (np + 1 + accumulate)),
+                [&] {
+                  return launch_reduce_slices2(part, s, (long)M * N, dW, bp, np, M, db, accumulate, m->stream);
+                });
 }
 
 hipError_t ln_fwd(Model* m, const bf16_t* x, const float* w, const float* b, bf16_t* y, float* mean, float* rstd) {
@@ -465,12 +475,11 @@ gpt2_status block_bwd(Model* m, int l, int acc, bool fcproj_bias_done, bool writ
   // MLP down projection; GELU backward fused into the input-gradient epilogue
   TRY(gemm(m, GPT2_K_GEMM_DX, BT, F, C, dres, C, 0, m->pb(K_FCPROJW) + oC * F, F, 1, EPI_GELU_BWD, dbig, F, nullptr,
            nullptr, nullptr, m->fc(l)));
-  TRY(weight_grad(m, C, F, dres, m->gelu(l), m->gf(K_FCPROJW) + oC * F, acc));
-  if (!fcproj_bias_done) TRY(bias_grad(m, dres, C, m->gf(K_FCPROJB) + oC, acc));
+  TRY(weight_grad(m, C, F, dres, m->gelu(l), m->gf(K_FCPROJW) + oC * F, acc, 0,
+                  fcproj_bias_done ? nullptr : m->gf(K_FCPROJB) + oC));
   // MLP up projection
   TRY(gemm(m, GPT2_K_GEMM_DX, BT, C, F, dbig, F, 0, m->pb(K_FCW) + oF * C, C, 1, EPI_BF16, dh, C));
-  TRY(weight_grad(m, F, C, dbig, m->ln2(l), m->gf(K_FCW) + oF * C, acc));
-  TRY(bias_grad(m, dbig, F, m->gf(K_FCB) + oF, acc));
+  TRY(weight_grad(m, F, C, dbig, m->ln2(l), m->gf(K_FCW) + oF * C, acc, 0, m->gf(K_FCB) + oF));
   TRY(ln_bwd(m, dh, m->xmid(l), m->ln2m(l), m->ln2r(l), m->pf(K_LN2W) + oC, 1, m->gf(K_LN2W) + oC,
              m->gf(K_LN2B) + oC, m->gf(K_ATTPROJB) + oC, acc));
   // attention output projection (its bias gradient came from the LayerNorm above)
@@ -481,8 +490,7 @@ gpt2_status block_bwd(Model* m, int l, int acc, bool fcproj_bias_done, bool writ
   TRY(m->run(GPT2_K_ATTN_BWD, 2.0 * attn_fwd_flops(d), 0.0, [&] { return launch_attention_bwd(aa, m->stream); }));
   // q|k|v projection
   TRY(gemm(m, GPT2_K_GEMM_DX, BT, C, 3 * C, dbig, 3 * C, 0, m->pb(K_QKVW) + o3C * C, C, 1, EPI_BF16, dh, C));
-  TRY(weight_grad(m, 3 * C, C, dbig, m->ln1(l), m->gf(K_QKVW) + o3C * C, acc));
-  TRY(bias_grad(m, dbig, 3 * C, m->gf(K_QKVB) + o3C, acc));
+  TRY(weight_grad(m, 3 * C, C, dbig, m->ln1(l), m->gf(K_QKVW) + o3C * C, acc, 0, m->gf(K_QKVB) + o3C));
   float* prev_bias = (write_prev_bias && l > 0) ? m->gf(K_FCPROJB) + (size_t)(l - 1) * C : nullptr;
   TRY(ln_bwd(m, dh, m->res(l), m->ln1m(l), m->ln1r(l), m->pf(K_LN1W) + oC, 1, m->gf(K_LN1W) + oC,
              m->gf(K_LN1B) + oC, prev_bias, acc));

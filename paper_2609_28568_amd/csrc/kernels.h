@@ -30,6 +30,11 @@ struct GemmArgs {
   int splits;              // split of the contraction over grid.z (EPI_F32 only)
   long split_stride;       // elements between split output slices
   int k_chunk;             // contraction length per split (from gemm_split_plan)
+  // EPI_F32 with A read transposed (a weight gradient dY^T X): when set, the
+  // GEMM also writes partial sums of A's rows over the contraction (the bias
+  // gradient, sum over tokens of dY) into [gemm_bias_parts(M, N, splits)][M];
+  // summing those rows gives the bias gradient
+  float* bsum;
 };
 
 // Block tile (bm x bn, contraction depth bk per stage) the GEMM uses for an
@@ -39,6 +44,8 @@ GemmConfig gemm_config(int M, int N, int a_t, int b_t, int epi);
 // Plan a contraction split of K into about `want` pieces: writes the chunk
 // length (a multiple of the 64-wide k tile) and returns the split count.
 int gemm_split_plan(int K, int want, int* k_chunk);
+// Partial rows a weight-gradient GEMM writes into GemmArgs::bsum
+int gemm_bias_parts(int M, int N, int splits);
 hipError_t launch_gemm(const GemmArgs& g, int a_t, int b_t, int epi, hipStream_t s);
 
 // ---------------------------------------------------------------- attention
@@ -71,15 +78,14 @@ hipError_t launch_layernorm_bwd(const bf16_t* dy, const bf16_t* x, const float* 
 // dst[i] (fp32, n elements) = (accumulate ? dst[i] : 0) + sum_s src[s*n + i]
 hipError_t launch_reduce_slices(const float* src, int nslices, long n, float* dst, int accumulate,
                                 hipStream_t s);
+// The same for two independent segments in one launch (n and n2 multiples of 4)
+hipError_t launch_reduce_slices2(const float* src, int nslices, long n, float* dst, const float* src2,
+                                 int nslices2, long n2, float* dst2, int accumulate, hipStream_t s);
 // Sum over S slices of partial rows, for narrow rows and many slices:
 // dst_j[c] (=|+=) sum_s part[s*stride + j*n + c], for j < nd (up to 3
 // destinations, null ones skipped) and c < n. Fixed summation order.
 hipError_t launch_reduce_parts(const float* part, int S, long stride, int n, int nd, float* d0, float* d1,
                                float* d2, int accumulate, hipStream_t s);
-// column sums of bf16 [rows][N] into partials [nparts][N]; returns nparts
-int colsum_parts(int rows);
-hipError_t launch_colsum(const bf16_t* x, int rows, int N, float* parts, hipStream_t s);
-
 hipError_t launch_embed_fwd(const int32_t* ids, const float* wte, const float* wpe, bf16_t* x, int B,
                             int T, int C, hipStream_t s);
 // dwte[ids[r]] += dx[r] (fp32 atomics; adds to what is there)
