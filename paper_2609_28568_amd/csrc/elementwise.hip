@@ -361,12 +361,14 @@ __global__ __launch_bounds__(256) void clip_coef_kernel(const float* __restrict_
   }
 }
 
+// Segments (parameter kinds) are walked in order, uniformly across the grid,
+// so each one's bounds and decay flag are scalars; within a segment every
+// thread updates 4-element chunks in a grid-stride loop, two chunks in
+// flight at a time. Segment ends are multiples of 4 (checked at launch).
 __global__ __launch_bounds__(256) void adamw_kernel(AdamArgs a) {
   const float coef = a.norm_coef[1];
-  for (long i = ((long)blockIdx.x * 256 + threadIdx.x) * 4; i < a.n; i += (long)gridDim.x * 256 * 4) {
-    int sidx = 0;
-    while (sidx < a.seg.count - 1 && i >= a.seg.end[sidx]) ++sidx;
-    const float wd = a.seg.decay[sidx] ? a.weight_decay : 0.0f;
+  const long stride = (long)gridDim.x * 256 * 4;
+  auto update = [&](long i, float wd) {
     float4 p = *reinterpret_cast<const float4*>(a.p + i);
     float4 g = *reinterpret_cast<const float4*>(a.g + i);
     float4 m = *reinterpret_cast<const float4*>(a.m + i);
@@ -385,6 +387,18 @@ __global__ __launch_bounds__(256) void adamw_kernel(AdamArgs a) {
     *reinterpret_cast<float4*>(a.m + i) = make_float4(mv[0], mv[1], mv[2], mv[3]);
     *reinterpret_cast<float4*>(a.v + i) = make_float4(vv[0], vv[1], vv[2], vv[3]);
     *reinterpret_cast<uint2*>(a.p_bf16 + i) = make_uint2(pack2(pv[0], pv[1]), pack2(pv[2], pv[3]));
+  };
+  long lo = 0;
+  for (int sg = 0; sg < a.seg.count; ++sg) {
+    const long hi = a.seg.end[sg];
+    const float wd = a.seg.decay[sg] ? a.weight_decay : 0.0f;
+    long i = lo + ((long)blockIdx.x * 256 + threadIdx.x) * 4;
+    for (; i + stride < hi; i += 2 * stride) {
+      update(i, wd);
+      update(i + stride, wd);
+    }
+    if (i < hi) update(i, wd);
+    lo = hi;
   }
 }
 
@@ -488,6 +502,8 @@ hipError_t launch_clip_coef(const float* parts, int nparts, float clip, float* n
 
 hipError_t launch_adamw(const AdamArgs& a, hipStream_t s) {
   if (a.n % 4) return hipErrorInvalidValue;
+  for (int k = 0; k < a.seg.count; ++k)
+    if (a.seg.end[k] % 4) return hipErrorInvalidValue;
   long n4 = a.n / 4;
   unsigned blocks = blocks_for(n4, 256);
   if (blocks > 8192) blocks = 8192;
