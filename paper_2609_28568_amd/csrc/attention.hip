@@ -419,21 +419,28 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_kernel(AttnArgs a) {
 
   const bf16_t* ob = a.out + (size_t)b * T * C + h * HD;
   bf16x8 qf[S::KS], df[S::KS];
+  // all of the query's loads first (rows past T read row T-1 and are unused),
+  // then the arithmetic, so no load waits behind another's use
+  uint4 q4[S::KS], d4[S::KS], o4[S::KS];
+  const int qr = min(q, T - 1);
+#pragma unroll
+  for (int s = 0; s < S::KS; ++s) {
+    q4[s] = *reinterpret_cast<const uint4*>(base + (size_t)qr * ld + 16 * s + 8 * g);
+    d4[s] = *reinterpret_cast<const uint4*>(dob + (size_t)qr * C + 16 * s + 8 * g);
+    o4[s] = *reinterpret_cast<const uint4*>(ob + (size_t)qr * C + 16 * s + 8 * g);
+  }
+  const float lse_q = a.lse[(size_t)bh * T + qr];
   float dpart = 0.0f;
 #pragma unroll
   for (int s = 0; s < S::KS; ++s) {
-    uint4 q4 = make_uint4(0, 0, 0, 0), d4 = make_uint4(0, 0, 0, 0), o4 = make_uint4(0, 0, 0, 0);
-    if (q < T) {
-      q4 = *reinterpret_cast<const uint4*>(base + (size_t)q * ld + 16 * s + 8 * g);
-      d4 = *reinterpret_cast<const uint4*>(dob + (size_t)q * C + 16 * s + 8 * g);
-      o4 = *reinterpret_cast<const uint4*>(ob + (size_t)q * C + 16 * s + 8 * g);
-    }
-    qf[s] = as_bf16x8(q4);
-    df[s] = as_bf16x8(d4);
-    dpart += lo_f(d4.x) * lo_f(o4.x) + hi_f(d4.x) * hi_f(o4.x) + lo_f(d4.y) * lo_f(o4.y) + hi_f(d4.y) * hi_f(o4.y);
-    dpart += lo_f(d4.z) * lo_f(o4.z) + hi_f(d4.z) * hi_f(o4.z) + lo_f(d4.w) * lo_f(o4.w) + hi_f(d4.w) * hi_f(o4.w);
+    if (q >= T) q4[s] = d4[s] = o4[s] = make_uint4(0, 0, 0, 0);
+    qf[s] = as_bf16x8(q4[s]);
+    df[s] = as_bf16x8(d4[s]);
+    const uint4 dd = d4[s], oo = o4[s];
+    dpart += lo_f(dd.x) * lo_f(oo.x) + hi_f(dd.x) * hi_f(oo.x) + lo_f(dd.y) * lo_f(oo.y) + hi_f(dd.y) * hi_f(oo.y);
+    dpart += lo_f(dd.z) * lo_f(oo.z) + hi_f(dd.z) * hi_f(oo.z) + lo_f(dd.w) * lo_f(oo.w) + hi_f(dd.w) * hi_f(oo.w);
   }
-  const float lse2 = q < T ? a.lse[(size_t)bh * T + q] * LOG2E : 0.0f;
+  const float lse2 = q < T ? lse_q * LOG2E : 0.0f;
   // D = rowsum(dO * O) of query q: lanes lq and lq + 32 hold the two halves of
   // its row. Stored for the dK/dV kernel, which runs after this one.
   const float dsum = dpart + __shfl_xor(dpart, 32);
