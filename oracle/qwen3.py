@@ -26,7 +26,8 @@ Readings where neither the paper nor that configuration fixes the detail
   A [r, in], B [out, r], s = alpha / sqrt(r); the loss is the mean over the
   unmasked positions (the last half of every sequence, as the benchmark
   configuration states it); adapter AdamW with betas (0.9, 0.999), eps 1e-8
-  and no weight decay unless configured.
+  and no weight decay unless configured; the adapter gradients clipped to
+  global norm 1.0, the clip the paper's optimisation section states.
 
 All arithmetic happens in the dtype of the parameters passed in.
 """
@@ -63,6 +64,7 @@ class Qwen3Config:
     beta2: float = 0.999
     adam_eps: float = 1e-8
     weight_decay: float = 0.0
+    grad_clip: float = 1.0      # global-norm clip of the adapter gradients
 
     @classmethod
     def from_dict(cls, d: dict) -> "Qwen3Config":
@@ -381,3 +383,18 @@ def adamw_step(lora: dict, grads: dict, m: dict, v: dict, step: int, cfg: Qwen3C
         v[k] = b2 * v[k] + (1 - b2) * g * g
         upd = (m[k] / bc1) / (np.sqrt(v[k] / bc2) + dt(cfg.adam_eps)) + dt(cfg.weight_decay) * lora[k]
         lora[k] -= dt(cfg.lr) * upd
+
+
+def train_step(base: dict, lora: dict, m: dict, v: dict, step: int, ids, targets, cfg: Qwen3Config):
+    """One adapter step: forward and masked loss, adapter gradients, global-norm
+    clipping of those gradients to grad_clip, AdamW. Returns (loss, norm
+    before clipping)."""
+    from .gpt2 import clip_coefficient, global_norm
+    cache = forward(base, lora, ids, targets, cfg)
+    grads = backward(base, lora, cache, cfg)
+    grads.pop("dx0")
+    norm = global_norm(grads)
+    coef = clip_coefficient(norm, cfg.grad_clip)
+    dt = next(iter(lora.values())).dtype.type
+    adamw_step(lora, {k: g * dt(coef) for k, g in grads.items()}, m, v, step, cfg)
+    return cache["loss"], norm

@@ -192,3 +192,26 @@ def test_adapter_adamw_first_step_closed_form():
     # step 1: m_hat = g, v_hat = g^2, so the update is lr * g / (|g| + eps)
     expect = np.array([[1.0 - 1e-3 * 0.5 / (0.5 + 1e-8), -2.0 + 1e-3 * 0.25 / (0.25 + 1e-8)]])
     np.testing.assert_allclose(lora["q_A"], expect, rtol=0, atol=1e-15)
+
+
+@pytest.mark.parametrize("clip", [1e-3, 1e9])
+def test_train_step_clips_then_takes_the_closed_form_first_step(clip):
+    """First step from zero moments: m_hat = c g and v_hat = (c g)^2, so every
+    adapter element moves by lr c g / (|c g| + eps) with c = clip / ||g|| when
+    the norm over all adapter elements exceeds the clip, else c = 1."""
+    cfg = q3.Qwen3Config.from_dict(dict(TINY, grad_clip=clip, lr=1e-3))
+    base, lora = _params(cfg, 13)
+    ids, tgt = _batch(cfg, 2, 10, 14)
+    g = q3.backward(base, lora, q3.forward(base, lora, ids, tgt, cfg), cfg)
+    g.pop("dx0")
+    norm = np.linalg.norm(np.concatenate([g[k].ravel() for k in sorted(g)]))
+    c = clip / norm if norm > clip else 1.0
+    assert (c < 1.0) == (clip < 1.0)
+    before = {k: v.copy() for k, v in lora.items()}
+    m = {k: np.zeros_like(v) for k, v in lora.items()}
+    v = {k: np.zeros_like(x) for k, x in lora.items()}
+    loss, got_norm = q3.train_step(base, lora, m, v, 0, ids, tgt, cfg)
+    assert abs(got_norm - norm) <= 1e-12 * norm
+    for k in lora:
+        step = 1e-3 * c * g[k] / (np.abs(c * g[k]) + 1e-8)
+        np.testing.assert_allclose(before[k] - lora[k], step, rtol=1e-9, atol=1e-15)
