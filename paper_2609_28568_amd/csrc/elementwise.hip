@@ -106,7 +106,8 @@ DEV float block_max(float v, float* sh) {
 }
 
 // one block of 1024 threads, each with up to 16 loads in flight at a time
-__global__ __launch_bounds__(1024) void mean_kernel(const float* __restrict__ x, int n, float* __restrict__ out) {
+__global__ __launch_bounds__(1024) void mean_kernel(const float* __restrict__ x, int n, float inv,
+                                                    float* __restrict__ out) {
   __shared__ float sh[16];
   float s = 0.0f;
   int i = threadIdx.x;
@@ -119,7 +120,7 @@ __global__ __launch_bounds__(1024) void mean_kernel(const float* __restrict__ x,
   }
   for (; i < n; i += 1024) s += x[i];
   s = block_sum<1024>(s, sh);
-  if (threadIdx.x == 0) out[0] = s / n;
+  if (threadIdx.x == 0) out[0] = s * inv;
 }
 
 // ------------------------------------------------------------ embedding
@@ -235,11 +236,18 @@ template <int NT, int MAXCH, bool GRAD>
 __global__ __launch_bounds__(NT) void cross_entropy_kernel(bf16_t* __restrict__ logits,
                                                            const int32_t* __restrict__ targets,
                                                            float* __restrict__ losses, int V, int Vp,
-                                                           float grad_scale) {
+                                                           float grad_scale, int T, int mask_from) {
   constexpr int NW = NT / 64;
   __shared__ float shm[NW], shs[NW];
   const int row = blockIdx.x, tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   bf16_t* lr = logits + (size_t)row * Vp;
+  if (mask_from > 0 && row % T < mask_from) {
+    // a position that carries no loss: zero loss and, with GRAD, zero gradient
+    if (GRAD)
+      for (int c = tid; c < Vp / 8; c += NT) *reinterpret_cast<uint4*>(lr + c * 8) = make_uint4(0, 0, 0, 0);
+    if (tid == 0) losses[row] = 0.0f;
+    return;
+  }
   const int tgt = targets[row];
   // the target's logit, read before the row is overwritten (by every thread,
   // one broadcast address, so the load needs no branch; thread 0 uses it)
@@ -431,7 +439,11 @@ hipError_t launch_reduce_parts(const float* part, int S, long stride, int n, int
 }
 
 hipError_t launch_mean(const float* x, int n, float* out, hipStream_t s) {
-  hipLaunchKernelGGL(mean_kernel, dim3(1), dim3(1024), 0, s, x, n, out);
+  return launch_sum_scaled(x, n, 1.0f / (float)n, out, s);
+}
+
+hipError_t launch_sum_scaled(const float* x, int n, float scale, float* out, hipStream_t s) {
+  hipLaunchKernelGGL(mean_kernel, dim3(1), dim3(1024), 0, s, x, n, scale, out);
   return hipGetLastError();
 }
 
@@ -461,24 +473,33 @@ hipError_t launch_embed_bwd_pos(const bf16_t* dx, float* dwpe, int B, int T, int
 
 template <int NT, int MAXCH>
 void ce_launch(bf16_t* logits, const int32_t* targets, float* losses, int rows, int V, int Vp, float grad_scale,
-               int write_grad, hipStream_t s) {
+               int write_grad, int T, int mask_from, hipStream_t s) {
   if (write_grad)
     hipLaunchKernelGGL((cross_entropy_kernel<NT, MAXCH, true>), dim3(rows), dim3(NT), 0, s, logits, targets, losses, V,
-                       Vp, grad_scale);
+                       Vp, grad_scale, T, mask_from);
   else
     hipLaunchKernelGGL((cross_entropy_kernel<NT, MAXCH, false>), dim3(rows), dim3(NT), 0, s, logits, targets, losses,
-                       V, Vp, grad_scale);
+                       V, Vp, grad_scale, T, mask_from);
+}
+
+hipError_t launch_cross_entropy_masked(bf16_t* logits, const int32_t* targets, float* losses, int rows, int V, int Vp,
+                                       float grad_scale, int write_grad, int T, int mask_from, hipStream_t s) {
+  if (Vp % 8 || T < 1) return hipErrorInvalidValue;
+  const int nch = Vp / 8;
+  if (nch <= 256 * 2) ce_launch<256, 2>(logits, targets, losses, rows, V, Vp, grad_scale, write_grad, T, mask_from, s);
+  else if (nch <= 512 * 13)
+    ce_launch<512, 13>(logits, targets, losses, rows, V, Vp, grad_scale, write_grad, T, mask_from, s);
+  else if (nch <= 1024 * 8)
+    ce_launch<1024, 8>(logits, targets, losses, rows, V, Vp, grad_scale, write_grad, T, mask_from, s);
+  else if (nch <= 1024 * 19)
+    ce_launch<1024, 19>(logits, targets, losses, rows, V, Vp, grad_scale, write_grad, T, mask_from, s);
+  else return hipErrorInvalidValue;
+  return hipGetLastError();
 }
 
 hipError_t launch_cross_entropy(bf16_t* logits, const int32_t* targets, float* losses, int rows, int V, int Vp,
                                 float grad_scale, int write_grad, hipStream_t s) {
-  if (Vp % 8) return hipErrorInvalidValue;
-  const int nch = Vp / 8;
-  if (nch <= 256 * 2) ce_launch<256, 2>(logits, targets, losses, rows, V, Vp, grad_scale, write_grad, s);
-  else if (nch <= 512 * 13) ce_launch<512, 13>(logits, targets, losses, rows, V, Vp, grad_scale, write_grad, s);
-  else if (nch <= 1024 * 8) ce_launch<1024, 8>(logits, targets, losses, rows, V, Vp, grad_scale, write_grad, s);
-  else return hipErrorInvalidValue;
-  return hipGetLastError();
+  return launch_cross_entropy_masked(logits, targets, losses, rows, V, Vp, grad_scale, write_grad, 1, 0, s);
 }
 
 hipError_t launch_cast_bf16(const float* src, bf16_t* dst, long n, hipStream_t s) {

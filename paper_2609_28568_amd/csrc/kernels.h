@@ -102,6 +102,35 @@ hipError_t launch_cross_entropy(bf16_t* logits, const int32_t* targets, float* l
                                 float grad_scale, int write_grad, hipStream_t s);
 // mean of n floats into out[0] (single block, fixed order)
 hipError_t launch_mean(const float* x, int n, float* out, hipStream_t s);
+// out[0] = scale * sum of x[0..n)
+hipError_t launch_sum_scaled(const float* x, int n, float scale, float* out, hipStream_t s);
+// Cross-entropy whose rows (tokens) at positions row % T < mask_from carry no
+// loss: their loss is 0 and, with write_grad, their gradient row is 0.
+hipError_t launch_cross_entropy_masked(bf16_t* logits, const int32_t* targets, float* losses, int rows, int V, int Vp,
+                                       float grad_scale, int write_grad, int T, int mask_from, hipStream_t s);
+
+// ---------------------------------------------------------------- Qwen3-shaped adapter step
+hipError_t launch_embed_gather(const int32_t* ids, const bf16_t* table, bf16_t* x, long rows, int C, hipStream_t s);
+// y = x / sqrt(mean(x^2) + eps) * w per row; rstd [rows] saved
+hipError_t launch_rmsnorm_fwd(const bf16_t* x, const bf16_t* w, bf16_t* y, float* rstd, int rows, int C, float eps,
+                              hipStream_t s);
+// dres (=|+=) the RMSNorm input gradient (the gain is frozen)
+hipError_t launch_rmsnorm_bwd(const bf16_t* dy, const bf16_t* x, const float* rstd, const bf16_t* w, bf16_t* dres,
+                              int accumulate, int rows, int C, hipStream_t s);
+// raw q|k|v [BT][(H + 2 Hkv) hd] -> packed q|k|v [BT][3 H hd] for the attention
+// kernels: query and key heads RMS-normalised and rotated, key/value heads
+// repeated over their query-head groups; rstd of every q and k head saved
+hipError_t launch_qknorm_rope_fwd(const bf16_t* raw, const bf16_t* qn_w, const bf16_t* kn_w, const float* cosT,
+                                  const float* sinT, bf16_t* packed, float* rq, float* rk, int BT, int T, int H, int Hkv,
+                                  int hd, float eps, hipStream_t s);
+hipError_t launch_qknorm_rope_bwd(const bf16_t* dpacked, const bf16_t* raw, const bf16_t* qn_w, const bf16_t* kn_w,
+                                  const float* cosT, const float* sinT, const float* rq, const float* rk, bf16_t* draw,
+                                  int BT, int T, int H, int Hkv, int hd, hipStream_t s);
+// m = silu(g) * u over gu = [g | u] ([rows][2F]); and the gradient pair
+hipError_t launch_swiglu_fwd(const bf16_t* gu, bf16_t* m, long rows, int F, hipStream_t s);
+hipError_t launch_swiglu_bwd(const bf16_t* dm, const bf16_t* gu, bf16_t* dgu, long rows, int F, hipStream_t s);
+// x[r][c] *= sc for r < rows, c < cols (row stride ld)
+hipError_t launch_scale_bf16(bf16_t* x, long rows, int cols, int ld, float sc, hipStream_t s);
 
 // fp32 -> bf16 copy of n elements (n % 4 == 0)
 hipError_t launch_cast_bf16(const float* src, bf16_t* dst, long n, hipStream_t s);

@@ -1,0 +1,344 @@
+// Elementwise and normalisation kernels of the Qwen3-shaped adapter step:
+// token gather from a bf16 table, RMSNorm forward and backward over rows, the
+// per-head RMSNorm + rotary embedding of queries and keys (which also repacks
+// q|k|v for the attention kernels, repeating each key/value head for its group
+// of query heads), the SwiGLU gate and its derivative, and an in-place scale.
+#include "common.h"
+#include "kernels.h"
+
+namespace {
+
+// x[row] = table[id[row]] (bf16 rows of C elements, C a multiple of 8)
+__global__ void embed_gather_kernel(const int32_t* __restrict__ ids, const bf16_t* __restrict__ table,
+                                    bf16_t* __restrict__ x, long rows, int C) {
+  const long i = ((long)blockIdx.x * blockDim.x + threadIdx.x) * 8;
+  if (i >= rows * C) return;
+  const long row = i / C;
+  const int c = (int)(i % C);
+  *reinterpret_cast<uint4*>(x + i) = *reinterpret_cast<const uint4*>(table + (size_t)ids[row] * C + c);
+}
+
+// One row per wave; lane owns 4-channel chunks c = 4*(lane + 64*i). Loads of
+// a row are issued at once from clamped addresses and masked afterwards.
+template <int MAXCH>
+__global__ __launch_bounds__(256) void rmsnorm_fwd_kernel(const bf16_t* __restrict__ x, const bf16_t* __restrict__ w,
+                                                          bf16_t* __restrict__ y, float* __restrict__ rstd_out,
+                                                          int rows, int C, float eps) {
+  const int lane = threadIdx.x & 63;
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= rows) return;
+  const bf16_t* xr = x + (size_t)row * C;
+  uint2 xu[MAXCH], wu[MAXCH];
+#pragma unroll
+  for (int i = 0; i < MAXCH; ++i) {
+    const int c = min(4 * (lane + 64 * i), C - 4);
+    xu[i] = *reinterpret_cast<const uint2*>(xr + c);
+    wu[i] = *reinterpret_cast<const uint2*>(w + c);
+  }
+  float v[MAXCH][4];
+  float ss = 0.0f;
+#pragma unroll
+  for (int i = 0; i < MAXCH; ++i) {
+    const bool in = 4 * (lane + 64 * i) < C;
+    v[i][0] = in ? lo_f(xu[i].x) : 0.0f;
+    v[i][1] = in ? hi_f(xu[i].x) : 0.0f;
+    v[i][2] = in ? lo_f(xu[i].y) : 0.0f;
+    v[i][3] = in ? hi_f(xu[i].y) : 0.0f;
+    ss += v[i][0] * v[i][0] + v[i][1] * v[i][1] + v[i][2] * v[i][2] + v[i][3] * v[i][3];
+  }
+  const float rstd = 1.0f / sqrtf(wave_sum(ss) / C + eps);
+  bf16_t* yr = y + (size_t)row * C;
+#pragma unroll
+  for (int i = 0; i < MAXCH; ++i) {
+    const int c = 4 * (lane + 64 * i);
+    if (c < C) {
+      const float o0 = v[i][0] * rstd * lo_f(wu[i].x), o1 = v[i][1] * rstd * hi_f(wu[i].x);
+      const float o2 = v[i][2] * rstd * lo_f(wu[i].y), o3 = v[i][3] * rstd * hi_f(wu[i].y);
+      *reinterpret_cast<uint2*>(yr + c) = make_uint2(pack2(o0, o1), pack2(o2, o3));
+    }
+  }
+  if (lane == 0) rstd_out[row] = rstd;
+}
+
+// dres (=|+=) rstd (g - xhat mean(g xhat)), g = dy w, xhat = x rstd (gain frozen)
+template <int MAXCH>
+__global__ __launch_bounds__(256) void rmsnorm_bwd_kernel(const bf16_t* __restrict__ dy, const bf16_t* __restrict__ x,
+                                                          const float* __restrict__ rstd_in,
+                                                          const bf16_t* __restrict__ w, bf16_t* __restrict__ dres,
+                                                          int accumulate, int rows, int C) {
+  const int lane = threadIdx.x & 63;
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= rows) return;
+  const bf16_t* xr = x + (size_t)row * C;
+  const bf16_t* dr = dy + (size_t)row * C;
+  bf16_t* rr = dres + (size_t)row * C;
+  uint2 xu[MAXCH], du[MAXCH], wu[MAXCH], ru[MAXCH];
+#pragma unroll
+  for (int i = 0; i < MAXCH; ++i) {
+    const int c = min(4 * (lane + 64 * i), C - 4);
+    xu[i] = *reinterpret_cast<const uint2*>(xr + c);
+    du[i] = *reinterpret_cast<const uint2*>(dr + c);
+    wu[i] = *reinterpret_cast<const uint2*>(w + c);
+    ru[i] = accumulate ? *reinterpret_cast<const uint2*>(rr + c) : make_uint2(0, 0);
+  }
+  const float rstd = rstd_in[row];
+  float xh[MAXCH][4], g[MAXCH][4];
+  float s = 0.0f;
+#pragma unroll
+  for (int i = 0; i < MAXCH; ++i) {
+    const bool in = 4 * (lane + 64 * i) < C;
+    const float xv[4] = {lo_f(xu[i].x), hi_f(xu[i].x), lo_f(xu[i].y), hi_f(xu[i].y)};
+    const float dv[4] = {lo_f(du[i].x), hi_f(du[i].x), lo_f(du[i].y), hi_f(du[i].y)};
+    const float wv[4] = {lo_f(wu[i].x), hi_f(wu[i].x), lo_f(wu[i].y), hi_f(wu[i].y)};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      xh[i][e] = in ? xv[e] * rstd : 0.0f;
+      g[i][e] = in ? dv[e] * wv[e] : 0.0f;
+      s += g[i][e] * xh[i][e];
+    }
+  }
+  const float m = wave_sum(s) / C;
+#pragma unroll
+  for (int i = 0; i < MAXCH; ++i) {
+    const int c = 4 * (lane + 64 * i);
+    if (c < C) {
+      float o[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) o[e] = rstd * (g[i][e] - xh[i][e] * m);
+      o[0] += lo_f(ru[i].x); o[1] += hi_f(ru[i].x); o[2] += lo_f(ru[i].y); o[3] += hi_f(ru[i].y);
+      *reinterpret_cast<uint2*>(rr + c) = make_uint2(pack2(o[0], o[1]), pack2(o[2], o[3]));
+    }
+  }
+}
+
+// Per (token, head) of width 128: one wave, lane l holding elements 2l, 2l+1
+// (l < 32: first half; l >= 32: second half), so rotary pair (i, i + 64) is
+// lanes (l, l ^ 32). Query heads 0..H-1 and key heads 0..Hkv-1 are
+// RMS-normalised with their gains and rotated by the token's angles
+// (cos/sin tables [T][64] in fp32); value heads are copied. Output layout:
+// q [H*128] | k [H*128] | v [H*128], key/value head j repeated for query
+// heads j*G .. j*G+G-1 (G = H / Hkv).
+constexpr int QK_HD = 128;
+__global__ __launch_bounds__(256) void qknorm_rope_fwd_kernel(const bf16_t* __restrict__ raw, const bf16_t* __restrict__ qn_w,
+                                                              const bf16_t* __restrict__ kn_w, const float* __restrict__ cosT,
+                                                              const float* __restrict__ sinT, bf16_t* __restrict__ packed,
+                                                              float* __restrict__ rq, float* __restrict__ rk, int BT, int T,
+                                                              int H, int Hkv, float eps) {
+  const int lane = threadIdx.x & 63;
+  const long item = (long)blockIdx.x * 4 + (threadIdx.x >> 6);   // (token, head slot) over H + 2 Hkv slots
+  const int slots = H + 2 * Hkv;
+  if (item >= (long)BT * slots) return;
+  const int tok = (int)(item / slots), hs = (int)(item % slots);
+  const int t = tok % T;
+  const int G = H / Hkv;
+  const int rawW = slots * QK_HD, outW = 3 * H * QK_HD;
+  const uint32_t u = *reinterpret_cast<const uint32_t*>(raw + (size_t)tok * rawW + hs * QK_HD + 2 * lane);
+  float a = lo_f(u), b = hi_f(u);
+  bf16_t* orow = packed + (size_t)tok * outW;
+  if (hs >= H + Hkv) {   // value head: copy to its G query-head slots
+    const int j = hs - H - Hkv;
+    for (int k = 0; k < G; ++k)
+      *reinterpret_cast<uint32_t*>(orow + 2 * H * QK_HD + (j * G + k) * QK_HD + 2 * lane) = u;
+    return;
+  }
+  const bool isq = hs < H;
+  const bf16_t* w = isq ? qn_w : kn_w;
+  const float rstd = 1.0f / sqrtf(wave_sum(a * a + b * b) / QK_HD + eps);
+  const uint32_t wu = *reinterpret_cast<const uint32_t*>(w + 2 * lane);
+  a = a * rstd * lo_f(wu);
+  b = b * rstd * hi_f(wu);
+  // rotate: pair index p = (2 lane) mod 64 and +1; first half x1, second half x2
+  const float pa = __shfl_xor(a, 32), pb = __shfl_xor(b, 32);
+  const int p = (2 * lane) & 63;
+  const float c0 = cosT[(size_t)t * 64 + p], c1 = cosT[(size_t)t * 64 + p + 1];
+  const float s0 = sinT[(size_t)t * 64 + p], s1 = sinT[(size_t)t * 64 + p + 1];
+  float ya, yb;
+  if (lane < 32) { ya = a * c0 - pa * s0; yb = b * c1 - pb * s1; }   // x1 cos - x2 sin
+  else { ya = a * c0 + pa * s0; yb = b * c1 + pb * s1; }             // x2 cos + x1 sin
+  const uint32_t o = pack2(ya, yb);
+  if (isq) {
+    *reinterpret_cast<uint32_t*>(orow + hs * QK_HD + 2 * lane) = o;
+    if (lane == 0) rq[(size_t)tok * H + hs] = rstd;
+  } else {
+    const int j = hs - H;
+    for (int k = 0; k < G; ++k) *reinterpret_cast<uint32_t*>(orow + H * QK_HD + (j * G + k) * QK_HD + 2 * lane) = o;
+    if (lane == 0) rk[(size_t)tok * Hkv + j] = rstd;
+  }
+}
+
+// Backward of qknorm_rope_fwd_kernel: dpacked (q | k | v over H heads each)
+// -> draw (q over H heads | k over Hkv | v over Hkv). A key/value head sums
+// the gradients of its G repeated slots; queries and keys then go back
+// through the rotation (its transpose) and the RMSNorm.
+__global__ __launch_bounds__(256) void qknorm_rope_bwd_kernel(const bf16_t* __restrict__ dpacked, const bf16_t* __restrict__ raw,
+                                                              const bf16_t* __restrict__ qn_w, const bf16_t* __restrict__ kn_w,
+                                                              const float* __restrict__ cosT, const float* __restrict__ sinT,
+                                                              const float* __restrict__ rq, const float* __restrict__ rk,
+                                                              bf16_t* __restrict__ draw, int BT, int T, int H, int Hkv) {
+  const int lane = threadIdx.x & 63;
+  const long item = (long)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int slots = H + 2 * Hkv;
+  if (item >= (long)BT * slots) return;
+  const int tok = (int)(item / slots), hs = (int)(item % slots);
+  const int t = tok % T;
+  const int G = H / Hkv;
+  const int rawW = slots * QK_HD, pW = 3 * H * QK_HD;
+  const bf16_t* prow = dpacked + (size_t)tok * pW;
+  float da = 0.0f, db = 0.0f;
+  if (hs < H) {
+    const uint32_t g = *reinterpret_cast<const uint32_t*>(prow + hs * QK_HD + 2 * lane);
+    da = lo_f(g); db = hi_f(g);
+  } else {
+    const int j = hs < H + Hkv ? hs - H : hs - H - Hkv;
+    const int base = hs < H + Hkv ? H * QK_HD : 2 * H * QK_HD;
+    for (int k = 0; k < G; ++k) {
+      const uint32_t g = *reinterpret_cast<const uint32_t*>(prow + base + (j * G + k) * QK_HD + 2 * lane);
+      da += lo_f(g); db += hi_f(g);
+    }
+  }
+  bf16_t* drow = draw + (size_t)tok * rawW + hs * QK_HD + 2 * lane;
+  if (hs >= H + Hkv) {
+    *reinterpret_cast<uint32_t*>(drow) = pack2(da, db);
+    return;
+  }
+  // transpose rotation: d1 cos + d2 sin (first half), d2 cos - d1 sin (second half)
+  const float pa = __shfl_xor(da, 32), pb = __shfl_xor(db, 32);
+  const int p = (2 * lane) & 63;
+  const float c0 = cosT[(size_t)t * 64 + p], c1 = cosT[(size_t)t * 64 + p + 1];
+  const float s0 = sinT[(size_t)t * 64 + p], s1 = sinT[(size_t)t * 64 + p + 1];
+  float na, nb;
+  if (lane < 32) { na = da * c0 + pa * s0; nb = db * c1 + pb * s1; }
+  else { na = da * c0 - pa * s0; nb = db * c1 - pb * s1; }
+  // RMSNorm backward over the head (gain frozen)
+  const bool isq = hs < H;
+  const uint32_t xu = *reinterpret_cast<const uint32_t*>(raw + (size_t)tok * rawW + hs * QK_HD + 2 * lane);
+  const uint32_t wu = *reinterpret_cast<const uint32_t*>((isq ? qn_w : kn_w) + 2 * lane);
+  const float rstd = isq ? rq[(size_t)tok * H + hs] : rk[(size_t)tok * Hkv + (hs - H)];
+  const float xa = lo_f(xu) * rstd, xb = hi_f(xu) * rstd;
+  const float ga = na * lo_f(wu), gb = nb * hi_f(wu);
+  const float m = wave_sum(ga * xa + gb * xb) / QK_HD;
+  *reinterpret_cast<uint32_t*>(drow) = pack2(rstd * (ga - xa * m), rstd * (gb - xb * m));
+}
+
+DEV float sigmoid_f(float x) { return 1.0f / (1.0f + __expf(-x)); }
+
+// m[r][c] = silu(gu[r][c]) * gu[r][F + c]; 4 columns per thread
+__global__ void swiglu_fwd_kernel(const bf16_t* __restrict__ gu, bf16_t* __restrict__ m, long rows, int F) {
+  const long i = ((long)blockIdx.x * blockDim.x + threadIdx.x) * 4;
+  if (i >= rows * F) return;
+  const long r = i / F;
+  const int c = (int)(i % F);
+  const uint2 g = *reinterpret_cast<const uint2*>(gu + (size_t)r * 2 * F + c);
+  const uint2 u = *reinterpret_cast<const uint2*>(gu + (size_t)r * 2 * F + F + c);
+  const float gv[4] = {lo_f(g.x), hi_f(g.x), lo_f(g.y), hi_f(g.y)};
+  const float uv[4] = {lo_f(u.x), hi_f(u.x), lo_f(u.y), hi_f(u.y)};
+  float o[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) o[e] = gv[e] * sigmoid_f(gv[e]) * uv[e];
+  *reinterpret_cast<uint2*>(m + i) = make_uint2(pack2(o[0], o[1]), pack2(o[2], o[3]));
+}
+
+// dgu = [dm * u * silu'(g) | dm * silu(g)], silu'(g) = s (1 + g (1 - s))
+__global__ void swiglu_bwd_kernel(const bf16_t* __restrict__ dm, const bf16_t* __restrict__ gu, bf16_t* __restrict__ dgu,
+                                  long rows, int F) {
+  const long i = ((long)blockIdx.x * blockDim.x + threadIdx.x) * 4;
+  if (i >= rows * F) return;
+  const long r = i / F;
+  const int c = (int)(i % F);
+  const uint2 d = *reinterpret_cast<const uint2*>(dm + i);
+  const uint2 g = *reinterpret_cast<const uint2*>(gu + (size_t)r * 2 * F + c);
+  const uint2 u = *reinterpret_cast<const uint2*>(gu + (size_t)r * 2 * F + F + c);
+  const float dv[4] = {lo_f(d.x), hi_f(d.x), lo_f(d.y), hi_f(d.y)};
+  const float gv[4] = {lo_f(g.x), hi_f(g.x), lo_f(g.y), hi_f(g.y)};
+  const float uv[4] = {lo_f(u.x), hi_f(u.x), lo_f(u.y), hi_f(u.y)};
+  float dg[4], du[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const float s = sigmoid_f(gv[e]);
+    dg[e] = dv[e] * uv[e] * s * (1.0f + gv[e] * (1.0f - s));
+    du[e] = dv[e] * gv[e] * s;
+  }
+  *reinterpret_cast<uint2*>(dgu + (size_t)r * 2 * F + c) = make_uint2(pack2(dg[0], dg[1]), pack2(dg[2], dg[3]));
+  *reinterpret_cast<uint2*>(dgu + (size_t)r * 2 * F + F + c) = make_uint2(pack2(du[0], du[1]), pack2(du[2], du[3]));
+}
+
+// x[r][c] *= s for rows x cols (row stride ld), bf16 in place
+__global__ void scale_bf16_kernel(bf16_t* __restrict__ x, long rows, int cols, int ld, float s) {
+  const long i = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= rows * cols) return;
+  const long r = i / cols;
+  const int c = (int)(i % cols);
+  bf16_t* p = x + (size_t)r * ld + c;
+  *p = f2bf(bf2f(*p) * s);
+}
+
+inline unsigned nblocks(long n, int nt) { return (unsigned)((n + nt - 1) / nt); }
+
+}  // namespace
+
+hipError_t launch_embed_gather(const int32_t* ids, const bf16_t* table, bf16_t* x, long rows, int C, hipStream_t s) {
+  if (C % 8) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(embed_gather_kernel, dim3(nblocks(rows * C / 8, 256)), dim3(256), 0, s, ids, table, x, rows, C);
+  return hipGetLastError();
+}
+
+hipError_t launch_rmsnorm_fwd(const bf16_t* x, const bf16_t* w, bf16_t* y, float* rstd, int rows, int C, float eps,
+                              hipStream_t s) {
+  if (C % 4) return hipErrorInvalidValue;
+  const dim3 g((rows + 3) / 4), b(256);
+  if (C <= 256) hipLaunchKernelGGL(rmsnorm_fwd_kernel<1>, g, b, 0, s, x, w, y, rstd, rows, C, eps);
+  else if (C <= 512) hipLaunchKernelGGL(rmsnorm_fwd_kernel<2>, g, b, 0, s, x, w, y, rstd, rows, C, eps);
+  else if (C <= 1024) hipLaunchKernelGGL(rmsnorm_fwd_kernel<4>, g, b, 0, s, x, w, y, rstd, rows, C, eps);
+  else if (C <= 2048) hipLaunchKernelGGL(rmsnorm_fwd_kernel<8>, g, b, 0, s, x, w, y, rstd, rows, C, eps);
+  else return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+hipError_t launch_rmsnorm_bwd(const bf16_t* dy, const bf16_t* x, const float* rstd, const bf16_t* w, bf16_t* dres,
+                              int accumulate, int rows, int C, hipStream_t s) {
+  if (C % 4) return hipErrorInvalidValue;
+  const dim3 g((rows + 3) / 4), b(256);
+  if (C <= 256) hipLaunchKernelGGL(rmsnorm_bwd_kernel<1>, g, b, 0, s, dy, x, rstd, w, dres, accumulate, rows, C);
+  else if (C <= 512) hipLaunchKernelGGL(rmsnorm_bwd_kernel<2>, g, b, 0, s, dy, x, rstd, w, dres, accumulate, rows, C);
+  else if (C <= 1024) hipLaunchKernelGGL(rmsnorm_bwd_kernel<4>, g, b, 0, s, dy, x, rstd, w, dres, accumulate, rows, C);
+  else if (C <= 2048) hipLaunchKernelGGL(rmsnorm_bwd_kernel<8>, g, b, 0, s, dy, x, rstd, w, dres, accumulate, rows, C);
+  else return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+hipError_t launch_qknorm_rope_fwd(const bf16_t* raw, const bf16_t* qn_w, const bf16_t* kn_w, const float* cosT,
+                                  const float* sinT, bf16_t* packed, float* rq, float* rk, int BT, int T, int H, int Hkv,
+                                  int hd, float eps, hipStream_t s) {
+  if (hd != QK_HD || Hkv < 1 || H % Hkv) return hipErrorInvalidValue;
+  const long items = (long)BT * (H + 2 * Hkv);
+  hipLaunchKernelGGL(qknorm_rope_fwd_kernel, dim3(nblocks(items, 4)), dim3(256), 0, s, raw, qn_w, kn_w, cosT, sinT,
+                     packed, rq, rk, BT, T, H, Hkv, eps);
+  return hipGetLastError();
+}
+
+hipError_t launch_qknorm_rope_bwd(const bf16_t* dpacked, const bf16_t* raw, const bf16_t* qn_w, const bf16_t* kn_w,
+                                  const float* cosT, const float* sinT, const float* rq, const float* rk, bf16_t* draw,
+                                  int BT, int T, int H, int Hkv, int hd, hipStream_t s) {
+  if (hd != QK_HD || Hkv < 1 || H % Hkv) return hipErrorInvalidValue;
+  const long items = (long)BT * (H + 2 * Hkv);
+  hipLaunchKernelGGL(qknorm_rope_bwd_kernel, dim3(nblocks(items, 4)), dim3(256), 0, s, dpacked, raw, qn_w, kn_w, cosT,
+                     sinT, rq, rk, draw, BT, T, H, Hkv);
+  return hipGetLastError();
+}
+
+hipError_t launch_swiglu_fwd(const bf16_t* gu, bf16_t* m, long rows, int F, hipStream_t s) {
+  if (F % 4) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(swiglu_fwd_kernel, dim3(nblocks(rows * F / 4, 256)), dim3(256), 0, s, gu, m, rows, F);
+  return hipGetLastError();
+}
+
+hipError_t launch_swiglu_bwd(const bf16_t* dm, const bf16_t* gu, bf16_t* dgu, long rows, int F, hipStream_t s) {
+  if (F % 4) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(swiglu_bwd_kernel, dim3(nblocks(rows * F / 4, 256)), dim3(256), 0, s, dm, gu, dgu, rows, F);
+  return hipGetLastError();
+}
+
+hipError_t launch_scale_bf16(bf16_t* x, long rows, int cols, int ld, float sc, hipStream_t s) {
+  hipLaunchKernelGGL(scale_bf16_kernel, dim3(nblocks(rows * cols, 256)), dim3(256), 0, s, x, rows, cols, ld, sc);
+  return hipGetLastError();
+}

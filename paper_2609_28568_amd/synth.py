@@ -148,3 +148,65 @@ def block_inputs(w: dict, seed: int = SEED):
     x = round_to_bf16(g.standard_normal(size=(BT, C), dtype=np.float32))
     dy = round_to_bf16(g.standard_normal(size=(BT, C), dtype=np.float32) * np.float32(1e-3))
     return x, dy
+
+
+# ---------------------------------------------------------------------------
+# Qwen3-shaped adapter step (section "The clinical stage")
+# ---------------------------------------------------------------------------
+
+# The paper's base model is Qwen3 at 0.6 billion parameters; its shape is the
+# public configuration of that model. The benchmark geometry is four
+# sequences of 2048 tokens, adapters on the attention projections q, k, v, o.
+QWEN3_WORKLOADS = {
+    # two layers, several GEMM and attention tiles, a ragged sequence tail
+    "qwen3_tiny": dict(n_layer=2, d_model=256, n_head=4, n_kv_head=2, head_dim=128, d_ff=512, vocab=1024,
+                       max_seq_len=128, B=2, T=96, lora_rank=16, lora_alpha=32.0,
+                       lora_targets=("q", "k", "v", "o", "gate", "up", "down"), loss_from=0.5,
+                       token_dist="zipf"),
+    "qwen3_06b_lora": dict(n_layer=28, d_model=1024, n_head=16, n_kv_head=8, head_dim=128, d_ff=3072,
+                           vocab=151936, max_seq_len=2048, B=4, T=2048, lora_rank=16, lora_alpha=32.0,
+                           lora_targets=("q", "k", "v", "o"), loss_from=0.5, token_dist="zipf"),
+}
+
+# Adapter optimiser: the paper gives no separate betas, decay or rate for this
+# stage; these are the usual adapter fine-tuning values, with the global-norm
+# clip of the paper's optimisation section.
+QWEN3_OPTIM = dict(lr=2e-4, beta1=0.9, beta2=0.999, adam_eps=1e-8, weight_decay=0.0, grad_clip=1.0,
+                   rms_eps=1e-6, rope_theta=1e6)
+
+
+def _qwen3_dims(w: dict) -> dict:
+    C, F = w["d_model"], w["d_ff"]
+    qd, kvd = w["n_head"] * w["head_dim"], w["n_kv_head"] * w["head_dim"]
+    return {"q": (C, qd), "k": (C, kvd), "v": (C, kvd), "o": (qd, C), "gate": (C, F), "up": (C, F),
+            "down": (F, C)}
+
+
+def init_qwen3(w: dict, seed: int = SEED, std: float = 0.02, b_std: float = 0.0, norm_jitter: float = 0.0):
+    """Frozen base parameters (bf16-representable fp32) and fp32 adapters,
+    drawn in a fixed order, named per projection as [out, in] stacked over
+    layers: matrices ~ N(0, std); RMSNorm gains 1 (+ N(0, norm_jitter));
+    adapter A ~ N(0, std) [L, r, in]; adapter B ~ N(0, b_std) [L, out, r]
+    (zero by default, the usual adapter initialisation)."""
+    g = rng(seed, STREAM_WEIGHTS)
+    L, C, V, hd, r = w["n_layer"], w["d_model"], w["vocab"], w["head_dim"], w["lora_rank"]
+    dims = _qwen3_dims(w)
+
+    def normal(shape, s):
+        return (g.standard_normal(size=shape, dtype=np.float32) * np.float32(s)).astype(np.float32)
+
+    def gain(shape):
+        return (np.ones(shape, np.float32) + normal(shape, norm_jitter)).astype(np.float32)
+
+    base = {"embed": normal((V, C), std), "in_norm": gain((L, C)), "q_norm": gain((L, hd)),
+            "k_norm": gain((L, hd)), "post_norm": gain((L, C)), "final_norm": gain((C,))}
+    for p in ("q", "k", "v", "o", "gate", "up", "down"):
+        i, o = dims[p]
+        base[p] = normal((L, o, i), std)
+    base = {k: round_to_bf16(v) for k, v in base.items()}
+    lora = {}
+    for p in w["lora_targets"]:
+        i, o = dims[p]
+        lora[p + "_A"] = normal((L, r, i), std)
+        lora[p + "_B"] = normal((L, o, r), b_std) if b_std > 0 else np.zeros((L, o, r), np.float32)
+    return base, lora

@@ -1,0 +1,203 @@
+"""GPU parity of the Qwen3-shaped adapter step against the CPU oracle on small
+models the oracle runs in seconds: the masked loss and its per-position
+terms, every adapter gradient (per layer), exact zeros where the method fixes
+them (padding, masked positions, A-gradients with zero B), and the clipped
+AdamW update."""
+import numpy as np
+import pytest
+
+from oracle import qwen3 as q3
+from paper_2609_28568_amd import synth
+from tests.util import LOSS_ATOL, REL_L2, rel_l2
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+CASES = {
+    # all seven projections, T = 96 (one full 64-row tile and a ragged one)
+    "tiny_all": dict(),
+    # attention projections only, T = 48 below one tile, four sequences
+    "tiny_qkvo_short": dict(lora_targets=("q", "k", "v", "o"), B=4, T=48),
+    # four query heads per key/value head, three tiles and a tail, loss from a quarter
+    "gqa4_long": dict(n_head=8, n_kv_head=2, d_model=384, d_ff=640, vocab=640, max_seq_len=256, B=2, T=160,
+                      loss_from=0.25, lora_rank=8, lora_alpha=16.0,
+                      lora_targets=("q", "k", "v", "gate", "up")),
+}
+
+
+def _w(**over):
+    w = dict(synth.QWEN3_WORKLOADS["qwen3_tiny"])
+    w.update(over)
+    return w
+
+
+def _model(w, **optim):
+    from paper_2609_28568_amd import qwen3_binding as qb
+    o = dict(synth.QWEN3_OPTIM)
+    o.update(optim)
+    return qb.Qwen3(qb.make_config(w, o))
+
+
+def _ocfg(w, **optim):
+    o = dict(synth.QWEN3_OPTIM)
+    o.update(optim)
+    return q3.Qwen3Config.from_dict({**w, **o})
+
+
+@pytest.fixture(scope="module", params=list(CASES))
+def case(request):
+    w = _w(**CASES[request.param])
+    print(f"qwen3 case {request.param}: {w}", flush=True)
+    base, lora = synth.init_qwen3(w, seed=51, b_std=0.02, norm_jitter=0.1)
+    ids, tgt = synth.token_batch(w, seed=52)
+    ocfg = _ocfg(w)
+    cache = q3.forward(base, lora, ids, tgt, ocfg)
+    grads = q3.backward(base, lora, cache, ocfg)
+    m = _model(w)
+    m.set_base(base)
+    m.set_lora(lora)
+    tl = torch.zeros(w["B"] * w["T"], device="cuda")
+    m.forward(torch.from_numpy(ids), torch.from_numpy(tgt))
+    loss = m.loss(tl)
+    m.backward()
+    g = m.adapters("lora_grads")
+    packed = m.packed("lora_grads")
+    yield dict(w=w, cache=cache, grads=grads, m=m, loss=loss, losses=tl.cpu().numpy().reshape(w["B"], w["T"]),
+               gpu_grads=g, packed=packed)
+    m.close()
+
+
+def test_loss(case):
+    ref = float(case["cache"]["loss"])
+    print(f"  loss gpu {case['loss']:.6f} oracle {ref:.6f}")
+    assert abs(case["loss"] - ref) < LOSS_ATOL
+
+
+def test_per_position_losses_and_mask(case):
+    w = case["w"]
+    mf = int(np.floor(w["loss_from"] * w["T"]))
+    got, ref = case["losses"], case["cache"]["losses"]
+    assert np.all(got[:, :mf] == 0.0)
+    assert np.all(got[:, mf:] > 0.0)
+    assert np.max(np.abs(got - ref)) < 5 * LOSS_ATOL
+    assert rel_l2(got, ref) < REL_L2
+
+
+def test_adapter_gradients(case):
+    worst = 0.0
+    for k, ref in case["grads"].items():
+        if k == "dx0":
+            continue
+        for l in range(ref.shape[0]):
+            e = rel_l2(case["gpu_grads"][k][l], ref[l])
+            worst = max(worst, e)
+            assert e < REL_L2, (k, l, e)
+    print(f"  worst adapter gradient rel_l2 {worst:.2e}")
+
+
+def test_padding_gradients_exactly_zero(case):
+    from paper_2609_28568_amd import qwen3_binding as qb
+    r = case["w"]["lora_rank"]
+    for name, arr in case["packed"].items():
+        if name.endswith("_A"):
+            n = arr.shape[1] // qb.RP
+            for j in range(n):
+                assert np.all(arr[:, j * qb.RP + r:(j + 1) * qb.RP, :] == 0.0), name
+        else:
+            assert np.all(arr[:, :, r:] == 0.0), name
+
+
+def test_zero_B_gives_exactly_zero_A_gradients():
+    w = _w()
+    base, lora = synth.init_qwen3(w, seed=53, norm_jitter=0.1)
+    ids, tgt = synth.token_batch(w, seed=54)
+    m = _model(w)
+    m.set_base(base)
+    m.set_lora(lora)
+    m.forward(torch.from_numpy(ids), torch.from_numpy(tgt))
+    loss = m.loss()
+    m.backward()
+    g = m.adapters("lora_grads")
+    m.close()
+    ocfg = _ocfg(w)
+    c = q3.forward(base, lora, ids, tgt, ocfg)
+    ref = q3.backward(base, lora, c, ocfg)
+    assert abs(loss - float(c["loss"])) < LOSS_ATOL
+    for k in g:
+        if k.endswith("_A"):
+            assert np.all(g[k] == 0.0), k
+        else:
+            assert rel_l2(g[k], ref[k]) < REL_L2, k
+
+
+def test_adamw_matches_oracle_on_oracle_gradients():
+    """The oracle's adapter gradients go into the gradient buffer; two
+    optimizer steps (the first clipped, the second not) must follow the
+    oracle's clipped AdamW, and the bf16 copy must track the fp32 master."""
+    from paper_2609_28568_amd import qwen3_binding as qb
+    w = _w()
+    ocfg = _ocfg(w, lr=1e-3, weight_decay=0.01)
+    base, lora = synth.init_qwen3(w, seed=55, b_std=0.02)
+    m = _model(w, lr=1e-3, weight_decay=0.01)
+    m.set_base(base)
+    m.set_lora(lora)
+    ref_p = {k: v.astype(np.float64) for k, v in lora.items()}
+    ref_m = {k: np.zeros_like(v) for k, v in ref_p.items()}
+    ref_v = {k: np.zeros_like(v) for k, v in ref_p.items()}
+    g = np.random.default_rng(56)
+    ids, tgt = synth.token_batch(w, seed=57)
+    for step, gscale in enumerate((3.0, 0.05)):
+        m.forward(torch.from_numpy(ids), torch.from_numpy(tgt))
+        m.backward()
+        grads = {k: (g.standard_normal(v.shape) * gscale / np.sqrt(v.size)).astype(np.float32)
+                 for k, v in lora.items()}
+        m.set_packed("lora_grads", grads)
+        norm_out = torch.zeros(1, device="cuda")
+        m.adamw_step(step, norm_out)
+        norm = float(np.linalg.norm(np.concatenate([v.ravel().astype(np.float64) for v in grads.values()])))
+        assert abs(float(norm_out.item()) - norm) < 1e-5 * norm
+        coef = min(1.0, 1.0 / norm)
+        assert (coef < 1.0) == (step == 0)
+        q3.adamw_step(ref_p, {k: v.astype(np.float64) * coef for k, v in grads.items()}, ref_m, ref_v, step,
+                      ocfg)
+        got = m.adapters("lora_f32")
+        for k in lora:
+            e = rel_l2(got[k].astype(np.float64) - lora[k], ref_p[k] - lora[k])
+            assert e < 1e-3, (step, k, e)
+        gm = m.adapters("adam_m")
+        for k in lora:
+            assert rel_l2(gm[k], ref_m[k]) < 1e-5, k
+    packed32, packed16 = m.packed("lora_f32"), m.packed("lora_bf16")
+    for n in packed32:
+        assert np.array_equal(packed16[n], synth.round_to_bf16(packed32[n])), n
+        if n.endswith("_B"):
+            assert np.all(packed32[n][:, :, w["lora_rank"]:] == 0.0)
+    m.close()
+    del qb
+
+
+def test_call_order_errors():
+    from paper_2609_28568_amd import binding
+    w = _w()
+    base, lora = synth.init_qwen3(w, seed=58)
+    m = _model(w)
+    m.set_base(base)
+    m.set_lora(lora)
+    with pytest.raises(binding.LibError) as e:
+        m.backward()
+    assert e.value.status == binding.GPT2_ERR_STATE
+    with pytest.raises(binding.LibError) as e:
+        m.adamw_step(0)
+    assert e.value.status == binding.GPT2_ERR_STATE
+    ids, tgt = synth.token_batch(w)
+    m.forward(torch.from_numpy(ids), None)
+    with pytest.raises(binding.LibError):
+        m.backward()
+    with pytest.raises(binding.LibError):
+        m.loss()
+    m.forward(torch.from_numpy(ids), torch.from_numpy(tgt))
+    m.backward()
+    m.adamw_step(0)
+    with pytest.raises(binding.LibError):
+        m.adamw_step(1)
+    m.close()
