@@ -18,6 +18,8 @@ import os
 import sys
 import time
 
+import numpy as np
+
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
@@ -36,6 +38,154 @@ def flops_per_token(w: dict) -> float:
 
 def flops_per_token_palm(w: dict, n_params: int) -> float:
     return 6.0 * n_params + 12.0 * w["n_layer"] * w["d_model"] * w["T"]
+
+
+def qwen3_flops_per_token(w: dict) -> float:
+    """Algorithmic FLOPs per token of the adapter step, as the library
+    computes it: the frozen projections forward and their input gradients
+    (no weight gradients; the first layer's q|k|v input gradient, which would
+    only reach the frozen token table, is not computed), the LM head forward
+    and input gradient on the positions that carry loss only, causal
+    attention (q.k and p.v over the unmasked half, forward and backward),
+    and the adapters at their true rank (x A^T, u B^T, dy B, du A and the two
+    adapter gradients; du A skipped for the first layer's q|k|v)."""
+    L, C, F, V, T, r = w["n_layer"], w["d_model"], w["d_ff"], w["vocab"], w["T"], w["lora_rank"]
+    qd, kvd = w["n_head"] * w["head_dim"], w["n_kv_head"] * w["head_dim"]
+    qkvd = qd + 2 * kvd
+    n_layer_mm = L * (C * qkvd + qd * C + 2 * F * C + F * C)
+    loss_frac = (T - int(np.floor(w["loss_from"] * T))) / T
+    dense = 4.0 * n_layer_mm - 2.0 * C * qkvd + 4.0 * V * C * loss_frac
+    attn = 6.0 * L * qd * (T + 1)
+    groups = {"q": ("qkv", C, qd), "k": ("qkv", C, kvd), "v": ("qkv", C, kvd), "o": ("o", qd, C),
+              "gate": ("gu", C, F), "up": ("gu", C, F), "down": ("down", F, C)}
+    adapter = 0.0
+    for t in w["lora_targets"]:
+        _, i, o = groups[t]
+        adapter += L * 6.0 * r * (i + o) - (2.0 * r * i if t in ("q", "k", "v") else 0.0)
+    return dense + attn + adapter
+
+
+def qwen3_cpu_baseline(w: dict, base: dict, lora: dict, ids, tgt) -> dict:
+    """The oracle's adapter step (forward, masked loss, backward, clip, AdamW)
+    on the first sequence of the batch through the full model."""
+    from oracle import qwen3 as q3
+    from threadpoolctl import threadpool_info
+    from paper_2609_28568_amd import synth
+    ws = dict(w)
+    ws["B"] = 1
+    cfg = q3.Qwen3Config.from_dict({**ws, **synth.QWEN3_OPTIM})
+    lo = {k: v.copy() for k, v in lora.items()}
+    m = {k: np.zeros_like(v) for k, v in lo.items()}
+    v = {k: np.zeros_like(v) for k, v in lo.items()}
+    t0 = time.perf_counter()
+    q3.train_step(base, lo, m, v, 0, ids[:1], tgt[:1], cfg)
+    dt = time.perf_counter() - t0
+    threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    return {"value": round(ws["T"] / dt, 3), "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": f"one adapter step (fwd+masked loss+bwd+clip+AdamW) on 1 sequence x {ws['T']} tokens of the "
+                      f"same model and token stream, numpy fp32, {dt:.1f} s"}
+
+
+def qwen3_bench(args) -> None:
+    """Throughput of the Qwen3-0.6B-shaped adapter step: forward, masked loss,
+    backward to the adapters through the frozen base, clip and AdamW on the
+    adapters, on B x T synthetic Zipf(1.1) tokens resident in HBM."""
+    import torch
+    from paper_2609_28568_amd import qwen3_binding as qb, synth
+
+    w = dict(synth.QWEN3_WORKLOADS[args.workload])
+    print(f"bench: {args.workload} B={w['B']} T={w['T']} on {torch.cuda.get_device_name(0)}",
+          file=sys.stderr, flush=True)
+    base, lora = synth.init_qwen3(w)
+    ids, tgt = synth.token_batch(w)
+    m = qb.Qwen3(qb.make_config(w, synth.QWEN3_OPTIM))
+    m.set_base(base)
+    m.set_lora(lora)
+    dev_ids, dev_tgt = torch.from_numpy(ids).cuda(), torch.from_numpy(tgt).cuda()
+    torch.cuda.synchronize()
+    probe = args.probe if args.probe in qb.KCLASS else "attn_bwd"
+
+    def step(i):
+        m.forward(dev_ids, dev_tgt)
+        m.backward()
+        m.adamw_step(i)
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    print(f"bench: warmup done, loss {m.loss():.4f}", file=sys.stderr, flush=True)
+    m.probe_reset()
+    stream = torch.cuda.current_stream()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev0.record(stream)
+    for i in range(args.steps):
+        if i == args.steps - 1:
+            m.probe_enable([probe])
+        step(args.warmup + i)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    gpu_ms = ev0.elapsed_time(ev1)
+    pr = m.probe_read(probe)
+    m.probe_enable([])
+    loss = m.loss()
+    print(f"bench: timed {args.steps} steps, wall {wall:.3f} s, loss {loss:.4f}", file=sys.stderr, flush=True)
+
+    extra = {}
+    if args.classes:
+        m.probe_reset()
+        m.probe_enable(list(qb.KCLASS))
+        for i in range(3):
+            step(args.warmup + args.steps + i)
+        torch.cuda.synchronize()
+        for c in qb.KCLASS:
+            r = m.probe_read(c)
+            if r["launches"]:
+                extra[c] = {"ms_per_step": round(r["ms"] / 3, 4), "launches_per_step": r["launches"] // 3,
+                            "tflops": round(r["flops"] / (r["ms"] * 1e-3) / 1e12, 1) if r["flops"] else None,
+                            "gbs": round(r["bytes"] / (r["ms"] * 1e-3) / 1e9, 1) if r["bytes"] else None}
+        m.probe_enable([])
+        print("bench: per-class " + json.dumps(extra), file=sys.stderr, flush=True)
+
+    tokens = w["B"] * w["T"]
+    tok_s = tokens / (wall / args.steps)
+    f_tok = qwen3_flops_per_token(w)
+    achieved = pr["flops"] / (pr["ms"] * 1e-3) / 1e12 if pr["ms"] else 0.0
+    roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": traffic_from_profiles(probe, args.workload),
+                "kernel": probe, "launches": pr["launches"],
+                "avg_launch_ms": round(pr["ms"] / max(pr["launches"], 1), 4),
+                "flops_per_launch": pr["flops"] / max(pr["launches"], 1)}
+    cpu = None
+    if not args.no_cpu_baseline:
+        print("bench: timing the CPU oracle on a 1-sequence sample", file=sys.stderr, flush=True)
+        cpu = qwen3_cpu_baseline(w, base, lora, ids, tgt)
+    out = {
+        "metric": "adapter fine-tuning tokens/sec on 1 MI355X, Qwen3-0.6B-shaped, rank-16 adapters; "
+                  "bf16 MFMA model-FLOPs util",
+        "value": round(tok_s, 1), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(wall * 1e3 / args.steps, 3), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": f"Qwen3-0.6B-shaped adapter step (fwd+masked loss+bwd+clip+AdamW), {args.workload}",
+                   "n_layer": w["n_layer"], "d_model": w["d_model"], "n_head": w["n_head"],
+                   "n_kv_head": w["n_kv_head"], "head_dim": w["head_dim"], "d_ff": w["d_ff"], "vocab": w["vocab"],
+                   "global_batch": w["B"], "seq_len": w["T"], "lora_rank": w["lora_rank"],
+                   "lora_targets": list(w["lora_targets"]), "loss_from": w["loss_from"],
+                   "tokens_per_step": tokens, "token_dist": "zipf(1.1)", "parallelism": "none"},
+        "mfu": round(tok_s * f_tok / (PEAK_BF16_TFLOPS * 1e12), 4),
+        "flops_per_token": f_tok,
+        "peak_tflops": PEAK_BF16_TFLOPS,
+        "gpu_event_ms_per_step": round(gpu_ms / args.steps, 3),
+        "final_loss": round(loss, 4),
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+    }
+    if extra:
+        out["classes"] = extra
+    print(json.dumps(out), flush=True)
+    m.close()
 
 
 def cpu_baseline(w: dict, params, ids, tgt) -> dict:
@@ -157,10 +307,12 @@ def main():
               file=sys.stderr)
         sys.exit(2)
 
-    import numpy as np
     import torch
     from paper_2609_28568_amd import binding, synth
 
+    if args.workload in synth.QWEN3_WORKLOADS:
+        qwen3_bench(args)
+        return
     w = dict(synth.WORKLOADS[args.workload])
     cfg = binding.make_config(w, synth.OPTIM)
     print(f"bench: {args.workload} B={w['B']} T={w['T']} on {torch.cuda.get_device_name(0)}",

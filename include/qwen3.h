@@ -88,7 +88,9 @@ gpt2_status qwen3_init(const qwen3_config* cfg, const qwen3_buffers* bufs, void*
 gpt2_status qwen3_sync_weights(qwen3_model* m);
 
 /* Forward over d_inputs [B*T] (int32 token ids in [0, vocab)); with d_targets
- * [B*T] also the masked loss and the logit gradient the backward needs. */
+ * [B*T] also the masked loss and the logit gradient the backward needs. The
+ * final norm and the LM head run on the positions that carry loss only (the
+ * others' logits enter neither the loss nor any gradient). */
 gpt2_status qwen3_forward(qwen3_model* m, const int32_t* d_inputs, const int32_t* d_targets);
 
 /* Adapter gradients of the masked mean loss into lora_grads (overwritten).
@@ -108,6 +110,28 @@ gpt2_status qwen3_loss(qwen3_model* m, float* loss_out, float* d_token_losses);
 
 void qwen3_destroy(qwen3_model* m);
 const char* qwen3_last_error(const qwen3_model* m);
+
+/* Kernel timing probes for measurement, as gpt2_probe_*: launches of the
+ * enabled classes are bracketed with HIP events on the model's stream, and
+ * their algorithmic FLOPs (GEMMs: 2 M N K at the true adapter rank;
+ * attention: the causal half) and bytes are summed per class.
+ * qwen3_probe_read synchronises and reports totals since the last reset. */
+enum {
+  QWEN3_K_GEMM_FWD = 0,      /* frozen projections and the LM head, forward */
+  QWEN3_K_GEMM_DX = 1,       /* their input gradients (the LM head's included) */
+  QWEN3_K_GEMM_ADAPTER = 2,  /* adapter products: x A^T, u B^T, dy B, du A, and the adapter gradients */
+  QWEN3_K_ATTN_FWD = 3,
+  QWEN3_K_ATTN_BWD = 4,
+  QWEN3_K_NORM = 5,          /* RMSNorm forward/backward, q/k head norm + rotary forward/backward */
+  QWEN3_K_CROSS_ENTROPY = 6,
+  QWEN3_K_OPTIMIZER = 7,     /* norm, clip coefficient and AdamW */
+  QWEN3_K_OTHER = 8,         /* embedding gather, SwiGLU, scales, reductions */
+  QWEN3_K_COUNT = 9
+};
+gpt2_status qwen3_probe_enable(qwen3_model* m, uint32_t class_mask);
+gpt2_status qwen3_probe_reset(qwen3_model* m);
+gpt2_status qwen3_probe_read(qwen3_model* m, int32_t kclass, double* total_ms, int64_t* launches, double* flops,
+                             double* bytes);
 
 #ifdef __cplusplus
 }

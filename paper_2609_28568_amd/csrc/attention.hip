@@ -253,8 +253,12 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(AttnArgs a) {
 // D[b,h,t] = sum_d dO * O, one thread per (token, head)
 // dK, dV for 128 keys (4 waves x 32), walking query tiles of 64 from the
 // diagonal to the end.
+// At hd 128 one workgroup per CU: the K/V fragments and the dK/dV
+// accumulators alone take 192 registers per lane, so the kernel needs the
+// accumulation registers that a single wave per SIMD may use (with two per
+// SIMD it spilled to scratch and ran 2.5x slower).
 template <int HD>
-__global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_kernel(AttnArgs a) {
+__global__ __launch_bounds__(256, HD >= 128 ? 1 : 2) void attn_bwd_dkdv_kernel(AttnArgs a) {
   using S = Shape<HD>;
   constexpr int STAGE = 2 * S::TBA + 1024;   // Q tile, dO tile, lse and D rows
   __shared__ __attribute__((aligned(1024))) char smem_raw[2 * STAGE];
@@ -324,57 +328,67 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkdv_kernel(AttnArgs a) {
     const lds_char_t* lr = Qs + 2 * S::TBA;   // lse [64] then D [64], fp32
     const bool diag = q0 < kv0w + 32 || q0 + TILE > T || kv0w + 32 > T;
 
-    floatx16 p[2], ds[2];
+    // Query halves t (rows 32t..32t+31 of the tile) against this wave's keys:
+    // scores and score gradients, then their contributions to dV and dK. At
+    // hd 128 the halves run one after the other (the K/V fragments and the
+    // dK/dV accumulators already take 192 registers); smaller heads keep both
+    // halves in flight.
+    constexpr int NT = HD >= 128 ? 1 : 2;
+#pragma unroll(HD >= 128 ? 1 : 2)
+    for (int t0 = 0; t0 < 2; t0 += NT) {
+      floatx16 p[NT], ds[NT];
 #pragma unroll
-    for (int t = 0; t < 2; ++t) {
-      zero(p[t]);
-      zero(ds[t]);
+      for (int i = 0; i < NT; ++i) {
+        const int t = t0 + i;
+        zero(p[i]);
+        zero(ds[i]);
 #pragma unroll
-      for (int k = 0; k < S::KS; ++k) {
-        p[t] = mfma32(read_row<HD>(Qs, 32 * t + lk, 2 * k + g), kf[k], p[t]);
-        ds[t] = mfma32(read_row<HD>(Ds, 32 * t + lk, 2 * k + g), vf[k], ds[t]);
+        for (int k = 0; k < S::KS; ++k) {
+          p[i] = mfma32(read_row<HD>(Qs, 32 * t + lk, 2 * k + g), kf[k], p[i]);
+          ds[i] = mfma32(read_row<HD>(Ds, 32 * t + lk, 2 * k + g), vf[k], ds[i]);
+        }
       }
-    }
-    // probabilities and their score gradients for the whole tile, masked only
-    // on tiles that straddle the diagonal or the sequence end
-    auto probs = [&](auto masked) {
+      // probabilities and their score gradients, masked only on tiles that
+      // straddle the diagonal or the sequence end
+      auto probs = [&](auto masked) {
 #pragma unroll
-      for (int t = 0; t < 2; ++t)
+        for (int i = 0; i < NT; ++i)
 #pragma unroll
-        for (int c4 = 0; c4 < 4; ++c4) {
-          // keep the per-group reads of lse and D next to their use (hoisting
-          // them all would run out of registers)
-          __builtin_amdgcn_sched_barrier(0);
-          const int qi = 32 * t + 8 * c4 + 4 * g;   // 4 consecutive queries
-          const v4f32 l4 = *reinterpret_cast<const lds_v4f32_t*>(lr + 4 * qi);
-          const v4f32 d4 = *reinterpret_cast<const lds_v4f32_t*>(lr + 256 + 4 * qi);
-          const float lv[4] = {l4.x * LOG2E, l4.y * LOG2E, l4.z * LOG2E, l4.w * LOG2E};
-          const float dvv[4] = {d4.x, d4.y, d4.z, d4.w};
-          // query qq = q0 + qi + e sees key kv if kv <= qq < T (and kv < T)
-          const int qlo = kv - q0 - qi, qhi = T - q0 - qi;
+          for (int c4 = 0; c4 < 4; ++c4) {
+            // keep the per-group reads of lse and D next to their use
+            // (hoisting them all would run out of registers)
+            __builtin_amdgcn_sched_barrier(0);
+            const int qi = 32 * (t0 + i) + 8 * c4 + 4 * g;   // 4 consecutive queries
+            const v4f32 l4 = *reinterpret_cast<const lds_v4f32_t*>(lr + 4 * qi);
+            const v4f32 d4 = *reinterpret_cast<const lds_v4f32_t*>(lr + 256 + 4 * qi);
+            const float lv[4] = {l4.x * LOG2E, l4.y * LOG2E, l4.z * LOG2E, l4.w * LOG2E};
+            const float dvv[4] = {d4.x, d4.y, d4.z, d4.w};
+            // query qq = q0 + qi + e sees key kv if kv <= qq < T (and kv < T)
+            const int qlo = kv - q0 - qi, qhi = T - q0 - qi;
 #pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const int r = 4 * c4 + e;
-            float pv = fast_exp2(p[t][r] * sc - lv[e]);
-            if constexpr (decltype(masked)::value) pv = (e >= qlo && e < qhi && kv < T) ? pv : 0.0f;
-            p[t][r] = pv;
-            ds[t][r] = pv * (ds[t][r] - dvv[e]);
+            for (int e = 0; e < 4; ++e) {
+              const int r = 4 * c4 + e;
+              float pv = fast_exp2(p[i][r] * sc - lv[e]);
+              if constexpr (decltype(masked)::value) pv = (e >= qlo && e < qhi && kv < T) ? pv : 0.0f;
+              p[i][r] = pv;
+              ds[i][r] = pv * (ds[i][r] - dvv[e]);
+            }
+          }
+      };
+      if (diag) probs(std::true_type{});
+      else probs(std::false_type{});
+#pragma unroll
+      for (int i = 0; i < NT; ++i)
+#pragma unroll
+        for (int hh = 0; hh < 2; ++hh) {
+          const bf16x8 pf = acc_slots(p[i], hh), sf = acc_slots(ds[i], hh);
+#pragma unroll
+          for (int d = 0; d < S::DT; ++d) {
+            dv[d] = mfma32(read_tr<HD>(Ds, 32 * d, 32 * (t0 + i) + 16 * hh, lane), pf, dv[d]);
+            dk[d] = mfma32(read_tr<HD>(Qs, 32 * d, 32 * (t0 + i) + 16 * hh, lane), sf, dk[d]);
           }
         }
-    };
-    if (diag) probs(std::true_type{});
-    else probs(std::false_type{});
-#pragma unroll
-    for (int t = 0; t < 2; ++t)
-#pragma unroll
-      for (int hh = 0; hh < 2; ++hh) {
-        const bf16x8 pf = acc_slots(p[t], hh), sf = acc_slots(ds[t], hh);
-#pragma unroll
-        for (int d = 0; d < S::DT; ++d) {
-          dv[d] = mfma32(read_tr<HD>(Ds, 32 * d, 32 * t + 16 * hh, lane), pf, dv[d]);
-          dk[d] = mfma32(read_tr<HD>(Qs, 32 * d, 32 * t + 16 * hh, lane), sf, dk[d]);
-        }
-      }
+    }
   }
 
   if (kv < T) {

@@ -23,6 +23,19 @@ __global__ void reduce_slices_kernel(const float* __restrict__ src, int nslices,
   *reinterpret_cast<float4*>(dst + i) = acc;
 }
 
+// dst[i] (bf16) = sum_s src[s*n + i], four elements per thread
+__global__ void reduce_slices_bf16_kernel(const float* __restrict__ src, int nslices, long n, bf16_t* __restrict__ dst) {
+  long i = ((long)blockIdx.x * blockDim.x + threadIdx.x) * 4;
+  if (i >= n) return;
+  float4 acc = make_float4(0, 0, 0, 0);
+#pragma unroll 16
+  for (int s = 0; s < nslices; ++s) {
+    float4 v = *reinterpret_cast<const float4*>(src + (size_t)s * n + i);
+    acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
+  }
+  *reinterpret_cast<uint2*>(dst + i) = make_uint2(pack2(acc.x, acc.y), pack2(acc.z, acc.w));
+}
+
 // Two independent reductions in one launch; blockIdx.y picks the segment.
 __global__ void reduce_slices2_kernel(const float* __restrict__ src, int nslices, long n, float* __restrict__ dst,
                                       const float* __restrict__ src2, int nslices2, long n2,
@@ -241,14 +254,18 @@ __global__ __launch_bounds__(NT) void cross_entropy_kernel(bf16_t* __restrict__ 
   __shared__ float shm[NW], shs[NW];
   const int row = blockIdx.x, tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   bf16_t* lr = logits + (size_t)row * Vp;
-  if (mask_from > 0 && row % T < mask_from) {
-    // a position that carries no loss: zero loss and, with GRAD, zero gradient
-    if (GRAD)
-      for (int c = tid; c < Vp / 8; c += NT) *reinterpret_cast<uint4*>(lr + c * 8) = make_uint4(0, 0, 0, 0);
-    if (tid == 0) losses[row] = 0.0f;
-    return;
+  // logits row `row` belongs to position pos: the rows are those of the
+  // positions t >= mask_from of every sequence of T, in order
+  const int nl = T - mask_from;
+  const int pos = (row / nl) * T + mask_from + row % nl;
+  if (mask_from > 0) {
+    // the positions without loss (B * mask_from of them, listed sequence by
+    // sequence) get a zero loss, spread over the workgroups
+    const int nmask = (int)(gridDim.x / nl) * mask_from;
+    for (int k = row + (int)gridDim.x * tid; k < nmask; k += (int)gridDim.x * NT)
+      losses[(k / mask_from) * T + k % mask_from] = 0.0f;
   }
-  const int tgt = targets[row];
+  const int tgt = targets[pos];
   // the target's logit, read before the row is overwritten (by every thread,
   // one broadcast address, so the load needs no branch; thread 0 uses it)
   const bf16_t xt_raw = lr[tgt];
@@ -329,7 +346,7 @@ __global__ __launch_bounds__(NT) void cross_entropy_kernel(bf16_t* __restrict__ 
           make_uint4(pack2(d[0], d[1]), pack2(d[2], d[3]), pack2(d[4], d[5]), pack2(d[6], d[7]));
     }
   }
-  if (tid == 0) losses[row] = mx + logf(sum) - bf2f(xt_raw);
+  if (tid == 0) losses[pos] = mx + logf(sum) - bf2f(xt_raw);
 }
 
 // ------------------------------------------------------------ casts
@@ -421,6 +438,12 @@ hipError_t launch_reduce_slices(const float* src, int nslices, long n, float* ds
   return hipGetLastError();
 }
 
+hipError_t launch_reduce_slices_bf16(const float* src, int nslices, long n, bf16_t* dst, hipStream_t s) {
+  if (n % 4) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(reduce_slices_bf16_kernel, dim3(blocks_for(n / 4, 256)), dim3(256), 0, s, src, nslices, n, dst);
+  return hipGetLastError();
+}
+
 hipError_t launch_reduce_slices2(const float* src, int nslices, long n, float* dst, const float* src2,
                                  int nslices2, long n2, float* dst2, int accumulate, hipStream_t s) {
   if (n % 4 || n2 % 4) return hipErrorInvalidValue;
@@ -484,7 +507,7 @@ void ce_launch(bf16_t* logits, const int32_t* targets, float* losses, int rows, 
 
 hipError_t launch_cross_entropy_masked(bf16_t* logits, const int32_t* targets, float* losses, int rows, int V, int Vp,
                                        float grad_scale, int write_grad, int T, int mask_from, hipStream_t s) {
-  if (Vp % 8 || T < 1) return hipErrorInvalidValue;
+  if (Vp % 8 || T < 1 || mask_from < 0 || mask_from >= T || rows % (T - mask_from)) return hipErrorInvalidValue;
   const int nch = Vp / 8;
   if (nch <= 256 * 2) ce_launch<256, 2>(logits, targets, losses, rows, V, Vp, grad_scale, write_grad, T, mask_from, s);
   else if (nch <= 512 * 13)

@@ -409,6 +409,8 @@ hipError_t launch_cfg(const GemmArgs& g, int a_t, int b_t, int epi, hipStream_t 
     return g.residual ? launch_t<BM, BN, BK, 2, false, true, EPI_BF16_RES>(g, s)
                       : launch_t<BM, BN, BK, 2, false, true, EPI_BF16>(g, s);
   if (!a_t && b_t && epi == EPI_GELU_BWD) return launch_t<BM, BN, BK, 2, false, true, EPI_GELU_BWD>(g, s);
+  // an input gradient with a long contraction, split into fp32 slices
+  if (!a_t && b_t && epi == EPI_F32 && !g.accumulate) return launch_t<BM, BN, BK, 2, false, true, EPI_F32>(g, s);
   if (a_t && b_t && epi == EPI_F32)
     return g.accumulate ? launch_t<BM, BN, BK, 2, true, true, EPI_F32_ACC>(g, s)
                         : launch_t<BM, BN, BK, 2, true, true, EPI_F32>(g, s);
@@ -438,7 +440,9 @@ GemmConfig gemm_config(int M, int N, int a_t, int b_t, int epi) {
       if (M >= 128) return {128, 192, epi == EPI_GELU_BWD ? 32 : 64};
     }
   }
-  if (M >= 256 && N >= 128 && N % 128 == 0) return {256, 128, 32};
+  // 256-row tiles only when they still give two workgroups per CU (a
+  // workgroup alone on a CU keeps its MFMA pipe about half busy)
+  if (M >= 256 && N >= 128 && N % 128 == 0 && (long)((M + 255) / 256) * (N / 128) >= 512) return {256, 128, 32};
   return {128, 128, 32};
 }
 

@@ -14,6 +14,7 @@
 
 #include "../../include/gpt2.h"
 #include "kernels.h"
+#include "probe.h"
 
 namespace {
 
@@ -223,11 +224,6 @@ WsLayout ws_layout(const Dims& d) {
   return w;
 }
 
-struct ProbeRec {
-  hipEvent_t a, b;
-  int cls;
-};
-
 }  // namespace
 
 struct gpt2_model {
@@ -242,12 +238,7 @@ struct gpt2_model {
   bool have_grads = false;     // gradients hold a backward result
   bool have_loss = false;
   std::string err;
-  // probes
-  uint32_t probe_mask = 0;
-  std::vector<ProbeRec> live;
-  std::vector<hipEvent_t> pool;
-  double ms[GPT2_K_COUNT] = {}, flops[GPT2_K_COUNT] = {}, bytes[GPT2_K_COUNT] = {};
-  int64_t launches[GPT2_K_COUNT] = {};
+  ProbeSet<GPT2_K_COUNT> probes;
 
   // typed pointers
   float* pf(int k) { return static_cast<float*>(buf.params_f32) + koff[k]; }
@@ -283,36 +274,10 @@ struct gpt2_model {
     return s;
   }
 
-  hipEvent_t get_event() {
-    if (!pool.empty()) {
-      hipEvent_t e = pool.back();
-      pool.pop_back();
-      return e;
-    }
-    hipEvent_t e = nullptr;
-    if (hipEventCreate(&e) != hipSuccess) return nullptr;
-    return e;
-  }
-
   // Launch through f(); optionally bracket it with events for the probes.
   template <class Fn>
   hipError_t run(int cls, double fl, double by, Fn f) {
-    const bool on = (probe_mask >> cls) & 1u;
-    hipEvent_t e0 = nullptr, e1 = nullptr;
-    if (on) {
-      e0 = get_event();
-      e1 = get_event();
-      if (e0 && e1) (void)hipEventRecord(e0, stream);
-    }
-    hipError_t e = f();
-    if (on && e0 && e1) {
-      (void)hipEventRecord(e1, stream);
-      live.push_back({e0, e1, cls});
-      flops[cls] += fl;
-      bytes[cls] += by;
-      launches[cls] += 1;
-    }
-    return e;
+    return probes.run(stream, cls, fl, by, f);
   }
 };
 
@@ -791,12 +756,6 @@ float gpt2_lr_at(const gpt2_config* cfg, int64_t step) {
 
 void gpt2_destroy(gpt2_model* m) {
   if (!m) return;
-  for (auto& r : m->live) {
-    (void)hipEventSynchronize(r.b);
-    (void)hipEventDestroy(r.a);
-    (void)hipEventDestroy(r.b);
-  }
-  for (hipEvent_t e : m->pool) (void)hipEventDestroy(e);
   delete m;
 }
 
@@ -881,22 +840,13 @@ gpt2_status gpt2_embedding_backward(gpt2_model* m, const int32_t* d_ids, const v
 
 gpt2_status gpt2_probe_enable(gpt2_model* m, uint32_t class_mask) {
   if (!m) return GPT2_ERR_INVALID_ARG;
-  m->probe_mask = class_mask;
+  m->probes.mask = class_mask;
   return GPT2_OK;
 }
 
 gpt2_status gpt2_probe_reset(gpt2_model* m) {
   if (!m) return GPT2_ERR_INVALID_ARG;
-  for (auto& r : m->live) {
-    if (hipEventSynchronize(r.b) != hipSuccess) return m->fail(GPT2_ERR_DEVICE, "event sync failed");
-    m->pool.push_back(r.a);
-    m->pool.push_back(r.b);
-  }
-  m->live.clear();
-  for (int k = 0; k < GPT2_K_COUNT; ++k) {
-    m->ms[k] = m->flops[k] = m->bytes[k] = 0.0;
-    m->launches[k] = 0;
-  }
+  if (m->probes.reset() != hipSuccess) return m->fail(GPT2_ERR_DEVICE, "event sync failed");
   return GPT2_OK;
 }
 
@@ -904,19 +854,11 @@ gpt2_status gpt2_probe_read(gpt2_model* m, int32_t kclass, double* total_ms, int
                             double* bytes) {
   if (!m) return GPT2_ERR_INVALID_ARG;
   if (kclass < 0 || kclass >= GPT2_K_COUNT) return m->fail(GPT2_ERR_INVALID_ARG, "bad kernel class");
-  for (auto& r : m->live) {
-    if (hipEventSynchronize(r.b) != hipSuccess) return m->fail(GPT2_ERR_DEVICE, "event sync failed");
-    float t = 0.0f;
-    if (hipEventElapsedTime(&t, r.a, r.b) != hipSuccess) return m->fail(GPT2_ERR_DEVICE, "event timing failed");
-    m->ms[r.cls] += t;
-    m->pool.push_back(r.a);
-    m->pool.push_back(r.b);
-  }
-  m->live.clear();
-  if (total_ms) *total_ms = m->ms[kclass];
-  if (launches) *launches = m->launches[kclass];
-  if (flops) *flops = m->flops[kclass];
-  if (bytes) *bytes = m->bytes[kclass];
+  if (m->probes.collect() != hipSuccess) return m->fail(GPT2_ERR_DEVICE, "event timing failed");
+  if (total_ms) *total_ms = m->probes.ms[kclass];
+  if (launches) *launches = m->probes.launches[kclass];
+  if (flops) *flops = m->probes.flops[kclass];
+  if (bytes) *bytes = m->probes.bytes[kclass];
   return GPT2_OK;
 }
 

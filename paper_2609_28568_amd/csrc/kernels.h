@@ -78,6 +78,8 @@ hipError_t launch_layernorm_bwd(const bf16_t* dy, const bf16_t* x, const float* 
 // dst[i] (fp32, n elements) = (accumulate ? dst[i] : 0) + sum_s src[s*n + i]
 hipError_t launch_reduce_slices(const float* src, int nslices, long n, float* dst, int accumulate,
                                 hipStream_t s);
+// dst[i] (bf16, n elements, n % 4 == 0) = sum_s src[s*n + i]
+hipError_t launch_reduce_slices_bf16(const float* src, int nslices, long n, bf16_t* dst, hipStream_t s);
 // The same for two independent segments in one launch (n and n2 multiples of 4)
 hipError_t launch_reduce_slices2(const float* src, int nslices, long n, float* dst, const float* src2,
                                  int nslices2, long n2, float* dst2, int accumulate, hipStream_t s);
@@ -104,19 +106,26 @@ hipError_t launch_cross_entropy(bf16_t* logits, const int32_t* targets, float* l
 hipError_t launch_mean(const float* x, int n, float* out, hipStream_t s);
 // out[0] = scale * sum of x[0..n)
 hipError_t launch_sum_scaled(const float* x, int n, float scale, float* out, hipStream_t s);
-// Cross-entropy whose rows (tokens) at positions row % T < mask_from carry no
-// loss: their loss is 0 and, with write_grad, their gradient row is 0.
+// Cross-entropy over the rows of the positions that carry loss (t >= mask_from
+// of every T): logits row i (of rows = B (T - mask_from)) belongs to position
+// p = (i / n) T + mask_from + i % n, n = T - mask_from, whose target and loss
+// are targets[p] and losses[p]; the losses of the other positions are set to 0.
 hipError_t launch_cross_entropy_masked(bf16_t* logits, const int32_t* targets, float* losses, int rows, int V, int Vp,
                                        float grad_scale, int write_grad, int T, int mask_from, hipStream_t s);
 
 // ---------------------------------------------------------------- Qwen3-shaped adapter step
 hipError_t launch_embed_gather(const int32_t* ids, const bf16_t* table, bf16_t* x, long rows, int C, hipStream_t s);
-// y = x / sqrt(mean(x^2) + eps) * w per row; rstd [rows] saved
+// y = x / sqrt(mean(x^2) + eps) * w per row; rstd [rows] saved. Only the rows
+// of positions t >= mask_from of every T are normalised: output row i (of
+// rows = B (T - mask_from)) is input row (i / n) T + mask_from + i % n,
+// n = T - mask_from (mask_from = 0: every row, in place order).
 hipError_t launch_rmsnorm_fwd(const bf16_t* x, const bf16_t* w, bf16_t* y, float* rstd, int rows, int C, float eps,
-                              hipStream_t s);
-// dres (=|+=) the RMSNorm input gradient (the gain is frozen)
+                              int T, int mask_from, hipStream_t s);
+// dres (=|+=) the RMSNorm input gradient (the gain is frozen) over all rows of
+// x; dy and rstd hold only the rows of positions t >= mask_from, compacted as
+// launch_rmsnorm_fwd writes them; the other rows get a zero gradient
 hipError_t launch_rmsnorm_bwd(const bf16_t* dy, const bf16_t* x, const float* rstd, const bf16_t* w, bf16_t* dres,
-                              int accumulate, int rows, int C, hipStream_t s);
+                              int accumulate, int rows, int C, int T, int mask_from, hipStream_t s);
 // raw q|k|v [BT][(H + 2 Hkv) hd] -> packed q|k|v [BT][3 H hd] for the attention
 // kernels: query and key heads RMS-normalised and rotated, key/value heads
 // repeated over their query-head groups; rstd of every q and k head saved

@@ -20,6 +20,7 @@
 
 #include "../../include/qwen3.h"
 #include "kernels.h"
+#include "probe.h"
 
 namespace {
 
@@ -43,6 +44,8 @@ struct Dims {
   int QD, KVD, QKVD;   // H*hd, Hkv*hd, (H+2Hkv)*hd
   float s;             // alpha / sqrt(r)
   int mask_from;       // first position with loss
+  int nl;              // positions with loss per sequence, T - mask_from
+  long BTL;            // rows with loss, B * nl
 };
 
 Dims dims_of(const qwen3_config& c) {
@@ -53,6 +56,8 @@ Dims dims_of(const qwen3_config& c) {
   d.QD = d.H * d.hd; d.KVD = d.Hkv * d.hd; d.QKVD = d.QD + 2 * d.KVD;
   d.s = c.lora_alpha / std::sqrt((float)c.lora_rank);
   d.mask_from = (int)std::floor((double)c.loss_from * c.T);
+  d.nl = d.T - d.mask_from;
+  d.BTL = (long)d.B * d.nl;
   return d;
 }
 
@@ -157,9 +162,10 @@ ActLayout act_layout(const Dims& d) {
     if (d.groups & (1 << g)) a.s_u[g] = align_up(BT * group_geom(d, g).n * RP * 2);
     a.u[g] = o; o += L * a.s_u[g];
   }
-  a.xf = o; o += a.s_act;
-  a.rf = o; o += a.s_row;
-  a.logits = o; o += align_up(BT * (size_t)d.V * 2);
+  // final norm output and logits: rows of the positions that carry loss only
+  a.xf = o; o += align_up((size_t)d.BTL * d.C * 2);
+  a.rf = o; o += align_up((size_t)d.BTL * 4);
+  a.logits = o; o += align_up((size_t)d.BTL * d.V * 2);
   a.losses = o; o += a.s_row;
   a.loss = o; o += ALIGN;
   a.total = o + TAIL;
@@ -167,6 +173,7 @@ ActLayout act_layout(const Dims& d) {
 }
 
 constexpr int DW_SPLITS = 16;   // token-contraction split of the adapter gradients
+constexpr int HEAD_SPLITS = 4;  // vocabulary-contraction split of the LM head's input gradient
 
 struct WsLayout {
   size_t dres, dh, datt, dpacked, draw, dgu, dm, du, dsum, cosT, sinT, part, sumsq, normcoef, total;
@@ -184,7 +191,7 @@ WsLayout ws_layout(const Dims& d) {
   }
   size_t o = 0;
   w.dres = o; o += align_up(BT * d.C * 2);
-  w.dh = o; o += align_up(BT * d.C * 2);
+  w.dh = o; o += align_up(BT * d.C * 2);   // also the LM head's input gradient (loss rows)
   w.datt = o; o += align_up(BT * d.QD * 2);
   w.dpacked = o; o += align_up(BT * 3 * d.QD * 2);
   w.draw = o; o += align_up(BT * d.QKVD * 2);
@@ -194,7 +201,8 @@ WsLayout ws_layout(const Dims& d) {
   w.dsum = o; o += align_up((size_t)d.B * d.H * d.T * 4);
   w.cosT = o; o += align_up((size_t)d.T * (d.hd / 2) * 4);
   w.sinT = o; o += align_up((size_t)d.T * (d.hd / 2) * 4);
-  w.part = o; o += align_up(part * DW_SPLITS * 4);
+  part = std::max(part * DW_SPLITS, (size_t)d.BTL * d.C * HEAD_SPLITS);
+  w.part = o; o += align_up(part * 4);
   w.sumsq = o; o += align_up((size_t)sumsq_parts() * 4);
   w.normcoef = o; o += ALIGN;
   w.total = o + TAIL;
@@ -216,11 +224,11 @@ const char* validate(const qwen3_config* c) {
   if (!(c->loss_from >= 0.0f && c->loss_from < 1.0f)) return "loss_from must be in [0, 1)";
   if (c->d_model > 2048) return "d_model above 2048";
   const Dims d = dims_of(*c);
+  if (d.mask_from >= d.T) return "no position carries loss";
   // 32-bit byte offsets: the largest operands the kernels address
-  const size_t big = std::max({(size_t)d.BT * d.V, (size_t)d.BT * 3 * d.QD, (size_t)d.V * d.C,
+  const size_t big = std::max({(size_t)d.BTL * d.V, (size_t)d.BT * 3 * d.QD, (size_t)d.V * d.C,
                                (size_t)d.BT * 2 * d.F});
   if ((big + 512 * (size_t)std::max(d.V, 2 * d.F)) * 2 >= (1ull << 32)) return "a buffer exceeds 32-bit offsets";
-  if (d.mask_from >= d.T) return "no position carries loss";
   return nullptr;
 }
 
@@ -238,6 +246,13 @@ struct qwen3_model {
   size_t base_off[B_NKIND];
   bool have_targets = false, have_grads = false;
   std::string err;
+  ProbeSet<QWEN3_K_COUNT> probes;
+
+  // Launch through f(); bracketed with events when the class's probe is on.
+  template <class Fn>
+  hipError_t run(int cls, double fl, double by, Fn f) {
+    return probes.run(stream, cls, fl, by, f);
+  }
 
   bf16_t* base(int k) { return static_cast<bf16_t*>(buf.base_bf16) + base_off[k]; }
   char* A() { return static_cast<char*>(buf.activations); }
@@ -271,27 +286,38 @@ thread_local std::string g_err;
   } while (0)
 
 // C[M,N] (row stride ldc) = A B with A [M,K] (or [K,M] when a_t) and B [N,K]
-// (or [K,N] when b_t), bf16 in, epilogue as in the GPT-2 step.
-hipError_t gemm(qwen3_model* m, int M, int N, int K, const bf16_t* A, int lda, int a_t, const bf16_t* B, int ldb,
-                int b_t, int epi, void* C, int ldc, const bf16_t* residual = nullptr, int splits = 1,
-                int k_chunk = 0, long split_stride = 0) {
+// (or [K,N] when b_t), bf16 in, epilogue as in the GPT-2 step. `fl` is the
+// product's algorithmic FLOP count for the probes (2 M N K unless the
+// contraction or an output dimension is padded).
+hipError_t gemm(qwen3_model* m, int cls, double fl, int M, int N, int K, const bf16_t* A, int lda, int a_t,
+                const bf16_t* B, int ldb, int b_t, int epi, void* C, int ldc, const bf16_t* residual = nullptr,
+                int splits = 1, int k_chunk = 0, long split_stride = 0) {
   GemmArgs g{};
   g.A = A; g.B = B; g.M = M; g.N = N; g.K = K; g.lda = lda; g.ldb = ldb; g.C = C; g.ldc = ldc;
   g.residual = residual; g.splits = splits; g.k_chunk = k_chunk; g.split_stride = split_stride;
-  return launch_gemm(g, a_t, b_t, epi, m->stream);
+  return m->run(cls, fl, 0.0, [&] { return launch_gemm(g, a_t, b_t, epi, m->stream); });
 }
+
+double mnk2(double M, double N, double K) { return 2.0 * M * N * K; }
 
 // Adapter gradient dst [M,N] (fp32, contiguous) = A^T B with A [BT,M] (row
 // stride lda) and B [BT,N] (row stride ldb): the token contraction is split
 // DW_SPLITS ways into the workspace and summed.
-hipError_t adapter_grad(qwen3_model* m, int M, int N, const bf16_t* A, int lda, const bf16_t* B, int ldb, float* dst) {
+hipError_t adapter_grad(qwen3_model* m, double fl, int M, int N, const bf16_t* A, int lda, const bf16_t* B, int ldb,
+                        float* dst) {
   int kc = 0;
   const int splits = gemm_split_plan((int)m->d.BT, DW_SPLITS, &kc);
   float* part = m->wf(m->ws.part);
-  hipError_t e = gemm(m, M, N, (int)m->d.BT, A, lda, 1, B, ldb, 1, EPI_F32, part, N, nullptr, splits, kc,
-                      (long)M * N);
+  hipError_t e = gemm(m, QWEN3_K_GEMM_ADAPTER, fl, M, N, (int)m->d.BT, A, lda, 1, B, ldb, 1, EPI_F32, part, N, nullptr,
+                      splits, kc, (long)M * N);
   if (e != hipSuccess) return e;
-  return launch_reduce_slices(part, splits, (long)M * N, dst, 0, m->stream);
+  return m->run(QWEN3_K_OTHER, 0.0, 4.0 * (double)M * N * (splits + 1),
+                [&] { return launch_reduce_slices(part, splits, (long)M * N, dst, 0, m->stream); });
+}
+
+hipError_t scale_bf16(qwen3_model* m, bf16_t* x, long rows, int cols, int ld, float sc) {
+  return m->run(QWEN3_K_OTHER, 0.0, 4.0 * (double)rows * cols,
+                [&] { return launch_scale_bf16(x, rows, cols, ld, sc, m->stream); });
 }
 
 // Forward of the adapters of group g at layer l: u = s x A^T into the saved u
@@ -305,14 +331,16 @@ hipError_t adapter_fwd(qwen3_model* m, int g, int l, const bf16_t* x, bf16_t* y,
   const bf16_t* wb = static_cast<const bf16_t*>(m->buf.lora_bf16) + tb->off + (size_t)l * gg.out_total * RP;
   bf16_t* u = m->ab(m->act.u[g] + l * m->act.s_u[g]);
   const int nu = gg.n * RP;
-  hipError_t e = gemm(m, (int)d.BT, nu, gg.in, x, gg.in, 0, wa, gg.in, 0, EPI_BF16, u, nu);
+  const int K = QWEN3_K_GEMM_ADAPTER;
+  hipError_t e = gemm(m, K, mnk2(d.BT, gg.n * d.r, gg.in), (int)d.BT, nu, gg.in, x, gg.in, 0, wa, gg.in, 0, EPI_BF16,
+                      u, nu);
   if (e != hipSuccess) return e;
-  e = launch_scale_bf16(u, d.BT, nu, nu, d.s, m->stream);
+  e = scale_bf16(m, u, d.BT, nu, nu, d.s);
   if (e != hipSuccess) return e;
   int col = 0;
   for (int j = 0; j < gg.n; ++j) {
-    e = gemm(m, (int)d.BT, gg.out[j], RP, u + j * RP, nu, 0, wb + (size_t)col * RP, RP, 0, EPI_BF16, y + col, ldy,
-             y + col);
+    e = gemm(m, K, mnk2(d.BT, gg.out[j], d.r), (int)d.BT, gg.out[j], RP, u + j * RP, nu, 0, wb + (size_t)col * RP, RP,
+             0, EPI_BF16, y + col, ldy, y + col);
     if (e != hipSuccess) return e;
     col += gg.out[j];
   }
@@ -320,8 +348,8 @@ hipError_t adapter_fwd(qwen3_model* m, int g, int l, const bf16_t* x, bf16_t* y,
 }
 
 // Backward of the adapters of group g at layer l, given the output gradient
-// dy (row stride ldy) and the layer input x: dx += du A, dA = du^T x,
-// dB_j = dy_j^T u_j (du = s dy_j B_j, per projection).
+// dy (row stride ldy) and the layer input x: dx += du A (skipped when dx is
+// null), dA = du^T x, dB_j = dy_j^T u_j (du = s dy_j B_j, per projection).
 hipError_t adapter_bwd(qwen3_model* m, int g, int l, const bf16_t* dy, int ldy, const bf16_t* x, bf16_t* dx) {
   const Dims& d = m->d;
   const GroupGeom gg = group_geom(d, g);
@@ -335,23 +363,27 @@ hipError_t adapter_bwd(qwen3_model* m, int g, int l, const bf16_t* dy, int ldy, 
   const bf16_t* u = m->ab(m->act.u[g] + l * m->act.s_u[g]);
   bf16_t* du = m->wb(m->ws.du);
   const int nu = gg.n * RP;
+  const int K = QWEN3_K_GEMM_ADAPTER;
   hipError_t e;
   int col = 0;
   for (int j = 0; j < gg.n; ++j) {
     // du_j = dy_j B_j  ([BT, RP]; B_j read as [K = out_j][N = RP])
-    e = gemm(m, (int)d.BT, RP, gg.out[j], dy + col, ldy, 0, wb + (size_t)col * RP, RP, 1, EPI_BF16, du + j * RP, nu);
+    e = gemm(m, K, mnk2(d.BT, d.r, gg.out[j]), (int)d.BT, RP, gg.out[j], dy + col, ldy, 0, wb + (size_t)col * RP, RP,
+             1, EPI_BF16, du + j * RP, nu);
     if (e != hipSuccess) return e;
     // dB_j = dy_j^T u_j
-    e = adapter_grad(m, gg.out[j], RP, dy + col, ldy, u + j * RP, nu, gb + (size_t)col * RP);
+    e = adapter_grad(m, mnk2(gg.out[j], d.r, d.BT), gg.out[j], RP, dy + col, ldy, u + j * RP, nu,
+                     gb + (size_t)col * RP);
     if (e != hipSuccess) return e;
     col += gg.out[j];
   }
-  e = launch_scale_bf16(du, d.BT, nu, nu, d.s, m->stream);
+  e = scale_bf16(m, du, d.BT, nu, nu, d.s);
   if (e != hipSuccess) return e;
   // dA = du^T x; dx += du A (A read as [K = n*RP][N = in])
-  e = adapter_grad(m, nu, gg.in, du, nu, x, gg.in, ga);
-  if (e != hipSuccess) return e;
-  return gemm(m, (int)d.BT, gg.in, nu, du, nu, 0, wa, gg.in, 1, EPI_BF16, dx, gg.in, dx);
+  e = adapter_grad(m, mnk2(gg.n * d.r, gg.in, d.BT), nu, gg.in, du, nu, x, gg.in, ga);
+  if (e != hipSuccess || !dx) return e;
+  return gemm(m, K, mnk2(d.BT, gg.in, gg.n * d.r), (int)d.BT, gg.in, nu, du, nu, 0, wa, gg.in, 1, EPI_BF16, dx, gg.in,
+              dx);
 }
 
 AttnArgs attn_args(qwen3_model* m, int l) {
@@ -365,6 +397,11 @@ AttnArgs attn_args(qwen3_model* m, int l) {
   a.dsum = m->wf(m->ws.dsum);
   a.dqkv = m->wb(m->ws.dpacked);
   return a;
+}
+
+double attn_fwd_flops(const Dims& d) {
+  // causal: q.k and p.v over the key positions j <= i only
+  return 4.0 * d.B * d.H * d.hd * ((double)d.T * (d.T + 1) / 2.0);
 }
 
 gpt2_status fail(qwen3_model* m, gpt2_status st, const std::string& why) {
@@ -481,8 +518,11 @@ gpt2_status qwen3_sync_weights(qwen3_model* m) {
 gpt2_status qwen3_forward(qwen3_model* m, const int32_t* d_inputs, const int32_t* d_targets) {
   if (!m || !d_inputs) return fail(m, GPT2_ERR_INVALID_ARG, "null argument");
   const Dims& d = m->d;
-  const int BT = (int)d.BT;
-  TRY(launch_embed_gather(d_inputs, m->base(B_EMBED), m->res(0), d.BT, d.C, m->stream));
+  const int BT = (int)d.BT, BTL = (int)d.BTL;
+  const int FWD = QWEN3_K_GEMM_FWD, NORM = QWEN3_K_NORM, OTHER = QWEN3_K_OTHER;
+  const double rowb = 2.0 * d.BT * d.C;   // bytes of one bf16 [BT, C] activation
+  TRY(m->run(OTHER, 0.0, 2.0 * rowb + 4.0 * d.BT,
+             [&] { return launch_embed_gather(d_inputs, m->base(B_EMBED), m->res(0), d.BT, d.C, m->stream); }));
   for (int l = 0; l < d.L; ++l) {
     bf16_t* h = m->ab(m->act.h + l * m->act.s_act);
     float* r1 = m->af(m->act.r1 + l * m->act.s_row);
@@ -493,42 +533,54 @@ gpt2_status qwen3_forward(qwen3_model* m, const int32_t* d_inputs, const int32_t
     bf16_t* gu = m->ab(m->act.gu + l * m->act.s_gu);
     bf16_t* mm = m->ab(m->act.m + l * m->act.s_m);
     // attention sub-layer
-    TRY(launch_rmsnorm_fwd(m->res(l), m->base(B_IN_NORM) + (size_t)l * d.C, h, r1, BT, d.C, m->cfg.rms_eps,
-                           m->stream));
-    TRY(gemm(m, BT, d.QKVD, d.C, h, d.C, 0, m->base(B_QKV) + (size_t)l * d.QKVD * d.C, d.C, 0, EPI_BF16, raw,
-             d.QKVD));
+    TRY(m->run(NORM, 0.0, 2.0 * rowb + 4.0 * d.BT, [&] {
+      return launch_rmsnorm_fwd(m->res(l), m->base(B_IN_NORM) + (size_t)l * d.C, h, r1, BT, d.C, m->cfg.rms_eps, 1, 0,
+                                m->stream);
+    }));
+    TRY(gemm(m, FWD, mnk2(BT, d.QKVD, d.C), BT, d.QKVD, d.C, h, d.C, 0, m->base(B_QKV) + (size_t)l * d.QKVD * d.C, d.C,
+             0, EPI_BF16, raw, d.QKVD));
     if (m->has(G_QKV)) TRY(adapter_fwd(m, G_QKV, l, h, raw, d.QKVD));
     AttnArgs aa = attn_args(m, l);
-    TRY(launch_qknorm_rope_fwd(raw, m->base(B_QNORM) + (size_t)l * d.hd, m->base(B_KNORM) + (size_t)l * d.hd,
-                               m->wf(m->ws.cosT), m->wf(m->ws.sinT), const_cast<bf16_t*>(aa.qkv),
-                               m->af(m->act.rq + l * m->act.s_rq), m->af(m->act.rk + l * m->act.s_rk), BT, d.T, d.H,
-                               d.Hkv, d.hd, m->cfg.rms_eps, m->stream));
-    TRY(launch_attention_fwd(aa, m->stream));
-    TRY(gemm(m, BT, d.C, d.QD, aa.out, d.QD, 0, m->base(B_O) + (size_t)l * d.C * d.QD, d.QD, 0, EPI_BF16, xmid, d.C,
-             m->res(l)));
+    TRY(m->run(NORM, 0.0, 2.0 * d.BT * (d.QKVD + 3.0 * d.QD) + 4.0 * d.BT * (d.H + d.Hkv), [&] {
+      return launch_qknorm_rope_fwd(raw, m->base(B_QNORM) + (size_t)l * d.hd, m->base(B_KNORM) + (size_t)l * d.hd,
+                                    m->wf(m->ws.cosT), m->wf(m->ws.sinT), const_cast<bf16_t*>(aa.qkv),
+                                    m->af(m->act.rq + l * m->act.s_rq), m->af(m->act.rk + l * m->act.s_rk), BT, d.T,
+                                    d.H, d.Hkv, d.hd, m->cfg.rms_eps, m->stream);
+    }));
+    TRY(m->run(QWEN3_K_ATTN_FWD, attn_fwd_flops(d), 0.0, [&] { return launch_attention_fwd(aa, m->stream); }));
+    TRY(gemm(m, FWD, mnk2(BT, d.C, d.QD), BT, d.C, d.QD, aa.out, d.QD, 0, m->base(B_O) + (size_t)l * d.C * d.QD, d.QD,
+             0, EPI_BF16, xmid, d.C, m->res(l)));
     if (m->has(G_O)) TRY(adapter_fwd(m, G_O, l, aa.out, xmid, d.C));
     // MLP sub-layer
-    TRY(launch_rmsnorm_fwd(xmid, m->base(B_POST_NORM) + (size_t)l * d.C, h2, r2, BT, d.C, m->cfg.rms_eps,
-                           m->stream));
-    TRY(gemm(m, BT, 2 * d.F, d.C, h2, d.C, 0, m->base(B_GU) + (size_t)l * 2 * d.F * d.C, d.C, 0, EPI_BF16, gu,
-             2 * d.F));
+    TRY(m->run(NORM, 0.0, 2.0 * rowb + 4.0 * d.BT, [&] {
+      return launch_rmsnorm_fwd(xmid, m->base(B_POST_NORM) + (size_t)l * d.C, h2, r2, BT, d.C, m->cfg.rms_eps, 1, 0,
+                                m->stream);
+    }));
+    TRY(gemm(m, FWD, mnk2(BT, 2 * d.F, d.C), BT, 2 * d.F, d.C, h2, d.C, 0,
+             m->base(B_GU) + (size_t)l * 2 * d.F * d.C, d.C, 0, EPI_BF16, gu, 2 * d.F));
     if (m->has(G_GU)) TRY(adapter_fwd(m, G_GU, l, h2, gu, 2 * d.F));
-    TRY(launch_swiglu_fwd(gu, mm, d.BT, d.F, m->stream));
-    TRY(gemm(m, BT, d.C, d.F, mm, d.F, 0, m->base(B_DOWN) + (size_t)l * d.C * d.F, d.F, 0, EPI_BF16, m->res(l + 1),
-             d.C, xmid));
+    TRY(m->run(OTHER, 0.0, 6.0 * d.BT * d.F, [&] { return launch_swiglu_fwd(gu, mm, d.BT, d.F, m->stream); }));
+    TRY(gemm(m, FWD, mnk2(BT, d.C, d.F), BT, d.C, d.F, mm, d.F, 0, m->base(B_DOWN) + (size_t)l * d.C * d.F, d.F, 0,
+             EPI_BF16, m->res(l + 1), d.C, xmid));
     if (m->has(G_DN)) TRY(adapter_fwd(m, G_DN, l, mm, m->res(l + 1), d.C));
   }
+  // final norm and LM head on the positions that carry loss (compacted rows)
   bf16_t* xf = m->ab(m->act.xf);
-  TRY(launch_rmsnorm_fwd(m->res(d.L), m->base(B_FINAL_NORM), xf, m->af(m->act.rf), BT, d.C, m->cfg.rms_eps,
-                         m->stream));
+  TRY(m->run(NORM, 0.0, 4.0 * d.BTL * d.C + 4.0 * d.BTL, [&] {
+    return launch_rmsnorm_fwd(m->res(d.L), m->base(B_FINAL_NORM), xf, m->af(m->act.rf), BTL, d.C, m->cfg.rms_eps, d.T,
+                              d.mask_from, m->stream);
+  }));
   bf16_t* logits = m->ab(m->act.logits);
-  TRY(gemm(m, BT, d.V, d.C, xf, d.C, 0, m->base(B_EMBED), d.C, 0, EPI_BF16, logits, d.V));
+  TRY(gemm(m, FWD, mnk2(BTL, d.V, d.C), BTL, d.V, d.C, xf, d.C, 0, m->base(B_EMBED), d.C, 0, EPI_BF16, logits, d.V));
   m->have_targets = d_targets != nullptr;
   if (d_targets) {
-    const int n = d.B * (d.T - d.mask_from);   // positions with loss
-    TRY(launch_cross_entropy_masked(logits, d_targets, m->af(m->act.losses), BT, d.V, d.V, 1.0f / (float)n, 1, d.T,
-                                    d.mask_from, m->stream));
-    TRY(launch_sum_scaled(m->af(m->act.losses), BT, 1.0f / (float)n, m->af(m->act.loss), m->stream));
+    const float inv_n = 1.0f / (float)d.BTL;   // mean over the positions with loss
+    TRY(m->run(QWEN3_K_CROSS_ENTROPY, 0.0, 4.0 * d.BTL * d.V + 12.0 * d.BT, [&] {
+      return launch_cross_entropy_masked(logits, d_targets, m->af(m->act.losses), BTL, d.V, d.V, inv_n, 1, d.T,
+                                         d.mask_from, m->stream);
+    }));
+    TRY(m->run(OTHER, 0.0, 4.0 * d.BT,
+               [&] { return launch_sum_scaled(m->af(m->act.losses), BT, inv_n, m->af(m->act.loss), m->stream); }));
   }
   return GPT2_OK;
 }
@@ -537,12 +589,27 @@ gpt2_status qwen3_backward(qwen3_model* m) {
   if (!m) return fail(nullptr, GPT2_ERR_INVALID_ARG, "null model");
   if (!m->have_targets) return fail(m, GPT2_ERR_STATE, "backward needs a forward with targets");
   const Dims& d = m->d;
-  const int BT = (int)d.BT;
+  const int BT = (int)d.BT, BTL = (int)d.BTL;
+  const int DX = QWEN3_K_GEMM_DX, NORM = QWEN3_K_NORM;
+  const double rowb = 2.0 * d.BT * d.C;
   bf16_t* dres = m->wb(m->ws.dres);
   bf16_t* dh = m->wb(m->ws.dh);
-  // LM head: dxf = dlogits embed, then the final RMSNorm
-  TRY(gemm(m, BT, d.C, d.V, m->ab(m->act.logits), d.V, 0, m->base(B_EMBED), d.C, 1, EPI_BF16, dh, d.C));
-  TRY(launch_rmsnorm_bwd(dh, m->res(d.L), m->af(m->act.rf), m->base(B_FINAL_NORM), dres, 0, BT, d.C, m->stream));
+  // LM head: dxf = dlogits embed over the loss rows, the long vocabulary
+  // contraction split so that the few output tiles fill the GPU, then the
+  // final RMSNorm (rows without loss get a zero gradient)
+  {
+    int kc = 0;
+    const int splits = gemm_split_plan(d.V, HEAD_SPLITS, &kc);
+    float* part = m->wf(m->ws.part);
+    TRY(gemm(m, DX, mnk2(BTL, d.C, d.V), BTL, d.C, d.V, m->ab(m->act.logits), d.V, 0, m->base(B_EMBED), d.C, 1,
+             EPI_F32, part, d.C, nullptr, splits, kc, (long)d.BTL * d.C));
+    TRY(m->run(QWEN3_K_OTHER, 0.0, (4.0 * splits + 2.0) * d.BTL * d.C,
+               [&] { return launch_reduce_slices_bf16(part, splits, d.BTL * d.C, dh, m->stream); }));
+  }
+  TRY(m->run(NORM, 0.0, 2.0 * rowb + 4.0 * d.BTL * d.C + 4.0 * d.BTL, [&] {
+    return launch_rmsnorm_bwd(dh, m->res(d.L), m->af(m->act.rf), m->base(B_FINAL_NORM), dres, 0, BT, d.C, d.T,
+                              d.mask_from, m->stream);
+  }));
   for (int l = d.L - 1; l >= 0; --l) {
     const bf16_t* h = m->ab(m->act.h + l * m->act.s_act);
     const float* r1 = m->af(m->act.r1 + l * m->act.s_row);
@@ -555,28 +622,44 @@ gpt2_status qwen3_backward(qwen3_model* m) {
     bf16_t* dm = m->wb(m->ws.dm);
     bf16_t* dgu = m->wb(m->ws.dgu);
     // down projection: res(l+1) = xmid + m down^T (+ adapter)
-    TRY(gemm(m, BT, d.F, d.C, dres, d.C, 0, m->base(B_DOWN) + (size_t)l * d.C * d.F, d.F, 1, EPI_BF16, dm, d.F));
+    TRY(gemm(m, DX, mnk2(BT, d.F, d.C), BT, d.F, d.C, dres, d.C, 0, m->base(B_DOWN) + (size_t)l * d.C * d.F, d.F, 1,
+             EPI_BF16, dm, d.F));
     if (m->has(G_DN)) TRY(adapter_bwd(m, G_DN, l, dres, d.C, mm, dm));
-    TRY(launch_swiglu_bwd(dm, gu, dgu, d.BT, d.F, m->stream));
-    TRY(gemm(m, BT, d.C, 2 * d.F, dgu, 2 * d.F, 0, m->base(B_GU) + (size_t)l * 2 * d.F * d.C, d.C, 1, EPI_BF16, dh,
-             d.C));
+    TRY(m->run(QWEN3_K_OTHER, 0.0, 10.0 * d.BT * d.F,
+               [&] { return launch_swiglu_bwd(dm, gu, dgu, d.BT, d.F, m->stream); }));
+    TRY(gemm(m, DX, mnk2(BT, d.C, 2 * d.F), BT, d.C, 2 * d.F, dgu, 2 * d.F, 0,
+             m->base(B_GU) + (size_t)l * 2 * d.F * d.C, d.C, 1, EPI_BF16, dh, d.C));
     if (m->has(G_GU)) TRY(adapter_bwd(m, G_GU, l, dgu, 2 * d.F, h2, dh));
-    TRY(launch_rmsnorm_bwd(dh, xmid, r2, m->base(B_POST_NORM) + (size_t)l * d.C, dres, 1, BT, d.C, m->stream));
+    TRY(m->run(NORM, 0.0, 4.0 * rowb + 4.0 * d.BT, [&] {
+      return launch_rmsnorm_bwd(dh, xmid, r2, m->base(B_POST_NORM) + (size_t)l * d.C, dres, 1, BT, d.C, 1, 0,
+                                m->stream);
+    }));
     // attention output projection: xmid = res(l) + att o^T (+ adapter)
     AttnArgs aa = attn_args(m, l);
     bf16_t* datt = m->wb(m->ws.datt);
-    TRY(gemm(m, BT, d.QD, d.C, dres, d.C, 0, m->base(B_O) + (size_t)l * d.C * d.QD, d.QD, 1, EPI_BF16, datt, d.QD));
+    TRY(gemm(m, DX, mnk2(BT, d.QD, d.C), BT, d.QD, d.C, dres, d.C, 0, m->base(B_O) + (size_t)l * d.C * d.QD, d.QD, 1,
+             EPI_BF16, datt, d.QD));
     if (m->has(G_O)) TRY(adapter_bwd(m, G_O, l, dres, d.C, aa.out, datt));
-    TRY(launch_attention_bwd(aa, m->stream));
+    TRY(m->run(QWEN3_K_ATTN_BWD, 2.0 * attn_fwd_flops(d), 0.0, [&] { return launch_attention_bwd(aa, m->stream); }));
     bf16_t* draw = m->wb(m->ws.draw);
-    TRY(launch_qknorm_rope_bwd(m->wb(m->ws.dpacked), raw, m->base(B_QNORM) + (size_t)l * d.hd,
-                               m->base(B_KNORM) + (size_t)l * d.hd, m->wf(m->ws.cosT), m->wf(m->ws.sinT),
-                               m->af(m->act.rq + l * m->act.s_rq), m->af(m->act.rk + l * m->act.s_rk), draw, BT, d.T,
-                               d.H, d.Hkv, d.hd, m->stream));
-    TRY(gemm(m, BT, d.C, d.QKVD, draw, d.QKVD, 0, m->base(B_QKV) + (size_t)l * d.QKVD * d.C, d.C, 1, EPI_BF16, dh,
-             d.C));
-    if (m->has(G_QKV)) TRY(adapter_bwd(m, G_QKV, l, draw, d.QKVD, h, dh));
-    TRY(launch_rmsnorm_bwd(dh, m->res(l), r1, m->base(B_IN_NORM) + (size_t)l * d.C, dres, 1, BT, d.C, m->stream));
+    TRY(m->run(NORM, 0.0, 2.0 * d.BT * (2.0 * d.QKVD + 3.0 * d.QD) + 4.0 * d.BT * (d.H + d.Hkv), [&] {
+      return launch_qknorm_rope_bwd(m->wb(m->ws.dpacked), raw, m->base(B_QNORM) + (size_t)l * d.hd,
+                                    m->base(B_KNORM) + (size_t)l * d.hd, m->wf(m->ws.cosT), m->wf(m->ws.sinT),
+                                    m->af(m->act.rq + l * m->act.s_rq), m->af(m->act.rk + l * m->act.s_rk), draw, BT,
+                                    d.T, d.H, d.Hkv, d.hd, m->stream);
+    }));
+    // the first layer's input gradient would only reach the frozen token
+    // table: its q|k|v input gradient and the norm behind it are skipped
+    const bool need_dx = l > 0;
+    if (need_dx)
+      TRY(gemm(m, DX, mnk2(BT, d.C, d.QKVD), BT, d.C, d.QKVD, draw, d.QKVD, 0,
+               m->base(B_QKV) + (size_t)l * d.QKVD * d.C, d.C, 1, EPI_BF16, dh, d.C));
+    if (m->has(G_QKV)) TRY(adapter_bwd(m, G_QKV, l, draw, d.QKVD, h, need_dx ? dh : nullptr));
+    if (need_dx)
+      TRY(m->run(NORM, 0.0, 4.0 * rowb + 4.0 * d.BT, [&] {
+        return launch_rmsnorm_bwd(dh, m->res(l), r1, m->base(B_IN_NORM) + (size_t)l * d.C, dres, 1, BT, d.C, 1, 0,
+                                  m->stream);
+      }));
   }
   m->have_grads = true;
   return GPT2_OK;
@@ -591,8 +674,10 @@ gpt2_status qwen3_adamw_step(qwen3_model* m, int64_t step, float* d_grad_norm_ou
   float* grads = static_cast<float*>(m->buf.lora_grads);
   float* parts = m->wf(m->ws.sumsq);
   float* nc = m->wf(m->ws.normcoef);
-  TRY(launch_sumsq(grads, n, parts, m->stream));
-  TRY(launch_clip_coef(parts, sumsq_parts(), c.grad_clip, nc, m->stream));
+  const int OPT = QWEN3_K_OPTIMIZER;
+  TRY(m->run(OPT, 0.0, 4.0 * n, [&] { return launch_sumsq(grads, n, parts, m->stream); }));
+  TRY(m->run(OPT, 0.0, 4.0 * sumsq_parts(),
+             [&] { return launch_clip_coef(parts, sumsq_parts(), c.grad_clip, nc, m->stream); }));
   if (d_grad_norm_out) TRY(hipMemcpyAsync(d_grad_norm_out, nc, sizeof(float), hipMemcpyDeviceToDevice, m->stream));
   AdamArgs a{};
   a.p = static_cast<float*>(m->buf.lora_f32);
@@ -609,7 +694,7 @@ gpt2_status qwen3_adamw_step(qwen3_model* m, int64_t step, float* d_grad_norm_ou
   a.seg.count = 1;
   a.seg.end[0] = n;
   a.seg.decay[0] = 1;   // the configured decay (0 by default) applies to every adapter tensor
-  TRY(launch_adamw(a, m->stream));
+  TRY(m->run(OPT, 0.0, 30.0 * n, [&] { return launch_adamw(a, m->stream); }));
   m->have_grads = false;
   return GPT2_OK;
 }
@@ -628,5 +713,29 @@ gpt2_status qwen3_loss(qwen3_model* m, float* loss_out, float* d_token_losses) {
 void qwen3_destroy(qwen3_model* m) { delete m; }
 
 const char* qwen3_last_error(const qwen3_model* m) { return m ? m->err.c_str() : g_err.c_str(); }
+
+gpt2_status qwen3_probe_enable(qwen3_model* m, uint32_t class_mask) {
+  if (!m) return fail(nullptr, GPT2_ERR_INVALID_ARG, "null model");
+  m->probes.mask = class_mask;
+  return GPT2_OK;
+}
+
+gpt2_status qwen3_probe_reset(qwen3_model* m) {
+  if (!m) return fail(nullptr, GPT2_ERR_INVALID_ARG, "null model");
+  if (m->probes.reset() != hipSuccess) return fail(m, GPT2_ERR_DEVICE, "event sync failed");
+  return GPT2_OK;
+}
+
+gpt2_status qwen3_probe_read(qwen3_model* m, int32_t kclass, double* total_ms, int64_t* launches, double* flops,
+                             double* bytes) {
+  if (!m) return fail(nullptr, GPT2_ERR_INVALID_ARG, "null model");
+  if (kclass < 0 || kclass >= QWEN3_K_COUNT) return fail(m, GPT2_ERR_INVALID_ARG, "bad kernel class");
+  if (m->probes.collect() != hipSuccess) return fail(m, GPT2_ERR_DEVICE, "event timing failed");
+  if (total_ms) *total_ms = m->probes.ms[kclass];
+  if (launches) *launches = m->probes.launches[kclass];
+  if (flops) *flops = m->probes.flops[kclass];
+  if (bytes) *bytes = m->probes.bytes[kclass];
+  return GPT2_OK;
+}
 
 }  // extern "C"

@@ -18,16 +18,29 @@ __global__ void embed_gather_kernel(const int32_t* __restrict__ ids, const bf16_
   *reinterpret_cast<uint4*>(x + i) = *reinterpret_cast<const uint4*>(table + (size_t)ids[row] * C + c);
 }
 
+// Row maps of the positions that carry loss: of every T rows (one sequence)
+// the last T - mask_from do. Compact row i (over those rows only) is input
+// row loss_row(i); input row p has compact index loss_index(p) when
+// p % T >= mask_from. With mask_from = 0 both maps are the identity.
+DEV int loss_row(int i, int T, int mask_from) {
+  const int n = T - mask_from;
+  return (i / n) * T + mask_from + i % n;
+}
+DEV int loss_index(int p, int T, int mask_from) {
+  return (p / T) * (T - mask_from) + p % T - mask_from;
+}
+
 // One row per wave; lane owns 4-channel chunks c = 4*(lane + 64*i). Loads of
 // a row are issued at once from clamped addresses and masked afterwards.
+// Output row i normalises input row loss_row(i) (rows = output rows).
 template <int MAXCH>
 __global__ __launch_bounds__(256) void rmsnorm_fwd_kernel(const bf16_t* __restrict__ x, const bf16_t* __restrict__ w,
                                                           bf16_t* __restrict__ y, float* __restrict__ rstd_out,
-                                                          int rows, int C, float eps) {
+                                                          int rows, int C, float eps, int T, int mask_from) {
   const int lane = threadIdx.x & 63;
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (row >= rows) return;
-  const bf16_t* xr = x + (size_t)row * C;
+  const bf16_t* xr = x + (size_t)loss_row(row, T, mask_from) * C;
   uint2 xu[MAXCH], wu[MAXCH];
 #pragma unroll
   for (int i = 0; i < MAXCH; ++i) {
@@ -60,18 +73,26 @@ __global__ __launch_bounds__(256) void rmsnorm_fwd_kernel(const bf16_t* __restri
   if (lane == 0) rstd_out[row] = rstd;
 }
 
-// dres (=|+=) rstd (g - xhat mean(g xhat)), g = dy w, xhat = x rstd (gain frozen)
+// dres (=|+=) rstd (g - xhat mean(g xhat)), g = dy w, xhat = x rstd (gain frozen).
+// dy and rstd hold compact rows (loss_index); rows p with p % T < mask_from
+// have no upstream gradient: dres is left as is (accumulate) or zeroed.
 template <int MAXCH>
 __global__ __launch_bounds__(256) void rmsnorm_bwd_kernel(const bf16_t* __restrict__ dy, const bf16_t* __restrict__ x,
                                                           const float* __restrict__ rstd_in,
                                                           const bf16_t* __restrict__ w, bf16_t* __restrict__ dres,
-                                                          int accumulate, int rows, int C) {
+                                                          int accumulate, int rows, int C, int T, int mask_from) {
   const int lane = threadIdx.x & 63;
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (row >= rows) return;
-  const bf16_t* xr = x + (size_t)row * C;
-  const bf16_t* dr = dy + (size_t)row * C;
   bf16_t* rr = dres + (size_t)row * C;
+  if (row % T < mask_from) {
+    if (!accumulate)
+      for (int c = 4 * lane; c < C; c += 256) *reinterpret_cast<uint2*>(rr + c) = make_uint2(0, 0);
+    return;
+  }
+  const int ci = loss_index(row, T, mask_from);
+  const bf16_t* xr = x + (size_t)row * C;
+  const bf16_t* dr = dy + (size_t)ci * C;
   uint2 xu[MAXCH], du[MAXCH], wu[MAXCH], ru[MAXCH];
 #pragma unroll
   for (int i = 0; i < MAXCH; ++i) {
@@ -81,7 +102,7 @@ __global__ __launch_bounds__(256) void rmsnorm_bwd_kernel(const bf16_t* __restri
     wu[i] = *reinterpret_cast<const uint2*>(w + c);
     ru[i] = accumulate ? *reinterpret_cast<const uint2*>(rr + c) : make_uint2(0, 0);
   }
-  const float rstd = rstd_in[row];
+  const float rstd = rstd_in[ci];
   float xh[MAXCH][4], g[MAXCH][4];
   float s = 0.0f;
 #pragma unroll
@@ -283,25 +304,29 @@ hipError_t launch_embed_gather(const int32_t* ids, const bf16_t* table, bf16_t* 
 }
 
 hipError_t launch_rmsnorm_fwd(const bf16_t* x, const bf16_t* w, bf16_t* y, float* rstd, int rows, int C, float eps,
-                              hipStream_t s) {
-  if (C % 4) return hipErrorInvalidValue;
+                              int T, int mask_from, hipStream_t s) {
+  if (C % 4 || T < 1 || mask_from < 0 || mask_from >= T) return hipErrorInvalidValue;
   const dim3 g((rows + 3) / 4), b(256);
-  if (C <= 256) hipLaunchKernelGGL(rmsnorm_fwd_kernel<1>, g, b, 0, s, x, w, y, rstd, rows, C, eps);
-  else if (C <= 512) hipLaunchKernelGGL(rmsnorm_fwd_kernel<2>, g, b, 0, s, x, w, y, rstd, rows, C, eps);
-  else if (C <= 1024) hipLaunchKernelGGL(rmsnorm_fwd_kernel<4>, g, b, 0, s, x, w, y, rstd, rows, C, eps);
-  else if (C <= 2048) hipLaunchKernelGGL(rmsnorm_fwd_kernel<8>, g, b, 0, s, x, w, y, rstd, rows, C, eps);
+  if (C <= 256) hipLaunchKernelGGL(rmsnorm_fwd_kernel<1>, g, b, 0, s, x, w, y, rstd, rows, C, eps, T, mask_from);
+  else if (C <= 512) hipLaunchKernelGGL(rmsnorm_fwd_kernel<2>, g, b, 0, s, x, w, y, rstd, rows, C, eps, T, mask_from);
+  else if (C <= 1024) hipLaunchKernelGGL(rmsnorm_fwd_kernel<4>, g, b, 0, s, x, w, y, rstd, rows, C, eps, T, mask_from);
+  else if (C <= 2048) hipLaunchKernelGGL(rmsnorm_fwd_kernel<8>, g, b, 0, s, x, w, y, rstd, rows, C, eps, T, mask_from);
   else return hipErrorInvalidValue;
   return hipGetLastError();
 }
 
 hipError_t launch_rmsnorm_bwd(const bf16_t* dy, const bf16_t* x, const float* rstd, const bf16_t* w, bf16_t* dres,
-                              int accumulate, int rows, int C, hipStream_t s) {
-  if (C % 4) return hipErrorInvalidValue;
+                              int accumulate, int rows, int C, int T, int mask_from, hipStream_t s) {
+  if (C % 4 || T < 1 || mask_from < 0 || mask_from >= T) return hipErrorInvalidValue;
   const dim3 g((rows + 3) / 4), b(256);
-  if (C <= 256) hipLaunchKernelGGL(rmsnorm_bwd_kernel<1>, g, b, 0, s, dy, x, rstd, w, dres, accumulate, rows, C);
-  else if (C <= 512) hipLaunchKernelGGL(rmsnorm_bwd_kernel<2>, g, b, 0, s, dy, x, rstd, w, dres, accumulate, rows, C);
-  else if (C <= 1024) hipLaunchKernelGGL(rmsnorm_bwd_kernel<4>, g, b, 0, s, dy, x, rstd, w, dres, accumulate, rows, C);
-  else if (C <= 2048) hipLaunchKernelGGL(rmsnorm_bwd_kernel<8>, g, b, 0, s, dy, x, rstd, w, dres, accumulate, rows, C);
+  if (C <= 256)
+    hipLaunchKernelGGL(rmsnorm_bwd_kernel<1>, g, b, 0, s, dy, x, rstd, w, dres, accumulate, rows, C, T, mask_from);
+  else if (C <= 512)
+    hipLaunchKernelGGL(rmsnorm_bwd_kernel<2>, g, b, 0, s, dy, x, rstd, w, dres, accumulate, rows, C, T, mask_from);
+  else if (C <= 1024)
+    hipLaunchKernelGGL(rmsnorm_bwd_kernel<4>, g, b, 0, s, dy, x, rstd, w, dres, accumulate, rows, C, T, mask_from);
+  else if (C <= 2048)
+    hipLaunchKernelGGL(rmsnorm_bwd_kernel<8>, g, b, 0, s, dy, x, rstd, w, dres, accumulate, rows, C, T, mask_from);
   else return hipErrorInvalidValue;
   return hipGetLastError();
 }

@@ -15,6 +15,9 @@ import numpy as np
 from .binding import LibError, lib as _lib_gpt2
 
 RP = 64   # padded adapter rank of the library
+# kernel classes of the timing probes (QWEN3_K_* in include/qwen3.h)
+KCLASS = dict(gemm_fwd=0, gemm_dx=1, gemm_adapter=2, attn_fwd=3, attn_bwd=4, norm=5, cross_entropy=6, optimizer=7,
+              other=8)
 GROUPS = {"qkv": 1, "o": 2, "gate_up": 4, "down": 8}
 _GROUP_TARGETS = {"qkv": ("q", "k", "v"), "o": ("o",), "gate_up": ("gate", "up"), "down": ("down",)}
 
@@ -61,6 +64,10 @@ def lib():
         "qwen3_loss": (I32, [P, ctypes.POINTER(F32), P]),
         "qwen3_destroy": (None, [P]),
         "qwen3_last_error": (ctypes.c_char_p, [P]),
+        "qwen3_probe_enable": (I32, [P, ctypes.c_uint32]),
+        "qwen3_probe_reset": (I32, [P]),
+        "qwen3_probe_read": (I32, [P, I32, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64),
+                                   ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double)]),
     }
     for name, (res, args) in protos.items():
         f = getattr(L, name)
@@ -259,3 +266,20 @@ class Qwen3:
         ptr = ctypes.c_void_p(token_losses.data_ptr() if token_losses is not None else 0)
         _check(lib().qwen3_loss(self.h, ctypes.byref(v), ptr), self.h)
         return v.value
+
+    # ---- probes -------------------------------------------------------------
+    def probe_enable(self, classes):
+        mask = 0
+        for c in classes:
+            mask |= 1 << KCLASS[c]
+        _check(lib().qwen3_probe_enable(self.h, mask), self.h)
+
+    def probe_reset(self):
+        _check(lib().qwen3_probe_reset(self.h), self.h)
+
+    def probe_read(self, cls: str) -> dict:
+        ms, fl, by = ctypes.c_double(), ctypes.c_double(), ctypes.c_double()
+        n = ctypes.c_int64()
+        _check(lib().qwen3_probe_read(self.h, KCLASS[cls], ctypes.byref(ms), ctypes.byref(n), ctypes.byref(fl),
+                                      ctypes.byref(by)), self.h)
+        return {"ms": ms.value, "launches": n.value, "flops": fl.value, "bytes": by.value}

@@ -1,0 +1,107 @@
+"""The Qwen3-0.6B-shaped adapter step at its benchmark size (28 layers,
+d_model 1024, 16/8 heads of 128, SwiGLU 3072, vocabulary 151,936, B = 4,
+T = 2048, loss on the last half of every sequence, rank-16 q/k/v/o
+adapters), in the launch configuration the benchmark times, against the
+oracle on one sequence:
+
+* with all four sequences equal, the loss, every position's loss and every
+  adapter gradient (per layer) equal the one-sequence oracle's, since the
+  masked mean over four copies is the mean over one;
+* with four different sequences, the first sequence's per-position losses
+  are bit-identical to those of the equal-sequence batch (no position reads
+  another sequence's rows), and every sequence's masked positions carry
+  exactly zero loss.
+
+Adapter B matrices start from N(0, 0.02) instead of zero so that every
+adapter gradient is non-zero."""
+import numpy as np
+import pytest
+
+from oracle import qwen3 as q3
+from paper_2609_28568_amd import synth
+from tests.util import LOSS_ATOL, REL_L2, rel_l2
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+NAME = "qwen3_06b_lora"
+
+
+@pytest.fixture(scope="module")
+def run():
+    from paper_2609_28568_amd import qwen3_binding as qb
+    w = dict(synth.QWEN3_WORKLOADS[NAME])
+    print(f"qwen3 full size: {w}", flush=True)
+    base, lora = synth.init_qwen3(w, seed=61, b_std=0.02)
+    ids, tgt = synth.token_batch(w, seed=62)
+    m = qb.Qwen3(qb.make_config(w, synth.QWEN3_OPTIM))
+    m.set_base(base)
+    m.set_lora(lora)
+    BT = w["B"] * w["T"]
+    same_ids = np.repeat(ids[:1], w["B"], axis=0)
+    same_tgt = np.repeat(tgt[:1], w["B"], axis=0)
+    tl_same = torch.zeros(BT, device="cuda")
+    m.forward(torch.from_numpy(same_ids), torch.from_numpy(same_tgt))
+    loss_same = m.loss(tl_same)
+    m.backward()
+    grads = m.adapters("lora_grads")
+    tl_diff = torch.zeros(BT, device="cuda")
+    m.forward(torch.from_numpy(ids), torch.from_numpy(tgt))
+    loss_diff = m.loss(tl_diff)
+    torch.cuda.synchronize()
+    m.close()
+    print("qwen3 full size: GPU done, running the one-sequence oracle", flush=True)
+    w1 = dict(w, B=1)
+    ocfg = q3.Qwen3Config.from_dict({**w1, **synth.QWEN3_OPTIM})
+    cache = q3.forward(base, lora, ids[:1], tgt[:1], ocfg)
+    ref = q3.backward(base, lora, cache, ocfg)
+    ref.pop("dx0")
+    print("qwen3 full size: oracle done", flush=True)
+    yield dict(w=w, loss_same=loss_same, loss_diff=loss_diff, grads=grads, cache=cache, ref=ref,
+               tl_same=tl_same.cpu().numpy().reshape(w["B"], w["T"]),
+               tl_diff=tl_diff.cpu().numpy().reshape(w["B"], w["T"]))
+
+
+def test_loss_of_equal_sequences_matches_one_sequence(run):
+    ref = float(run["cache"]["loss"])
+    print(f"  loss gpu {run['loss_same']:.6f} oracle {ref:.6f}")
+    assert abs(run["loss_same"] - ref) < LOSS_ATOL
+
+
+def test_every_position_loss(run):
+    ref = run["cache"]["losses"][0]
+    mf = int(np.floor(run["w"]["loss_from"] * run["w"]["T"]))
+    for b in range(run["w"]["B"]):
+        got = run["tl_same"][b]
+        assert np.all(got[:mf] == 0.0)
+        assert np.max(np.abs(got - ref)) < 5 * LOSS_ATOL
+        assert rel_l2(got, ref) < REL_L2
+
+
+# Per-layer slices of the adapter gradients: bf16 activations already differ
+# from the fp32 oracle by 0.5-1 % relative L2 one layer in (measured: the
+# q/k/v projections 0.3 %, the attention output 0.5 %, the SwiGLU output
+# 0.9 %), and the gradient of a 28-layer model through the q/k head norms
+# sits at 1.4 % on average with single layers up to 2.6 %; the bar for a
+# single layer's slice is therefore 3e-2, while every adapter tensor of the
+# library's layout (stacked over the layers) stays within the 2e-2 bar.
+LAYER_REL_L2 = 3e-2
+
+
+def test_adapter_gradients(run):
+    errs = {k: [rel_l2(run["grads"][k][l], ref[l]) for l in range(ref.shape[0])] for k, ref in run["ref"].items()}
+    for k, e in errs.items():
+        whole = rel_l2(run["grads"][k], run["ref"][k])
+        print(f"  {k}: rel_l2 {whole:.2e}; per layer worst {max(e):.2e} (layer {int(np.argmax(e))}), "
+              f"mean {np.mean(e):.2e}")
+        assert whole < REL_L2, (k, whole)
+        assert max(e) < LAYER_REL_L2, (k, int(np.argmax(e)), max(e))
+
+
+def test_sequences_are_independent(run):
+    mf = int(np.floor(run["w"]["loss_from"] * run["w"]["T"]))
+    assert np.array_equal(run["tl_diff"][0], run["tl_same"][0])
+    assert np.all(run["tl_diff"][:, :mf] == 0.0)
+    assert np.all(run["tl_diff"][:, mf:] > 0.0)
+    # the batch loss is the mean over all positions with loss
+    assert abs(run["loss_diff"] - float(run["tl_diff"].sum()) / (run["w"]["B"] * (run["w"]["T"] - mf))) < 1e-4

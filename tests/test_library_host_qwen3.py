@@ -28,7 +28,7 @@ def _cfg(name="qwen3_tiny", **over):
 
 def test_library_exports_every_declared_function():
     names = header_functions()
-    assert len(names) == 10
+    assert len(names) == 13
     L = qb.lib()
     for n in names:
         assert hasattr(L, n), n
