@@ -117,9 +117,10 @@ const char* qwen3_last_error(const qwen3_model* m);
  * attention: the causal half) and bytes are summed per class.
  * qwen3_probe_read synchronises and reports totals since the last reset. */
 enum {
-  QWEN3_K_GEMM_FWD = 0,      /* frozen projections and the LM head, forward */
-  QWEN3_K_GEMM_DX = 1,       /* their input gradients (the LM head's included) */
-  QWEN3_K_GEMM_ADAPTER = 2,  /* adapter products: x A^T, u B^T, dy B, du A, and the adapter gradients */
+  QWEN3_K_GEMM_FWD = 0,      /* frozen projections (with the adapter's u B^T as a second contraction
+                                segment of the same GEMM) and the LM head, forward */
+  QWEN3_K_GEMM_DX = 1,       /* their input gradients (with du A likewise; the LM head's included) */
+  QWEN3_K_GEMM_ADAPTER = 2,  /* the other adapter products: s x A^T, s dy B, and the adapter gradients */
   QWEN3_K_ATTN_FWD = 3,
   QWEN3_K_ATTN_BWD = 4,
   QWEN3_K_NORM = 5,          /* RMSNorm forward/backward, q/k head norm + rotary forward/backward */

@@ -23,8 +23,9 @@ __global__ void reduce_slices_kernel(const float* __restrict__ src, int nslices,
   *reinterpret_cast<float4*>(dst + i) = acc;
 }
 
-// dst[i] (bf16) = sum_s src[s*n + i], four elements per thread
-__global__ void reduce_slices_bf16_kernel(const float* __restrict__ src, int nslices, long n, bf16_t* __restrict__ dst) {
+// dst[i] (bf16) = scale * sum_s src[s*n + i], four elements per thread
+__global__ void reduce_slices_bf16_kernel(const float* __restrict__ src, int nslices, long n, float scale,
+                                          bf16_t* __restrict__ dst) {
   long i = ((long)blockIdx.x * blockDim.x + threadIdx.x) * 4;
   if (i >= n) return;
   float4 acc = make_float4(0, 0, 0, 0);
@@ -33,7 +34,8 @@ __global__ void reduce_slices_bf16_kernel(const float* __restrict__ src, int nsl
     float4 v = *reinterpret_cast<const float4*>(src + (size_t)s * n + i);
     acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
   }
-  *reinterpret_cast<uint2*>(dst + i) = make_uint2(pack2(acc.x, acc.y), pack2(acc.z, acc.w));
+  *reinterpret_cast<uint2*>(dst + i) =
+      make_uint2(pack2(acc.x * scale, acc.y * scale), pack2(acc.z * scale, acc.w * scale));
 }
 
 // Two independent reductions in one launch; blockIdx.y picks the segment.
@@ -438,9 +440,11 @@ hipError_t launch_reduce_slices(const float* src, int nslices, long n, float* ds
   return hipGetLastError();
 }
 
-hipError_t launch_reduce_slices_bf16(const float* src, int nslices, long n, bf16_t* dst, hipStream_t s) {
+hipError_t launch_reduce_slices_bf16(const float* src, int nslices, long n, float scale, bf16_t* dst,
+                                     hipStream_t s) {
   if (n % 4) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(reduce_slices_bf16_kernel, dim3(blocks_for(n / 4, 256)), dim3(256), 0, s, src, nslices, n, dst);
+  hipLaunchKernelGGL(reduce_slices_bf16_kernel, dim3(blocks_for(n / 4, 256)), dim3(256), 0, s, src, nslices, n, scale,
+                     dst);
   return hipGetLastError();
 }
 

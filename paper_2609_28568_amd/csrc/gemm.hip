@@ -48,6 +48,7 @@ typedef __attribute__((address_space(3))) float lds_f32_t;
 // the others do not reserve registers for those reads.
 constexpr int EPI_BF16_RES = 4;
 constexpr int EPI_F32_ACC = 5;
+constexpr int EPI_BF16_SCALE = 6;   // EPI_BF16 with the accumulator scaled by alpha
 
 DEV int bitrev3(int x) { return ((x & 1) << 2) | (x & 2) | ((x >> 2) & 1); }
 
@@ -119,7 +120,7 @@ DEV bf16x8 read_frag(const lds_char_t* stage, int row_base, int s, int lane) {
   }
 }
 
-template <int BM, int BN, int BK, int NS, bool A_T, bool B_T, int EPI>
+template <int BM, int BN, int BK, int NS, bool A_T, bool B_T, int EPI, bool SEG2 = false>
 __global__ __launch_bounds__(256, (NS <= 2 ? 2 : 1)) void gemm_kernel(GemmArgs g) {
   constexpr int WTM = BM / 2, WTN = BN / 2;   // 2 x 2 waves
   constexpr int TM = WTM / 32, TN = WTN / 32;
@@ -159,7 +160,9 @@ __global__ __launch_bounds__(256, (NS <= 2 ? 2 : 1)) void gemm_kernel(GemmArgs g
 
   const int kbeg = split * g.k_chunk;
   const int kend = min(g.K, kbeg + g.k_chunk);
-  const int nk = (kend - kbeg + BK - 1) / BK;
+  // k-tiles of the first segment, then (SEG2) those of the second
+  const int nk1 = (kend - kbeg + BK - 1) / BK;
+  const int nk = SEG2 ? nk1 + g.K2 / BK : nk1;
 
   // buffer ranges: the whole operand matrices; reads past the end return 0
   const uint32_t a_rows = A_T ? (uint32_t)g.K : (uint32_t)g.M;
@@ -167,12 +170,28 @@ __global__ __launch_bounds__(256, (NS <= 2 ? 2 : 1)) void gemm_kernel(GemmArgs g
   const v4i32 ra = make_rsrc(g.A, a_rows * (uint32_t)g.lda * 2u);
   const v4i32 rb = make_rsrc(g.B, b_rows * (uint32_t)g.ldb * 2u);
 
+  // second segment: A2 column offset of this tile's output column block
+  v4i32 ra2 = ra, rb2 = rb;
+  int a2col = 0;
+  if constexpr (SEG2) {
+    static_assert(!A_T, "second segment with a non-transposed A only");
+    ra2 = make_rsrc(g.A2, (uint32_t)g.M * (uint32_t)g.lda2 * 2u);
+    rb2 = make_rsrc(g.B2, (B_T ? (uint32_t)g.K2 : (uint32_t)g.N) * (uint32_t)g.ldb2 * 2u);
+    a2col = g.K2 * ((g.a2_bound[0] > 0 && n0 >= g.a2_bound[0]) + (g.a2_bound[1] > 0 && n0 >= g.a2_bound[1]));
+  }
+
   auto stage = [&](int kt) { return smem + (kt % NS) * STAGE; };
   auto issue = [&](int kt) {
     lds_char_t* st = stage(kt);
-    const int k0 = kbeg + kt * BK;
-    issue_tile<BM, BK, A_T>(ra, g.lda, m0, k0, st, wave, lane);
-    issue_tile<BN, BK, B_T>(rb, g.ldb, n0, k0, st + A_BYTES, wave, lane);
+    if (!SEG2 || kt < nk1) {
+      const int k0 = kbeg + kt * BK;
+      issue_tile<BM, BK, A_T>(ra, g.lda, m0, k0, st, wave, lane);
+      issue_tile<BN, BK, B_T>(rb, g.ldb, n0, k0, st + A_BYTES, wave, lane);
+    } else {
+      const int k2 = (kt - nk1) * BK;
+      issue_tile<BM, BK, A_T>(ra2, g.lda2, m0, a2col + k2, st, wave, lane);
+      issue_tile<BN, BK, B_T>(rb2, g.ldb2, n0, k2, st + A_BYTES, wave, lane);
+    }
   };
   auto load = [&](bf16x8* fa, bf16x8* fb, int kt, int s) {
     const lds_char_t* st = stage(kt);
@@ -281,7 +300,7 @@ __global__ __launch_bounds__(256, (NS <= 2 ? 2 : 1)) void gemm_kernel(GemmArgs g
   bf16_t* Cb = static_cast<bf16_t*>(g.C);
   const int ncol0 = n0 + wn * WTN;
   float4 bias4[NB];
-  if constexpr (EPI == EPI_BF16 || EPI == EPI_BF16_RES || EPI == EPI_GELU) {
+  if constexpr (EPI == EPI_BF16 || EPI == EPI_BF16_RES || EPI == EPI_GELU || EPI == EPI_BF16_SCALE) {
 #pragma unroll
     for (int q = 0; q < NB; ++q) {
       const int n = ncol0 + ((lane + 64 * q) % CPR) * 4;
@@ -371,6 +390,9 @@ __global__ __launch_bounds__(256, (NS <= 2 ? 2 : 1)) void gemm_kernel(GemmArgs g
           v2 *= gelu_tanh_grad(lo_f(rd[cc].y)); v3 *= gelu_tanh_grad(hi_f(rd[cc].y));
           *reinterpret_cast<uint2*>(Cb + off) = make_uint2(pack2(v0, v1), pack2(v2, v3));
         } else {
+          if constexpr (EPI == EPI_BF16_SCALE) {
+            v0 *= g.alpha; v1 *= g.alpha; v2 *= g.alpha; v3 *= g.alpha;
+          }
           const float4 bb = bias4[cc % NB];
           v0 += bb.x; v1 += bb.y; v2 += bb.z; v3 += bb.w;
           if constexpr (EPI == EPI_GELU) {
@@ -391,23 +413,34 @@ __global__ __launch_bounds__(256, (NS <= 2 ? 2 : 1)) void gemm_kernel(GemmArgs g
   }
 }
 
-template <int BM, int BN, int BK, int NS, bool A_T, bool B_T, int EPI>
+template <int BM, int BN, int BK, int NS, bool A_T, bool B_T, int EPI, bool SEG2 = false>
 hipError_t launch_t(const GemmArgs& g, hipStream_t s) {
   const unsigned tn = (g.N + BN - 1) / BN, tm = (g.M + BM - 1) / BM;
   dim3 grid = g.splits > 1 ? dim3(tn * tm * g.splits) : dim3(tn, tm);
-  hipLaunchKernelGGL((gemm_kernel<BM, BN, BK, NS, A_T, B_T, EPI>), grid, dim3(256), 0, s, g);
+  hipLaunchKernelGGL((gemm_kernel<BM, BN, BK, NS, A_T, B_T, EPI, SEG2>), grid, dim3(256), 0, s, g);
   return hipGetLastError();
+}
+
+// Non-transposed A with an optional second contraction segment and output scale.
+template <int BM, int BN, int BK, bool B_T>
+hipError_t launch_bf16(const GemmArgs& g, hipStream_t s) {
+  const bool scale = g.alpha != 0.0f && g.alpha != 1.0f;
+  if (g.K2 > 0) {
+    if (scale) return hipErrorInvalidValue;
+    return g.residual ? launch_t<BM, BN, BK, 2, false, B_T, EPI_BF16_RES, true>(g, s)
+                      : launch_t<BM, BN, BK, 2, false, B_T, EPI_BF16, true>(g, s);
+  }
+  if (g.residual) return scale ? hipErrorInvalidValue : launch_t<BM, BN, BK, 2, false, B_T, EPI_BF16_RES>(g, s);
+  return scale ? launch_t<BM, BN, BK, 2, false, B_T, EPI_BF16_SCALE>(g, s)
+               : launch_t<BM, BN, BK, 2, false, B_T, EPI_BF16>(g, s);
 }
 
 template <int BM, int BN, int BK>
 hipError_t launch_cfg(const GemmArgs& g, int a_t, int b_t, int epi, hipStream_t s) {
-  if (!a_t && !b_t && epi == EPI_BF16)
-    return g.residual ? launch_t<BM, BN, BK, 2, false, false, EPI_BF16_RES>(g, s)
-                      : launch_t<BM, BN, BK, 2, false, false, EPI_BF16>(g, s);
+  if (g.K2 > 0 && (a_t || epi != EPI_BF16)) return hipErrorInvalidValue;
+  if (!a_t && !b_t && epi == EPI_BF16) return launch_bf16<BM, BN, BK, false>(g, s);
   if (!a_t && !b_t && epi == EPI_GELU) return launch_t<BM, BN, BK, 2, false, false, EPI_GELU>(g, s);
-  if (!a_t && b_t && epi == EPI_BF16)
-    return g.residual ? launch_t<BM, BN, BK, 2, false, true, EPI_BF16_RES>(g, s)
-                      : launch_t<BM, BN, BK, 2, false, true, EPI_BF16>(g, s);
+  if (!a_t && b_t && epi == EPI_BF16) return launch_bf16<BM, BN, BK, true>(g, s);
   if (!a_t && b_t && epi == EPI_GELU_BWD) return launch_t<BM, BN, BK, 2, false, true, EPI_GELU_BWD>(g, s);
   // an input gradient with a long contraction, split into fp32 slices
   if (!a_t && b_t && epi == EPI_F32 && !g.accumulate) return launch_t<BM, BN, BK, 2, false, true, EPI_F32>(g, s);
@@ -478,7 +511,22 @@ hipError_t launch_gemm(const GemmArgs& g0, int a_t, int b_t, int epi, hipStream_
       return hipErrorInvalidValue;
     if (epi != EPI_F32) return hipErrorInvalidValue;
   }
-  const GemmConfig c = gemm_config(g.M, g.N, a_t, b_t, epi);
+  if (g.K2 > 0) {
+    if (g.splits > 1 || g.K % 64 || g.K2 % 64 || !g.A2 || !g.B2 || a_t) return hipErrorInvalidValue;
+    if ((size_t)(g.M + 256) * g.lda2 * 2 >= (1ull << 32) ||
+        (size_t)((b_t ? g.K2 : g.N) + 256) * g.ldb2 * 2 >= (1ull << 32))
+      return hipErrorInvalidValue;
+  }
+  GemmConfig c = gemm_config(g.M, g.N, a_t, b_t, epi);
+  // a tile's output columns must lie within one block of the second segment
+  const bool bounded = g.K2 > 0 && (g.a2_bound[0] > 0 || g.a2_bound[1] > 0);
+  if (bounded) {
+    for (int i = 0; i < 2; ++i)
+      if (g.a2_bound[i] < 0 || g.a2_bound[i] % 128) return hipErrorInvalidValue;
+    if ((g.a2_bound[0] % c.bn) || (g.a2_bound[1] % c.bn))
+      c = (g.M >= 256 && (long)((g.M + 255) / 256) * ((g.N + 127) / 128) >= 512) ? GemmConfig{256, 128, 32}
+                                                                                  : GemmConfig{128, 128, 32};
+  }
   if (c.bm == 192) return launch_cfg<192, 192, 32>(g, a_t, b_t, epi, s);
   if (c.bm == 256 && c.bn == 192) return launch_cfg<256, 192, 32>(g, a_t, b_t, epi, s);
   if (c.bm == 128 && c.bn == 192) {

@@ -35,6 +35,19 @@ struct GemmArgs {
   // gradient, sum over tokens of dY) into [gemm_bias_parts(M, N, splits)][M];
   // summing those rows gives the bias gradient
   float* bsum;
+  // EPI_BF16 without residual: the accumulator is multiplied by alpha before
+  // the bias (0 or 1: no scaling)
+  float alpha;
+  // Optional second contraction segment (K2 > 0; A not transposed, no split,
+  // K and K2 multiples of 64): C += A2 B2 over K2 more indices, A2 [M][lda2]
+  // and B2 in B's orientation (row stride ldb2). Output columns n >=
+  // a2_bound[i] (for each non-zero bound, multiples of 128) read A2 from K2
+  // columns further right per bound passed, so column blocks of the output
+  // can contract with different column blocks of A2.
+  const bf16_t* A2;
+  const bf16_t* B2;
+  int K2, lda2, ldb2;
+  int a2_bound[2];
 };
 
 // Block tile (bm x bn, contraction depth bk per stage) the GEMM uses for an
@@ -78,8 +91,8 @@ hipError_t launch_layernorm_bwd(const bf16_t* dy, const bf16_t* x, const float* 
 // dst[i] (fp32, n elements) = (accumulate ? dst[i] : 0) + sum_s src[s*n + i]
 hipError_t launch_reduce_slices(const float* src, int nslices, long n, float* dst, int accumulate,
                                 hipStream_t s);
-// dst[i] (bf16, n elements, n % 4 == 0) = sum_s src[s*n + i]
-hipError_t launch_reduce_slices_bf16(const float* src, int nslices, long n, bf16_t* dst, hipStream_t s);
+// dst[i] (bf16, n elements, n % 4 == 0) = scale * sum_s src[s*n + i]
+hipError_t launch_reduce_slices_bf16(const float* src, int nslices, long n, float scale, bf16_t* dst, hipStream_t s);
 // The same for two independent segments in one launch (n and n2 multiples of 4)
 hipError_t launch_reduce_slices2(const float* src, int nslices, long n, float* dst, const float* src2,
                                  int nslices2, long n2, float* dst2, int accumulate, hipStream_t s);

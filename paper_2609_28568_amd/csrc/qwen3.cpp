@@ -174,20 +174,25 @@ ActLayout act_layout(const Dims& d) {
 
 constexpr int DW_SPLITS = 16;   // token-contraction split of the adapter gradients
 constexpr int HEAD_SPLITS = 4;  // vocabulary-contraction split of the LM head's input gradient
+constexpr int DU_SPLITS = 8;    // contraction split of du = s dy B (a few output tiles, long contraction)
 
 struct WsLayout {
-  size_t dres, dh, datt, dpacked, draw, dgu, dm, du, dsum, cosT, sinT, part, sumsq, normcoef, total;
+  size_t dres, dh, datt, dpacked, draw, dgu, dm, du, dsum, cosT, sinT, part, part2, sumsq, normcoef, total;
 };
 
 WsLayout ws_layout(const Dims& d) {
   WsLayout w{};
   const size_t BT = d.BT;
-  size_t part = 0;
+  // split partial slices: adapter B gradients [split][out][RP] (or the LM
+  // head's input gradient [split][BTL][C]) and adapter A gradients
+  // [split][n RP][in]
+  // and du [split][BT][n RP] (before the adapter gradients use the first area)
+  size_t part = (size_t)d.BTL * d.C * HEAD_SPLITS, part2 = 0;
   for (int g = 0; g < G_N; ++g) {
     if (!(d.groups & (1 << g))) continue;
     const GroupGeom gg = group_geom(d, g);
-    part = std::max(part, (size_t)gg.n * RP * gg.in);
-    for (int j = 0; j < gg.n; ++j) part = std::max(part, (size_t)gg.out[j] * RP);
+    part = std::max({part, (size_t)DW_SPLITS * gg.out_total * RP, (size_t)DU_SPLITS * BT * gg.n * RP});
+    part2 = std::max(part2, (size_t)DW_SPLITS * gg.n * RP * gg.in);
   }
   size_t o = 0;
   w.dres = o; o += align_up(BT * d.C * 2);
@@ -201,8 +206,8 @@ WsLayout ws_layout(const Dims& d) {
   w.dsum = o; o += align_up((size_t)d.B * d.H * d.T * 4);
   w.cosT = o; o += align_up((size_t)d.T * (d.hd / 2) * 4);
   w.sinT = o; o += align_up((size_t)d.T * (d.hd / 2) * 4);
-  part = std::max(part * DW_SPLITS, (size_t)d.BTL * d.C * HEAD_SPLITS);
   w.part = o; o += align_up(part * 4);
+  w.part2 = o; o += align_up(part2 * 4);
   w.sumsq = o; o += align_up((size_t)sumsq_parts() * 4);
   w.normcoef = o; o += ALIGN;
   w.total = o + TAIL;
@@ -300,90 +305,126 @@ hipError_t gemm(qwen3_model* m, int cls, double fl, int M, int N, int K, const b
 
 double mnk2(double M, double N, double K) { return 2.0 * M * N * K; }
 
-// Adapter gradient dst [M,N] (fp32, contiguous) = A^T B with A [BT,M] (row
-// stride lda) and B [BT,N] (row stride ldb): the token contraction is split
-// DW_SPLITS ways into the workspace and summed.
-hipError_t adapter_grad(qwen3_model* m, double fl, int M, int N, const bf16_t* A, int lda, const bf16_t* B, int ldb,
-                        float* dst) {
-  int kc = 0;
-  const int splits = gemm_split_plan((int)m->d.BT, DW_SPLITS, &kc);
-  float* part = m->wf(m->ws.part);
-  hipError_t e = gemm(m, QWEN3_K_GEMM_ADAPTER, fl, M, N, (int)m->d.BT, A, lda, 1, B, ldb, 1, EPI_F32, part, N, nullptr,
-                      splits, kc, (long)M * N);
-  if (e != hipSuccess) return e;
-  return m->run(QWEN3_K_OTHER, 0.0, 4.0 * (double)M * N * (splits + 1),
-                [&] { return launch_reduce_slices(part, splits, (long)M * N, dst, 0, m->stream); });
+hipError_t run_gemm(qwen3_model* m, int cls, double fl, const GemmArgs& g, int a_t, int b_t, int epi) {
+  return m->run(cls, fl, 0.0, [&] { return launch_gemm(g, a_t, b_t, epi, m->stream); });
 }
 
-hipError_t scale_bf16(qwen3_model* m, bf16_t* x, long rows, int cols, int ld, float sc) {
-  return m->run(QWEN3_K_OTHER, 0.0, 4.0 * (double)rows * cols,
-                [&] { return launch_scale_bf16(x, rows, cols, ld, sc, m->stream); });
-}
-
-// Forward of the adapters of group g at layer l: u = s x A^T into the saved u
-// buffer, then y[:, col block of projection j] += u_j B_j^T in place.
-hipError_t adapter_fwd(qwen3_model* m, int g, int l, const bf16_t* x, bf16_t* y, int ldy) {
+// Frozen projection of group g at layer l: y (row stride ldy) = x W^T
+// (+ residual). When the group is adapted, u = s x A^T first (its own small
+// GEMM, kept for the backward), and the adapter's up-projection u B^T rides
+// in the same GEMM as a second contraction segment, projection j's output
+// columns contracting with u's j-th block of RP columns.
+hipError_t proj_fwd(qwen3_model* m, int g, int l, const bf16_t* x, const bf16_t* W, bf16_t* y, int ldy,
+                    const bf16_t* residual) {
   const Dims& d = m->d;
   const GroupGeom gg = group_geom(d, g);
-  const LoraTensor* ta = m->lora_t(g, false);
-  const LoraTensor* tb = m->lora_t(g, true);
-  const bf16_t* wa = static_cast<const bf16_t*>(m->buf.lora_bf16) + ta->off + (size_t)l * gg.n * RP * gg.in;
-  const bf16_t* wb = static_cast<const bf16_t*>(m->buf.lora_bf16) + tb->off + (size_t)l * gg.out_total * RP;
-  bf16_t* u = m->ab(m->act.u[g] + l * m->act.s_u[g]);
-  const int nu = gg.n * RP;
-  const int K = QWEN3_K_GEMM_ADAPTER;
-  hipError_t e = gemm(m, K, mnk2(d.BT, gg.n * d.r, gg.in), (int)d.BT, nu, gg.in, x, gg.in, 0, wa, gg.in, 0, EPI_BF16,
-                      u, nu);
-  if (e != hipSuccess) return e;
-  e = scale_bf16(m, u, d.BT, nu, nu, d.s);
-  if (e != hipSuccess) return e;
-  int col = 0;
-  for (int j = 0; j < gg.n; ++j) {
-    e = gemm(m, K, mnk2(d.BT, gg.out[j], d.r), (int)d.BT, gg.out[j], RP, u + j * RP, nu, 0, wb + (size_t)col * RP, RP,
-             0, EPI_BF16, y + col, ldy, y + col);
+  GemmArgs a{};
+  a.A = x; a.lda = gg.in; a.B = W; a.ldb = gg.in; a.M = (int)d.BT; a.N = gg.out_total; a.K = gg.in;
+  a.C = y; a.ldc = ldy; a.residual = residual;
+  double fl = mnk2(d.BT, gg.out_total, gg.in);
+  if (m->has(g)) {
+    const LoraTensor* ta = m->lora_t(g, false);
+    const LoraTensor* tb = m->lora_t(g, true);
+    const bf16_t* wa = static_cast<const bf16_t*>(m->buf.lora_bf16) + ta->off + (size_t)l * gg.n * RP * gg.in;
+    const bf16_t* wb = static_cast<const bf16_t*>(m->buf.lora_bf16) + tb->off + (size_t)l * gg.out_total * RP;
+    bf16_t* u = m->ab(m->act.u[g] + l * m->act.s_u[g]);
+    const int nu = gg.n * RP;
+    GemmArgs ua{};
+    ua.A = x; ua.lda = gg.in; ua.B = wa; ua.ldb = gg.in; ua.M = (int)d.BT; ua.N = nu; ua.K = gg.in;
+    ua.C = u; ua.ldc = nu; ua.alpha = d.s;
+    hipError_t e = run_gemm(m, QWEN3_K_GEMM_ADAPTER, mnk2(d.BT, gg.n * d.r, gg.in), ua, 0, 0, EPI_BF16);
     if (e != hipSuccess) return e;
-    col += gg.out[j];
+    a.A2 = u; a.lda2 = nu; a.B2 = wb; a.ldb2 = RP; a.K2 = RP;
+    // projection j + 1 starts at output column out[0] + ... + out[j]
+    int bound = 0;
+    for (int j = 0; j + 1 < gg.n; ++j) {
+      bound += gg.out[j];
+      a.a2_bound[j] = bound;
+    }
+    fl += mnk2(d.BT, gg.out_total, d.r);
   }
-  return hipSuccess;
+  return run_gemm(m, QWEN3_K_GEMM_FWD, fl, a, 0, 0, EPI_BF16);
 }
 
-// Backward of the adapters of group g at layer l, given the output gradient
-// dy (row stride ldy) and the layer input x: dx += du A (skipped when dx is
-// null), dA = du^T x, dB_j = dy_j^T u_j (du = s dy_j B_j, per projection).
-hipError_t adapter_bwd(qwen3_model* m, int g, int l, const bf16_t* dy, int ldy, const bf16_t* x, bf16_t* dx) {
+// Backward of proj_fwd given the output gradient dy (row stride ldy) and the
+// input x: the adapter gradients (when adapted) and, unless dx is null,
+// dx = dy W (+ du A with du = s dy_j B_j per projection, as a second
+// contraction segment of the same GEMM). The adapter gradients contract over
+// the tokens, split DW_SPLITS ways into the partial areas and summed by one
+// launch: dB_j = dy_j^T u_j, dA = du^T x.
+hipError_t proj_bwd(qwen3_model* m, int g, int l, const bf16_t* dy, int ldy, const bf16_t* x, const bf16_t* W,
+                    bf16_t* dx) {
   const Dims& d = m->d;
   const GroupGeom gg = group_geom(d, g);
-  const LoraTensor* ta = m->lora_t(g, false);
-  const LoraTensor* tb = m->lora_t(g, true);
-  const size_t oa = ta->off + (size_t)l * gg.n * RP * gg.in, ob = tb->off + (size_t)l * gg.out_total * RP;
-  const bf16_t* wa = static_cast<const bf16_t*>(m->buf.lora_bf16) + oa;
-  const bf16_t* wb = static_cast<const bf16_t*>(m->buf.lora_bf16) + ob;
-  float* ga = static_cast<float*>(m->buf.lora_grads) + oa;
-  float* gb = static_cast<float*>(m->buf.lora_grads) + ob;
-  const bf16_t* u = m->ab(m->act.u[g] + l * m->act.s_u[g]);
-  bf16_t* du = m->wb(m->ws.du);
-  const int nu = gg.n * RP;
-  const int K = QWEN3_K_GEMM_ADAPTER;
-  hipError_t e;
-  int col = 0;
-  for (int j = 0; j < gg.n; ++j) {
-    // du_j = dy_j B_j  ([BT, RP]; B_j read as [K = out_j][N = RP])
-    e = gemm(m, K, mnk2(d.BT, d.r, gg.out[j]), (int)d.BT, RP, gg.out[j], dy + col, ldy, 0, wb + (size_t)col * RP, RP,
-             1, EPI_BF16, du + j * RP, nu);
+  const int BT = (int)d.BT, nu = gg.n * RP;
+  GemmArgs a{};
+  a.A = dy; a.lda = ldy; a.B = W; a.ldb = gg.in; a.M = BT; a.N = gg.in; a.K = gg.out_total;
+  a.C = dx; a.ldc = gg.in;
+  double fl = mnk2(d.BT, gg.in, gg.out_total);
+  if (m->has(g)) {
+    const int AD = QWEN3_K_GEMM_ADAPTER;
+    const LoraTensor* ta = m->lora_t(g, false);
+    const LoraTensor* tb = m->lora_t(g, true);
+    const size_t oa = ta->off + (size_t)l * gg.n * RP * gg.in, ob = tb->off + (size_t)l * gg.out_total * RP;
+    const bf16_t* wa = static_cast<const bf16_t*>(m->buf.lora_bf16) + oa;
+    const bf16_t* wb = static_cast<const bf16_t*>(m->buf.lora_bf16) + ob;
+    const bf16_t* u = m->ab(m->act.u[g] + l * m->act.s_u[g]);
+    bf16_t* du = m->wb(m->ws.du);
+    float* pb = m->wf(m->ws.part);
+    float* pa = m->wf(m->ws.part2);
+    hipError_t e;
+    // du_j = s dy_j B_j  ([BT, RP]; B_j read as [K = out_j][N = RP]): one
+    // column of output tiles, so the contraction over out_j is split into
+    // fp32 slices [split][BT][n RP], summed and scaled into du by one launch
+    // (every projection of the group must cut its contraction into the same
+    // number of slices, else none is split)
+    int su = gemm_split_plan(gg.out[0], DU_SPLITS, nullptr);
+    for (int j = 1; j < gg.n; ++j)
+      if (gemm_split_plan(gg.out[j], su, nullptr) != su) su = 1;
+    int col = 0;
+    for (int j = 0; j < gg.n; ++j) {
+      int kcu = 0;
+      if (gemm_split_plan(gg.out[j], su, &kcu) != su) return hipErrorInvalidValue;
+      GemmArgs q{};
+      q.A = dy + col; q.lda = ldy; q.B = wb + (size_t)col * RP; q.ldb = RP; q.M = BT; q.N = RP; q.K = gg.out[j];
+      q.C = pb + j * RP; q.ldc = nu; q.splits = su; q.k_chunk = kcu; q.split_stride = (long)BT * nu;
+      e = run_gemm(m, AD, mnk2(d.BT, d.r, gg.out[j]), q, 0, 1, EPI_F32);
+      if (e != hipSuccess) return e;
+      col += gg.out[j];
+    }
+    e = m->run(QWEN3_K_OTHER, 0.0, (4.0 * su + 2.0) * d.BT * nu,
+               [&] { return launch_reduce_slices_bf16(pb, su, (long)BT * nu, d.s, du, m->stream); });
     if (e != hipSuccess) return e;
-    // dB_j = dy_j^T u_j
-    e = adapter_grad(m, mnk2(gg.out[j], d.r, d.BT), gg.out[j], RP, dy + col, ldy, u + j * RP, nu,
-                     gb + (size_t)col * RP);
+    int kc = 0;
+    const int splits = gemm_split_plan(BT, DW_SPLITS, &kc);
+    col = 0;
+    for (int j = 0; j < gg.n; ++j) {
+      // dB_j = dy_j^T u_j into rows col.. of every partial slice [out_total][RP]
+      GemmArgs r{};
+      r.A = dy + col; r.lda = ldy; r.B = u + j * RP; r.ldb = nu; r.M = gg.out[j]; r.N = RP; r.K = BT;
+      r.C = pb + (size_t)col * RP; r.ldc = RP; r.splits = splits; r.k_chunk = kc;
+      r.split_stride = (long)gg.out_total * RP;
+      e = run_gemm(m, AD, mnk2(gg.out[j], d.r, d.BT), r, 1, 1, EPI_F32);
+      if (e != hipSuccess) return e;
+      col += gg.out[j];
+    }
+    // dA = du^T x
+    GemmArgs r{};
+    r.A = du; r.lda = nu; r.B = x; r.ldb = gg.in; r.M = nu; r.N = gg.in; r.K = BT;
+    r.C = pa; r.ldc = gg.in; r.splits = splits; r.k_chunk = kc; r.split_stride = (long)nu * gg.in;
+    e = run_gemm(m, AD, mnk2(gg.n * d.r, gg.in, d.BT), r, 1, 1, EPI_F32);
     if (e != hipSuccess) return e;
-    col += gg.out[j];
+    const long nb = (long)gg.out_total * RP, na = (long)nu * gg.in;
+    e = m->run(QWEN3_K_OTHER, 0.0, 4.0 * (double)(nb + na) * (splits + 1), [&] {
+      return launch_reduce_slices2(pb, splits, nb, static_cast<float*>(m->buf.lora_grads) + ob, pa, splits, na,
+                                   static_cast<float*>(m->buf.lora_grads) + oa, 0, m->stream);
+    });
+    if (e != hipSuccess || !dx) return e;
+    a.A2 = du; a.lda2 = nu; a.B2 = wa; a.ldb2 = gg.in; a.K2 = nu;
+    fl += mnk2(d.BT, gg.in, gg.n * d.r);
   }
-  e = scale_bf16(m, du, d.BT, nu, nu, d.s);
-  if (e != hipSuccess) return e;
-  // dA = du^T x; dx += du A (A read as [K = n*RP][N = in])
-  e = adapter_grad(m, mnk2(gg.n * d.r, gg.in, d.BT), nu, gg.in, du, nu, x, gg.in, ga);
-  if (e != hipSuccess || !dx) return e;
-  return gemm(m, K, mnk2(d.BT, gg.in, gg.n * d.r), (int)d.BT, gg.in, nu, du, nu, 0, wa, gg.in, 1, EPI_BF16, dx, gg.in,
-              dx);
+  if (!dx) return hipSuccess;
+  return run_gemm(m, QWEN3_K_GEMM_DX, fl, a, 0, 1, EPI_BF16);
 }
 
 AttnArgs attn_args(qwen3_model* m, int l) {
@@ -537,9 +578,7 @@ gpt2_status qwen3_forward(qwen3_model* m, const int32_t* d_inputs, const int32_t
       return launch_rmsnorm_fwd(m->res(l), m->base(B_IN_NORM) + (size_t)l * d.C, h, r1, BT, d.C, m->cfg.rms_eps, 1, 0,
                                 m->stream);
     }));
-    TRY(gemm(m, FWD, mnk2(BT, d.QKVD, d.C), BT, d.QKVD, d.C, h, d.C, 0, m->base(B_QKV) + (size_t)l * d.QKVD * d.C, d.C,
-             0, EPI_BF16, raw, d.QKVD));
-    if (m->has(G_QKV)) TRY(adapter_fwd(m, G_QKV, l, h, raw, d.QKVD));
+    TRY(proj_fwd(m, G_QKV, l, h, m->base(B_QKV) + (size_t)l * d.QKVD * d.C, raw, d.QKVD, nullptr));
     AttnArgs aa = attn_args(m, l);
     TRY(m->run(NORM, 0.0, 2.0 * d.BT * (d.QKVD + 3.0 * d.QD) + 4.0 * d.BT * (d.H + d.Hkv), [&] {
       return launch_qknorm_rope_fwd(raw, m->base(B_QNORM) + (size_t)l * d.hd, m->base(B_KNORM) + (size_t)l * d.hd,
@@ -548,21 +587,15 @@ gpt2_status qwen3_forward(qwen3_model* m, const int32_t* d_inputs, const int32_t
                                     d.H, d.Hkv, d.hd, m->cfg.rms_eps, m->stream);
     }));
     TRY(m->run(QWEN3_K_ATTN_FWD, attn_fwd_flops(d), 0.0, [&] { return launch_attention_fwd(aa, m->stream); }));
-    TRY(gemm(m, FWD, mnk2(BT, d.C, d.QD), BT, d.C, d.QD, aa.out, d.QD, 0, m->base(B_O) + (size_t)l * d.C * d.QD, d.QD,
-             0, EPI_BF16, xmid, d.C, m->res(l)));
-    if (m->has(G_O)) TRY(adapter_fwd(m, G_O, l, aa.out, xmid, d.C));
+    TRY(proj_fwd(m, G_O, l, aa.out, m->base(B_O) + (size_t)l * d.C * d.QD, xmid, d.C, m->res(l)));
     // MLP sub-layer
     TRY(m->run(NORM, 0.0, 2.0 * rowb + 4.0 * d.BT, [&] {
       return launch_rmsnorm_fwd(xmid, m->base(B_POST_NORM) + (size_t)l * d.C, h2, r2, BT, d.C, m->cfg.rms_eps, 1, 0,
                                 m->stream);
     }));
-    TRY(gemm(m, FWD, mnk2(BT, 2 * d.F, d.C), BT, 2 * d.F, d.C, h2, d.C, 0,
-             m->base(B_GU) + (size_t)l * 2 * d.F * d.C, d.C, 0, EPI_BF16, gu, 2 * d.F));
-    if (m->has(G_GU)) TRY(adapter_fwd(m, G_GU, l, h2, gu, 2 * d.F));
+    TRY(proj_fwd(m, G_GU, l, h2, m->base(B_GU) + (size_t)l * 2 * d.F * d.C, gu, 2 * d.F, nullptr));
     TRY(m->run(OTHER, 0.0, 6.0 * d.BT * d.F, [&] { return launch_swiglu_fwd(gu, mm, d.BT, d.F, m->stream); }));
-    TRY(gemm(m, FWD, mnk2(BT, d.C, d.F), BT, d.C, d.F, mm, d.F, 0, m->base(B_DOWN) + (size_t)l * d.C * d.F, d.F, 0,
-             EPI_BF16, m->res(l + 1), d.C, xmid));
-    if (m->has(G_DN)) TRY(adapter_fwd(m, G_DN, l, mm, m->res(l + 1), d.C));
+    TRY(proj_fwd(m, G_DN, l, mm, m->base(B_DOWN) + (size_t)l * d.C * d.F, m->res(l + 1), d.C, xmid));
   }
   // final norm and LM head on the positions that carry loss (compacted rows)
   bf16_t* xf = m->ab(m->act.xf);
@@ -604,7 +637,7 @@ gpt2_status qwen3_backward(qwen3_model* m) {
     TRY(gemm(m, DX, mnk2(BTL, d.C, d.V), BTL, d.C, d.V, m->ab(m->act.logits), d.V, 0, m->base(B_EMBED), d.C, 1,
              EPI_F32, part, d.C, nullptr, splits, kc, (long)d.BTL * d.C));
     TRY(m->run(QWEN3_K_OTHER, 0.0, (4.0 * splits + 2.0) * d.BTL * d.C,
-               [&] { return launch_reduce_slices_bf16(part, splits, d.BTL * d.C, dh, m->stream); }));
+               [&] { return launch_reduce_slices_bf16(part, splits, d.BTL * d.C, 1.0f, dh, m->stream); }));
   }
   TRY(m->run(NORM, 0.0, 2.0 * rowb + 4.0 * d.BTL * d.C + 4.0 * d.BTL, [&] {
     return launch_rmsnorm_bwd(dh, m->res(d.L), m->af(m->act.rf), m->base(B_FINAL_NORM), dres, 0, BT, d.C, d.T,
@@ -622,14 +655,10 @@ gpt2_status qwen3_backward(qwen3_model* m) {
     bf16_t* dm = m->wb(m->ws.dm);
     bf16_t* dgu = m->wb(m->ws.dgu);
     // down projection: res(l+1) = xmid + m down^T (+ adapter)
-    TRY(gemm(m, DX, mnk2(BT, d.F, d.C), BT, d.F, d.C, dres, d.C, 0, m->base(B_DOWN) + (size_t)l * d.C * d.F, d.F, 1,
-             EPI_BF16, dm, d.F));
-    if (m->has(G_DN)) TRY(adapter_bwd(m, G_DN, l, dres, d.C, mm, dm));
+    TRY(proj_bwd(m, G_DN, l, dres, d.C, mm, m->base(B_DOWN) + (size_t)l * d.C * d.F, dm));
     TRY(m->run(QWEN3_K_OTHER, 0.0, 10.0 * d.BT * d.F,
                [&] { return launch_swiglu_bwd(dm, gu, dgu, d.BT, d.F, m->stream); }));
-    TRY(gemm(m, DX, mnk2(BT, d.C, 2 * d.F), BT, d.C, 2 * d.F, dgu, 2 * d.F, 0,
-             m->base(B_GU) + (size_t)l * 2 * d.F * d.C, d.C, 1, EPI_BF16, dh, d.C));
-    if (m->has(G_GU)) TRY(adapter_bwd(m, G_GU, l, dgu, 2 * d.F, h2, dh));
+    TRY(proj_bwd(m, G_GU, l, dgu, 2 * d.F, h2, m->base(B_GU) + (size_t)l * 2 * d.F * d.C, dh));
     TRY(m->run(NORM, 0.0, 4.0 * rowb + 4.0 * d.BT, [&] {
       return launch_rmsnorm_bwd(dh, xmid, r2, m->base(B_POST_NORM) + (size_t)l * d.C, dres, 1, BT, d.C, 1, 0,
                                 m->stream);
@@ -637,9 +666,7 @@ gpt2_status qwen3_backward(qwen3_model* m) {
     // attention output projection: xmid = res(l) + att o^T (+ adapter)
     AttnArgs aa = attn_args(m, l);
     bf16_t* datt = m->wb(m->ws.datt);
-    TRY(gemm(m, DX, mnk2(BT, d.QD, d.C), BT, d.QD, d.C, dres, d.C, 0, m->base(B_O) + (size_t)l * d.C * d.QD, d.QD, 1,
-             EPI_BF16, datt, d.QD));
-    if (m->has(G_O)) TRY(adapter_bwd(m, G_O, l, dres, d.C, aa.out, datt));
+    TRY(proj_bwd(m, G_O, l, dres, d.C, aa.out, m->base(B_O) + (size_t)l * d.C * d.QD, datt));
     TRY(m->run(QWEN3_K_ATTN_BWD, 2.0 * attn_fwd_flops(d), 0.0, [&] { return launch_attention_bwd(aa, m->stream); }));
     bf16_t* draw = m->wb(m->ws.draw);
     TRY(m->run(NORM, 0.0, 2.0 * d.BT * (2.0 * d.QKVD + 3.0 * d.QD) + 4.0 * d.BT * (d.H + d.Hkv), [&] {
@@ -651,10 +678,7 @@ gpt2_status qwen3_backward(qwen3_model* m) {
     // the first layer's input gradient would only reach the frozen token
     // table: its q|k|v input gradient and the norm behind it are skipped
     const bool need_dx = l > 0;
-    if (need_dx)
-      TRY(gemm(m, DX, mnk2(BT, d.C, d.QKVD), BT, d.C, d.QKVD, draw, d.QKVD, 0,
-               m->base(B_QKV) + (size_t)l * d.QKVD * d.C, d.C, 1, EPI_BF16, dh, d.C));
-    if (m->has(G_QKV)) TRY(adapter_bwd(m, G_QKV, l, draw, d.QKVD, h, need_dx ? dh : nullptr));
+    TRY(proj_bwd(m, G_QKV, l, draw, d.QKVD, h, m->base(B_QKV) + (size_t)l * d.QKVD * d.C, need_dx ? dh : nullptr));
     if (need_dx)
       TRY(m->run(NORM, 0.0, 4.0 * rowb + 4.0 * d.BT, [&] {
         return launch_rmsnorm_bwd(dh, m->res(l), r1, m->base(B_IN_NORM) + (size_t)l * d.C, dres, 1, BT, d.C, 1, 0,

@@ -132,72 +132,108 @@ __global__ __launch_bounds__(256) void rmsnorm_bwd_kernel(const bf16_t* __restri
   }
 }
 
-// Per (token, head) of width 128: one wave, lane l holding elements 2l, 2l+1
-// (l < 32: first half; l >= 32: second half), so rotary pair (i, i + 64) is
-// lanes (l, l ^ 32). Query heads 0..H-1 and key heads 0..Hkv-1 are
-// RMS-normalised with their gains and rotated by the token's angles
-// (cos/sin tables [T][64] in fp32); value heads are copied. Output layout:
-// q [H*128] | k [H*128] | v [H*128], key/value head j repeated for query
-// heads j*G .. j*G+G-1 (G = H / Hkv).
+// Per (token, head slot) item of width 128: 16 lanes, lane i of the group
+// holding elements 8i..8i+7, four items per wave; the rotary pair (e, e + 64)
+// is lanes (i, i ^ 8) of the group. Query heads 0..H-1 and key heads
+// 0..Hkv-1 are RMS-normalised with their gains and rotated by the token's
+// angles (cos/sin tables [T][64] in fp32); value heads are copied. Output
+// layout: q [H*128] | k [H*128] | v [H*128], key/value head j repeated for
+// query heads j*G .. j*G+G-1 (G = H / Hkv). Items are whole 16-lane groups,
+// so a group that runs past the end exits as a whole and every shuffle stays
+// inside a group.
 constexpr int QK_HD = 128;
+
+DEV float group16_sum(float v) {
+  v += __shfl_xor(v, 8);
+  v += __shfl_xor(v, 4);
+  v += __shfl_xor(v, 2);
+  v += __shfl_xor(v, 1);
+  return v;
+}
+
+DEV void unpack8(const uint4& u, float* v) {
+  v[0] = lo_f(u.x); v[1] = hi_f(u.x); v[2] = lo_f(u.y); v[3] = hi_f(u.y);
+  v[4] = lo_f(u.z); v[5] = hi_f(u.z); v[6] = lo_f(u.w); v[7] = hi_f(u.w);
+}
+
+DEV uint4 pack8(const float* v) {
+  return make_uint4(pack2(v[0], v[1]), pack2(v[2], v[3]), pack2(v[4], v[5]), pack2(v[6], v[7]));
+}
+
+// the 8 cos and sin values of elements 8i..8i+7 (frequency index (8i) mod 64)
+DEV void rope_coefs(const float* __restrict__ cosT, const float* __restrict__ sinT, int t, int sub, float* c,
+                    float* sn) {
+  const int p = (8 * sub) & 63;
+  const float4 c0 = *reinterpret_cast<const float4*>(cosT + (size_t)t * 64 + p);
+  const float4 c1 = *reinterpret_cast<const float4*>(cosT + (size_t)t * 64 + p + 4);
+  const float4 s0 = *reinterpret_cast<const float4*>(sinT + (size_t)t * 64 + p);
+  const float4 s1 = *reinterpret_cast<const float4*>(sinT + (size_t)t * 64 + p + 4);
+  c[0] = c0.x; c[1] = c0.y; c[2] = c0.z; c[3] = c0.w; c[4] = c1.x; c[5] = c1.y; c[6] = c1.z; c[7] = c1.w;
+  sn[0] = s0.x; sn[1] = s0.y; sn[2] = s0.z; sn[3] = s0.w; sn[4] = s1.x; sn[5] = s1.y; sn[6] = s1.z; sn[7] = s1.w;
+}
+
 __global__ __launch_bounds__(256) void qknorm_rope_fwd_kernel(const bf16_t* __restrict__ raw, const bf16_t* __restrict__ qn_w,
                                                               const bf16_t* __restrict__ kn_w, const float* __restrict__ cosT,
                                                               const float* __restrict__ sinT, bf16_t* __restrict__ packed,
                                                               float* __restrict__ rq, float* __restrict__ rk, int BT, int T,
                                                               int H, int Hkv, float eps) {
-  const int lane = threadIdx.x & 63;
-  const long item = (long)blockIdx.x * 4 + (threadIdx.x >> 6);   // (token, head slot) over H + 2 Hkv slots
+  const int sub = threadIdx.x & 15;
+  const long item = ((long)blockIdx.x * blockDim.x + threadIdx.x) >> 4;   // (token, head slot) over H + 2 Hkv slots
   const int slots = H + 2 * Hkv;
   if (item >= (long)BT * slots) return;
   const int tok = (int)(item / slots), hs = (int)(item % slots);
   const int t = tok % T;
   const int G = H / Hkv;
   const int rawW = slots * QK_HD, outW = 3 * H * QK_HD;
-  const uint32_t u = *reinterpret_cast<const uint32_t*>(raw + (size_t)tok * rawW + hs * QK_HD + 2 * lane);
-  float a = lo_f(u), b = hi_f(u);
+  const uint4 u = *reinterpret_cast<const uint4*>(raw + (size_t)tok * rawW + hs * QK_HD + 8 * sub);
   bf16_t* orow = packed + (size_t)tok * outW;
   if (hs >= H + Hkv) {   // value head: copy to its G query-head slots
     const int j = hs - H - Hkv;
     for (int k = 0; k < G; ++k)
-      *reinterpret_cast<uint32_t*>(orow + 2 * H * QK_HD + (j * G + k) * QK_HD + 2 * lane) = u;
+      *reinterpret_cast<uint4*>(orow + 2 * H * QK_HD + (j * G + k) * QK_HD + 8 * sub) = u;
     return;
   }
   const bool isq = hs < H;
-  const bf16_t* w = isq ? qn_w : kn_w;
-  const float rstd = 1.0f / sqrtf(wave_sum(a * a + b * b) / QK_HD + eps);
-  const uint32_t wu = *reinterpret_cast<const uint32_t*>(w + 2 * lane);
-  a = a * rstd * lo_f(wu);
-  b = b * rstd * hi_f(wu);
-  // rotate: pair index p = (2 lane) mod 64 and +1; first half x1, second half x2
-  const float pa = __shfl_xor(a, 32), pb = __shfl_xor(b, 32);
-  const int p = (2 * lane) & 63;
-  const float c0 = cosT[(size_t)t * 64 + p], c1 = cosT[(size_t)t * 64 + p + 1];
-  const float s0 = sinT[(size_t)t * 64 + p], s1 = sinT[(size_t)t * 64 + p + 1];
-  float ya, yb;
-  if (lane < 32) { ya = a * c0 - pa * s0; yb = b * c1 - pb * s1; }   // x1 cos - x2 sin
-  else { ya = a * c0 + pa * s0; yb = b * c1 + pb * s1; }             // x2 cos + x1 sin
-  const uint32_t o = pack2(ya, yb);
+  float x[8];
+  unpack8(u, x);
+  float ss = 0.0f;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) ss += x[e] * x[e];
+  const float rstd = 1.0f / sqrtf(group16_sum(ss) / QK_HD + eps);
+  const uint4 wu = *reinterpret_cast<const uint4*>((isq ? qn_w : kn_w) + 8 * sub);
+  float w[8];
+  unpack8(wu, w);
+#pragma unroll
+  for (int e = 0; e < 8; ++e) x[e] = x[e] * rstd * w[e];
+  // rotate: first half x1 cos - x2 sin, second half x2 cos + x1 sin
+  float c[8], sn[8];
+  rope_coefs(cosT, sinT, t, sub, c, sn);
+  const float sgn = sub < 8 ? -1.0f : 1.0f;
+  float y[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) y[e] = x[e] * c[e] + sgn * __shfl_xor(x[e], 8) * sn[e];
+  const uint4 o = pack8(y);
   if (isq) {
-    *reinterpret_cast<uint32_t*>(orow + hs * QK_HD + 2 * lane) = o;
-    if (lane == 0) rq[(size_t)tok * H + hs] = rstd;
+    *reinterpret_cast<uint4*>(orow + hs * QK_HD + 8 * sub) = o;
+    if (sub == 0) rq[(size_t)tok * H + hs] = rstd;
   } else {
     const int j = hs - H;
-    for (int k = 0; k < G; ++k) *reinterpret_cast<uint32_t*>(orow + H * QK_HD + (j * G + k) * QK_HD + 2 * lane) = o;
-    if (lane == 0) rk[(size_t)tok * Hkv + j] = rstd;
+    for (int k = 0; k < G; ++k) *reinterpret_cast<uint4*>(orow + H * QK_HD + (j * G + k) * QK_HD + 8 * sub) = o;
+    if (sub == 0) rk[(size_t)tok * Hkv + j] = rstd;
   }
 }
 
 // Backward of qknorm_rope_fwd_kernel: dpacked (q | k | v over H heads each)
 // -> draw (q over H heads | k over Hkv | v over Hkv). A key/value head sums
 // the gradients of its G repeated slots; queries and keys then go back
-// through the rotation (its transpose) and the RMSNorm.
+// through the rotation (its transpose) and the RMSNorm. Same item layout.
 __global__ __launch_bounds__(256) void qknorm_rope_bwd_kernel(const bf16_t* __restrict__ dpacked, const bf16_t* __restrict__ raw,
                                                               const bf16_t* __restrict__ qn_w, const bf16_t* __restrict__ kn_w,
                                                               const float* __restrict__ cosT, const float* __restrict__ sinT,
                                                               const float* __restrict__ rq, const float* __restrict__ rk,
                                                               bf16_t* __restrict__ draw, int BT, int T, int H, int Hkv) {
-  const int lane = threadIdx.x & 63;
-  const long item = (long)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int sub = threadIdx.x & 15;
+  const long item = ((long)blockIdx.x * blockDim.x + threadIdx.x) >> 4;
   const int slots = H + 2 * Hkv;
   if (item >= (long)BT * slots) return;
   const int tok = (int)(item / slots), hs = (int)(item % slots);
@@ -205,40 +241,51 @@ __global__ __launch_bounds__(256) void qknorm_rope_bwd_kernel(const bf16_t* __re
   const int G = H / Hkv;
   const int rawW = slots * QK_HD, pW = 3 * H * QK_HD;
   const bf16_t* prow = dpacked + (size_t)tok * pW;
-  float da = 0.0f, db = 0.0f;
+  float d[8];
   if (hs < H) {
-    const uint32_t g = *reinterpret_cast<const uint32_t*>(prow + hs * QK_HD + 2 * lane);
-    da = lo_f(g); db = hi_f(g);
+    unpack8(*reinterpret_cast<const uint4*>(prow + hs * QK_HD + 8 * sub), d);
   } else {
     const int j = hs < H + Hkv ? hs - H : hs - H - Hkv;
     const int base = hs < H + Hkv ? H * QK_HD : 2 * H * QK_HD;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) d[e] = 0.0f;
     for (int k = 0; k < G; ++k) {
-      const uint32_t g = *reinterpret_cast<const uint32_t*>(prow + base + (j * G + k) * QK_HD + 2 * lane);
-      da += lo_f(g); db += hi_f(g);
+      float g[8];
+      unpack8(*reinterpret_cast<const uint4*>(prow + base + (j * G + k) * QK_HD + 8 * sub), g);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) d[e] += g[e];
     }
   }
-  bf16_t* drow = draw + (size_t)tok * rawW + hs * QK_HD + 2 * lane;
+  bf16_t* drow = draw + (size_t)tok * rawW + hs * QK_HD + 8 * sub;
   if (hs >= H + Hkv) {
-    *reinterpret_cast<uint32_t*>(drow) = pack2(da, db);
+    *reinterpret_cast<uint4*>(drow) = pack8(d);
     return;
   }
-  // transpose rotation: d1 cos + d2 sin (first half), d2 cos - d1 sin (second half)
-  const float pa = __shfl_xor(da, 32), pb = __shfl_xor(db, 32);
-  const int p = (2 * lane) & 63;
-  const float c0 = cosT[(size_t)t * 64 + p], c1 = cosT[(size_t)t * 64 + p + 1];
-  const float s0 = sinT[(size_t)t * 64 + p], s1 = sinT[(size_t)t * 64 + p + 1];
-  float na, nb;
-  if (lane < 32) { na = da * c0 + pa * s0; nb = db * c1 + pb * s1; }
-  else { na = da * c0 - pa * s0; nb = db * c1 - pb * s1; }
+  // transposed rotation: first half d1 cos + d2 sin, second half d2 cos - d1 sin
+  float c[8], sn[8];
+  rope_coefs(cosT, sinT, t, sub, c, sn);
+  const float sgn = sub < 8 ? 1.0f : -1.0f;
+  float n[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) n[e] = d[e] * c[e] + sgn * __shfl_xor(d[e], 8) * sn[e];
   // RMSNorm backward over the head (gain frozen)
   const bool isq = hs < H;
-  const uint32_t xu = *reinterpret_cast<const uint32_t*>(raw + (size_t)tok * rawW + hs * QK_HD + 2 * lane);
-  const uint32_t wu = *reinterpret_cast<const uint32_t*>((isq ? qn_w : kn_w) + 2 * lane);
+  float x[8], w[8];
+  unpack8(*reinterpret_cast<const uint4*>(raw + (size_t)tok * rawW + hs * QK_HD + 8 * sub), x);
+  unpack8(*reinterpret_cast<const uint4*>((isq ? qn_w : kn_w) + 8 * sub), w);
   const float rstd = isq ? rq[(size_t)tok * H + hs] : rk[(size_t)tok * Hkv + (hs - H)];
-  const float xa = lo_f(xu) * rstd, xb = hi_f(xu) * rstd;
-  const float ga = na * lo_f(wu), gb = nb * hi_f(wu);
-  const float m = wave_sum(ga * xa + gb * xb) / QK_HD;
-  *reinterpret_cast<uint32_t*>(drow) = pack2(rstd * (ga - xa * m), rstd * (gb - xb * m));
+  float dot = 0.0f;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    x[e] *= rstd;          // xhat
+    n[e] *= w[e];          // g
+    dot += n[e] * x[e];
+  }
+  const float m = group16_sum(dot) / QK_HD;
+  float o[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) o[e] = rstd * (n[e] - x[e] * m);
+  *reinterpret_cast<uint4*>(drow) = pack8(o);
 }
 
 DEV float sigmoid_f(float x) { return 1.0f / (1.0f + __expf(-x)); }
@@ -336,7 +383,7 @@ hipError_t launch_qknorm_rope_fwd(const bf16_t* raw, const bf16_t* qn_w, const b
                                   int hd, float eps, hipStream_t s) {
   if (hd != QK_HD || Hkv < 1 || H % Hkv) return hipErrorInvalidValue;
   const long items = (long)BT * (H + 2 * Hkv);
-  hipLaunchKernelGGL(qknorm_rope_fwd_kernel, dim3(nblocks(items, 4)), dim3(256), 0, s, raw, qn_w, kn_w, cosT, sinT,
+  hipLaunchKernelGGL(qknorm_rope_fwd_kernel, dim3(nblocks(items, 16)), dim3(256), 0, s, raw, qn_w, kn_w, cosT, sinT,
                      packed, rq, rk, BT, T, H, Hkv, eps);
   return hipGetLastError();
 }
@@ -346,7 +393,7 @@ hipError_t launch_qknorm_rope_bwd(const bf16_t* dpacked, const bf16_t* raw, cons
                                   int BT, int T, int H, int Hkv, int hd, hipStream_t s) {
   if (hd != QK_HD || Hkv < 1 || H % Hkv) return hipErrorInvalidValue;
   const long items = (long)BT * (H + 2 * Hkv);
-  hipLaunchKernelGGL(qknorm_rope_bwd_kernel, dim3(nblocks(items, 4)), dim3(256), 0, s, dpacked, raw, qn_w, kn_w, cosT,
+  hipLaunchKernelGGL(qknorm_rope_bwd_kernel, dim3(nblocks(items, 16)), dim3(256), 0, s, dpacked, raw, qn_w, kn_w, cosT,
                      sinT, rq, rk, draw, BT, T, H, Hkv);
   return hipGetLastError();
 }
