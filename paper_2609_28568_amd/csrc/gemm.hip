@@ -442,8 +442,9 @@ hipError_t launch_cfg(const GemmArgs& g, int a_t, int b_t, int epi, hipStream_t 
   if (!a_t && !b_t && epi == EPI_GELU) return launch_t<BM, BN, BK, 2, false, false, EPI_GELU>(g, s);
   if (!a_t && b_t && epi == EPI_BF16) return launch_bf16<BM, BN, BK, true>(g, s);
   if (!a_t && b_t && epi == EPI_GELU_BWD) return launch_t<BM, BN, BK, 2, false, true, EPI_GELU_BWD>(g, s);
-  // an input gradient with a long contraction, split into fp32 slices
+  // products with few output tiles and a long contraction, split into fp32 slices
   if (!a_t && b_t && epi == EPI_F32 && !g.accumulate) return launch_t<BM, BN, BK, 2, false, true, EPI_F32>(g, s);
+  if (!a_t && !b_t && epi == EPI_F32 && !g.accumulate) return launch_t<BM, BN, BK, 2, false, false, EPI_F32>(g, s);
   if (a_t && b_t && epi == EPI_F32)
     return g.accumulate ? launch_t<BM, BN, BK, 2, true, true, EPI_F32_ACC>(g, s)
                         : launch_t<BM, BN, BK, 2, true, true, EPI_F32>(g, s);

@@ -186,7 +186,7 @@ WsLayout ws_layout(const Dims& d) {
   // split partial slices: adapter B gradients [split][out][RP] (or the LM
   // head's input gradient [split][BTL][C]) and adapter A gradients
   // [split][n RP][in]
-  // and du [split][BT][n RP] (before the adapter gradients use the first area)
+  // and u or du [split][BT][n RP] (before the adapter gradients use the first area)
   size_t part = (size_t)d.BTL * d.C * HEAD_SPLITS, part2 = 0;
   for (int g = 0; g < G_N; ++g) {
     if (!(d.groups & (1 << g))) continue;
@@ -329,10 +329,18 @@ hipError_t proj_fwd(qwen3_model* m, int g, int l, const bf16_t* x, const bf16_t*
     const bf16_t* wb = static_cast<const bf16_t*>(m->buf.lora_bf16) + tb->off + (size_t)l * gg.out_total * RP;
     bf16_t* u = m->ab(m->act.u[g] + l * m->act.s_u[g]);
     const int nu = gg.n * RP;
+    // u has one or two columns of output tiles: its contraction over the
+    // input width is split into fp32 slices, summed and scaled by s into u
+    int kc = 0;
+    const int su = gemm_split_plan(gg.in, DU_SPLITS, &kc);
+    float* part = m->wf(m->ws.part);
     GemmArgs ua{};
     ua.A = x; ua.lda = gg.in; ua.B = wa; ua.ldb = gg.in; ua.M = (int)d.BT; ua.N = nu; ua.K = gg.in;
-    ua.C = u; ua.ldc = nu; ua.alpha = d.s;
-    hipError_t e = run_gemm(m, QWEN3_K_GEMM_ADAPTER, mnk2(d.BT, gg.n * d.r, gg.in), ua, 0, 0, EPI_BF16);
+    ua.C = part; ua.ldc = nu; ua.splits = su; ua.k_chunk = kc; ua.split_stride = (long)d.BT * nu;
+    hipError_t e = run_gemm(m, QWEN3_K_GEMM_ADAPTER, mnk2(d.BT, gg.n * d.r, gg.in), ua, 0, 0, EPI_F32);
+    if (e != hipSuccess) return e;
+    e = m->run(QWEN3_K_OTHER, 0.0, (4.0 * su + 2.0) * d.BT * nu,
+               [&] { return launch_reduce_slices_bf16(part, su, d.BT * nu, d.s, u, m->stream); });
     if (e != hipSuccess) return e;
     a.A2 = u; a.lda2 = nu; a.B2 = wb; a.ldb2 = RP; a.K2 = RP;
     // projection j + 1 starts at output column out[0] + ... + out[j]
