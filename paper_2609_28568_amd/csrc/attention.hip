@@ -26,6 +26,9 @@
 //   dK, dV:  per 128 keys (4 waves x 32), walk query tiles from the diagonal:
 //            S = Q K^T, dP = dO V^T (one key per lane), dV^T += dO^T P,
 //            dK^T += Q^T dS; runs after dQ, reading the stored D.
+// Grouped-query attention: a key/value head serves H / Hkv query heads; the
+// forward and dQ kernels read the key/value head of their query head, and a
+// dK/dV workgroup walks the query tiles of every query head of its group.
 #include <type_traits>
 
 #include "common.h"
@@ -131,7 +134,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(AttnArgs a) {
   using S = Shape<HD>;
   __shared__ __attribute__((aligned(1024))) char smem_raw[2 * 2 * S::TBA];   // 2 stages x (K, V)
   lds_char_t* smem = (lds_char_t*)smem_raw;
-  const int T = a.T, H = a.H, C = H * HD, ld = 3 * C;
+  const int T = a.T, H = a.H, C = H * HD, Hkv = a.Hkv > 0 ? a.Hkv : H, ld = (H + 2 * Hkv) * HD;
   // 1-D grid, head fastest: every head's heaviest (last) query block is
   // dispatched first, then the next heaviest of every head, and so on, so the
   // causal imbalance leaves no long blocks for the end; and with B*H a
@@ -147,6 +150,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(AttnArgs a) {
   const int q0w = qb * BQ + wave * 32;
   const int q = q0w + lq;
   const bf16_t* base = a.qkv + (size_t)b * T * ld + h * HD;
+  const bf16_t* kbase = a.qkv + (size_t)b * T * ld + (H + h / (H / Hkv)) * HD;
   const v4i32 rs = make_rsrc(a.qkv, (uint32_t)((size_t)a.B * T * ld * 2));
 
   bf16x8 qf[S::KS];
@@ -166,8 +170,8 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(AttnArgs a) {
   const int ntiles = (kv_end + TILE - 1) / TILE;
   auto issue = [&](int it) {
     lds_char_t* st = smem + (it & 1) * 2 * S::TBA;
-    issue_rows<HD>(rs, a.qkv, base + C, it * TILE, ld, st, wave, lane);
-    issue_rows<HD>(rs, a.qkv, base + 2 * C, it * TILE, ld, st + S::TBA, wave, lane);
+    issue_rows<HD>(rs, a.qkv, kbase, it * TILE, ld, st, wave, lane);
+    issue_rows<HD>(rs, a.qkv, kbase + Hkv * HD, it * TILE, ld, st + S::TBA, wave, lane);
   };
   issue(0);
   for (int it = 0; it < ntiles; ++it) {
@@ -263,11 +267,13 @@ __global__ __launch_bounds__(256, HD >= 128 ? 1 : 2) void attn_bwd_dkdv_kernel(A
   constexpr int STAGE = 2 * S::TBA + 1024;   // Q tile, dO tile, lse and D rows
   __shared__ __attribute__((aligned(1024))) char smem_raw[2 * STAGE];
   lds_char_t* smem = (lds_char_t*)smem_raw;
-  const int T = a.T, H = a.H, C = H * HD, ld = 3 * C;
-  // 1-D grid, head fastest: the heaviest (first) key blocks of every head are
-  // dispatched first (see the forward kernel)
-  const int BH = a.B * H;
-  const int bh = blockIdx.x % BH, b = bh / H, h = bh % H;
+  const int T = a.T, H = a.H, C = H * HD, Hkv = a.Hkv > 0 ? a.Hkv : H, ld = (H + 2 * Hkv) * HD;
+  const int G = H / Hkv;   // query heads per key/value head
+  // 1-D grid over (sequence, key/value head) pairs, head fastest: the
+  // heaviest (first) key blocks of every head are dispatched first (see the
+  // forward kernel)
+  const int BH = a.B * Hkv;
+  const int bj = blockIdx.x % BH, b = bj / Hkv, j = bj % Hkv;
   const int kb = (int)(blockIdx.x / BH);
   // the wave index is uniform across the wave: say so, so that per-wave
   // conditions compile to scalar branches
@@ -275,8 +281,7 @@ __global__ __launch_bounds__(256, HD >= 128 ? 1 : 2) void attn_bwd_dkdv_kernel(A
   const int lk = lane & 31, g = lane >> 5;
   const int kv0w = kb * BQ + wave * 32;
   const int kv = kv0w + lk;
-  const bf16_t* base = a.qkv + (size_t)b * T * ld + h * HD;
-  const bf16_t* dob = a.dout + (size_t)b * T * C + h * HD;
+  const bf16_t* kbase = a.qkv + (size_t)b * T * ld + (H + j) * HD;   // key head j; value head j at + Hkv HD
   const v4i32 rq = make_rsrc(a.qkv, (uint32_t)((size_t)a.B * T * ld * 2));
   const v4i32 rd = make_rsrc(a.dout, (uint32_t)((size_t)a.B * T * C * 2));
   const v4i32 rl = make_rsrc(a.lse, (uint32_t)((size_t)a.B * H * T * 4));
@@ -287,8 +292,8 @@ __global__ __launch_bounds__(256, HD >= 128 ? 1 : 2) void attn_bwd_dkdv_kernel(A
   for (int s = 0; s < S::KS; ++s) {
     uint4 k4 = make_uint4(0, 0, 0, 0), v4 = make_uint4(0, 0, 0, 0);
     if (kv < T) {
-      k4 = *reinterpret_cast<const uint4*>(base + (size_t)kv * ld + C + 16 * s + 8 * g);
-      v4 = *reinterpret_cast<const uint4*>(base + (size_t)kv * ld + 2 * C + 16 * s + 8 * g);
+      k4 = *reinterpret_cast<const uint4*>(kbase + (size_t)kv * ld + 16 * s + 8 * g);
+      v4 = *reinterpret_cast<const uint4*>(kbase + (size_t)kv * ld + Hkv * HD + 16 * s + 8 * g);
     }
     kf[s] = as_bf16x8(k4);
     vf[s] = as_bf16x8(v4);
@@ -302,16 +307,20 @@ __global__ __launch_bounds__(256, HD >= 128 ? 1 : 2) void attn_bwd_dkdv_kernel(A
   const float scale = 1.0f / sqrtf((float)HD);
   const float sc = scale * LOG2E;
 
+  // query tiles from the diagonal to the end, for each query head h = j G + gi
+  // of the group in turn: step it is tile it % nt of head gi = it / nt
   const int qstart = kb * BQ;
-  const int ntiles = qstart < T ? (T - qstart + TILE - 1) / TILE : 0;
+  const int nt = qstart < T ? (T - qstart + TILE - 1) / TILE : 0;
+  const int ntiles = nt * G;
   auto issue = [&](int it) {
     lds_char_t* st = smem + (it & 1) * STAGE;
-    const int q0 = qstart + it * TILE;
-    issue_rows<HD>(rq, a.qkv, base, q0, ld, st, wave, lane);
-    issue_rows<HD>(rd, a.dout, dob, q0, C, st + S::TBA, wave, lane);
+    const int h = j * G + it / nt;
+    const int q0 = qstart + (it % nt) * TILE;
+    issue_rows<HD>(rq, a.qkv, a.qkv + (size_t)b * T * ld + h * HD, q0, ld, st, wave, lane);
+    issue_rows<HD>(rd, a.dout, a.dout + (size_t)b * T * C + h * HD, q0, C, st + S::TBA, wave, lane);
     // the tile's 64 log-sum-exp and D values (256 bytes each): 16 lanes
     if (wave == 0 && lane < 16) {
-      const uint32_t off = ((uint32_t)bh * (uint32_t)T + (uint32_t)q0) * 4u + 16u * lane;
+      const uint32_t off = ((uint32_t)(b * H + h) * (uint32_t)T + (uint32_t)q0) * 4u + 16u * lane;
       dma16(rl, off, lds_addr(st + 2 * S::TBA));
       dma16(rD, off, lds_addr(st + 2 * S::TBA + 256));
     }
@@ -321,7 +330,7 @@ __global__ __launch_bounds__(256, HD >= 128 ? 1 : 2) void attn_bwd_dkdv_kernel(A
     wait_vmcnt<0>();
     block_barrier();
     if (it + 1 < ntiles) issue(it + 1);
-    const int q0 = qstart + it * TILE;
+    const int q0 = qstart + (it % nt) * TILE;
     if (q0 + TILE - 1 < kv0w) continue;   // every query precedes this wave's keys
     const lds_char_t* Qs = smem + (it & 1) * STAGE;
     const lds_char_t* Ds = Qs + S::TBA;
@@ -392,17 +401,17 @@ __global__ __launch_bounds__(256, HD >= 128 ? 1 : 2) void attn_bwd_dkdv_kernel(A
   }
 
   if (kv < T) {
-    bf16_t* dst = a.dqkv + ((size_t)b * T + kv) * ld + h * HD;
+    bf16_t* dst = a.dqkv + ((size_t)b * T + kv) * ld + (H + j) * HD;
 #pragma unroll
     for (int d = 0; d < S::DT; ++d)
 #pragma unroll
       for (int c = 0; c < 4; ++c) {
         const int dd = 32 * d + 8 * c + 4 * g;
         if (dd < HD) {
-          *reinterpret_cast<uint2*>(dst + C + dd) =
+          *reinterpret_cast<uint2*>(dst + dd) =
               make_uint2(pack2(dk[d][4 * c] * scale, dk[d][4 * c + 1] * scale),
                          pack2(dk[d][4 * c + 2] * scale, dk[d][4 * c + 3] * scale));
-          *reinterpret_cast<uint2*>(dst + 2 * C + dd) =
+          *reinterpret_cast<uint2*>(dst + Hkv * HD + dd) =
               make_uint2(pack2(dv[d][4 * c], dv[d][4 * c + 1]), pack2(dv[d][4 * c + 2], dv[d][4 * c + 3]));
         }
       }
@@ -415,7 +424,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_kernel(AttnArgs a) {
   using S = Shape<HD>;
   __shared__ __attribute__((aligned(1024))) char smem_raw[2 * 2 * S::TBA];   // 2 stages x (K, V)
   lds_char_t* smem = (lds_char_t*)smem_raw;
-  const int T = a.T, H = a.H, C = H * HD, ld = 3 * C;
+  const int T = a.T, H = a.H, C = H * HD, Hkv = a.Hkv > 0 ? a.Hkv : H, ld = (H + 2 * Hkv) * HD;
   // 1-D grid, head fastest, heaviest (last) query blocks first, as in the
   // forward pass
   const int BH = a.B * H, nqb = (T + BQ - 1) / BQ;
@@ -428,6 +437,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_kernel(AttnArgs a) {
   const int q0w = qb * BQ + wave * 32;
   const int q = q0w + lq;
   const bf16_t* base = a.qkv + (size_t)b * T * ld + h * HD;
+  const bf16_t* kbase = a.qkv + (size_t)b * T * ld + (H + h / (H / Hkv)) * HD;
   const bf16_t* dob = a.dout + (size_t)b * T * C + h * HD;
   const v4i32 rs = make_rsrc(a.qkv, (uint32_t)((size_t)a.B * T * ld * 2));
 
@@ -469,8 +479,8 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_kernel(AttnArgs a) {
   const int ntiles = (kv_end + TILE - 1) / TILE;
   auto issue = [&](int it) {
     lds_char_t* st = smem + (it & 1) * 2 * S::TBA;
-    issue_rows<HD>(rs, a.qkv, base + C, it * TILE, ld, st, wave, lane);
-    issue_rows<HD>(rs, a.qkv, base + 2 * C, it * TILE, ld, st + S::TBA, wave, lane);
+    issue_rows<HD>(rs, a.qkv, kbase, it * TILE, ld, st, wave, lane);
+    issue_rows<HD>(rs, a.qkv, kbase + Hkv * HD, it * TILE, ld, st + S::TBA, wave, lane);
   };
   issue(0);
   for (int it = 0; it < ntiles; ++it) {
@@ -541,18 +551,26 @@ hipError_t fwd_t(const AttnArgs& a, hipStream_t s) {
 template <int HD>
 hipError_t bwd_t(const AttnArgs& a, hipStream_t s) {
   // dQ first: it also computes D = rowsum(dO * O), which dK/dV reads
-  dim3 grid(((a.T + BQ - 1) / BQ) * a.B * a.H);
-  hipLaunchKernelGGL(attn_bwd_dq_kernel<HD>, grid, dim3(256), 0, s, a);
+  const int nb = (a.T + BQ - 1) / BQ, Hkv = a.Hkv > 0 ? a.Hkv : a.H;
+  hipLaunchKernelGGL(attn_bwd_dq_kernel<HD>, dim3(nb * a.B * a.H), dim3(256), 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(attn_bwd_dkdv_kernel<HD>, grid, dim3(256), 0, s, a);
+  hipLaunchKernelGGL(attn_bwd_dkdv_kernel<HD>, dim3(nb * a.B * Hkv), dim3(256), 0, s, a);
   return hipGetLastError();
+}
+
+// Shapes the kernels support: head sizes 16..128, H a multiple of Hkv, and
+// every byte offset into q|k|v (rows of (H + 2 Hkv) hd) within 32 bits.
+bool attn_ok(const AttnArgs& a) {
+  const int Hkv = a.Hkv > 0 ? a.Hkv : a.H;
+  if (a.H < 1 || Hkv < 1 || a.H % Hkv) return false;
+  return (size_t)a.B * a.T * (a.H + 2 * Hkv) * a.hd * 2 < (1ull << 32);
 }
 
 }  // namespace
 
 hipError_t launch_attention_fwd(const AttnArgs& a, hipStream_t s) {
-  if ((size_t)a.B * a.T * 3 * a.H * a.hd * 2 >= (1ull << 32)) return hipErrorInvalidValue;
+  if (!attn_ok(a)) return hipErrorInvalidValue;
   switch (a.hd) {
     case 16: return fwd_t<16>(a, s);
     case 32: return fwd_t<32>(a, s);
@@ -563,7 +581,7 @@ hipError_t launch_attention_fwd(const AttnArgs& a, hipStream_t s) {
 }
 
 hipError_t launch_attention_bwd(const AttnArgs& a, hipStream_t s) {
-  if ((size_t)a.B * a.T * 3 * a.H * a.hd * 2 >= (1ull << 32)) return hipErrorInvalidValue;
+  if (!attn_ok(a)) return hipErrorInvalidValue;
   switch (a.hd) {
     case 16: return bwd_t<16>(a, s);
     case 32: return bwd_t<32>(a, s);

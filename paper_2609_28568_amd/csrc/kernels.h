@@ -62,15 +62,20 @@ int gemm_bias_parts(int M, int N, int splits);
 hipError_t launch_gemm(const GemmArgs& g, int a_t, int b_t, int epi, hipStream_t s);
 
 // ---------------------------------------------------------------- attention
+// Grouped-query attention: H query heads, Hkv key/value heads (0: Hkv = H),
+// query head h reading key/value head h / (H / Hkv). q|k|v rows hold the H
+// query heads, then the Hkv key heads, then the Hkv value heads, hd channels
+// each: row stride W = (H + 2 Hkv) hd. C = H hd.
 struct AttnArgs {
   int B, T, H, hd;
-  const bf16_t* qkv;   // [B*T, 3C]
+  const bf16_t* qkv;   // [B*T, W]
   bf16_t* out;         // [B*T, C]
   float* lse;          // [B, H, T]
   // backward
   const bf16_t* dout;  // [B*T, C]
   float* dsum;         // [B, H, T] rowsum(dout * out)
-  bf16_t* dqkv;        // [B*T, 3C]
+  bf16_t* dqkv;        // [B*T, W]; a key/value head's gradient sums over its query heads
+  int Hkv;
 };
 hipError_t launch_attention_fwd(const AttnArgs& a, hipStream_t s);
 hipError_t launch_attention_bwd(const AttnArgs& a, hipStream_t s);
@@ -139,9 +144,9 @@ hipError_t launch_rmsnorm_fwd(const bf16_t* x, const bf16_t* w, bf16_t* y, float
 // launch_rmsnorm_fwd writes them; the other rows get a zero gradient
 hipError_t launch_rmsnorm_bwd(const bf16_t* dy, const bf16_t* x, const float* rstd, const bf16_t* w, bf16_t* dres,
                               int accumulate, int rows, int C, int T, int mask_from, hipStream_t s);
-// raw q|k|v [BT][(H + 2 Hkv) hd] -> packed q|k|v [BT][3 H hd] for the attention
-// kernels: query and key heads RMS-normalised and rotated, key/value heads
-// repeated over their query-head groups; rstd of every q and k head saved
+// raw q|k|v [BT][(H + 2 Hkv) hd] -> packed q|k|v in the same layout for the
+// grouped-query attention kernels: query and key heads RMS-normalised and
+// rotated, value heads copied; rstd of every q and k head saved
 hipError_t launch_qknorm_rope_fwd(const bf16_t* raw, const bf16_t* qn_w, const bf16_t* kn_w, const float* cosT,
                                   const float* sinT, bf16_t* packed, float* rq, float* rk, int BT, int T, int H, int Hkv,
                                   int hd, float eps, hipStream_t s);

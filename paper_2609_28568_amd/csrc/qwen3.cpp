@@ -137,7 +137,7 @@ ActLayout act_layout(const Dims& d) {
   a.s_raw = align_up(BT * d.QKVD * 2);
   a.s_rq = align_up(BT * d.H * 4);
   a.s_rk = align_up(BT * d.Hkv * 4);
-  a.s_packed = align_up(BT * 3 * d.QD * 2);
+  a.s_packed = align_up(BT * d.QKVD * 2);
   a.s_lse = align_up((size_t)d.B * d.H * d.T * 4);
   a.s_att = align_up(BT * d.QD * 2);
   a.s_gu = align_up(BT * 2 * d.F * 2);
@@ -198,7 +198,7 @@ WsLayout ws_layout(const Dims& d) {
   w.dres = o; o += align_up(BT * d.C * 2);
   w.dh = o; o += align_up(BT * d.C * 2);   // also the LM head's input gradient (loss rows)
   w.datt = o; o += align_up(BT * d.QD * 2);
-  w.dpacked = o; o += align_up(BT * 3 * d.QD * 2);
+  w.dpacked = o; o += align_up(BT * d.QKVD * 2);
   w.draw = o; o += align_up(BT * d.QKVD * 2);
   w.dgu = o; o += align_up(BT * 2 * d.F * 2);
   w.dm = o; o += align_up(BT * d.F * 2);
@@ -231,7 +231,7 @@ const char* validate(const qwen3_config* c) {
   const Dims d = dims_of(*c);
   if (d.mask_from >= d.T) return "no position carries loss";
   // 32-bit byte offsets: the largest operands the kernels address
-  const size_t big = std::max({(size_t)d.BTL * d.V, (size_t)d.BT * 3 * d.QD, (size_t)d.V * d.C,
+  const size_t big = std::max({(size_t)d.BTL * d.V, (size_t)d.BT * d.QKVD, (size_t)d.V * d.C,
                                (size_t)d.BT * 2 * d.F});
   if ((big + 512 * (size_t)std::max(d.V, 2 * d.F)) * 2 >= (1ull << 32)) return "a buffer exceeds 32-bit offsets";
   return nullptr;
@@ -438,7 +438,7 @@ hipError_t proj_bwd(qwen3_model* m, int g, int l, const bf16_t* dy, int ldy, con
 AttnArgs attn_args(qwen3_model* m, int l) {
   const Dims& d = m->d;
   AttnArgs a{};
-  a.B = d.B; a.T = d.T; a.H = d.H; a.hd = d.hd;
+  a.B = d.B; a.T = d.T; a.H = d.H; a.Hkv = d.Hkv; a.hd = d.hd;
   a.qkv = m->ab(m->act.packed + l * m->act.s_packed);
   a.out = m->ab(m->act.att + l * m->act.s_att);
   a.lse = m->af(m->act.lse + l * m->act.s_lse);
@@ -588,7 +588,7 @@ gpt2_status qwen3_forward(qwen3_model* m, const int32_t* d_inputs, const int32_t
     }));
     TRY(proj_fwd(m, G_QKV, l, h, m->base(B_QKV) + (size_t)l * d.QKVD * d.C, raw, d.QKVD, nullptr));
     AttnArgs aa = attn_args(m, l);
-    TRY(m->run(NORM, 0.0, 2.0 * d.BT * (d.QKVD + 3.0 * d.QD) + 4.0 * d.BT * (d.H + d.Hkv), [&] {
+    TRY(m->run(NORM, 0.0, 4.0 * d.BT * d.QKVD + 4.0 * d.BT * (d.H + d.Hkv), [&] {
       return launch_qknorm_rope_fwd(raw, m->base(B_QNORM) + (size_t)l * d.hd, m->base(B_KNORM) + (size_t)l * d.hd,
                                     m->wf(m->ws.cosT), m->wf(m->ws.sinT), const_cast<bf16_t*>(aa.qkv),
                                     m->af(m->act.rq + l * m->act.s_rq), m->af(m->act.rk + l * m->act.s_rk), BT, d.T,
@@ -677,7 +677,7 @@ gpt2_status qwen3_backward(qwen3_model* m) {
     TRY(proj_bwd(m, G_O, l, dres, d.C, aa.out, m->base(B_O) + (size_t)l * d.C * d.QD, datt));
     TRY(m->run(QWEN3_K_ATTN_BWD, 2.0 * attn_fwd_flops(d), 0.0, [&] { return launch_attention_bwd(aa, m->stream); }));
     bf16_t* draw = m->wb(m->ws.draw);
-    TRY(m->run(NORM, 0.0, 2.0 * d.BT * (2.0 * d.QKVD + 3.0 * d.QD) + 4.0 * d.BT * (d.H + d.Hkv), [&] {
+    TRY(m->run(NORM, 0.0, 6.0 * d.BT * d.QKVD + 4.0 * d.BT * (d.H + d.Hkv), [&] {
       return launch_qknorm_rope_bwd(m->wb(m->ws.dpacked), raw, m->base(B_QNORM) + (size_t)l * d.hd,
                                     m->base(B_KNORM) + (size_t)l * d.hd, m->wf(m->ws.cosT), m->wf(m->ws.sinT),
                                     m->af(m->act.rq + l * m->act.s_rq), m->af(m->act.rk + l * m->act.s_rk), draw, BT,

@@ -136,11 +136,11 @@ __global__ __launch_bounds__(256) void rmsnorm_bwd_kernel(const bf16_t* __restri
 // holding elements 8i..8i+7, four items per wave; the rotary pair (e, e + 64)
 // is lanes (i, i ^ 8) of the group. Query heads 0..H-1 and key heads
 // 0..Hkv-1 are RMS-normalised with their gains and rotated by the token's
-// angles (cos/sin tables [T][64] in fp32); value heads are copied. Output
-// layout: q [H*128] | k [H*128] | v [H*128], key/value head j repeated for
-// query heads j*G .. j*G+G-1 (G = H / Hkv). Items are whole 16-lane groups,
-// so a group that runs past the end exits as a whole and every shuffle stays
-// inside a group.
+// angles (cos/sin tables [T][64] in fp32); value heads are copied. The output
+// has the input's layout, q [H*128] | k [Hkv*128] | v [Hkv*128] per token,
+// which the grouped-query attention kernels read directly. Items are whole
+// 16-lane groups, so a group that runs past the end exits as a whole and
+// every shuffle stays inside a group.
 constexpr int QK_HD = 128;
 
 DEV float group16_sum(float v) {
@@ -183,14 +183,10 @@ __global__ __launch_bounds__(256) void qknorm_rope_fwd_kernel(const bf16_t* __re
   if (item >= (long)BT * slots) return;
   const int tok = (int)(item / slots), hs = (int)(item % slots);
   const int t = tok % T;
-  const int G = H / Hkv;
-  const int rawW = slots * QK_HD, outW = 3 * H * QK_HD;
-  const uint4 u = *reinterpret_cast<const uint4*>(raw + (size_t)tok * rawW + hs * QK_HD + 8 * sub);
-  bf16_t* orow = packed + (size_t)tok * outW;
-  if (hs >= H + Hkv) {   // value head: copy to its G query-head slots
-    const int j = hs - H - Hkv;
-    for (int k = 0; k < G; ++k)
-      *reinterpret_cast<uint4*>(orow + 2 * H * QK_HD + (j * G + k) * QK_HD + 8 * sub) = u;
+  const size_t off = (size_t)tok * slots * QK_HD + hs * QK_HD + 8 * sub;
+  const uint4 u = *reinterpret_cast<const uint4*>(raw + off);
+  if (hs >= H + Hkv) {   // value head: copied
+    *reinterpret_cast<uint4*>(packed + off) = u;
     return;
   }
   const bool isq = hs < H;
@@ -212,21 +208,18 @@ __global__ __launch_bounds__(256) void qknorm_rope_fwd_kernel(const bf16_t* __re
   float y[8];
 #pragma unroll
   for (int e = 0; e < 8; ++e) y[e] = x[e] * c[e] + sgn * __shfl_xor(x[e], 8) * sn[e];
-  const uint4 o = pack8(y);
-  if (isq) {
-    *reinterpret_cast<uint4*>(orow + hs * QK_HD + 8 * sub) = o;
-    if (sub == 0) rq[(size_t)tok * H + hs] = rstd;
-  } else {
-    const int j = hs - H;
-    for (int k = 0; k < G; ++k) *reinterpret_cast<uint4*>(orow + H * QK_HD + (j * G + k) * QK_HD + 8 * sub) = o;
-    if (sub == 0) rk[(size_t)tok * Hkv + j] = rstd;
+  *reinterpret_cast<uint4*>(packed + off) = pack8(y);
+  if (sub == 0) {
+    if (isq) rq[(size_t)tok * H + hs] = rstd;
+    else rk[(size_t)tok * Hkv + (hs - H)] = rstd;
   }
 }
 
-// Backward of qknorm_rope_fwd_kernel: dpacked (q | k | v over H heads each)
-// -> draw (q over H heads | k over Hkv | v over Hkv). A key/value head sums
-// the gradients of its G repeated slots; queries and keys then go back
-// through the rotation (its transpose) and the RMSNorm. Same item layout.
+// Backward of qknorm_rope_fwd_kernel: dpacked -> draw, both in the q|k|v
+// layout (the attention backward has already summed a key/value head's
+// gradient over its query heads); queries and keys go back through the
+// rotation (its transpose) and the RMSNorm, values pass through. Same item
+// layout.
 __global__ __launch_bounds__(256) void qknorm_rope_bwd_kernel(const bf16_t* __restrict__ dpacked, const bf16_t* __restrict__ raw,
                                                               const bf16_t* __restrict__ qn_w, const bf16_t* __restrict__ kn_w,
                                                               const float* __restrict__ cosT, const float* __restrict__ sinT,
@@ -238,29 +231,14 @@ __global__ __launch_bounds__(256) void qknorm_rope_bwd_kernel(const bf16_t* __re
   if (item >= (long)BT * slots) return;
   const int tok = (int)(item / slots), hs = (int)(item % slots);
   const int t = tok % T;
-  const int G = H / Hkv;
-  const int rawW = slots * QK_HD, pW = 3 * H * QK_HD;
-  const bf16_t* prow = dpacked + (size_t)tok * pW;
-  float d[8];
-  if (hs < H) {
-    unpack8(*reinterpret_cast<const uint4*>(prow + hs * QK_HD + 8 * sub), d);
-  } else {
-    const int j = hs < H + Hkv ? hs - H : hs - H - Hkv;
-    const int base = hs < H + Hkv ? H * QK_HD : 2 * H * QK_HD;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) d[e] = 0.0f;
-    for (int k = 0; k < G; ++k) {
-      float g[8];
-      unpack8(*reinterpret_cast<const uint4*>(prow + base + (j * G + k) * QK_HD + 8 * sub), g);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) d[e] += g[e];
-    }
-  }
-  bf16_t* drow = draw + (size_t)tok * rawW + hs * QK_HD + 8 * sub;
-  if (hs >= H + Hkv) {
-    *reinterpret_cast<uint4*>(drow) = pack8(d);
+  const size_t off = (size_t)tok * slots * QK_HD + hs * QK_HD + 8 * sub;
+  const uint4 du = *reinterpret_cast<const uint4*>(dpacked + off);
+  if (hs >= H + Hkv) {   // value head: passes through
+    *reinterpret_cast<uint4*>(draw + off) = du;
     return;
   }
+  float d[8];
+  unpack8(du, d);
   // transposed rotation: first half d1 cos + d2 sin, second half d2 cos - d1 sin
   float c[8], sn[8];
   rope_coefs(cosT, sinT, t, sub, c, sn);
@@ -271,7 +249,7 @@ __global__ __launch_bounds__(256) void qknorm_rope_bwd_kernel(const bf16_t* __re
   // RMSNorm backward over the head (gain frozen)
   const bool isq = hs < H;
   float x[8], w[8];
-  unpack8(*reinterpret_cast<const uint4*>(raw + (size_t)tok * rawW + hs * QK_HD + 8 * sub), x);
+  unpack8(*reinterpret_cast<const uint4*>(raw + off), x);
   unpack8(*reinterpret_cast<const uint4*>((isq ? qn_w : kn_w) + 8 * sub), w);
   const float rstd = isq ? rq[(size_t)tok * H + hs] : rk[(size_t)tok * Hkv + (hs - H)];
   float dot = 0.0f;
@@ -285,7 +263,7 @@ __global__ __launch_bounds__(256) void qknorm_rope_bwd_kernel(const bf16_t* __re
   float o[8];
 #pragma unroll
   for (int e = 0; e < 8; ++e) o[e] = rstd * (n[e] - x[e] * m);
-  *reinterpret_cast<uint4*>(drow) = pack8(o);
+  *reinterpret_cast<uint4*>(draw + off) = pack8(o);
 }
 
 DEV float sigmoid_f(float x) { return 1.0f / (1.0f + __expf(-x)); }
