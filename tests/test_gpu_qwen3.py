@@ -22,6 +22,8 @@ CASES = {
     "gqa4_long": dict(n_head=8, n_kv_head=2, d_model=384, d_ff=640, vocab=640, max_seq_len=256, B=2, T=160,
                       loss_from=0.25, lora_rank=8, lora_alpha=16.0,
                       lora_targets=("q", "k", "v", "gate", "up")),
+    # degenerate: two-token sequences, only the second position carries loss
+    "two_tokens": dict(B=32, T=2),
 }
 
 

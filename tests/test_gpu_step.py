@@ -40,6 +40,9 @@ CASES = {
     "tiny_ragged": dict(vocab=500, vocab_padded=512, B=3, T=29, max_seq_len=32),
     "wide_hd64": dict(n_layer=2, n_head=4, d_model=256, d_ff=1024, vocab=1000, vocab_padded=1024,
                       max_seq_len=160, B=2, T=150),
+    # degenerate: one-token sequences (attention over a single key, 5 rows in
+    # every product, token contractions far shorter than one k-tile)
+    "single_token": dict(B=5, T=1),
 }
 
 
