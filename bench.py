@@ -158,6 +158,8 @@ def qwen3_bench(args) -> None:
                 "kernel": probe, "launches": pr["launches"],
                 "avg_launch_ms": round(pr["ms"] / max(pr["launches"], 1), 4),
                 "flops_per_launch": pr["flops"] / max(pr["launches"], 1)}
+    if args.calibration_copy:
+        calibration_copy()
     cpu = None
     if not args.no_cpu_baseline:
         print("bench: timing the CPU oracle on a 1-sequence sample", file=sys.stderr, flush=True)
@@ -209,26 +211,45 @@ def cpu_baseline(w: dict, params, ids, tgt) -> dict:
                       f"model and token stream, numpy fp32, {dt:.1f} s"}
 
 
-# Kernel class -> (sources its code comes from, rocprofv3 kernel-name pattern)
-# Each class: the sources its launches depend on (the kernels, and gpt2.cpp,
-# which plans the launches: shapes, splits, tile configurations) and the
-# pattern of its kernel names in rocprofv3 output.
+# Kernel classes with counter-derived traffic: the sources their kernels are
+# built from, the pattern of their kernel names in rocprofv3 output, and how
+# many kernels one launch of the class runs (the attention backward is the
+# dQ kernel and then the dK/dV kernel). The host file that plans the launches
+# (shapes, splits, tile configurations) is added per workload.
 KERNEL_CLASSES = {
-    "gemm_fwd": (("gemm.hip", "common.h", "lds_dma.h", "kernels.h", "gpt2.cpp"),
-                 r"gemm_kernel<\d+, \d+, \d+, \d+, false, false, 0>"),
-    "gemm_dw": (("gemm.hip", "common.h", "lds_dma.h", "kernels.h", "gpt2.cpp"),
-                r"gemm_kernel<\d+, \d+, \d+, \d+, true, true, 3>"),
-    "attn_bwd": (("attention.hip", "common.h", "lds_dma.h", "kernels.h", "gpt2.cpp"), r"attn_bwd"),
+    "gemm_fwd": (("gemm.hip", "common.h", "lds_dma.h", "kernels.h"),
+                 r"gemm_kernel<\d+, \d+, \d+, \d+, false, false, 0(, false)?>", 1),
+    "gemm_dw": (("gemm.hip", "common.h", "lds_dma.h", "kernels.h"),
+                r"gemm_kernel<\d+, \d+, \d+, \d+, true, true, 3(, false)?>", 1),
+    "attn_bwd": (("attention.hip", "common.h", "lds_dma.h", "kernels.h"), r"attn_bwd", 2),
 }
+
+
+def calibration_copy() -> None:
+    """A device-to-device copy of CALIBRATION_BYTES, whose counter readings
+    scale the kernels' FETCH_SIZE and WRITE_SIZE to bytes."""
+    import torch
+    src = torch.empty(CALIBRATION_BYTES, dtype=torch.uint8, device="cuda").fill_(1)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    del src, dst
+
+
+def plan_source(workload: str) -> str:
+    return "qwen3.cpp" if workload.startswith("qwen3") else "gpt2.cpp"
+
+
 CALIBRATION_BYTES = 1 << 30
 
 
-def kernel_source_hash(kernel_tag: str) -> str:
-    """Hash of the sources the kernel class is built from, so that stored
-    counter readings go stale when its code changes."""
+def kernel_source_hash(kernel_tag: str, workload: str) -> str:
+    """Hash of the sources the kernel class is built from and of the file that
+    plans its launches, so that stored counter readings go stale when either
+    changes."""
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2609_28568_amd", "csrc")
-    for f in KERNEL_CLASSES[kernel_tag][0]:
+    for f in KERNEL_CLASSES[kernel_tag][0] + (plan_source(workload),):
         h.update(open(os.path.join(csrc, f), "rb").read())
     return h.hexdigest()
 
@@ -244,18 +265,20 @@ def traffic_from_profiles(kernel_tag: str, workload: str):
     if kernel_tag not in KERNEL_CLASSES or not os.path.exists(path):
         return None
     d = json.load(open(path))
-    if d.get("source_sha256") != kernel_source_hash(kernel_tag):
+    if d.get("source_sha256") != kernel_source_hash(kernel_tag, workload):
         return None
     return d.get("bytes_per_launch")
 
 
-def pmc_summary(kernel_tag: str, fetch_csv: str, write_csv: str, command: str) -> dict:
+def pmc_summary(kernel_tag: str, workload: str, fetch_csv: str, write_csv: str, command: str) -> dict:
     """Turn two rocprofv3 counter passes (FETCH_SIZE, WRITE_SIZE; KiB per
-    dispatch) into HBM bytes per launch of one kernel class, each counter
-    scaled by its reading on a device-to-device copy of CALIBRATION_BYTES."""
+    dispatch) into HBM bytes per launch of one kernel class (the class's
+    kernels per launch summed), each counter scaled by its reading on a
+    device-to-device copy of CALIBRATION_BYTES."""
     import csv
     import re
     pat = re.compile(KERNEL_CLASSES[kernel_tag][1])
+    per_launch = KERNEL_CLASSES[kernel_tag][2]
 
     def read(path, counter):
         kern, copy = [], []
@@ -274,10 +297,12 @@ def pmc_summary(kernel_tag: str, fetch_csv: str, write_csv: str, command: str) -
     fk, fc, n = read(fetch_csv, "FETCH_SIZE")
     wk, wc, _ = read(write_csv, "WRITE_SIZE")
     f_scale, w_scale = CALIBRATION_BYTES / fc, CALIBRATION_BYTES / wc
-    return {"kernel": kernel_tag, "dispatches": n, "fetch_bytes_raw": fk, "write_bytes_raw": wk,
+    # read() averages over dispatches; a launch of the class runs per_launch kernels
+    return {"kernel": kernel_tag, "dispatches": n, "kernels_per_launch": per_launch,
+            "fetch_bytes_raw": fk * per_launch, "write_bytes_raw": wk * per_launch,
             "copy_fetch_bytes_raw": fc, "copy_write_bytes_raw": wc, "fetch_scale": f_scale,
-            "write_scale": w_scale, "bytes_per_launch": fk * f_scale + wk * w_scale,
-            "source_sha256": kernel_source_hash(kernel_tag), "command": command}
+            "write_scale": w_scale, "bytes_per_launch": (fk * f_scale + wk * w_scale) * per_launch,
+            "source_sha256": kernel_source_hash(kernel_tag, workload), "command": command}
 
 
 def main():
@@ -296,7 +321,7 @@ def main():
     ap.add_argument("--pmc-command", default="", help="the profiling command, recorded with --pmc-summary")
     args = ap.parse_args()
     if args.pmc_summary:
-        d = pmc_summary(args.probe, *args.pmc_summary, args.pmc_command)
+        d = pmc_summary(args.probe, args.workload, *args.pmc_summary, args.pmc_command)
         d["workload"] = args.workload
         with open(traffic_path(args.probe, args.workload), "w") as f:
             json.dump(d, f, indent=1)
@@ -409,11 +434,7 @@ def main():
                 "flops_per_launch": flops_launch}
 
     if args.calibration_copy:
-        src = torch.empty(CALIBRATION_BYTES, dtype=torch.uint8, device="cuda").fill_(1)
-        dst = torch.empty_like(src)
-        dst.copy_(src)
-        torch.cuda.synchronize()
-        del src, dst
+        calibration_copy()
 
     cpu = None
     if not args.no_cpu_baseline:
