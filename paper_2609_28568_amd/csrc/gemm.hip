@@ -246,11 +246,57 @@ __global__ __launch_bounds__(256, (NS <= 2 ? 2 : 1)) void gemm_kernel(GemmArgs g
 
   // Tile kt: wait for it, publish it with the barrier (which also frees the
   // stage of tile kt-1 for tile kt+NS-1), then walk its k-steps reading the
-  // fragments of step s+1 while the MFMAs of step s run.
+  // fragments of step s+1 while the MFMAs of step s run. Left to itself the
+  // compiler sinks each fragment read next to its first MFMA and waits for
+  // it there; the schedule fences below keep a whole step's reads ahead of
+  // the previous step's MFMAs. Chosen per product from timings of the GPT-2
+  // step (tiles up to 192 x 192; the larger ones would spill):
+  //   weight gradients: fences only (-3 %);
+  //   input gradients: fences, and the last k-step of a tile deferred past
+  //     the next tile's barrier so that its MFMAs cover the latency of that
+  //     tile's first reads (-1 to -1.5 %);
+  //   forward products: the compiler's own schedule.
   bf16x8 fa[2][TM], fb[2][TN];
 #pragma unroll
   for (int s = 0; s < NS - 1; ++s)
     if (s < nk) issue(s);
+  constexpr int KL = BM * BN > 192 * 192 ? 0 : A_T ? 1 : B_T ? 2 : 0;
+  if constexpr (KL == 2) {
+  for (int kt = 0; kt < nk; ++kt) {
+    // issued so far: tiles up to kt + NS - 2
+    wait_later(min(NS - 2, nk - 1 - kt));
+    __builtin_amdgcn_s_waitcnt(0xC07F);   // this wave's reads of the stage the DMA below may overwrite are done
+    block_barrier();
+    if (kt + NS - 1 < nk) issue(kt + NS - 1);
+    load(fa[0], fb[0], kt, 0);
+    __builtin_amdgcn_sched_barrier(0);
+    if (kt > 0) {
+      // the last k-step of the previous tile, deferred past the barrier so
+      // that its MFMAs cover the latency of this tile's first reads
+      mma(fa[1], fb[1]);
+      if constexpr (BSUM) {
+        if (bsum_on && ((KSTEPS - 1) & 1) == wn && (kt - 1) % ntn == tn) bias_sums(fa[1]);
+      }
+    }
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int s = 0; s + 1 < KSTEPS; ++s) {
+      load(fa[(s + 1) & 1], fb[(s + 1) & 1], kt, s + 1);
+      __builtin_amdgcn_sched_barrier(0);
+      mma(fa[s & 1], fb[s & 1]);
+      if constexpr (BSUM) {
+        if (bsum_on && (s & 1) == wn && kt % ntn == tn) bias_sums(fa[s & 1]);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+  if (nk > 0) {
+    mma(fa[1], fb[1]);
+    if constexpr (BSUM) {
+      if (bsum_on && ((KSTEPS - 1) & 1) == wn && (nk - 1) % ntn == tn) bias_sums(fa[1]);
+    }
+  }
+  } else {
   for (int kt = 0; kt < nk; ++kt) {
     // issued so far: tiles up to kt + NS - 2
     wait_later(min(NS - 2, nk - 1 - kt));
@@ -260,11 +306,14 @@ __global__ __launch_bounds__(256, (NS <= 2 ? 2 : 1)) void gemm_kernel(GemmArgs g
 #pragma unroll
     for (int s = 0; s < KSTEPS; ++s) {
       if (s + 1 < KSTEPS) load(fa[(s + 1) & 1], fb[(s + 1) & 1], kt, s + 1);
+      if constexpr (KL == 1) __builtin_amdgcn_sched_barrier(0);
       mma(fa[s & 1], fb[s & 1]);
       if constexpr (BSUM) {
         if (bsum_on && (s & 1) == wn && kt % ntn == tn) bias_sums(fa[s & 1]);
       }
+      if constexpr (KL == 1) __builtin_amdgcn_sched_barrier(0);
     }
+  }
   }
   if constexpr (BSUM) {
     // lanes l and l+32 hold the two k-halves of row l; each wave writes its
