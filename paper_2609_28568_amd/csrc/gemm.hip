@@ -137,7 +137,9 @@ __global__ __launch_bounds__(256, (NS <= 2 ? 2 : 1)) void gemm_kernel(GemmArgs g
   __shared__ __attribute__((aligned(1024))) char smem_raw[SMEM];
   lds_char_t* smem = (lds_char_t*)smem_raw;
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // the wave index is uniform across the wave: say so, so that LDS addresses
+  // and per-wave conditions are computed on the scalar unit
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave >> 1, wn = wave & 1;
 
   // Blocks are dealt round-robin to the 8 XCDs; renumber them so each XCD
