@@ -65,9 +65,39 @@ DEV int unit(int row, int c) {
   return row * U + (c ^ f);
 }
 
-// Load rows [r0, r0+64) of one head's slice (row stride ld elements, buffer
-// over the whole q|k|v or dO matrix) into an LDS tile. Instruction i of the
-// tile goes to bytes [1024 i, 1024 i + 1024); waves take instructions in turn.
+// Loads rows [r0, r0+64) of one head's slice (row stride ld elements) of a
+// buffer into an LDS tile. Instruction i of the tile goes to bytes
+// [1024 i, 1024 i + 1024); waves take instructions in turn. A lane's byte
+// offset within the tile's rows is the same for every tile, so it is
+// computed once; a tile adds only its (scalar) starting offset.
+template <int HD>
+struct RowLoader {
+  static constexpr int U = HD / 8, UNITS = TILE * U, INSTR = (UNITS + 63) / 64, PER = (INSTR + 3) / 4;
+  uint32_t rel[PER];
+
+  DEV void init(int ld, int wave, int lane) {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int u = (wave + 4 * i) * 64 + lane;
+      const int row = u / U, p = u % U;
+      const int c = unit<HD>(row, p) - row * U;   // the XOR is its own inverse
+      rel[i] = ((uint32_t)row * (uint32_t)ld + (uint32_t)(c * 8)) * 2u;
+    }
+  }
+
+  // off: byte offset in the buffer of row r0 of the head's slice
+  DEV void issue(v4i32 rs, uint32_t off, lds_char_t* dst, int wave, int lane) const {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int ins = wave + 4 * i;
+      if (ins < INSTR && (UNITS % 64 == 0 || ins * 64 + lane < UNITS))
+        dma16(rs, off + rel[i], lds_addr(dst + ins * 1024));
+    }
+  }
+};
+
+// The same load with the lane offsets recomputed per tile (for kernels whose
+// registers are at the limit). src: row 0 of the head's slice.
 template <int HD>
 DEV void issue_rows(v4i32 rs, const bf16_t* base_of_buffer, const bf16_t* src, int r0, int ld, lds_char_t* dst,
                     int wave, int lane) {
@@ -168,10 +198,21 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(AttnArgs a) {
 
   const int kv_end = min(T, qb * BQ + BQ);
   const int ntiles = (kv_end + TILE - 1) / TILE;
+  // the lane offsets of the K/V loads computed once (at hd 128 the registers
+  // they take cost more than recomputing them per tile)
+  RowLoader<HD> kvl;
+  if constexpr (HD < 128) kvl.init(ld, wave, lane);
+  const uint32_t koff = (uint32_t)((kbase - a.qkv) * 2), voff = koff + (uint32_t)(Hkv * HD * 2);
   auto issue = [&](int it) {
     lds_char_t* st = smem + (it & 1) * 2 * S::TBA;
-    issue_rows<HD>(rs, a.qkv, kbase, it * TILE, ld, st, wave, lane);
-    issue_rows<HD>(rs, a.qkv, kbase + Hkv * HD, it * TILE, ld, st + S::TBA, wave, lane);
+    if constexpr (HD < 128) {
+      const uint32_t r = (uint32_t)(it * TILE) * (uint32_t)ld * 2u;
+      kvl.issue(rs, koff + r, st, wave, lane);
+      kvl.issue(rs, voff + r, st + S::TBA, wave, lane);
+    } else {
+      issue_rows<HD>(rs, a.qkv, kbase, it * TILE, ld, st, wave, lane);
+      issue_rows<HD>(rs, a.qkv, kbase + Hkv * HD, it * TILE, ld, st + S::TBA, wave, lane);
+    }
   };
   issue(0);
   for (int it = 0; it < ntiles; ++it) {
@@ -477,10 +518,14 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_kernel(AttnArgs a) {
 
   const int kv_end = min(T, qb * BQ + BQ);
   const int ntiles = (kv_end + TILE - 1) / TILE;
+  RowLoader<HD> kvl;
+  kvl.init(ld, wave, lane);
+  const uint32_t koff = (uint32_t)((kbase - a.qkv) * 2), voff = koff + (uint32_t)(Hkv * HD * 2);
   auto issue = [&](int it) {
     lds_char_t* st = smem + (it & 1) * 2 * S::TBA;
-    issue_rows<HD>(rs, a.qkv, kbase, it * TILE, ld, st, wave, lane);
-    issue_rows<HD>(rs, a.qkv, kbase + Hkv * HD, it * TILE, ld, st + S::TBA, wave, lane);
+    const uint32_t r = (uint32_t)(it * TILE) * (uint32_t)ld * 2u;
+    kvl.issue(rs, koff + r, st, wave, lane);
+    kvl.issue(rs, voff + r, st + S::TBA, wave, lane);
   };
   issue(0);
   for (int it = 0; it < ntiles; ++it) {
