@@ -142,3 +142,65 @@ def test_gpt2_124m_evaluate_equals_forward(full_setup):
     m.close()
     assert np.array_equal(got, ref)
     assert ev == loss
+
+
+def test_gpt2_124m_accumulation_configuration():
+    """The accumulation configuration (32 micro-batches of 16 x 1024 tokens per
+    optimizer step, dlogits scaled by 1/(16*1024*32)) at full size:
+    accumulating two micro-batches gives the sum of their separate gradients;
+    sampled sequences of micro-batches 0 and 31 have the oracle's per-token
+    losses; and the first AdamW step on the accumulated gradient is its
+    closed form: with the clipped gradient h = c g, bias correction makes
+    m-hat = h and v-hat = h^2, so p1 - p0 = -lr0 (h / (|h| + eps) + decay p0)
+    for every parameter (within the fp32 rounding of p1)."""
+    from paper_2609_28568_amd import binding
+    w = workload("gpt2_124m_accum32")
+    p = synth.init_params(w)
+    b0, b31 = synth.token_batch(w, micro=0), synth.token_batch(w, micro=31)
+    m = _model(w)
+    m.set_params(p)
+
+    def fb(b, accumulate):
+        m.forward(torch.from_numpy(b[0]), torch.from_numpy(b[1]))
+        m.backward(accumulate=accumulate)
+
+    fb(b0, False)
+    g0 = m.flat("grads").double()
+    losses0 = _np(m.activation("losses")).reshape(w["B"], w["T"])
+    fb(b31, False)
+    g1 = m.flat("grads").double()
+    losses31 = _np(m.activation("losses")).reshape(w["B"], w["T"])
+    fb(b0, False)
+    fb(b31, True)
+    g = m.flat("grads").double()
+    e = float(torch.linalg.norm(g - (g0 + g1)) / torch.linalg.norm(g0 + g1))
+    print(f"gpt2_124m_accum32: accumulated vs summed gradients rel_l2 {e:.2e}")
+    assert e < 1e-5
+
+    p0 = m.flat("params").double().clone()
+    norm = torch.zeros(1, device="cuda")
+    lr0 = m.adamw_step(0, norm)
+    torch.cuda.synchronize()
+    assert abs(lr0 - synth.OPTIM["lr_max"] / synth.OPTIM["warmup_steps"]) < 1e-12
+    coef = 1.0 / max(1.0, float(norm.item()))
+    decay = torch.zeros_like(p0)
+    for _, off, shape, dec in binding.tensor_table(binding.make_config(w, synth.OPTIM)):
+        if dec:
+            decay[off:off + int(np.prod(shape))] = synth.OPTIM["weight_decay"]
+    h = coef * g
+    want = -lr0 * (h / (h.abs() + synth.OPTIM["adam_eps"]) + decay * p0)
+    got = m.flat("params").double() - p0
+    # p1 is rounded to fp32: allow one unit in its last place, plus 1e-5 lr0
+    tol = 1e-5 * lr0 + (p0.abs() + lr0) * 2.0 ** -23
+    excess = float(((got - want).abs() - tol).max())
+    print(f"  first AdamW step: max |dp - closed form| beyond tolerance {excess:.2e} (lr0 {lr0:.3e})")
+    assert excess <= 0.0
+    m.close()
+
+    ocfg = oracle_config(w)
+    for (ids, tgt), losses, b in ((b0, losses0, 0), (b31, losses31, 15)):
+        print(f"  oracle forward of sequence {b}", flush=True)
+        c = oracle.forward(p, ids[b:b + 1], tgt[b:b + 1], ocfg)
+        d = np.abs(losses[b] - c["losses"][0])
+        assert abs(losses[b].mean() - float(c["loss"])) < LOSS_ATOL
+        assert d.max() < 5 * LOSS_ATOL
