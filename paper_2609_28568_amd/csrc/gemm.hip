@@ -182,13 +182,16 @@ __global__ __launch_bounds__(256, (NS <= 2 ? 2 : 1)) void gemm_kernel(GemmArgs g
     a2col = g.K2 * ((g.a2_bound[0] > 0 && n0 >= g.a2_bound[0]) + (g.a2_bound[1] > 0 && n0 >= g.a2_bound[1]));
   }
 
+  // B column offset of this tile's output row block
+  const int bcol = g.b_step * ((g.b_bound[0] > 0 && m0 >= g.b_bound[0]) + (g.b_bound[1] > 0 && m0 >= g.b_bound[1]));
+
   auto stage = [&](int kt) { return smem + (kt % NS) * STAGE; };
   auto issue = [&](int kt) {
     lds_char_t* st = stage(kt);
     if (!SEG2 || kt < nk1) {
       const int k0 = kbeg + kt * BK;
       issue_tile<BM, BK, A_T>(ra, g.lda, m0, k0, st, wave, lane);
-      issue_tile<BN, BK, B_T>(rb, g.ldb, n0, k0, st + A_BYTES, wave, lane);
+      issue_tile<BN, BK, B_T>(rb, g.ldb, n0 + bcol, k0, st + A_BYTES, wave, lane);
     } else {
       const int k2 = (kt - nk1) * BK;
       issue_tile<BM, BK, A_T>(ra2, g.lda2, m0, a2col + k2, st, wave, lane);
@@ -569,7 +572,14 @@ hipError_t launch_gemm(const GemmArgs& g0, int a_t, int b_t, int epi, hipStream_
         (size_t)((b_t ? g.K2 : g.N) + 256) * g.ldb2 * 2 >= (1ull << 32))
       return hipErrorInvalidValue;
   }
+  if (g.b_step != 0) {
+    // row blocks must not straddle a bound; B must be read transposed ([K][N])
+    if (!b_t || g.b_step < 0) return hipErrorInvalidValue;
+    for (int i = 0; i < 2; ++i)
+      if (g.b_bound[i] < 0 || g.b_bound[i] % 128) return hipErrorInvalidValue;
+  }
   GemmConfig c = gemm_config(g.M, g.N, a_t, b_t, epi);
+  if (g.b_step != 0 && ((g.b_bound[0] % c.bm) || (g.b_bound[1] % c.bm))) return hipErrorInvalidValue;
   // a tile's output columns must lie within one block of the second segment
   const bool bounded = g.K2 > 0 && (g.a2_bound[0] > 0 || g.a2_bound[1] > 0);
   if (bounded) {

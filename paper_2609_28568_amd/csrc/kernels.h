@@ -48,6 +48,10 @@ struct GemmArgs {
   const bf16_t* B2;
   int K2, lda2, ldb2;
   int a2_bound[2];
+  // Output rows m >= b_bound[i] (for each non-zero bound, multiples of 128)
+  // read B from b_step columns further right per bound passed, so row blocks
+  // of the output can contract with different column blocks of B.
+  int b_bound[2], b_step;
 };
 
 // Block tile (bm x bn, contraction depth bk per stage) the GEMM uses for an

@@ -405,16 +405,20 @@ hipError_t proj_bwd(qwen3_model* m, int g, int l, const bf16_t* dy, int ldy, con
     if (e != hipSuccess) return e;
     int kc = 0;
     const int splits = gemm_split_plan(BT, DW_SPLITS, &kc);
-    col = 0;
-    for (int j = 0; j < gg.n; ++j) {
-      // dB_j = dy_j^T u_j into rows col.. of every partial slice [out_total][RP]
+    {
+      // dB_j = dy_j^T u_j for every projection in one product over all
+      // out_total rows: projection j's rows read u's j-th block of RP columns
       GemmArgs r{};
-      r.A = dy + col; r.lda = ldy; r.B = u + j * RP; r.ldb = nu; r.M = gg.out[j]; r.N = RP; r.K = BT;
-      r.C = pb + (size_t)col * RP; r.ldc = RP; r.splits = splits; r.k_chunk = kc;
-      r.split_stride = (long)gg.out_total * RP;
-      e = run_gemm(m, AD, mnk2(gg.out[j], d.r, d.BT), r, 1, 1, EPI_F32);
+      r.A = dy; r.lda = ldy; r.B = u; r.ldb = nu; r.M = gg.out_total; r.N = RP; r.K = BT;
+      r.C = pb; r.ldc = RP; r.splits = splits; r.k_chunk = kc; r.split_stride = (long)gg.out_total * RP;
+      r.b_step = RP;
+      int bound = 0;
+      for (int j = 0; j + 1 < gg.n; ++j) {
+        bound += gg.out[j];
+        r.b_bound[j] = bound;
+      }
+      e = run_gemm(m, AD, mnk2(gg.out_total, d.r, d.BT), r, 1, 1, EPI_F32);
       if (e != hipSuccess) return e;
-      col += gg.out[j];
     }
     // dA = du^T x
     GemmArgs r{};
