@@ -586,6 +586,175 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_kernel(AttnArgs a) {
   }
 }
 
+// Row loads for an eight-wave workgroup: instruction i of the 64-row tile
+// goes to bytes [1024 i, 1024 i + 1024), waves taking instructions in turn.
+// off: byte offset in the buffer of row 0 of the head's slice.
+template <int HD>
+DEV void issue_rows8(v4i32 rs, uint32_t off, int r0, int ld, lds_char_t* dst, int wave, int lane) {
+  constexpr int U = HD / 8, INSTR = TILE * U / 64;
+  static_assert(INSTR % 8 == 0, "tile must split evenly over 8 waves");
+#pragma unroll
+  for (int i = 0; i < INSTR / 8; ++i) {
+    const int ins = wave + 8 * i;
+    const int u = ins * 64 + lane;
+    const int row = u / U, p = u % U;
+    const int c = unit<HD>(row, p) - row * U;   // the XOR is its own inverse
+    dma16(rs, off + ((uint32_t)(r0 + row) * (uint32_t)ld + (uint32_t)(c * 8)) * 2u, lds_addr(dst + ins * 1024));
+  }
+}
+
+// dK, dV at hd 128 with eight waves per 128 keys: wave w owns keys
+// 32 (w % 4) .. +31 of the block and the query half w / 4 (rows 32 (w / 4)
+// .. +31) of every 64-query tile, so each SIMD runs two waves (the four-wave
+// form needs more registers than two waves per SIMD allow: its K/V fragments
+// live in registers). The block's K and V rows stay in LDS for the whole walk
+// and are read per k-step; at the end the two waves of a key group add their
+// dK/dV partial sums through LDS.
+template <int HD>
+__global__ __launch_bounds__(512, 1) void attn_bwd_dkdv8_kernel(AttnArgs a) {
+  using S = Shape<HD>;
+  constexpr int KVB = BQ * HD * 2;             // one 128-row block of K or V
+  constexpr int STAGE = 2 * S::TBA + 1024;     // Q tile, dO tile, lse and D rows
+  constexpr int SMEM = 2 * KVB + 2 * STAGE;
+  constexpr int NACC = 2 * S::DT * 16;         // dK and dV registers per lane
+  static_assert(4 * NACC * 64 * 4 <= SMEM, "dK/dV exchange fits the tiles' space");
+  __shared__ __attribute__((aligned(1024))) char smem_raw[SMEM];
+  lds_char_t* smem = (lds_char_t*)smem_raw;
+  lds_char_t* Ks = smem;
+  lds_char_t* Vs = smem + KVB;
+  lds_char_t* stages = smem + 2 * KVB;
+  const int T = a.T, H = a.H, C = H * HD, Hkv = a.Hkv > 0 ? a.Hkv : H, ld = (H + 2 * Hkv) * HD;
+  const int G = H / Hkv;
+  const int BH = a.B * Hkv;
+  const int bj = blockIdx.x % BH, b = bj / Hkv, j = bj % Hkv;
+  const int kb = (int)(blockIdx.x / BH);
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int kw = wave & 3, th = wave >> 2;   // key group, query half
+  const int lk = lane & 31, g = lane >> 5;
+  const int kv0w = kb * BQ + kw * 32;
+  const int kv = kv0w + lk;
+  const v4i32 rq = make_rsrc(a.qkv, (uint32_t)((size_t)a.B * T * ld * 2));
+  const v4i32 rd = make_rsrc(a.dout, (uint32_t)((size_t)a.B * T * C * 2));
+  const v4i32 rl = make_rsrc(a.lse, (uint32_t)((size_t)a.B * H * T * 4));
+  const v4i32 rD = make_rsrc(a.dsum, (uint32_t)((size_t)a.B * H * T * 4));
+  const uint32_t seq_q = (uint32_t)b * (uint32_t)T * (uint32_t)ld * 2u;   // byte offset of the sequence's qkv rows
+  const uint32_t seq_d = (uint32_t)b * (uint32_t)T * (uint32_t)C * 2u;
+
+  floatx16 dk[S::DT], dv[S::DT];
+#pragma unroll
+  for (int d = 0; d < S::DT; ++d) {
+    zero(dk[d]);
+    zero(dv[d]);
+  }
+  const float scale = 1.0f / sqrtf((float)HD);
+  const float sc = scale * LOG2E;
+
+  const int qstart = kb * BQ;
+  const int nt = qstart < T ? (T - qstart + TILE - 1) / TILE : 0;
+  const int ntiles = nt * G;
+  auto issue = [&](int it) {
+    lds_char_t* st = stages + (it & 1) * STAGE;
+    const int h = j * G + it / nt;
+    const int q0 = qstart + (it % nt) * TILE;
+    issue_rows8<HD>(rq, seq_q + (uint32_t)(h * HD) * 2u, q0, ld, st, wave, lane);
+    issue_rows8<HD>(rd, seq_d + (uint32_t)(h * HD) * 2u, q0, C, st + S::TBA, wave, lane);
+    if (wave == 0 && lane < 16) {
+      const uint32_t off = ((uint32_t)(b * H + h) * (uint32_t)T + (uint32_t)q0) * 4u + 16u * lane;
+      dma16(rl, off, lds_addr(st + 2 * S::TBA));
+      dma16(rD, off, lds_addr(st + 2 * S::TBA + 256));
+    }
+  };
+  if (ntiles > 0) {
+    // the block's key and value rows (key head j; value head j at + Hkv hd)
+    const uint32_t koff = seq_q + (uint32_t)((H + j) * HD) * 2u, voff = koff + (uint32_t)(Hkv * HD) * 2u;
+    issue_rows8<HD>(rq, koff, qstart, ld, Ks, wave, lane);
+    issue_rows8<HD>(rq, koff, qstart + TILE, ld, Ks + S::TB, wave, lane);
+    issue_rows8<HD>(rq, voff, qstart, ld, Vs, wave, lane);
+    issue_rows8<HD>(rq, voff, qstart + TILE, ld, Vs + S::TB, wave, lane);
+    issue(0);
+  }
+  for (int it = 0; it < ntiles; ++it) {
+    wait_vmcnt<0>();
+    block_barrier();
+    if (it + 1 < ntiles) issue(it + 1);
+    const int qh0 = qstart + (it % nt) * TILE + 32 * th;   // this wave's first query
+    if (qh0 + 31 < kv0w) continue;   // every query of the half precedes this wave's keys
+    const lds_char_t* Qs = stages + (it & 1) * STAGE;
+    const lds_char_t* Ds = Qs + S::TBA;
+    const lds_char_t* lr = Qs + 2 * S::TBA;   // lse [64] then D [64], fp32
+    const bool diag = qh0 < kv0w + 32 || qh0 + 32 > T || kv0w + 32 > T;
+
+    // S = Q K^T and dP = dO V^T for the half's 32 queries x the wave's 32 keys
+    floatx16 p, ds;
+    zero(p);
+    zero(ds);
+#pragma unroll
+    for (int k = 0; k < S::KS; ++k) {
+      p = mfma32(read_row<HD>(Qs, 32 * th + lk, 2 * k + g), read_row<HD>(Ks, 32 * kw + lk, 2 * k + g), p);
+      ds = mfma32(read_row<HD>(Ds, 32 * th + lk, 2 * k + g), read_row<HD>(Vs, 32 * kw + lk, 2 * k + g), ds);
+    }
+    auto probs = [&](auto masked) {
+#pragma unroll
+      for (int c4 = 0; c4 < 4; ++c4) {
+        const int qi = 32 * th + 8 * c4 + 4 * g;   // 4 consecutive queries of the tile
+        const v4f32 l4 = *reinterpret_cast<const lds_v4f32_t*>(lr + 4 * qi);
+        const v4f32 d4 = *reinterpret_cast<const lds_v4f32_t*>(lr + 256 + 4 * qi);
+        const float lv[4] = {l4.x * LOG2E, l4.y * LOG2E, l4.z * LOG2E, l4.w * LOG2E};
+        const float dvv[4] = {d4.x, d4.y, d4.z, d4.w};
+        // query qh0 - 32 th + qi + e sees key kv if kv <= query < T (and kv < T)
+        const int qlo = kv - (qh0 - 32 * th) - qi, qhi = T - (qh0 - 32 * th) - qi;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int r = 4 * c4 + e;
+          float pv = fast_exp2(p[r] * sc - lv[e]);
+          if constexpr (decltype(masked)::value) pv = (e >= qlo && e < qhi && kv < T) ? pv : 0.0f;
+          p[r] = pv;
+          ds[r] = pv * (ds[r] - dvv[e]);
+        }
+      }
+    };
+    if (diag) probs(std::true_type{});
+    else probs(std::false_type{});
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh) {
+      const bf16x8 pf = acc_slots(p, hh), sf = acc_slots(ds, hh);
+#pragma unroll
+      for (int d = 0; d < S::DT; ++d) {
+        dv[d] = mfma32(read_tr<HD>(Ds, 32 * d, 32 * th + 16 * hh, lane), pf, dv[d]);
+        dk[d] = mfma32(read_tr<HD>(Qs, 32 * d, 32 * th + 16 * hh, lane), sf, dk[d]);
+      }
+    }
+  }
+
+  // the second query half's waves hand their partial sums to the first's
+  __syncthreads();
+  lds_v4f32_t* red = (lds_v4f32_t*)smem_raw + kw * (NACC / 4) * 64 + lane;
+  if (th == 1) {
+#pragma unroll
+    for (int d = 0; d < S::DT; ++d)
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        red[((2 * d) * 4 + c) * 64] = v4f32{dk[d][4 * c], dk[d][4 * c + 1], dk[d][4 * c + 2], dk[d][4 * c + 3]};
+        red[((2 * d + 1) * 4 + c) * 64] = v4f32{dv[d][4 * c], dv[d][4 * c + 1], dv[d][4 * c + 2], dv[d][4 * c + 3]};
+      }
+  }
+  __syncthreads();
+  if (th == 1 || kv >= T) return;
+  bf16_t* dst = a.dqkv + ((size_t)b * T + kv) * ld + (H + j) * HD;
+#pragma unroll
+  for (int d = 0; d < S::DT; ++d)
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const v4f32 ok = red[((2 * d) * 4 + c) * 64], ov = red[((2 * d + 1) * 4 + c) * 64];
+      const int dd = 32 * d + 8 * c + 4 * g;
+      *reinterpret_cast<uint2*>(dst + dd) =
+          make_uint2(pack2((dk[d][4 * c] + ok.x) * scale, (dk[d][4 * c + 1] + ok.y) * scale),
+                     pack2((dk[d][4 * c + 2] + ok.z) * scale, (dk[d][4 * c + 3] + ok.w) * scale));
+      *reinterpret_cast<uint2*>(dst + Hkv * HD + dd) =
+          make_uint2(pack2(dv[d][4 * c] + ov.x, dv[d][4 * c + 1] + ov.y), pack2(dv[d][4 * c + 2] + ov.z, dv[d][4 * c + 3] + ov.w));
+    }
+}
+
 template <int HD>
 hipError_t fwd_t(const AttnArgs& a, hipStream_t s) {
   dim3 grid(((a.T + BQ - 1) / BQ) * a.B * a.H);
@@ -600,7 +769,10 @@ hipError_t bwd_t(const AttnArgs& a, hipStream_t s) {
   hipLaunchKernelGGL(attn_bwd_dq_kernel<HD>, dim3(nb * a.B * a.H), dim3(256), 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(attn_bwd_dkdv_kernel<HD>, dim3(nb * a.B * Hkv), dim3(256), 0, s, a);
+  if constexpr (HD == 128)
+    hipLaunchKernelGGL(attn_bwd_dkdv8_kernel<HD>, dim3(nb * a.B * Hkv), dim3(512), 0, s, a);
+  else
+    hipLaunchKernelGGL(attn_bwd_dkdv_kernel<HD>, dim3(nb * a.B * Hkv), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
