@@ -72,18 +72,23 @@ DEV int unit_t(int k, int c) {
   else return k * (R / 8) + (c ^ (((k >> 1) & 1) << 2));
 }
 
+// Waves per workgroup: 4 in a 2 x 2 arrangement; 8 (4 x 2) for 256-row tiles
+// with 64-deep stages, whose two 128-row halves share each B tile in LDS
+// (one workgroup per CU, two waves per SIMD).
+constexpr int gemm_waves(int bm, int bk) { return bm >= 256 && bk >= 64 ? 8 : 4; }
+
 // Issue the direct-to-LDS loads of one operand tile (R rows of the operand,
-// BK contraction steps starting at k0) into the stage at `dst`. Wave w issues
-// instructions w, w+4, ...; each instruction moves 64 units (1 KB), unit u of
-// the tile going to byte 16*u.
-template <int R, int BK, bool TR>
+// BK contraction steps starting at k0) into the stage at `dst`. Wave w of NW
+// issues instructions w, w+NW, ...; each instruction moves 64 units (1 KB),
+// unit u of the tile going to byte 16*u.
+template <int R, int BK, bool TR, int NW>
 DEV void issue_tile(v4i32 rs, int ld, int r0, int k0, lds_char_t* dst, int wave, int lane) {
   constexpr int UNITS = R * BK / 8;
   constexpr int INSTR = UNITS / 64;
-  static_assert(UNITS % 256 == 0, "tile must split evenly over 4 waves");
+  static_assert(UNITS % (64 * NW) == 0, "tile must split evenly over the waves");
 #pragma unroll
-  for (int i = 0; i < INSTR / 4; ++i) {
-    const int ins = wave + 4 * i;
+  for (int i = 0; i < INSTR / NW; ++i) {
+    const int ins = wave + NW * i;
     const int u = ins * 64 + lane;   // physical unit written by this lane
     uint32_t off;
     if constexpr (!TR) {
@@ -121,16 +126,17 @@ DEV bf16x8 read_frag(const lds_char_t* stage, int row_base, int s, int lane) {
 }
 
 template <int BM, int BN, int BK, int NS, bool A_T, bool B_T, int EPI, bool SEG2 = false>
-__global__ __launch_bounds__(256, (NS <= 2 ? 2 : 1)) void gemm_kernel(GemmArgs g) {
-  constexpr int WTM = BM / 2, WTN = BN / 2;   // 2 x 2 waves
+__global__ __launch_bounds__(64 * gemm_waves(BM, BK), (NS <= 2 ? 2 : 1)) void gemm_kernel(GemmArgs g) {
+  constexpr int NW = gemm_waves(BM, BK), WM = NW / 2;
+  constexpr int WTM = BM / WM, WTN = BN / 2;   // WM x 2 waves
   constexpr int TM = WTM / 32, TN = WTN / 32;
   constexpr int KSTEPS = BK / 16;
   constexpr int A_BYTES = BM * BK * 2, B_BYTES = BN * BK * 2;
   constexpr int STAGE = A_BYTES + B_BYTES;
-  constexpr int LOADS = (BM + BN) * BK / 2048;   // load instructions per wave per stage
+  constexpr int LOADS = (BM + BN) * BK / (512 * NW);   // load instructions per wave per stage
   // epilogue staging: per wave 32 rows x WTN fp32 (row stride padded by 4)
   constexpr int EP_LD = WTN + 4;
-  constexpr int EP_BYTES = 4 * 32 * EP_LD * 4;
+  constexpr int EP_BYTES = NW * 32 * EP_LD * 4;
   constexpr int SMEM = NS * STAGE > EP_BYTES ? NS * STAGE : EP_BYTES;
   static_assert(KSTEPS % 2 == 0, "fragment double buffer alternates per k-step");
   static_assert(NS >= 2 && NS - 2 <= 3 && (NS - 2) * LOADS < 64, "ring depth / vmcnt range");
@@ -190,12 +196,12 @@ __global__ __launch_bounds__(256, (NS <= 2 ? 2 : 1)) void gemm_kernel(GemmArgs g
     lds_char_t* st = stage(kt);
     if (!SEG2 || kt < nk1) {
       const int k0 = kbeg + kt * BK;
-      issue_tile<BM, BK, A_T>(ra, g.lda, m0, k0, st, wave, lane);
-      issue_tile<BN, BK, B_T>(rb, g.ldb, n0 + bcol, k0, st + A_BYTES, wave, lane);
+      issue_tile<BM, BK, A_T, NW>(ra, g.lda, m0, k0, st, wave, lane);
+      issue_tile<BN, BK, B_T, NW>(rb, g.ldb, n0 + bcol, k0, st + A_BYTES, wave, lane);
     } else {
       const int k2 = (kt - nk1) * BK;
-      issue_tile<BM, BK, A_T>(ra2, g.lda2, m0, a2col + k2, st, wave, lane);
-      issue_tile<BN, BK, B_T>(rb2, g.ldb2, n0, k2, st + A_BYTES, wave, lane);
+      issue_tile<BM, BK, A_T, NW>(ra2, g.lda2, m0, a2col + k2, st, wave, lane);
+      issue_tile<BN, BK, B_T, NW>(rb2, g.ldb2, n0, k2, st + A_BYTES, wave, lane);
     }
   };
   auto load = [&](bf16x8* fa, bf16x8* fb, int kt, int s) {
@@ -265,7 +271,7 @@ __global__ __launch_bounds__(256, (NS <= 2 ? 2 : 1)) void gemm_kernel(GemmArgs g
 #pragma unroll
   for (int s = 0; s < NS - 1; ++s)
     if (s < nk) issue(s);
-  constexpr int KL = BM * BN > 192 * 192 ? 0 : A_T ? 1 : B_T ? 2 : 0;
+  constexpr int KL = WTM * WTN > 96 * 96 ? 0 : A_T ? 1 : B_T ? 2 : 0;
   if constexpr (KL == 2) {
   for (int kt = 0; kt < nk; ++kt) {
     // issued so far: tiles up to kt + NS - 2
@@ -471,7 +477,7 @@ template <int BM, int BN, int BK, int NS, bool A_T, bool B_T, int EPI, bool SEG2
 hipError_t launch_t(const GemmArgs& g, hipStream_t s) {
   const unsigned tn = (g.N + BN - 1) / BN, tm = (g.M + BM - 1) / BM;
   dim3 grid = g.splits > 1 ? dim3(tn * tm * g.splits) : dim3(tn, tm);
-  hipLaunchKernelGGL((gemm_kernel<BM, BN, BK, NS, A_T, B_T, EPI, SEG2>), grid, dim3(256), 0, s, g);
+  hipLaunchKernelGGL((gemm_kernel<BM, BN, BK, NS, A_T, B_T, EPI, SEG2>), grid, dim3(64 * gemm_waves(BM, BK)), 0, s, g);
   return hipGetLastError();
 }
 
@@ -512,6 +518,10 @@ hipError_t launch_cfg(const GemmArgs& g, int a_t, int b_t, int epi, hipStream_t 
 //   weight gradients: 192 x 192 tiles, 32-deep stages;
 //   forward MLP-up with GELU, and products with at least 8192 such tiles
 //   (the tied head): 256 x 192 x 32, whose rounds of 512 tiles fill the chip;
+//   input gradients without the GELU derivative: 256 x 192 x 64 with eight
+//   waves, the two 128-row halves sharing each B tile (-2 to -3 % against
+//   two four-wave 128 x 192 workgroups per CU; slower for the forward and
+//   GELU-derivative products);
 //   other forward and input-gradient products: 128 x 192, 64-deep stages
 //   (32-deep when the epilogue applies the GELU derivative).
 // Widths that are not multiples of 192 (the Qwen3-shaped model, small test
@@ -519,12 +529,12 @@ hipError_t launch_cfg(const GemmArgs& g, int a_t, int b_t, int epi, hipStream_t 
 // 128 x 128, 64-deep except for weight gradients (the Qwen3-shaped step:
 // input gradients -17 %, forward products -4 % against 32-deep stages).
 GemmConfig gemm_config(int M, int N, int a_t, int b_t, int epi) {
-  (void)b_t;
   if (N >= 192 && N % 192 == 0) {
     if (a_t) {
       if (M >= 192 && M % 192 == 0) return {192, 192, 32};
       if (M >= 128) return {128, 192, 32};
     } else {
+      if (M >= 256 && b_t && epi == EPI_BF16) return {256, 192, 64};
       const long tiles256 = (long)((M + 255) / 256) * (N / 192);
       if (M >= 256 && (epi == EPI_GELU || tiles256 >= 8192)) return {256, 192, 32};
       if (M >= 128) return {128, 192, epi == EPI_GELU_BWD ? 32 : 64};
@@ -592,7 +602,10 @@ hipError_t launch_gemm(const GemmArgs& g0, int a_t, int b_t, int epi, hipStream_
                                                                                   : GemmConfig{128, 128, 64};
   }
   if (c.bm == 192) return launch_cfg<192, 192, 32>(g, a_t, b_t, epi, s);
-  if (c.bm == 256 && c.bn == 192) return launch_cfg<256, 192, 32>(g, a_t, b_t, epi, s);
+  if (c.bm == 256 && c.bn == 192) {
+    if (c.bk == 64) return launch_cfg<256, 192, 64>(g, a_t, b_t, epi, s);
+    return launch_cfg<256, 192, 32>(g, a_t, b_t, epi, s);
+  }
   if (c.bm == 128 && c.bn == 192) {
     if (c.bk == 64) return launch_cfg<128, 192, 64>(g, a_t, b_t, epi, s);
     return launch_cfg<128, 192, 32>(g, a_t, b_t, epi, s);
