@@ -518,10 +518,12 @@ hipError_t launch_cfg(const GemmArgs& g, int a_t, int b_t, int epi, hipStream_t 
 //   weight gradients: 192 x 192 tiles, 32-deep stages;
 //   forward MLP-up with GELU, and products with at least 8192 such tiles
 //   (the tied head): 256 x 192 x 32, whose rounds of 512 tiles fill the chip;
-//   input gradients without the GELU derivative: 256 x 192 x 64 with eight
-//   waves, the two 128-row halves sharing each B tile (-2 to -3 % against
-//   two four-wave 128 x 192 workgroups per CU; slower for the forward and
-//   GELU-derivative products);
+//   input gradients without the GELU derivative, and forward products of
+//   1024 to 8191 such tiles (the Qwen3-shaped gate/up projection): 256 x 192
+//   x 64 with eight waves, the two 128-row halves sharing each B tile (-2 to
+//   -3 % on the GPT-2 input gradients, -3.5 % on the gate/up product, against
+//   two four-wave 128 x 192 workgroups per CU; slower for the GPT-2 forward
+//   and GELU-derivative products);
 //   other forward and input-gradient products: 128 x 192, 64-deep stages
 //   (32-deep when the epilogue applies the GELU derivative).
 // Widths that are not multiples of 192 (the Qwen3-shaped model, small test
@@ -536,6 +538,7 @@ GemmConfig gemm_config(int M, int N, int a_t, int b_t, int epi) {
     } else {
       if (M >= 256 && b_t && epi == EPI_BF16) return {256, 192, 64};
       const long tiles256 = (long)((M + 255) / 256) * (N / 192);
+      if (M >= 256 && epi == EPI_BF16 && tiles256 >= 1024 && tiles256 < 8192) return {256, 192, 64};
       if (M >= 256 && (epi == EPI_GELU || tiles256 >= 8192)) return {256, 192, 32};
       if (M >= 128) return {128, 192, epi == EPI_GELU_BWD ? 32 : 64};
     }
