@@ -40,6 +40,11 @@ CASES = {
     "tiny_ragged": dict(vocab=500, vocab_padded=512, B=3, T=29, max_seq_len=32),
     "wide_hd64": dict(n_layer=2, n_head=4, d_model=256, d_ff=1024, vocab=1000, vocab_padded=1024,
                       max_seq_len=160, B=2, T=150),
+    # widths that are multiples of 192 with 300 token rows: the input
+    # gradients run on the eight-wave 256-row tiles, the second row tile
+    # ragged
+    "wide_c384": dict(n_layer=2, n_head=6, d_model=384, d_ff=1536, vocab=1000, vocab_padded=1024,
+                      max_seq_len=160, B=2, T=150),
     # degenerate: one-token sequences (attention over a single key, 5 rows in
     # every product, token contractions far shorter than one k-tile)
     "single_token": dict(B=5, T=1),
