@@ -594,7 +594,6 @@ hipError_t launch_gemm(const GemmArgs& g0, int a_t, int b_t, int epi, hipStream_
       if (g.b_bound[i] < 0 || g.b_bound[i] % 128) return hipErrorInvalidValue;
   }
   GemmConfig c = gemm_config(g.M, g.N, a_t, b_t, epi);
-  if (g.b_step != 0 && ((g.b_bound[0] % c.bm) || (g.b_bound[1] % c.bm))) return hipErrorInvalidValue;
   // a tile's output columns must lie within one block of the second segment
   const bool bounded = g.K2 > 0 && (g.a2_bound[0] > 0 || g.a2_bound[1] > 0);
   if (bounded) {
@@ -604,6 +603,8 @@ hipError_t launch_gemm(const GemmArgs& g0, int a_t, int b_t, int epi, hipStream_
       c = (g.M >= 256 && (long)((g.M + 255) / 256) * ((g.N + 127) / 128) >= 512) ? GemmConfig{256, 128, 32}
                                                                                   : GemmConfig{128, 128, 64};
   }
+  // an output row block must not straddle a B column-offset bound
+  if (g.b_step != 0 && ((g.b_bound[0] % c.bm) || (g.b_bound[1] % c.bm))) return hipErrorInvalidValue;
   if (c.bm == 192) return launch_cfg<192, 192, 32>(g, a_t, b_t, epi, s);
   if (c.bm == 256 && c.bn == 192) {
     if (c.bk == 64) return launch_cfg<256, 192, 64>(g, a_t, b_t, epi, s);
