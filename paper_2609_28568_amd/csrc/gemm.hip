@@ -524,8 +524,9 @@ hipError_t launch_cfg(const GemmArgs& g, int a_t, int b_t, int epi, hipStream_t 
 //   -3 % on the GPT-2 input gradients, -3.5 % on the gate/up product, against
 //   two four-wave 128 x 192 workgroups per CU; slower for the GPT-2 forward
 //   and GELU-derivative products);
-//   other forward and input-gradient products: 128 x 192, 64-deep stages
-//   (32-deep when the epilogue applies the GELU derivative).
+//   other forward and input-gradient products, the GELU-derivative input
+//   gradient included: 128 x 192, 64-deep stages (-5 % on the latter
+//   against 32-deep stages since the k-loop schedule fences).
 // Widths that are not multiples of 192 (the Qwen3-shaped model, small test
 // models) take 256 x 128 tiles when they give at least 512 of them, else
 // 128 x 128, 64-deep except for weight gradients (the Qwen3-shaped step:
@@ -540,7 +541,7 @@ GemmConfig gemm_config(int M, int N, int a_t, int b_t, int epi) {
       const long tiles256 = (long)((M + 255) / 256) * (N / 192);
       if (M >= 256 && epi == EPI_BF16 && tiles256 >= 1024 && tiles256 < 8192) return {256, 192, 64};
       if (M >= 256 && (epi == EPI_GELU || tiles256 >= 8192)) return {256, 192, 32};
-      if (M >= 128) return {128, 192, epi == EPI_GELU_BWD ? 32 : 64};
+      if (M >= 128) return {128, 192, 64};
     }
   }
   // 256-row tiles only when they still give two workgroups per CU (a
