@@ -729,7 +729,7 @@ gpt2_status qwen3_adamw_step(qwen3_model* m, int64_t step, float* d_grad_norm_ou
   a.bc2 = (float)(1.0 - std::pow((double)c.beta2, (double)(step + 1)));
   a.seg.count = 1;
   a.seg.end[0] = n;
-  a.seg.decay[0] = 1;   // the configured decay (0 by default) applies to every adapter tensor
+  a.seg.decay[0] = 1;   // the configured decay applies to every adapter tensor (all are 2-D)
   TRY(m->run(OPT, 0.0, 30.0 * n, [&] { return launch_adamw(a, m->stream); }));
   m->have_grads = false;
   return GPT2_OK;

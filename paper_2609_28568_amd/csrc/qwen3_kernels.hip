@@ -1,8 +1,8 @@
 // Elementwise and normalisation kernels of the Qwen3-shaped adapter step:
 // token gather from a bf16 table, RMSNorm forward and backward over rows, the
-// per-head RMSNorm + rotary embedding of queries and keys (which also repacks
-// q|k|v for the attention kernels, repeating each key/value head for its group
-// of query heads), the SwiGLU gate and its derivative, and an in-place scale.
+// per-head RMSNorm + rotary embedding of queries and keys (output in the same
+// q|k|v layout, which the grouped-query attention kernels read in place), the
+// SwiGLU gate and its derivative, and an in-place scale.
 #include "common.h"
 #include "kernels.h"
 

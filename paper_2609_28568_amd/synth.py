@@ -168,10 +168,12 @@ QWEN3_WORKLOADS = {
                            lora_targets=("q", "k", "v", "o"), loss_from=0.5, token_dist="zipf"),
 }
 
-# Adapter optimiser: the paper gives no separate betas, decay or rate for this
-# stage; these are the usual adapter fine-tuning values, with the global-norm
-# clip of the paper's optimisation section.
-QWEN3_OPTIM = dict(lr=2e-4, beta1=0.9, beta2=0.999, adam_eps=1e-8, weight_decay=0.0, grad_clip=1.0,
+# Adapter optimiser: the clinical stage names AdamW without values, so the one
+# AdamW recipe the paper states (section "Optimisation and precision": betas
+# 0.9/0.95, eps 1e-8, decay 0.1 on two-dimensional tensors, which every
+# adapter tensor is, global-norm clip 1.0) applies; the rate is the one free
+# choice.
+QWEN3_OPTIM = dict(lr=2e-4, beta1=0.9, beta2=0.95, adam_eps=1e-8, weight_decay=0.1, grad_clip=1.0,
                    rms_eps=1e-6, rope_theta=1e6)
 
 

@@ -374,3 +374,55 @@ def test_accumulation_equals_big_batch():
     big = oracle.backward(p, oracle.forward(p, np.concatenate([i1, i2]), np.concatenate([t1, t2]), cfg), cfg)
     for k in oracle.KINDS:
         assert np.allclose(g[k], big[k], rtol=1e-10, atol=1e-15), k
+
+
+def _torch_schedule(opt, cfg):
+    """Warmup then cosine built from torch's own schedulers: LinearLR from
+    lr_max/W to lr_max over W-1 steps, then CosineAnnealingLR to lr_min over
+    total_steps - W steps."""
+    W = cfg.warmup_steps
+    warm = torch.optim.lr_scheduler.LinearLR(opt, start_factor=1.0 / W, end_factor=1.0, total_iters=W - 1)
+    cos = torch.optim.lr_scheduler.CosineAnnealingLR(opt, T_max=cfg.total_steps - W, eta_min=cfg.lr_min)
+    return torch.optim.lr_scheduler.SequentialLR(opt, [warm, cos], milestones=[W])
+
+
+def test_train_step_matches_torch_composition():
+    """Four optimiser steps of train_step, each over two micro-batches, against
+    an fp64 torch composition written from library pieces: autograd of the
+    mean loss over both micro-batches, clip_grad_norm_ to 1.0, AdamW with the
+    decay on 2-D weights, the rate from torch's LinearLR + CosineAnnealingLR.
+    Catches a missing 1/n micro-batch scale, a wrong loss mean, a skipped or
+    misplaced clip and a rate taken at the wrong step."""
+    w, cfg = tiny_cfg(vocab=500, vocab_padded=512, B=2, T=16)
+    cfg.warmup_steps, cfg.total_steps, cfg.lr_max, cfg.lr_min = 2, 6, 2e-2, 2e-3
+    p = as64(synth.perturb_params(synth.init_params(w), seed=31))
+    tp = {k: torch.tensor(v.copy(), requires_grad=True) for k, v in p.items()}
+    groups = [{"params": [tp[k] for k in oracle.KINDS if k in oracle.DECAYED], "weight_decay": cfg.weight_decay},
+              {"params": [tp[k] for k in oracle.KINDS if k not in oracle.DECAYED], "weight_decay": 0.0}]
+    opt = torch.optim.AdamW(groups, lr=cfg.lr_max, betas=(cfg.beta1, cfg.beta2), eps=cfg.adam_eps, foreach=False)
+    sched = _torch_schedule(opt, cfg)
+    m, v = oracle.zero_grads(p), oracle.zero_grads(p)
+    for step in range(4):
+        mbs = [synth.token_batch(w, seed=40 + step, micro=k) for k in range(2)]
+        opt.zero_grad()
+        tl = sum(_torch_gpt2_loss(tp, ids, tgt, cfg) for ids, tgt in mbs) / len(mbs)
+        tl.backward()
+        # the gradient norms here are well above 1, so the clip is active.
+        # torch's own clip scales by clip/(norm + 1e-6); the reading taken is
+        # clip/norm, which torch's clip_grads_with_norm_ gives when handed
+        # norm - 1e-6 (gradients that reach eps-sized values after clipping
+        # make AdamW's first step sensitive to that 1e-6)
+        params = list(tp.values())
+        tn = torch.nn.utils.get_total_norm([q.grad for q in params])
+        torch.nn.utils.clip_grads_with_norm_(params, cfg.grad_clip, tn - 1e-6, foreach=False)
+        tnorm = float(tn)
+        t_lr = opt.param_groups[0]["lr"]
+        opt.step()
+        sched.step()
+        loss, norm, lr = oracle.train_step(p, m, v, step, mbs, cfg)
+        assert abs(loss - float(tl)) <= 1e-12, (step, loss, float(tl))
+        assert abs(norm - tnorm) <= 1e-10 * tnorm, (step, norm, tnorm)
+        assert norm > cfg.grad_clip
+        assert abs(lr - t_lr) <= 1e-15, (step, lr, t_lr)
+        for k in oracle.KINDS:
+            np.testing.assert_allclose(p[k], tp[k].detach().numpy(), rtol=1e-9, atol=1e-12, err_msg=f"{step} {k}")

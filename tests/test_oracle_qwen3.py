@@ -189,16 +189,20 @@ def test_adapter_adamw_first_step_closed_form():
     m = {"q_A": np.zeros((1, 2))}
     v = {"q_A": np.zeros((1, 2))}
     q3.adamw_step(lora, grads, m, v, 0, cfg)
-    # step 1: m_hat = g, v_hat = g^2, so the update is lr * g / (|g| + eps)
-    expect = np.array([[1.0 - 1e-3 * 0.5 / (0.5 + 1e-8), -2.0 + 1e-3 * 0.25 / (0.25 + 1e-8)]])
+    # step 1: m_hat = g, v_hat = g^2, so the update is lr * (g / (|g| + eps)
+    # + decay * p), the decay 0.1 of the paper's optimisation section
+    assert cfg.weight_decay == 0.1
+    expect = np.array([[1.0 - 1e-3 * (0.5 / (0.5 + 1e-8) + 0.1 * 1.0),
+                        -2.0 + 1e-3 * (0.25 / (0.25 + 1e-8) + 0.1 * 2.0)]])
     np.testing.assert_allclose(lora["q_A"], expect, rtol=0, atol=1e-15)
 
 
 @pytest.mark.parametrize("clip", [1e-3, 1e9])
 def test_train_step_clips_then_takes_the_closed_form_first_step(clip):
     """First step from zero moments: m_hat = c g and v_hat = (c g)^2, so every
-    adapter element moves by lr c g / (|c g| + eps) with c = clip / ||g|| when
-    the norm over all adapter elements exceeds the clip, else c = 1."""
+    adapter element moves by lr (c g / (|c g| + eps) + decay p) with
+    c = clip / ||g|| when the norm over all adapter elements exceeds the clip,
+    else c = 1."""
     cfg = q3.Qwen3Config.from_dict(dict(TINY, grad_clip=clip, lr=1e-3))
     base, lora = _params(cfg, 13)
     ids, tgt = _batch(cfg, 2, 10, 14)
@@ -213,5 +217,42 @@ def test_train_step_clips_then_takes_the_closed_form_first_step(clip):
     loss, got_norm = q3.train_step(base, lora, m, v, 0, ids, tgt, cfg)
     assert abs(got_norm - norm) <= 1e-12 * norm
     for k in lora:
-        step = 1e-3 * c * g[k] / (np.abs(c * g[k]) + 1e-8)
+        step = 1e-3 * (c * g[k] / (np.abs(c * g[k]) + 1e-8) + cfg.weight_decay * before[k])
         np.testing.assert_allclose(before[k] - lora[k], step, rtol=1e-9, atol=1e-15)
+
+
+def test_adapter_adamw_hand_steps():
+    """Three steps against hand arithmetic with betas (0.9, 0.999): from t=2 on
+    the moments' history matters, so wrong or swapped betas or a wrong bias
+    correction change the result."""
+    gold = json.load(open(os.path.join(os.path.dirname(GOLDEN), "adamw_adapter_hand.json")))
+    cfg = q3.Qwen3Config.from_dict(dict(TINY, lr=gold["lr"], beta1=gold["beta1"], beta2=gold["beta2"],
+                                        adam_eps=gold["eps"], weight_decay=0.0))
+    lora = {"q_A": np.array([[gold["p0"]]])}
+    m = {"q_A": np.zeros((1, 1))}
+    v = {"q_A": np.zeros((1, 1))}
+    for step, (g, want) in enumerate(zip(gold["grads"], gold["p_after"])):
+        q3.adamw_step(lora, {"q_A": np.array([[g]])}, m, v, step, cfg)
+        assert abs(float(lora["q_A"][0, 0]) - want) <= 1e-15, (step, float(lora["q_A"][0, 0]), want)
+
+
+@pytest.mark.parametrize("betas,wd", [((0.9, 0.999), 0.0), ((0.9, 0.95), 0.0), ((0.8, 0.99), 0.1)])
+def test_adapter_adamw_matches_torch_over_steps(betas, wd):
+    """Five steps of the oracle's AdamW against torch.optim.AdamW in fp64
+    (decoupled decay, bias correction), with gradients that change sign."""
+    cfg = q3.Qwen3Config.from_dict(dict(TINY, lr=3e-3, beta1=betas[0], beta2=betas[1], adam_eps=1e-8,
+                                        weight_decay=wd))
+    rng = np.random.default_rng(21)
+    lora = {"q_A": rng.standard_normal((3, 5)), "o_B": rng.standard_normal((4, 2))}
+    tp = {k: torch.tensor(x.copy(), requires_grad=True) for k, x in lora.items()}
+    opt = torch.optim.AdamW(list(tp.values()), lr=3e-3, betas=betas, eps=1e-8, weight_decay=wd, foreach=False)
+    m = {k: np.zeros_like(x) for k, x in lora.items()}
+    v = {k: np.zeros_like(x) for k, x in lora.items()}
+    for step in range(5):
+        grads = {k: rng.standard_normal(x.shape) * (0.5 + step) for k, x in lora.items()}
+        for k in lora:
+            tp[k].grad = torch.tensor(grads[k])
+        opt.step()
+        q3.adamw_step(lora, grads, m, v, step, cfg)
+        for k in lora:
+            np.testing.assert_allclose(lora[k], tp[k].detach().numpy(), rtol=1e-13, atol=1e-15)
