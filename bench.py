@@ -220,9 +220,9 @@ def cpu_baseline(w: dict, params, ids, tgt) -> dict:
 # (shapes, splits, tile configurations) is added per workload.
 KERNEL_CLASSES = {
     "gemm_fwd": (("gemm.hip", "common.h", "lds_dma.h", "kernels.h"),
-                 r"gemm_kernel<\d+, \d+, \d+, \d+, false, false, 0(, false)?>", 1),
+                 r"gemm_kernel<\d+, \d+, \d+, \d+, false, false, 0(, (false|true))*>", 1),
     "gemm_dw": (("gemm.hip", "common.h", "lds_dma.h", "kernels.h"),
-                r"gemm_kernel<\d+, \d+, \d+, \d+, true, true, 3(, false)?>", 1),
+                r"gemm_kernel<\d+, \d+, \d+, \d+, true, true, [35](, (false|true))*>", 1),
     "attn_bwd": (("attention.hip", "common.h", "lds_dma.h", "kernels.h"), r"attn_bwd", 2),
 }
 

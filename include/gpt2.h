@@ -89,11 +89,15 @@ typedef struct gpt2_buffers {
 
 typedef struct gpt2_model gpt2_model;   /* opaque host-side handle */
 
-/* Sizes for cfg. Returns INVALID_ARG for a config that fails validation. */
+/* Sizes for cfg (the model of section "Model" at the micro-batch geometry
+ * of "Batch geometry"; fp32 master weights, gradients and moments and a bf16
+ * copy, "Optimisation and precision"). out (host) receives byte sizes.
+ * Returns INVALID_ARG for a config that fails validation or a NULL pointer. */
 gpt2_status gpt2_query_sizes(const gpt2_config* cfg, gpt2_sizes* out);
 
 /* Number of parameter tensors: 2 + 12*n_layer + 2 (148 for 12 layers, the
- * count of gradient tensors the paper checks). */
+ * count of gradient tensors the paper checks against its reference dump,
+ * section "What is checked before training starts"). 0 for an invalid cfg. */
 int32_t gpt2_num_tensors(const gpt2_config* cfg);
 
 /* Describe parameter tensor idx (0 <= idx < gpt2_num_tensors): name in
@@ -104,43 +108,72 @@ gpt2_status gpt2_tensor_info(const gpt2_config* cfg, int32_t idx, char* name,
                              size_t* offset, int32_t* shape, int32_t* ndim,
                              int32_t* decay);
 
-/* Create a handle over caller-owned buffers. The caller has filled
- * params_f32 (and zeroed adam_m, adam_v); init enqueues the bf16 weight copy
- * on hip_stream (a hipStream_t, NULL for the default stream). */
+/* Create a handle over caller-owned buffers (bufs, host struct of device
+ * pointers; the library keeps the pointers, never the memory) and enqueue the
+ * initial state on hip_stream (a hipStream_t, NULL for the default stream).
+ *   init_mode 0: the caller has filled params_f32 (and adam_m, adam_v: zero
+ *     for a fresh run); init writes the bf16 weight copy. seed is unused.
+ *   init_mode 1: seeded initialisation of section "Model": every 2-D weight
+ *     (both embedding tables included) N(0, 0.02), the attention and MLP
+ *     output projections (the two that write into the residual stream)
+ *     N(0, 0.02/sqrt(2 n_layer)), biases and LayerNorm shifts 0, gains 1, the
+ *     padding rows vocab..vocab_padded-1 of the token table exactly 0; adam_m
+ *     and adam_v cleared; bf16 copy written. Element i of the flat buffer
+ *     takes the Box-Muller normal (fp64) of the first two words of
+ *     Philox4x32-10 (Salmon et al., SC 2011) at counter (i mod 2^32,
+ *     i div 2^32, 0, 0) and key (seed mod 2^32, seed div 2^32), multiplied by
+ *     its standard deviation in fp64 and rounded once to fp32, so a given seed
+ *     gives the same weights on every device.
+ * *out (host) receives the handle. INVALID_ARG for a bad config, a NULL or
+ * unaligned buffer, or an init_mode other than 0 and 1 (nothing enqueued). */
 gpt2_status gpt2_init(const gpt2_config* cfg, const gpt2_buffers* bufs,
-                      void* hip_stream, gpt2_model** out);
+                      void* hip_stream, uint64_t seed, int32_t init_mode,
+                      gpt2_model** out);
 
-/* Refresh the bf16 weight copy after the caller changed params_f32. */
+/* Refresh the bf16 weight copy ("Optimisation and precision": bf16 compute
+ * from fp32 master weights) after the caller changed params_f32. */
 gpt2_status gpt2_sync_weights(gpt2_model* m);
 
-/* Forward pass (Figure 1): embedding, n_layer blocks, final LayerNorm, tied
- * LM head over all vocab_padded columns. d_inputs: int32 [B*T] token ids in
- * [0, vocab), row-major [B, T]. d_targets: int32 [B*T] next-token ids in
- * [0, vocab), or NULL. With targets the softmax cross-entropy over the first
- * vocab columns runs too: per-token losses are kept and the logits buffer is
- * overwritten by dlogits = (softmax - onehot) / (B*T*grad_accum), exactly 0
- * on padding columns. Without targets the logits are kept. Ids outside
- * [0, vocab) are a contract violation (not checked on the device). */
+/* Forward pass (section "Model", Figure 1): embedding, n_layer blocks, final
+ * LayerNorm, tied LM head over all vocab_padded columns. d_inputs: int32
+ * [B*T] token ids in [0, vocab), row-major [B, T]. d_targets: int32 [B*T]
+ * next-token ids in [0, vocab), or NULL. With targets the softmax
+ * cross-entropy over the first vocab columns runs too: per-token losses are
+ * kept and the logits buffer is overwritten by dlogits = (softmax - onehot) /
+ * (B*T*grad_accum), exactly 0 on padding columns. Without targets the logits
+ * are kept. Ids outside [0, vocab) are a contract violation: the kernels
+ * read row (or column) 0 in their place, so nothing is read out of bounds,
+ * and note it on the device; the next gpt2_loss or gpt2_evaluate returns
+ * GPT2_ERR_INVALID_ARG for it (a malformed request, told apart from a
+ * failed run, section "The stack under test"). */
 gpt2_status gpt2_forward(gpt2_model* m, const int32_t* d_inputs,
                          const int32_t* d_targets);
 
-/* Backward pass for the last forward (which must have had targets).
+/* Backward pass (the analytic gradient of the forward of section "Model")
+ * for the last forward, which must have had targets (STATE otherwise).
  * accumulate = 0 overwrites the fp32 gradients, 1 adds to them (micro-steps
- * of gradient accumulation, "Batch geometry"). */
+ * of gradient accumulation, "Batch geometry"; STATE when there is no
+ * gradient to add to). */
 gpt2_status gpt2_backward(gpt2_model* m, int32_t accumulate);
 
-/* Optimiser step (0-based step index): global gradient norm over all
- * tensors, clip coefficient grad_clip/norm when the norm exceeds grad_clip,
- * then AdamW with bias correction, decay on 2-D weights only and the
- * scheduled learning rate; the bf16 weight copy is refreshed. *lr_out (host,
- * optional) receives the rate used; d_grad_norm_out (device fp32, optional)
- * receives the pre-clip norm. */
+/* Optimiser step ("Optimisation and precision"), 0-based step index >= 0:
+ * global gradient norm over all tensors, clip coefficient grad_clip/norm when
+ * the norm exceeds grad_clip, then AdamW (betas, eps, bias correction with
+ * t = step + 1, decoupled decay on the 2-D weights only) at the scheduled
+ * learning rate gpt2_lr_at(cfg, step); the bf16 weight copy is refreshed.
+ * *lr_out (host, optional) receives the rate used; d_grad_norm_out (device
+ * fp32, optional) receives the pre-clip norm. STATE when no backward has run
+ * since the last step. */
 gpt2_status gpt2_adamw_step(gpt2_model* m, int64_t step, float* lr_out,
                             float* d_grad_norm_out);
 
-/* Mean loss of the last forward with targets, copied to *loss_out (host).
- * Synchronises the stream. */
-gpt2_status gpt2_loss(gpt2_model* m, float* loss_out);
+/* Loss of the last forward with targets ("Optimisation and precision": loss
+ * in fp32, the mean over the B*T positions): *loss_out (host) receives the
+ * mean; d_token_losses (device fp32 [B*T], row-major [B, T], optional)
+ * receives each position's loss. Synchronises the stream. STATE before any
+ * forward with targets; INVALID_ARG, with the loss still written, when a
+ * forward since the last report was given ids outside [0, vocab). */
+gpt2_status gpt2_loss(gpt2_model* m, float* loss_out, float* d_token_losses);
 
 /* Forward-only evaluation of held-out tokens (the held-out loss of section
  * "Batch geometry" and the evaluation cadence of "Method"): the same forward
@@ -155,18 +188,26 @@ gpt2_status gpt2_loss(gpt2_model* m, float* loss_out);
 gpt2_status gpt2_evaluate(gpt2_model* m, const int32_t* d_inputs, const int32_t* d_targets, float* loss_out,
                           float* d_token_losses);
 
-/* Learning rate at a 0-based step: lr_max*(step+1)/warmup for step < warmup,
- * then lr_min + (lr_max-lr_min)*(1+cos(pi*f))/2 with f the fraction of the
- * remaining steps elapsed, clamped to [0,1]. Pure function. */
+/* Learning rate at a 0-based step ("Optimisation and precision": linear
+ * warmup, then cosine decay): lr_max*(step+1)/warmup for step < warmup, then
+ * lr_min + (lr_max-lr_min)*(1+cos(pi*f))/2 with f the fraction of the
+ * remaining steps elapsed, clamped to [0,1]. Pure function; 0 for a NULL cfg
+ * or a negative step. */
 float gpt2_lr_at(const gpt2_config* cfg, int64_t step);
 
+/* Free the host handle (device buffers stay the caller's); m may be NULL. */
 void gpt2_destroy(gpt2_model* m);
-const char* gpt2_last_error(const gpt2_model* m);   /* m may be NULL */
+/* Reason for the last failure of a call on m, or of a call that had no
+ * handle when m is NULL ("The stack under test": typed diagnostics). The
+ * string lives until the next failing call. */
+const char* gpt2_last_error(const gpt2_model* m);
 
-/* Saved forward state, for inspection. which: one of gpt2_act; layer selects
- * the block for per-block entries. Reports the byte offset into the
+/* Saved forward state, for inspection: the per-layer activations of Figure 1
+ * that the paper compares against a reference dump (section "What is checked
+ * before training starts"). which: one of gpt2_act; layer selects the block
+ * for per-block entries. Reports (host pointers) the byte offset into the
  * activations buffer, the element count and the element type (0 = fp32,
- * 1 = bf16, 2 = int32). */
+ * 1 = bf16, 2 = int32). INVALID_ARG for an unknown entry or layer. */
 typedef enum gpt2_act {
   GPT2_ACT_RESIDUAL = 0,  /* bf16 [BT,C]: block input (layer 0 = embedding
                              output; layer n_layer = last block's output) */
@@ -195,7 +236,8 @@ gpt2_status gpt2_activation_info(const gpt2_model* m, int32_t which,
                                  int32_t layer, size_t* offset_bytes,
                                  size_t* numel, int32_t* dtype);
 
-/* One block in isolation (used to measure and check a single block):
+/* One block of section "Model" (pre-LayerNorm attention and MLP with their
+ * residual connections) in isolation, used to measure and check one block:
  * d_x_in bf16 [BT,C] is copied into the residual slot of `layer`, the block
  * runs, and its output is copied to d_x_out (bf16 [BT,C], optional). The
  * backward takes the upstream gradient d_dx_out (bf16 [BT,C]), writes the
@@ -207,7 +249,8 @@ gpt2_status gpt2_block_backward(gpt2_model* m, int32_t layer,
                                 const void* d_dx_out, void* d_dx_in,
                                 int32_t accumulate);
 
-/* Embedding backward in isolation (used to check its index handling): the
+/* Embedding backward (the stage table's "embedding backward" row, section
+ * "Speed") in isolation, used to check its index handling: the
  * token-table gradient receives, for each position r, the row d_dx[r] (bf16
  * [B*T, C]) at row d_ids[r] (int32 [B*T], in [0, vocab)), and the position
  * table gradient receives the batch sum per position. accumulate = 0 first
@@ -216,10 +259,12 @@ gpt2_status gpt2_block_backward(gpt2_model* m, int32_t layer,
 gpt2_status gpt2_embedding_backward(gpt2_model* m, const int32_t* d_ids,
                                     const void* d_dx, int32_t accumulate);
 
-/* Kernel timing probes for measurement. Kernels are grouped in classes; for
+/* Kernel timing probes for measurement, per stage in the manner of the
+ * paper's stage table (section "Speed"). Kernels are grouped in classes; for
  * classes in the enabled mask, every launch is bracketed by HIP events on
  * the model's stream and its algorithmic work (flops or bytes) is counted.
- * gpt2_probe_read synchronises and reports totals since the last reset. */
+ * gpt2_probe_read synchronises and reports (host pointers, each optional)
+ * totals since the last reset. */
 typedef enum gpt2_kclass {
   GPT2_K_GEMM_FWD = 0,       /* x W^T + bias (+ residual): one kernel */
   GPT2_K_GEMM_FWD_GELU = 1,  /* x W^T + bias with the GELU epilogue */
@@ -227,7 +272,7 @@ typedef enum gpt2_kclass {
   GPT2_K_GEMM_DX_GELU = 3,   /* dY W times GELU'(pre-activation) */
   GPT2_K_GEMM_DW = 4,        /* dY^T X into fp32 gradients (or split slices) */
   GPT2_K_ATTN_FWD = 5,
-  GPT2_K_ATTN_BWD = 6,       /* D pre-pass, dK/dV and dQ kernels */
+  GPT2_K_ATTN_BWD = 6,       /* dQ (which also computes D), then dK/dV */
   GPT2_K_LAYERNORM = 7,      /* forward and backward */
   GPT2_K_CROSS_ENTROPY = 8,
   GPT2_K_OPTIMIZER = 9,      /* norm, clip coefficient and AdamW */

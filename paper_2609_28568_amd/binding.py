@@ -70,12 +70,12 @@ def lib():
         "gpt2_num_tensors": (I32, [cfgp]),
         "gpt2_tensor_info": (I32, [cfgp, I32, ctypes.c_char_p, ctypes.POINTER(ctypes.c_size_t),
                                    ctypes.POINTER(I32), ctypes.POINTER(I32), ctypes.POINTER(I32)]),
-        "gpt2_init": (I32, [cfgp, ctypes.POINTER(Buffers), P, ctypes.POINTER(P)]),
+        "gpt2_init": (I32, [cfgp, ctypes.POINTER(Buffers), P, ctypes.c_uint64, I32, ctypes.POINTER(P)]),
         "gpt2_sync_weights": (I32, [P]),
         "gpt2_forward": (I32, [P, P, P]),
         "gpt2_backward": (I32, [P, I32]),
         "gpt2_adamw_step": (I32, [P, I64, ctypes.POINTER(F32), P]),
-        "gpt2_loss": (I32, [P, ctypes.POINTER(F32)]),
+        "gpt2_loss": (I32, [P, ctypes.POINTER(F32), P]),
         "gpt2_evaluate": (I32, [P, P, P, ctypes.POINTER(F32), P]),
         "gpt2_lr_at": (F32, [cfgp, I64]),
         "gpt2_destroy": (None, [P]),
@@ -160,9 +160,13 @@ def kind_table(cfg: Config):
 
 
 class GPT2:
-    """One model over torch-allocated device buffers on the current stream."""
+    """One model over torch-allocated device buffers on the current stream.
 
-    def __init__(self, cfg: Config, device="cuda"):
+    seed=None: the weights start at zero until set_params fills them
+    (init_mode 0); seed=int: the library draws them on the device from that
+    seed (init_mode 1) and clears the Adam moments."""
+
+    def __init__(self, cfg: Config, device="cuda", seed=None):
         import torch
         self.torch = torch
         self.cfg = cfg
@@ -186,6 +190,7 @@ class GPT2:
                                               self.params_bf16, self.activations, self.workspace)))
         self.handle = ctypes.c_void_p()
         _check(self.L.gpt2_init(ctypes.byref(cfg), ctypes.byref(b), ctypes.c_void_p(self.stream.cuda_stream),
+                                0 if seed is None else int(seed), 0 if seed is None else 1,
                                 ctypes.byref(self.handle)))
 
     def close(self):
@@ -244,9 +249,12 @@ class GPT2:
         _check(self.L.gpt2_adamw_step(self.handle, int(step), ctypes.byref(lr), ptr), self.handle)
         return lr.value
 
-    def loss(self) -> float:
+    def loss(self, token_losses=None) -> float:
+        """Mean loss of the last forward with targets; optionally fills a
+        device fp32 [B*T] tensor with the per-position losses."""
         out = ctypes.c_float()
-        _check(self.L.gpt2_loss(self.handle, ctypes.byref(out)), self.handle)
+        tl = ctypes.c_void_p(token_losses.data_ptr()) if token_losses is not None else ctypes.c_void_p(0)
+        _check(self.L.gpt2_loss(self.handle, ctypes.byref(out), tl), self.handle)
         return out.value
 
     def evaluate(self, ids, targets, token_losses=None) -> float:

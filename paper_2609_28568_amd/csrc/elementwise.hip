@@ -122,7 +122,7 @@ DEV float block_max(float v, float* sh) {
 
 // one block of 1024 threads, each with up to 16 loads in flight at a time
 __global__ __launch_bounds__(1024) void mean_kernel(const float* __restrict__ x, int n, float inv,
-                                                    float* __restrict__ out) {
+                                                    float* __restrict__ out, uint32_t* __restrict__ flag) {
   __shared__ float sh[16];
   float s = 0.0f;
   int i = threadIdx.x;
@@ -135,17 +135,30 @@ __global__ __launch_bounds__(1024) void mean_kernel(const float* __restrict__ x,
   }
   for (; i < n; i += 1024) s += x[i];
   s = block_sum<1024>(s, sh);
-  if (threadIdx.x == 0) out[0] = s * inv;
+  if (threadIdx.x == 0) {
+    out[0] = s * inv;
+    if (flag) {
+      // the kernels that set the flag ran before this one on the stream
+      reinterpret_cast<uint32_t*>(out)[1] = *flag;
+      *flag = 0u;
+    }
+  }
 }
 
 // ------------------------------------------------------------ embedding
 
 __global__ void embed_fwd_kernel(const int32_t* __restrict__ ids, const float* __restrict__ wte,
-                                 const float* __restrict__ wpe, bf16_t* __restrict__ x, int BT, int T, int C) {
+                                 const float* __restrict__ wpe, bf16_t* __restrict__ x, int BT, int T, int C, int V,
+                                 uint32_t* __restrict__ bad) {
   long i = ((long)blockIdx.x * blockDim.x + threadIdx.x) * 4;
   if (i >= (long)BT * C) return;
   const int row = i / C, c = i % C, t = row % T;
-  const int id = ids[row];
+  int id = ids[row];
+  if ((unsigned)id >= (unsigned)V) {
+    // contract violation: reported, and row 0 read in its place
+    if (bad && c == 0) atomicOr(bad, ID_BAD_INPUT);
+    id = 0;
+  }
   float4 a = *reinterpret_cast<const float4*>(wte + (size_t)id * C + c);
   float4 p = *reinterpret_cast<const float4*>(wpe + (size_t)t * C + c);
   *reinterpret_cast<uint2*>(x + i) = make_uint2(pack2(a.x + p.x, a.y + p.y), pack2(a.z + p.z, a.w + p.w));
@@ -161,14 +174,17 @@ __global__ void embed_fwd_kernel(const int32_t* __restrict__ ids, const float* _
 constexpr int EMB_P = 256;
 __global__ __launch_bounds__(256) void embed_bwd_wte_kernel(const int32_t* __restrict__ ids,
                                                             const bf16_t* __restrict__ dx, float* __restrict__ dwte,
-                                                            int BT, int C) {
+                                                            int BT, int C, int V) {
   __shared__ unsigned long long key[EMB_P];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int p0 = blockIdx.x * EMB_P;
   const int c = blockIdx.y * 256 + 4 * lane;
   {
+    // positions past the end and ids outside [0, V) (a contract violation,
+    // reported by the forward pass) take the key that sorts last and is skipped
     const int p = p0 + tid;
-    key[tid] = p < BT ? ((unsigned long long)(uint32_t)ids[p] << 32) | (uint32_t)p : ~0ull;
+    const int id = p < BT ? ids[p] : -1;
+    key[tid] = (unsigned)id < (unsigned)V ? ((unsigned long long)(uint32_t)id << 32) | (uint32_t)p : ~0ull;
   }
   __syncthreads();
   // bitonic sort of the EMB_P keys, one per thread
@@ -251,7 +267,8 @@ template <int NT, int MAXCH, bool GRAD>
 __global__ __launch_bounds__(NT) void cross_entropy_kernel(bf16_t* __restrict__ logits,
                                                            const int32_t* __restrict__ targets,
                                                            float* __restrict__ losses, int V, int Vp,
-                                                           float grad_scale, int T, int mask_from) {
+                                                           float grad_scale, int T, int mask_from,
+                                                           uint32_t* __restrict__ bad) {
   constexpr int NW = NT / 64;
   __shared__ float shm[NW], shs[NW];
   const int row = blockIdx.x, tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
@@ -267,7 +284,12 @@ __global__ __launch_bounds__(NT) void cross_entropy_kernel(bf16_t* __restrict__ 
     for (int k = row + (int)gridDim.x * tid; k < nmask; k += (int)gridDim.x * NT)
       losses[(k / mask_from) * T + k % mask_from] = 0.0f;
   }
-  const int tgt = targets[pos];
+  int tgt = targets[pos];
+  if ((unsigned)tgt >= (unsigned)V) {
+    // contract violation: reported, and column 0 taken in its place
+    if (bad && tid == 0) atomicOr(bad, ID_BAD_TARGET);
+    tgt = 0;
+  }
   // the target's logit, read before the row is overwritten (by every thread,
   // one broadcast address, so the load needs no branch; thread 0 uses it)
   const bf16_t xt_raw = lr[tgt];
@@ -429,6 +451,55 @@ __global__ __launch_bounds__(256) void adamw_kernel(AdamArgs a) {
   }
 }
 
+// ------------------------------------------------------------ seeded init
+
+// Philox4x32-10 (Salmon, Moraes, Dror, Shaw, SC 2011): ten rounds of two
+// 32x32->64-bit products whose high halves are XORed with the other counter
+// words and the key; the key is bumped by the Weyl constants between rounds.
+DEV uint4 philox4x32_10(uint4 c, uint32_t k0, uint32_t k1) {
+  constexpr uint32_t M0 = 0xD2511F53u, M1 = 0xCD9E8D57u, W0 = 0x9E3779B9u, W1 = 0xBB67AE85u;
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    if (r > 0) {
+      k0 += W0;
+      k1 += W1;
+    }
+    const uint32_t hi0 = __umulhi(M0, c.x), lo0 = M0 * c.x;
+    const uint32_t hi1 = __umulhi(M1, c.z), lo1 = M1 * c.z;
+    c = make_uint4(hi1 ^ c.y ^ k0, lo1, hi0 ^ c.w ^ k1, lo0);
+  }
+  return c;
+}
+
+// standard normal of flat element i: Box-Muller of the first two words, fp64
+DEV double normal_at(long i, uint32_t k0, uint32_t k1) {
+  const uint4 x = philox4x32_10(make_uint4((uint32_t)i, (uint32_t)((unsigned long)i >> 32), 0u, 0u), k0, k1);
+  const double u1 = ((double)x.x + 0.5) * 0x1p-32, u2 = ((double)x.y + 0.5) * 0x1p-32;
+  return sqrt(-2.0 * log(u1)) * cos(2.0 * M_PI * u2);
+}
+
+// 4 elements per thread, grid-stride; the segment of a 4-element chunk is
+// found by a walk over the (at most 16) segment ends, which are multiples of 4
+__global__ __launch_bounds__(256) void init_params_kernel(InitArgs a) {
+  const long stride = (long)gridDim.x * 256 * 4;
+  for (long i = ((long)blockIdx.x * 256 + threadIdx.x) * 4; i < a.n; i += stride) {
+    int k = 0;
+    while (k + 1 < a.count && i >= a.end[k]) ++k;
+    float v[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const long j = i + e;
+      if (j >= a.zero_lo && j < a.zero_hi) v[e] = 0.0f;
+      else if (a.std[k] > 0.0) v[e] = (float)(normal_at(j, a.key0, a.key1) * a.std[k]);
+      else v[e] = a.fill[k];
+    }
+    *reinterpret_cast<float4*>(a.p + i) = make_float4(v[0], v[1], v[2], v[3]);
+    *reinterpret_cast<float4*>(a.m + i) = make_float4(0.f, 0.f, 0.f, 0.f);
+    *reinterpret_cast<float4*>(a.v + i) = make_float4(0.f, 0.f, 0.f, 0.f);
+    *reinterpret_cast<uint2*>(a.p_bf16 + i) = make_uint2(pack2(v[0], v[1]), pack2(v[2], v[3]));
+  }
+}
+
 inline unsigned blocks_for(long n4, int nt) { return (unsigned)((n4 + nt - 1) / nt); }
 
 }  // namespace
@@ -465,28 +536,31 @@ hipError_t launch_reduce_parts(const float* part, int S, long stride, int n, int
   return hipGetLastError();
 }
 
-hipError_t launch_mean(const float* x, int n, float* out, hipStream_t s) {
-  return launch_sum_scaled(x, n, 1.0f / (float)n, out, s);
+hipError_t launch_mean(const float* x, int n, float* out, hipStream_t s, uint32_t* flag) {
+  hipLaunchKernelGGL(mean_kernel, dim3(1), dim3(1024), 0, s, x, n, 1.0f / (float)n, out, flag);
+  return hipGetLastError();
 }
 
 hipError_t launch_sum_scaled(const float* x, int n, float scale, float* out, hipStream_t s) {
-  hipLaunchKernelGGL(mean_kernel, dim3(1), dim3(1024), 0, s, x, n, scale, out);
+  hipLaunchKernelGGL(mean_kernel, dim3(1), dim3(1024), 0, s, x, n, scale, out, nullptr);
   return hipGetLastError();
 }
 
 hipError_t launch_embed_fwd(const int32_t* ids, const float* wte, const float* wpe, bf16_t* x, int B, int T, int C,
-                            hipStream_t s) {
+                            int V, uint32_t* bad, hipStream_t s) {
+  if (C % 4) return hipErrorInvalidValue;
   long n4 = (long)B * T * C / 4;
-  hipLaunchKernelGGL(embed_fwd_kernel, dim3(blocks_for(n4, 256)), dim3(256), 0, s, ids, wte, wpe, x, B * T, T, C);
+  hipLaunchKernelGGL(embed_fwd_kernel, dim3(blocks_for(n4, 256)), dim3(256), 0, s, ids, wte, wpe, x, B * T, T, C, V,
+                     bad);
   return hipGetLastError();
 }
 
-hipError_t launch_embed_bwd(const int32_t* ids, const bf16_t* dx, float* dwte, int B, int T, int C,
+hipError_t launch_embed_bwd(const int32_t* ids, const bf16_t* dx, float* dwte, int B, int T, int C, int V,
                             hipStream_t s) {
   if (C % 4) return hipErrorInvalidValue;
   const int BT = B * T;
   dim3 grid((BT + EMB_P - 1) / EMB_P, (C + 255) / 256);
-  hipLaunchKernelGGL(embed_bwd_wte_kernel, grid, dim3(256), 0, s, ids, dx, dwte, BT, C);
+  hipLaunchKernelGGL(embed_bwd_wte_kernel, grid, dim3(256), 0, s, ids, dx, dwte, BT, C, V);
   return hipGetLastError();
 }
 
@@ -500,33 +574,36 @@ hipError_t launch_embed_bwd_pos(const bf16_t* dx, float* dwpe, int B, int T, int
 
 template <int NT, int MAXCH>
 void ce_launch(bf16_t* logits, const int32_t* targets, float* losses, int rows, int V, int Vp, float grad_scale,
-               int write_grad, int T, int mask_from, hipStream_t s) {
+               int write_grad, int T, int mask_from, uint32_t* bad, hipStream_t s) {
   if (write_grad)
     hipLaunchKernelGGL((cross_entropy_kernel<NT, MAXCH, true>), dim3(rows), dim3(NT), 0, s, logits, targets, losses, V,
-                       Vp, grad_scale, T, mask_from);
+                       Vp, grad_scale, T, mask_from, bad);
   else
     hipLaunchKernelGGL((cross_entropy_kernel<NT, MAXCH, false>), dim3(rows), dim3(NT), 0, s, logits, targets, losses,
-                       V, Vp, grad_scale, T, mask_from);
+                       V, Vp, grad_scale, T, mask_from, bad);
 }
 
 hipError_t launch_cross_entropy_masked(bf16_t* logits, const int32_t* targets, float* losses, int rows, int V, int Vp,
-                                       float grad_scale, int write_grad, int T, int mask_from, hipStream_t s) {
-  if (Vp % 8 || T < 1 || mask_from < 0 || mask_from >= T || rows % (T - mask_from)) return hipErrorInvalidValue;
+                                       float grad_scale, int write_grad, int T, int mask_from, hipStream_t s,
+                                       uint32_t* bad) {
+  if (Vp % 8 || V < 1 || T < 1 || mask_from < 0 || mask_from >= T || rows % (T - mask_from))
+    return hipErrorInvalidValue;
   const int nch = Vp / 8;
-  if (nch <= 256 * 2) ce_launch<256, 2>(logits, targets, losses, rows, V, Vp, grad_scale, write_grad, T, mask_from, s);
+  if (nch <= 256 * 2)
+    ce_launch<256, 2>(logits, targets, losses, rows, V, Vp, grad_scale, write_grad, T, mask_from, bad, s);
   else if (nch <= 512 * 13)
-    ce_launch<512, 13>(logits, targets, losses, rows, V, Vp, grad_scale, write_grad, T, mask_from, s);
+    ce_launch<512, 13>(logits, targets, losses, rows, V, Vp, grad_scale, write_grad, T, mask_from, bad, s);
   else if (nch <= 1024 * 8)
-    ce_launch<1024, 8>(logits, targets, losses, rows, V, Vp, grad_scale, write_grad, T, mask_from, s);
+    ce_launch<1024, 8>(logits, targets, losses, rows, V, Vp, grad_scale, write_grad, T, mask_from, bad, s);
   else if (nch <= 1024 * 19)
-    ce_launch<1024, 19>(logits, targets, losses, rows, V, Vp, grad_scale, write_grad, T, mask_from, s);
+    ce_launch<1024, 19>(logits, targets, losses, rows, V, Vp, grad_scale, write_grad, T, mask_from, bad, s);
   else return hipErrorInvalidValue;
   return hipGetLastError();
 }
 
 hipError_t launch_cross_entropy(bf16_t* logits, const int32_t* targets, float* losses, int rows, int V, int Vp,
-                                float grad_scale, int write_grad, hipStream_t s) {
-  return launch_cross_entropy_masked(logits, targets, losses, rows, V, Vp, grad_scale, write_grad, 1, 0, s);
+                                float grad_scale, int write_grad, uint32_t* bad, hipStream_t s) {
+  return launch_cross_entropy_masked(logits, targets, losses, rows, V, Vp, grad_scale, write_grad, 1, 0, s, bad);
 }
 
 hipError_t launch_cast_bf16(const float* src, bf16_t* dst, long n, hipStream_t s) {
@@ -556,5 +633,15 @@ hipError_t launch_adamw(const AdamArgs& a, hipStream_t s) {
   unsigned blocks = blocks_for(n4, 256);
   if (blocks > 8192) blocks = 8192;
   hipLaunchKernelGGL(adamw_kernel, dim3(blocks), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_init_params(const InitArgs& a, hipStream_t s) {
+  if (a.n % 4 || a.count < 1 || a.count > 16 || a.end[a.count - 1] != a.n) return hipErrorInvalidValue;
+  for (int k = 0; k < a.count; ++k)
+    if (a.end[k] % 4) return hipErrorInvalidValue;
+  unsigned blocks = blocks_for(a.n / 4, 256);
+  if (blocks > 8192) blocks = 8192;
+  hipLaunchKernelGGL(init_params_kernel, dim3(blocks), dim3(256), 0, s, a);
   return hipGetLastError();
 }

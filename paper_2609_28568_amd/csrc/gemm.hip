@@ -125,8 +125,26 @@ DEV bf16x8 read_frag(const lds_char_t* stage, int row_base, int s, int lane) {
   }
 }
 
-template <int BM, int BN, int BK, int NS, bool A_T, bool B_T, int EPI, bool SEG2 = false>
-__global__ __launch_bounds__(64 * gemm_waves(BM, BK), (NS <= 2 ? 2 : 1)) void gemm_kernel(GemmArgs g) {
+// Kernel parameters: the product's arguments, plus the group table of a
+// grouped launch
+struct GroupedParams {
+  GemmArgs g;
+  GemmGroupedArgs gg;
+};
+template <bool GROUPED>
+using KParams = std::conditional_t<GROUPED, GroupedParams, GemmArgs>;
+DEV const GemmArgs& args_of(const GemmArgs& p) { return p; }
+DEV const GemmArgs& args_of(const GroupedParams& p) { return p.g; }
+
+// Tiles of one product of group gr (the grouped launch's tile shape)
+template <int BM, int BN>
+DEV int group_tiles(const GemmGroup& gr) {
+  return ((gr.M + BM - 1) / BM) * ((gr.N + BN - 1) / BN);
+}
+
+template <int BM, int BN, int BK, int NS, bool A_T, bool B_T, int EPI, bool SEG2 = false, bool GROUPED = false>
+__global__ __launch_bounds__(64 * gemm_waves(BM, BK), (NS <= 2 ? 2 : 1)) void gemm_kernel(KParams<GROUPED> P) {
+  GemmArgs g = args_of(P);
   constexpr int NW = gemm_waves(BM, BK), WM = NW / 2;
   constexpr int WTM = BM / WM, WTN = BN / 2;   // WM x 2 waves
   constexpr int TM = WTM / 32, TN = WTN / 32;
@@ -154,9 +172,47 @@ __global__ __launch_bounds__(64 * gemm_waves(BM, BK), (NS <= 2 ? 2 : 1)) void ge
   // With a contraction split over 8k blocks the grid is 1-D: block b works on
   // split b % splits... arranged so that split z always lands on XCD z % 8 and
   // each XCD's L2 serves one contraction range for all of its tiles.
+  int bid = 0, split = 0;
+  if constexpr (GROUPED) {
+    // one tile of one product of one group: the 1-D grid runs through the
+    // groups in order, each group's products in order, each product's tiles
+    // n fastest; every XCD takes a contiguous run of that order
+    int b = blockIdx.x;
+    const int tot = gridDim.x;
+    if ((tot & 7) == 0) b = (b & 7) * (tot >> 3) + (b >> 3);
+    int k = 0;
+#pragma unroll
+    for (int i = 0; i + 1 < GEMM_GROUPS; ++i) {
+      const int t = group_tiles<BM, BN>(P.gg.grp[i]) * P.gg.grp[i].count;
+      if (k == i && i + 1 < P.gg.ngroups && b >= t) {
+        b -= t;
+        k = i + 1;
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < GEMM_GROUPS; ++i) {
+      if (i == k) {
+        const GemmGroup& gr = P.gg.grp[i];
+        const int tpp = group_tiles<BM, BN>(gr);
+        const int pidx = b / tpp;
+        bid = b - pidx * tpp;
+        g.A = gr.A + (size_t)pidx * gr.a_stride;
+        g.B = gr.B + (size_t)pidx * gr.b_stride;
+        g.C = gr.C + (size_t)pidx * gr.c_stride;
+        g.M = gr.M;
+        g.N = gr.N;
+        g.lda = gr.lda;
+        g.ldb = gr.ldb;
+        g.ldc = gr.N;
+        g.bsum = gr.bsum ? gr.bsum + (size_t)pidx * gr.M : nullptr;
+        g.bsum_ld = gr.count * gr.M;
+      }
+    }
+    split = 0;
+  }
   const int ntn = (g.N + BN - 1) / BN, ntiles = ntn * ((g.M + BM - 1) / BM);
-  int bid, split;
-  if (g.splits > 1) {
+  if constexpr (GROUPED) {
+  } else if (g.splits > 1) {
     split = blockIdx.x % g.splits;
     bid = blockIdx.x / g.splits;
   } else {
@@ -335,7 +391,7 @@ __global__ __launch_bounds__(64 * gemm_waves(BM, BK), (NS <= 2 ? 2 : 1)) void ge
       for (int i = 0; i < TM; ++i) {
         const float v = bs[i] + __shfl_xor(bs[i], 32);
         const int m = m0 + wm * WTM + 32 * i + (lane & 31);
-        if (lane < 32 && m < g.M) g.bsum[slot * g.M + m] = v;
+        if (lane < 32 && m < g.M) g.bsum[slot * (g.bsum_ld ? g.bsum_ld : g.M) + m] = v;
       }
     }
   }
@@ -481,6 +537,31 @@ hipError_t launch_t(const GemmArgs& g, hipStream_t s) {
   return hipGetLastError();
 }
 
+// Grouped weight gradients: every tile of every product in one 1-D grid.
+template <int BM, int BN, int BK>
+hipError_t launch_grouped_t(const GemmGroupedArgs& gg, hipStream_t s) {
+  GroupedParams P{};
+  P.gg = gg;
+  GemmArgs& g = P.g;
+  g.K = gg.K;
+  g.splits = 1;
+  g.k_chunk = (gg.K + 63) / 64 * 64;
+  g.accumulate = gg.accumulate;
+  // fields the kernel sets per product; these keep the shared code's reads in range
+  g.A = gg.grp[0].A; g.B = gg.grp[0].B; g.C = gg.grp[0].C; g.M = gg.grp[0].M; g.N = gg.grp[0].N;
+  long tiles = 0;
+  for (int i = 0; i < gg.ngroups; ++i)
+    tiles += (long)((gg.grp[i].M + BM - 1) / BM) * ((gg.grp[i].N + BN - 1) / BN) * gg.grp[i].count;
+  if (tiles < 1 || tiles > (1L << 30)) return hipErrorInvalidValue;
+  if (gg.accumulate)
+    hipLaunchKernelGGL((gemm_kernel<BM, BN, BK, 2, true, true, EPI_F32_ACC, false, true>), dim3((unsigned)tiles),
+                       dim3(64 * gemm_waves(BM, BK)), 0, s, P);
+  else
+    hipLaunchKernelGGL((gemm_kernel<BM, BN, BK, 2, true, true, EPI_F32, false, true>), dim3((unsigned)tiles),
+                       dim3(64 * gemm_waves(BM, BK)), 0, s, P);
+  return hipGetLastError();
+}
+
 // Non-transposed A with an optional second contraction segment and output scale.
 template <int BM, int BN, int BK, bool B_T>
 hipError_t launch_bf16(const GemmArgs& g, hipStream_t s) {
@@ -620,3 +701,28 @@ hipError_t launch_gemm(const GemmArgs& g0, int a_t, int b_t, int epi, hipStream_
   return launch_cfg<128, 128, 32>(g, a_t, b_t, epi, s);
 }
 
+// One tile shape for every group: 192 x 192 when all of them are multiples of
+// 192 in both output dimensions (the weight-gradient tile of gemm_config),
+// else 128 x 128. Each group's operands (plus the up to 256 rows a tile may
+// address past their end) must stay within 32-bit byte offsets.
+static bool grouped_uses_192(const GemmGroupedArgs& gg) {
+  for (int i = 0; i < gg.ngroups; ++i)
+    if (gg.grp[i].M % 192 || gg.grp[i].N % 192) return false;
+  return true;
+}
+
+int gemm_grouped_bias_parts(const GemmGroupedArgs& gg, int i) {
+  const int bn = grouped_uses_192(gg) ? 192 : 128;
+  return ((gg.grp[i].N + bn - 1) / bn) * 2;
+}
+
+hipError_t launch_gemm_grouped(const GemmGroupedArgs& gg, hipStream_t s) {
+  if (gg.ngroups < 1 || gg.ngroups > GEMM_GROUPS || gg.K < 1) return hipErrorInvalidValue;
+  for (int i = 0; i < gg.ngroups; ++i) {
+    const GemmGroup& gr = gg.grp[i];
+    if (!gr.A || !gr.B || !gr.C || gr.M < 1 || gr.N < 1 || gr.count < 1 || gr.N % 4) return hipErrorInvalidValue;
+    if ((size_t)(gg.K + 256) * gr.lda * 2 >= (1ull << 32) || (size_t)(gg.K + 256) * gr.ldb * 2 >= (1ull << 32))
+      return hipErrorInvalidValue;
+  }
+  return grouped_uses_192(gg) ? launch_grouped_t<192, 192, 32>(gg, s) : launch_grouped_t<128, 128, 32>(gg, s);
+}

@@ -153,6 +153,14 @@ struct ActLayout {
 struct WsLayout {
   size_t dres, dh, datt, dbig, dsum, splitk, bsum, lnpart, sumsq, normcoef, total;
   size_t splitk_elems, bsum_elems;
+  // the training backward keeps every layer's output gradients until one
+  // grouped launch computes all block weight gradients: residual-stream
+  // gradients [2L+1][BT][C] (slot 2l+2 enters block l, 2l+1 is after its MLP
+  // branch, 2l leaves it), MLP pre-activation gradients [L][BT][F], q|k|v
+  // gradients [L][BT][3C], and the bias partial sums of the q|k|v and MLP-up
+  // groups
+  size_t dres_l, dfc_l, dqkv_l, gbs_qkv, gbs_fc;
+  size_t s_dres, s_dfc, s_dqkv;
 };
 
 ActLayout act_layout(const Dims& d) {
@@ -188,6 +196,23 @@ ActLayout act_layout(const Dims& d) {
   return a;
 }
 
+// The four groups of the grouped weight-gradient launch, shapes only (the
+// pointers are filled in by the backward): q|k|v [3C, C], attention
+// projection [C, C], MLP up [F, C], MLP down [C, F], each over the L layers.
+enum { G_QKV, G_ATTPROJ, G_FC, G_FCPROJ };
+GemmGroupedArgs dw_groups(const Dims& d) {
+  GemmGroupedArgs g{};
+  g.ngroups = 4;
+  g.K = (int)d.BT;
+  const int mn[4][2] = {{3 * d.C, d.C}, {d.C, d.C}, {d.F, d.C}, {d.C, d.F}};
+  for (int i = 0; i < 4; ++i) {
+    g.grp[i].M = mn[i][0];
+    g.grp[i].N = mn[i][1];
+    g.grp[i].count = d.L;
+  }
+  return g;
+}
+
 WsLayout ws_layout(const Dims& d) {
   WsLayout w{};
   const size_t BT = d.BT, C = d.C, F = d.F;
@@ -220,6 +245,15 @@ WsLayout ws_layout(const Dims& d) {
   w.lnpart = o; o += align_up((size_t)layernorm_bwd_blocks((int)BT) * 3 * C * 4);
   w.sumsq = o; o += align_up((size_t)sumsq_parts() * 4);
   w.normcoef = o; o += ALIGN;
+  w.s_dres = align_up(BT * C * 2);
+  w.s_dfc = align_up(BT * F * 2);
+  w.s_dqkv = align_up(BT * 3 * C * 2);
+  w.dres_l = o; o += (2 * (size_t)d.L + 1) * w.s_dres;
+  w.dfc_l = o; o += (size_t)d.L * w.s_dfc;
+  w.dqkv_l = o; o += (size_t)d.L * w.s_dqkv;
+  const GemmGroupedArgs gg = dw_groups(d);
+  w.gbs_qkv = o; o += align_up((size_t)gemm_grouped_bias_parts(gg, G_QKV) * d.L * 3 * C * 4);
+  w.gbs_fc = o; o += align_up((size_t)gemm_grouped_bias_parts(gg, G_FC) * d.L * F * 4);
   w.total = o;
   return w;
 }
@@ -264,7 +298,10 @@ struct gpt2_model {
   float* lnfr() { return reinterpret_cast<float*>(A(act.lnf_rstd)); }
   bf16_t* logits() { return reinterpret_cast<bf16_t*>(A(act.logits)); }
   float* losses() { return reinterpret_cast<float*>(A(act.losses)); }
+  // loss_mean()[0]: mean loss; [1]: the id-range flag bits moved there with it
   float* loss_mean() { return reinterpret_cast<float*>(A(act.loss_mean)); }
+  // live id-range flag (bits ID_BAD_INPUT, ID_BAD_TARGET), in the same slot
+  uint32_t* id_flag() { return reinterpret_cast<uint32_t*>(A(act.loss_mean + 64)); }
   int32_t* ids() { return reinterpret_cast<int32_t*>(A(act.ids)); }
   bf16_t* wsb(size_t off) { return reinterpret_cast<bf16_t*>(W(off)); }
   float* wsf(size_t off) { return reinterpret_cast<float*>(W(off)); }
@@ -370,16 +407,17 @@ hipError_t ln_fwd(Model* m, const bf16_t* x, const float* w, const float* b, bf1
                 [&] { return launch_layernorm_fwd(x, w, b, y, mean, rstd, BT, C, m->cfg.ln_eps, m->stream); });
 }
 
-// LayerNorm backward into the residual-stream gradient; also writes the gain
-// and shift gradients and, when dbias is given, the column sum of the new
-// residual gradient (the bias gradient of the projection that produced it).
+// LayerNorm backward into the residual-stream gradient: dres_out = (has_res ?
+// dres_in : 0) + dx; also writes the gain and shift gradients and, when dbias
+// is given, the column sum of the new residual gradient (the bias gradient of
+// the projection that produced it).
 hipError_t ln_bwd(Model* m, const bf16_t* dy, const bf16_t* x, const float* mean, const float* rstd, const float* w,
-                  int has_res, float* dw, float* db, float* dbias, int accumulate) {
+                  const bf16_t* dres_in, bf16_t* dres_out, int has_res, float* dw, float* db, float* dbias,
+                  int accumulate) {
   const int BT = (int)m->d.BT, C = m->d.C;
   float* part = m->wsf(m->ws.lnpart);
-  bf16_t* dres = m->wsb(m->ws.dres);
   hipError_t e = m->run(GPT2_K_LAYERNORM, 0.0, 2.0 * BT * C * (3 + has_res) + 8.0 * BT, [&] {
-    return launch_layernorm_bwd(dy, x, mean, rstd, w, dres, has_res, part, BT, C, m->stream);
+    return launch_layernorm_bwd(dy, x, mean, rstd, w, dres_in, dres_out, has_res, part, BT, C, m->stream);
   });
   if (e != hipSuccess) return e;
   int nb = layernorm_bwd_blocks(BT);
@@ -388,11 +426,11 @@ hipError_t ln_bwd(Model* m, const bf16_t* dy, const bf16_t* x, const float* mean
   });
 }
 
-AttnArgs attn_args(Model* m, int slot) {
+AttnArgs attn_args(Model* m, int slot, bf16_t* dqkv = nullptr) {
   AttnArgs a{};
   a.B = m->d.B; a.T = m->d.T; a.H = m->d.H; a.hd = m->d.hd;
   a.qkv = m->qkv(slot); a.out = m->att(slot); a.lse = m->lse(slot);
-  a.dout = m->wsb(m->ws.datt); a.dsum = m->wsf(m->ws.dsum); a.dqkv = m->wsb(m->ws.dbig);
+  a.dout = m->wsb(m->ws.datt); a.dsum = m->wsf(m->ws.dsum); a.dqkv = dqkv ? dqkv : m->wsb(m->ws.dbig);
   return a;
 }
 
@@ -424,41 +462,109 @@ gpt2_status block_fwd(Model* m, int l, int in, int out, int a) {
   return GPT2_OK;
 }
 
-// Backward of block l. The residual-stream gradient enters in dres. When
-// fcproj_bias_done, the MLP output bias gradient (the column sum of dres) was
-// already produced by the LayerNorm backward that wrote dres. When
-// write_prev_bias, the column sum of the outgoing dres is the MLP output bias
-// gradient of block l-1.
-gpt2_status block_bwd(Model* m, int l, int acc, bool fcproj_bias_done, bool write_prev_bias) {
+// Gradient buffers of one block's backward: the residual-stream gradient
+// entering the block (at its output), after its MLP branch, and leaving it
+// (at its input); the MLP pre-activation gradient and the q|k|v gradient.
+// They may alias (the single-block path runs in place).
+struct BlockGrads {
+  bf16_t *dres_out, *dres_mid, *dres_in, *dfc, *dqkv;
+};
+
+BlockGrads grads_in_place(Model* m) {
+  bf16_t* dres = m->wsb(m->ws.dres);
+  bf16_t* dbig = m->wsb(m->ws.dbig);
+  return {dres, dres, dres, dbig, dbig};
+}
+
+// the per-layer buffers the training backward keeps for the grouped
+// weight-gradient launch
+BlockGrads grads_of_layer(Model* m, int l) {
+  const WsLayout& w = m->ws;
+  return {m->wsb(w.dres_l + (size_t)(2 * l + 2) * w.s_dres), m->wsb(w.dres_l + (size_t)(2 * l + 1) * w.s_dres),
+          m->wsb(w.dres_l + (size_t)(2 * l) * w.s_dres), m->wsb(w.dfc_l + (size_t)l * w.s_dfc),
+          m->wsb(w.dqkv_l + (size_t)l * w.s_dqkv)};
+}
+
+// Backward of block l from the residual-stream gradient in gb.dres_out. When
+// fcproj_bias_done, the MLP output bias gradient (the column sum of dres_out)
+// was already produced by the LayerNorm backward that wrote it. When
+// write_prev_bias, the column sum of the outgoing gradient is the MLP output
+// bias gradient of block l-1. With defer_dw the four weight gradients (and
+// the q|k|v and MLP-up bias gradients) are left to the grouped launch.
+gpt2_status block_bwd(Model* m, int l, int acc, bool fcproj_bias_done, bool write_prev_bias, const BlockGrads& gb,
+                      bool defer_dw) {
   const Dims& d = m->d;
   const int BT = (int)d.BT, C = d.C, F = d.F;
   const size_t oC = (size_t)l * C, o3C = (size_t)l * 3 * C, oF = (size_t)l * F;
-  bf16_t* dres = m->wsb(m->ws.dres);
   bf16_t* dh = m->wsb(m->ws.dh);
   bf16_t* datt = m->wsb(m->ws.datt);
-  bf16_t* dbig = m->wsb(m->ws.dbig);
   // MLP down projection; GELU backward fused into the input-gradient epilogue
-  TRY(gemm(m, GPT2_K_GEMM_DX, BT, F, C, dres, C, 0, m->pb(K_FCPROJW) + oC * F, F, 1, EPI_GELU_BWD, dbig, F, nullptr,
-           nullptr, nullptr, m->fc(l)));
-  TRY(weight_grad(m, C, F, dres, m->gelu(l), m->gf(K_FCPROJW) + oC * F, acc, 0,
-                  fcproj_bias_done ? nullptr : m->gf(K_FCPROJB) + oC));
+  TRY(gemm(m, GPT2_K_GEMM_DX, BT, F, C, gb.dres_out, C, 0, m->pb(K_FCPROJW) + oC * F, F, 1, EPI_GELU_BWD, gb.dfc, F,
+           nullptr, nullptr, nullptr, m->fc(l)));
+  if (!defer_dw)
+    TRY(weight_grad(m, C, F, gb.dres_out, m->gelu(l), m->gf(K_FCPROJW) + oC * F, acc, 0,
+                    fcproj_bias_done ? nullptr : m->gf(K_FCPROJB) + oC));
   // MLP up projection
-  TRY(gemm(m, GPT2_K_GEMM_DX, BT, C, F, dbig, F, 0, m->pb(K_FCW) + oF * C, C, 1, EPI_BF16, dh, C));
-  TRY(weight_grad(m, F, C, dbig, m->ln2(l), m->gf(K_FCW) + oF * C, acc, 0, m->gf(K_FCB) + oF));
-  TRY(ln_bwd(m, dh, m->xmid(l), m->ln2m(l), m->ln2r(l), m->pf(K_LN2W) + oC, 1, m->gf(K_LN2W) + oC,
-             m->gf(K_LN2B) + oC, m->gf(K_ATTPROJB) + oC, acc));
+  TRY(gemm(m, GPT2_K_GEMM_DX, BT, C, F, gb.dfc, F, 0, m->pb(K_FCW) + oF * C, C, 1, EPI_BF16, dh, C));
+  if (!defer_dw) TRY(weight_grad(m, F, C, gb.dfc, m->ln2(l), m->gf(K_FCW) + oF * C, acc, 0, m->gf(K_FCB) + oF));
+  TRY(ln_bwd(m, dh, m->xmid(l), m->ln2m(l), m->ln2r(l), m->pf(K_LN2W) + oC, gb.dres_out, gb.dres_mid, 1,
+             m->gf(K_LN2W) + oC, m->gf(K_LN2B) + oC, m->gf(K_ATTPROJB) + oC, acc));
   // attention output projection (its bias gradient came from the LayerNorm above)
-  TRY(gemm(m, GPT2_K_GEMM_DX, BT, C, C, dres, C, 0, m->pb(K_ATTPROJW) + oC * C, C, 1, EPI_BF16, datt, C));
-  TRY(weight_grad(m, C, C, dres, m->att(l), m->gf(K_ATTPROJW) + oC * C, acc));
+  TRY(gemm(m, GPT2_K_GEMM_DX, BT, C, C, gb.dres_mid, C, 0, m->pb(K_ATTPROJW) + oC * C, C, 1, EPI_BF16, datt, C));
+  if (!defer_dw) TRY(weight_grad(m, C, C, gb.dres_mid, m->att(l), m->gf(K_ATTPROJW) + oC * C, acc));
   // attention
-  AttnArgs aa = attn_args(m, l);
+  AttnArgs aa = attn_args(m, l, gb.dqkv);
   TRY(m->run(GPT2_K_ATTN_BWD, 2.0 * attn_fwd_flops(d), 0.0, [&] { return launch_attention_bwd(aa, m->stream); }));
   // q|k|v projection
-  TRY(gemm(m, GPT2_K_GEMM_DX, BT, C, 3 * C, dbig, 3 * C, 0, m->pb(K_QKVW) + o3C * C, C, 1, EPI_BF16, dh, C));
-  TRY(weight_grad(m, 3 * C, C, dbig, m->ln1(l), m->gf(K_QKVW) + o3C * C, acc, 0, m->gf(K_QKVB) + o3C));
+  TRY(gemm(m, GPT2_K_GEMM_DX, BT, C, 3 * C, gb.dqkv, 3 * C, 0, m->pb(K_QKVW) + o3C * C, C, 1, EPI_BF16, dh, C));
+  if (!defer_dw)
+    TRY(weight_grad(m, 3 * C, C, gb.dqkv, m->ln1(l), m->gf(K_QKVW) + o3C * C, acc, 0, m->gf(K_QKVB) + o3C));
   float* prev_bias = (write_prev_bias && l > 0) ? m->gf(K_FCPROJB) + (size_t)(l - 1) * C : nullptr;
-  TRY(ln_bwd(m, dh, m->res(l), m->ln1m(l), m->ln1r(l), m->pf(K_LN1W) + oC, 1, m->gf(K_LN1W) + oC,
-             m->gf(K_LN1B) + oC, prev_bias, acc));
+  TRY(ln_bwd(m, dh, m->res(l), m->ln1m(l), m->ln1r(l), m->pf(K_LN1W) + oC, gb.dres_mid, gb.dres_in, 1,
+             m->gf(K_LN1W) + oC, m->gf(K_LN1B) + oC, prev_bias, acc));
+  return GPT2_OK;
+}
+
+// Every block weight gradient in one launch, from the layers' kept gradients
+// and saved activations: no contraction split, so no partial slices; then the
+// q|k|v and MLP-up bias gradients from the launch's partial sums.
+gpt2_status grouped_weight_grads(Model* m, int acc) {
+  const Dims& d = m->d;
+  const WsLayout& w = m->ws;
+  const ActLayout& a = m->act;
+  const size_t C = d.C, F = d.F;
+  GemmGroupedArgs g = dw_groups(d);
+  g.accumulate = acc;
+  GemmGroup* q = &g.grp[G_QKV];
+  q->A = m->wsb(w.dqkv_l); q->a_stride = (long)(w.s_dqkv / 2); q->lda = (int)(3 * C);
+  q->B = m->ln1(0); q->b_stride = (long)(a.s_act / 2); q->ldb = (int)C;
+  q->C = m->gf(K_QKVW); q->c_stride = (long)(3 * C * C);
+  q->bsum = m->wsf(w.gbs_qkv);
+  GemmGroup* ap = &g.grp[G_ATTPROJ];
+  ap->A = m->wsb(w.dres_l + w.s_dres); ap->a_stride = (long)(w.s_dres); ap->lda = (int)C;   // slots 2l+1
+  ap->B = m->att(0); ap->b_stride = (long)(a.s_act / 2); ap->ldb = (int)C;
+  ap->C = m->gf(K_ATTPROJW); ap->c_stride = (long)(C * C);
+  GemmGroup* fc = &g.grp[G_FC];
+  fc->A = m->wsb(w.dfc_l); fc->a_stride = (long)(w.s_dfc / 2); fc->lda = (int)F;
+  fc->B = m->ln2(0); fc->b_stride = (long)(a.s_act / 2); fc->ldb = (int)C;
+  fc->C = m->gf(K_FCW); fc->c_stride = (long)(F * C);
+  fc->bsum = m->wsf(w.gbs_fc);
+  GemmGroup* fp = &g.grp[G_FCPROJ];
+  fp->A = m->wsb(w.dres_l + 2 * w.s_dres); fp->a_stride = (long)(w.s_dres); fp->lda = (int)C;   // slots 2l+2
+  fp->B = m->gelu(0); fp->b_stride = (long)(a.s_ff / 2); fp->ldb = (int)F;
+  fp->C = m->gf(K_FCPROJW); fp->c_stride = (long)(C * F);
+  double fl = 0.0;
+  for (int i = 0; i < g.ngroups; ++i) fl += 2.0 * g.grp[i].M * (double)g.grp[i].N * d.BT * g.grp[i].count;
+  TRY(m->run(GPT2_K_GEMM_DW, fl, 0.0, [&] { return launch_gemm_grouped(g, m->stream); }));
+  const int pq = gemm_grouped_bias_parts(g, G_QKV), pf = gemm_grouped_bias_parts(g, G_FC);
+  const long nq = (long)d.L * 3 * C, nf = (long)d.L * F;
+  TRY(m->run(GPT2_K_OTHER, 0.0, 4.0 * nq * (pq + 1 + acc), [&] {
+    return launch_reduce_parts(m->wsf(w.gbs_qkv), pq, nq, (int)nq, 1, m->gf(K_QKVB), nullptr, nullptr, acc,
+                               m->stream);
+  }));
+  TRY(m->run(GPT2_K_OTHER, 0.0, 4.0 * nf * (pf + 1 + acc), [&] {
+    return launch_reduce_parts(m->wsf(w.gbs_fc), pf, nf, (int)nf, 1, m->gf(K_FCB), nullptr, nullptr, acc, m->stream);
+  }));
   return GPT2_OK;
 }
 
@@ -471,6 +577,52 @@ double lr_schedule(const gpt2_config& c, int64_t step) {
 }
 
 thread_local std::string g_last_error;
+
+// Seeded initialisation on the device (section "Model": N(0, 0.02), the two
+// projections that write into the residual stream scaled by 1/sqrt(2L);
+// biases and LayerNorm shifts 0, gains 1, padding rows of the token table 0);
+// the Adam moments are cleared and the bf16 copy written in the same pass.
+gpt2_status seeded_init(Model* m, uint64_t seed) {
+  InitArgs a{};
+  a.p = static_cast<float*>(m->buf.params_f32);
+  a.m = static_cast<float*>(m->buf.adam_m);
+  a.v = static_cast<float*>(m->buf.adam_v);
+  a.p_bf16 = static_cast<bf16_t*>(m->buf.params_bf16);
+  a.n = (long)m->n_params;
+  a.count = K_NKIND;
+  const double std = 0.02, rstd = 0.02 / std::sqrt(2.0 * m->d.L);
+  for (int k = 0; k < K_NKIND; ++k) {
+    a.end[k] = (long)(m->koff[k] + m->kn[k]);
+    const bool weight = k == K_WTE || k == K_WPE || k == K_QKVW || k == K_FCW;
+    const bool resid = k == K_ATTPROJW || k == K_FCPROJW;
+    a.std[k] = weight ? std : resid ? rstd : 0.0;
+    a.fill[k] = (k == K_LN1W || k == K_LN2W || k == K_LNFW) ? 1.0f : 0.0f;
+  }
+  a.zero_lo = (long)m->koff[K_WTE] + (long)m->d.V * m->d.C;
+  a.zero_hi = (long)m->koff[K_WTE] + (long)m->d.Vp * m->d.C;
+  a.key0 = (uint32_t)seed;
+  a.key1 = (uint32_t)(seed >> 32);
+  TRY(m->run(GPT2_K_OTHER, 0.0, 14.0 * m->n_params, [&] { return launch_init_params(a, m->stream); }));
+  return GPT2_OK;
+}
+
+// Copy the mean loss and the id-range flag moved next to it, synchronise, and
+// report ids outside [0, vocab) seen since the last report.
+gpt2_status read_loss(Model* m, float* loss_out) {
+  float host[2];
+  TRY(hipMemcpyAsync(host, m->loss_mean(), sizeof(host), hipMemcpyDeviceToHost, m->stream));
+  TRY(hipStreamSynchronize(m->stream));
+  *loss_out = host[0];
+  uint32_t bad;
+  std::memcpy(&bad, &host[1], 4);
+  if (bad)
+    return m->fail(GPT2_ERR_INVALID_ARG, std::string("token ids outside [0, vocab) in the ") +
+                                             ((bad & ID_BAD_INPUT) && (bad & ID_BAD_TARGET) ? "inputs and targets"
+                                              : (bad & ID_BAD_INPUT)                         ? "inputs"
+                                                                                             : "targets") +
+                                             " of a forward pass since the last loss: the loss is not meaningful");
+  return GPT2_OK;
+}
 
 }  // namespace
 
@@ -561,13 +713,18 @@ gpt2_status gpt2_tensor_info(const gpt2_config* cfg, int32_t idx, char* name, si
   return GPT2_OK;
 }
 
-gpt2_status gpt2_init(const gpt2_config* cfg, const gpt2_buffers* bufs, void* hip_stream, gpt2_model** out) {
+gpt2_status gpt2_init(const gpt2_config* cfg, const gpt2_buffers* bufs, void* hip_stream, uint64_t seed,
+                      int32_t init_mode, gpt2_model** out) {
   if (const char* why = validate(cfg)) {
     g_last_error = why;
     return GPT2_ERR_INVALID_ARG;
   }
   if (!bufs || !out) {
     g_last_error = "bufs or out is NULL";
+    return GPT2_ERR_INVALID_ARG;
+  }
+  if (init_mode != 0 && init_mode != 1) {
+    g_last_error = "init_mode must be 0 (caller-filled weights) or 1 (seeded initialisation)";
     return GPT2_ERR_INVALID_ARG;
   }
   const void* ptrs[7] = {bufs->params_f32, bufs->grads_f32, bufs->adam_m, bufs->adam_v,
@@ -596,7 +753,12 @@ gpt2_status gpt2_init(const gpt2_config* cfg, const gpt2_buffers* bufs, void* hi
   m->n_params = o;
   m->act = act_layout(m->d);
   m->ws = ws_layout(m->d);
-  gpt2_status st = gpt2_sync_weights(m);
+  gpt2_status st = init_mode == 1 ? seeded_init(m, seed) : gpt2_sync_weights(m);
+  // the id-range flag starts clear (a fill kernel, not a memset, so the
+  // enqueued work stays capturable)
+  if (st == GPT2_OK &&
+      launch_reduce_slices(nullptr, 0, 4, reinterpret_cast<float*>(m->id_flag()), 0, m->stream) != hipSuccess)
+    st = m->fail(GPT2_ERR_DEVICE, "clearing the id-range flag failed");
   if (st != GPT2_OK) {
     g_last_error = m->err;
     delete m;
@@ -625,7 +787,10 @@ gpt2_status gpt2_forward(gpt2_model* m, const int32_t* d_inputs, const int32_t* 
   // keep the ids for the embedding backward
   TRY(hipMemcpyAsync(m->ids(), d_inputs, (size_t)BT * 4, hipMemcpyDeviceToDevice, m->stream));
   TRY(m->run(GPT2_K_OTHER, 0.0, 4.0 * BT + 8.0 * BT * C + 2.0 * BT * C,
-             [&] { return launch_embed_fwd(d_inputs, m->pf(K_WTE), m->pf(K_WPE), m->res(0), d.B, d.T, C, m->stream); }));
+             [&] {
+               return launch_embed_fwd(d_inputs, m->pf(K_WTE), m->pf(K_WPE), m->res(0), d.B, d.T, C, d.V, m->id_flag(),
+                                       m->stream);
+             }));
   for (int l = 0; l < d.L; ++l) {
     gpt2_status s = block_fwd(m, l, l, l + 1, l);
     if (s != GPT2_OK) return s;
@@ -636,9 +801,11 @@ gpt2_status gpt2_forward(gpt2_model* m, const int32_t* d_inputs, const int32_t* 
   if (d_targets) {
     const float scale = (float)(1.0 / ((double)BT * d.accum));
     TRY(m->run(GPT2_K_CROSS_ENTROPY, 0.0, 4.0 * BT * d.Vp + 8.0 * BT, [&] {
-      return launch_cross_entropy(m->logits(), d_targets, m->losses(), BT, d.V, d.Vp, scale, 1, m->stream);
+      return launch_cross_entropy(m->logits(), d_targets, m->losses(), BT, d.V, d.Vp, scale, 1, m->id_flag(),
+                                  m->stream);
     }));
-    TRY(m->run(GPT2_K_OTHER, 0.0, 4.0 * BT, [&] { return launch_mean(m->losses(), BT, m->loss_mean(), m->stream); }));
+    TRY(m->run(GPT2_K_OTHER, 0.0, 4.0 * BT,
+               [&] { return launch_mean(m->losses(), BT, m->loss_mean(), m->stream, m->id_flag()); }));
     m->have_dlogits = true;
     m->have_loss = true;
   }
@@ -655,7 +822,10 @@ gpt2_status gpt2_evaluate(gpt2_model* m, const int32_t* d_inputs, const int32_t*
   m->have_dlogits = false;
   m->have_loss = false;
   TRY(m->run(GPT2_K_OTHER, 0.0, 4.0 * BT + 8.0 * BT * C + 2.0 * BT * C,
-             [&] { return launch_embed_fwd(d_inputs, m->pf(K_WTE), m->pf(K_WPE), m->res(0), d.B, d.T, C, m->stream); }));
+             [&] {
+               return launch_embed_fwd(d_inputs, m->pf(K_WTE), m->pf(K_WPE), m->res(0), d.B, d.T, C, d.V, m->id_flag(),
+                                       m->stream);
+             }));
   for (int l = 0; l < d.L; ++l) {
     gpt2_status s = block_fwd(m, l, l & 1, (l + 1) & 1, 0);
     if (s != GPT2_OK) return s;
@@ -664,14 +834,13 @@ gpt2_status gpt2_evaluate(gpt2_model* m, const int32_t* d_inputs, const int32_t*
   TRY(gemm(m, GPT2_K_GEMM_FWD, BT, d.Vp, C, m->lnf(), C, 0, m->pb(K_WTE), C, 0, EPI_BF16, m->logits(), d.Vp,
            nullptr, nullptr, nullptr, nullptr, 0, 1, 0, 0, 2.0 * BT * (double)d.V * C));
   TRY(m->run(GPT2_K_CROSS_ENTROPY, 0.0, 2.0 * BT * d.Vp + 8.0 * BT, [&] {
-    return launch_cross_entropy(m->logits(), d_targets, m->losses(), BT, d.V, d.Vp, 0.0f, 0, m->stream);
+    return launch_cross_entropy(m->logits(), d_targets, m->losses(), BT, d.V, d.Vp, 0.0f, 0, m->id_flag(), m->stream);
   }));
-  TRY(m->run(GPT2_K_OTHER, 0.0, 4.0 * BT, [&] { return launch_mean(m->losses(), BT, m->loss_mean(), m->stream); }));
+  TRY(m->run(GPT2_K_OTHER, 0.0, 4.0 * BT,
+             [&] { return launch_mean(m->losses(), BT, m->loss_mean(), m->stream, m->id_flag()); }));
   if (d_token_losses)
     TRY(hipMemcpyAsync(d_token_losses, m->losses(), (size_t)BT * 4, hipMemcpyDeviceToDevice, m->stream));
-  TRY(hipMemcpyAsync(loss_out, m->loss_mean(), sizeof(float), hipMemcpyDeviceToHost, m->stream));
-  TRY(hipStreamSynchronize(m->stream));
-  return GPT2_OK;
+  return read_loss(m, loss_out);
 }
 
 gpt2_status gpt2_backward(gpt2_model* m, int32_t accumulate) {
@@ -682,35 +851,42 @@ gpt2_status gpt2_backward(gpt2_model* m, int32_t accumulate) {
   const int BT = (int)d.BT, C = d.C;
   const int acc = accumulate ? 1 : 0;
   bf16_t* dh = m->wsb(m->ws.dh);
-  bf16_t* dres = m->wsb(m->ws.dres);
   // tied LM head: input gradient and the head's share of the token-table gradient
   TRY(gemm(m, GPT2_K_GEMM_DX, BT, C, d.Vp, m->logits(), d.Vp, 0, m->pb(K_WTE), C, 1, EPI_BF16, dh, C, nullptr,
            nullptr, nullptr, nullptr, 0, 1, 0, 0, 2.0 * BT * (double)d.V * C));
   TRY(weight_grad(m, d.Vp, C, m->logits(), m->lnf(), m->gf(K_WTE), acc, d.V));
-  TRY(ln_bwd(m, dh, m->res(d.L), m->lnfm(), m->lnfr(), m->pf(K_LNFW), 0, m->gf(K_LNFW), m->gf(K_LNFB),
-             m->gf(K_FCPROJB) + (size_t)(d.L - 1) * C, acc));
+  bf16_t* dres_top = grads_of_layer(m, d.L - 1).dres_out;   // written, not read (has_res 0)
+  TRY(ln_bwd(m, dh, m->res(d.L), m->lnfm(), m->lnfr(), m->pf(K_LNFW), dres_top, dres_top, 0, m->gf(K_LNFW),
+             m->gf(K_LNFB), m->gf(K_FCPROJB) + (size_t)(d.L - 1) * C, acc));
   for (int l = d.L - 1; l >= 0; --l) {
-    gpt2_status s = block_bwd(m, l, acc, true, true);
+    gpt2_status s = block_bwd(m, l, acc, true, true, grads_of_layer(m, l), true);
     if (s != GPT2_OK) return s;
   }
+  const bf16_t* dres = grads_of_layer(m, 0).dres_in;
   // embedding: scatter into the token table (after the head's share), sum into positions
   TRY(m->run(GPT2_K_OTHER, 0.0, 4.0 * BT + 2.0 * BT * C + 8.0 * BT * C,
-             [&] { return launch_embed_bwd(m->ids(), dres, m->gf(K_WTE), d.B, d.T, C, m->stream); }));
+             [&] { return launch_embed_bwd(m->ids(), dres, m->gf(K_WTE), d.B, d.T, C, d.V, m->stream); }));
   TRY(m->run(GPT2_K_OTHER, 0.0, 2.0 * BT * C + 4.0 * d.Tmax * C * (1 + acc),
              [&] { return launch_embed_bwd_pos(dres, m->gf(K_WPE), d.B, d.T, d.Tmax, C, acc, m->stream); }));
+  {
+    gpt2_status s = grouped_weight_grads(m, acc);
+    if (s != GPT2_OK) return s;
+  }
   m->have_grads = true;
   return GPT2_OK;
 }
 
-gpt2_status gpt2_adamw_step(gpt2_model* m, int64_t step, float* lr_out, float* d_grad_norm_out) {
-  if (!m) return GPT2_ERR_INVALID_ARG;
-  if (step < 0) return m->fail(GPT2_ERR_INVALID_ARG, "step must be >= 0");
-  if (!m->have_grads) return m->fail(GPT2_ERR_STATE, "optimizer step with no gradient");
+}  // extern "C"
+
+namespace {
+
+// The optimizer step with its scratch (sum-of-squares partials, norm and clip
+// coefficient) at the given device addresses.
+gpt2_status adamw_step_with(gpt2_model* m, int64_t step, float* lr_out, float* d_grad_norm_out, float* parts,
+                            float* nc) {
   const gpt2_config& c = m->cfg;
   const long n = (long)m->n_params;
   float* grads = static_cast<float*>(m->buf.grads_f32);
-  float* parts = m->wsf(m->ws.sumsq);
-  float* nc = m->wsf(m->ws.normcoef);
   TRY(m->run(GPT2_K_OPTIMIZER, 0.0, 4.0 * n, [&] { return launch_sumsq(grads, n, parts, m->stream); }));
   TRY(m->run(GPT2_K_OPTIMIZER, 0.0, 4.0 * sumsq_parts(),
              [&] { return launch_clip_coef(parts, sumsq_parts(), c.grad_clip, nc, m->stream); }));
@@ -740,13 +916,24 @@ gpt2_status gpt2_adamw_step(gpt2_model* m, int64_t step, float* lr_out, float* d
   return GPT2_OK;
 }
 
-gpt2_status gpt2_loss(gpt2_model* m, float* loss_out) {
+}  // namespace
+
+extern "C" {
+
+gpt2_status gpt2_adamw_step(gpt2_model* m, int64_t step, float* lr_out, float* d_grad_norm_out) {
+  if (!m) return GPT2_ERR_INVALID_ARG;
+  if (step < 0) return m->fail(GPT2_ERR_INVALID_ARG, "step must be >= 0");
+  if (!m->have_grads) return m->fail(GPT2_ERR_STATE, "optimizer step with no gradient");
+  return adamw_step_with(m, step, lr_out, d_grad_norm_out, m->wsf(m->ws.sumsq), m->wsf(m->ws.normcoef));
+}
+
+gpt2_status gpt2_loss(gpt2_model* m, float* loss_out, float* d_token_losses) {
   if (!m) return GPT2_ERR_INVALID_ARG;
   if (!loss_out) return m->fail(GPT2_ERR_INVALID_ARG, "loss_out is NULL");
   if (!m->have_loss) return m->fail(GPT2_ERR_STATE, "no forward with targets yet");
-  TRY(hipMemcpyAsync(loss_out, m->loss_mean(), sizeof(float), hipMemcpyDeviceToHost, m->stream));
-  TRY(hipStreamSynchronize(m->stream));
-  return GPT2_OK;
+  if (d_token_losses)
+    TRY(hipMemcpyAsync(d_token_losses, m->losses(), (size_t)m->d.BT * 4, hipMemcpyDeviceToDevice, m->stream));
+  return read_loss(m, loss_out);
 }
 
 float gpt2_lr_at(const gpt2_config* cfg, int64_t step) {
@@ -817,7 +1004,7 @@ gpt2_status gpt2_block_backward(gpt2_model* m, int32_t layer, const void* d_dx_o
   const size_t bytes = (size_t)m->d.BT * m->d.C * 2;
   bf16_t* dres = m->wsb(m->ws.dres);
   TRY(hipMemcpyAsync(dres, d_dx_out, bytes, hipMemcpyDeviceToDevice, m->stream));
-  gpt2_status s = block_bwd(m, layer, accumulate ? 1 : 0, false, false);
+  gpt2_status s = block_bwd(m, layer, accumulate ? 1 : 0, false, false, grads_in_place(m), false);
   if (s != GPT2_OK) return s;
   if (d_dx_in) TRY(hipMemcpyAsync(d_dx_in, dres, bytes, hipMemcpyDeviceToDevice, m->stream));
   return GPT2_OK;
@@ -832,7 +1019,7 @@ gpt2_status gpt2_embedding_backward(gpt2_model* m, const int32_t* d_ids, const v
   if (!acc)  // zero-slice reduction writes zeros
     TRY(launch_reduce_slices(nullptr, 0, (long)m->kn[K_WTE], m->gf(K_WTE), 0, m->stream));
   TRY(m->run(GPT2_K_OTHER, 0.0, 4.0 * d.BT + 10.0 * d.BT * d.C,
-             [&] { return launch_embed_bwd(d_ids, dx, m->gf(K_WTE), d.B, d.T, d.C, m->stream); }));
+             [&] { return launch_embed_bwd(d_ids, dx, m->gf(K_WTE), d.B, d.T, d.C, d.V, m->stream); }));
   TRY(m->run(GPT2_K_OTHER, 0.0, 2.0 * d.BT * d.C + 4.0 * d.Tmax * d.C * (1 + acc),
              [&] { return launch_embed_bwd_pos(dx, m->gf(K_WPE), d.B, d.T, d.Tmax, d.C, acc, m->stream); }));
   return GPT2_OK;

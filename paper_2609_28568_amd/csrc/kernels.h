@@ -52,7 +52,39 @@ struct GemmArgs {
   // read B from b_step columns further right per bound passed, so row blocks
   // of the output can contract with different column blocks of B.
   int b_bound[2], b_step;
+  // row stride of the bsum partial rows (0: M)
+  int bsum_ld;
 };
+
+// Grouped weight gradients: launch_gemm_grouped runs, in one launch, every
+// tile of up to GEMM_GROUPS groups of products C_p[m][n] (=|+=) sum_k A_p[k][m]
+// B_p[k][n] (A and B read transposed, fp32 output, contraction length K
+// shared by all). Group i holds `count` products of the same M x N whose
+// operands and outputs sit at fixed element strides from the group's first
+// one (C_p row stride N). With bsum, product p also writes the partial sums of
+// A_p's rows (its bias gradient) into rows [slot][p][M] of bsum, slot <
+// gemm_bias_parts(M, N, 1); summing over slots gives the bias gradients of
+// the group's products, stored one after another.
+constexpr int GEMM_GROUPS = 4;
+struct GemmGroup {
+  const bf16_t* A;
+  const bf16_t* B;
+  float* C;
+  float* bsum;
+  long a_stride, b_stride, c_stride;
+  int M, N, lda, ldb;
+  int count;
+};
+struct GemmGroupedArgs {
+  GemmGroup grp[GEMM_GROUPS];
+  int ngroups;
+  int K;
+  int accumulate;
+};
+hipError_t launch_gemm_grouped(const GemmGroupedArgs& g, hipStream_t s);
+// Partial rows (slots) a grouped launch writes for group i's bias sums; it
+// depends only on the groups' M and N
+int gemm_grouped_bias_parts(const GemmGroupedArgs& g, int i);
 
 // Block tile (bm x bn, contraction depth bk per stage) the GEMM uses for an
 // M x N product with the given operand orientation and epilogue.
@@ -87,14 +119,15 @@ hipError_t launch_attention_bwd(const AttnArgs& a, hipStream_t s);
 // ---------------------------------------------------------------- layernorm
 hipError_t launch_layernorm_fwd(const bf16_t* x, const float* w, const float* b, bf16_t* y,
                                 float* mean, float* rstd, int rows, int C, float eps, hipStream_t s);
-// dres (in/out; only written when has_res == 0): dres = (has_res ? dres : 0) + dx.
+// dres_out = (has_res ? dres_in : 0) + dx (dres_in may be dres_out; it is not
+// read when has_res == 0).
 // Each block writes one row of partials part[blk][3][C]: sums over its rows of
 // dy*xhat (gain gradient), dy (shift gradient) and the new dres (the bias
 // gradient of the linear layer whose output gradient dres is).
 int layernorm_bwd_blocks(int rows);
 hipError_t launch_layernorm_bwd(const bf16_t* dy, const bf16_t* x, const float* mean,
-                                const float* rstd, const float* w, bf16_t* dres, int has_res,
-                                float* part, int rows, int C, hipStream_t s);
+                                const float* rstd, const float* w, const bf16_t* dres_in, bf16_t* dres_out,
+                                int has_res, float* part, int rows, int C, hipStream_t s);
 
 // ---------------------------------------------------------------- misc
 // dst[i] (fp32, n elements) = (accumulate ? dst[i] : 0) + sum_s src[s*n + i]
@@ -110,10 +143,15 @@ hipError_t launch_reduce_slices2(const float* src, int nslices, long n, float* d
 // destinations, null ones skipped) and c < n. Fixed summation order.
 hipError_t launch_reduce_parts(const float* part, int S, long stride, int n, int nd, float* d0, float* d1,
                                float* d2, int accumulate, hipStream_t s);
+// Token ids outside [0, V) are a caller's contract violation: the kernels
+// that read ids (embedding forward, cross-entropy target gather) read row 0
+// in their place and set bit ID_BAD_INPUT or ID_BAD_TARGET of *bad (when bad
+// is not null); the embedding backward skips them.
+constexpr uint32_t ID_BAD_INPUT = 1u, ID_BAD_TARGET = 2u;
 hipError_t launch_embed_fwd(const int32_t* ids, const float* wte, const float* wpe, bf16_t* x, int B,
-                            int T, int C, hipStream_t s);
+                            int T, int C, int V, uint32_t* bad, hipStream_t s);
 // dwte[ids[r]] += dx[r] (fp32 atomics; adds to what is there)
-hipError_t launch_embed_bwd(const int32_t* ids, const bf16_t* dx, float* dwte, int B, int T, int C,
+hipError_t launch_embed_bwd(const int32_t* ids, const bf16_t* dx, float* dwte, int B, int T, int C, int V,
                             hipStream_t s);
 // dwpe[t] = (accumulate ? dwpe[t] : 0) + sum_b dx[b, t] for t < T; rows T..Tmax-1 get 0 added
 hipError_t launch_embed_bwd_pos(const bf16_t* dx, float* dwpe, int B, int T, int Tmax, int C,
@@ -123,9 +161,10 @@ hipError_t launch_embed_bwd_pos(const bf16_t* dx, float* dwpe, int B, int T, int
 // (scaled) overwrite the logits; losses fp32 [rows]
 // write_grad: overwrite the logits with dlogits (training) or leave them
 hipError_t launch_cross_entropy(bf16_t* logits, const int32_t* targets, float* losses, int rows, int V, int Vp,
-                                float grad_scale, int write_grad, hipStream_t s);
-// mean of n floats into out[0] (single block, fixed order)
-hipError_t launch_mean(const float* x, int n, float* out, hipStream_t s);
+                                float grad_scale, int write_grad, uint32_t* bad, hipStream_t s);
+// mean of n floats into out[0] (single block, fixed order); with flag (not
+// null), also moves *flag into out[1] (its bits) and clears *flag
+hipError_t launch_mean(const float* x, int n, float* out, hipStream_t s, uint32_t* flag = nullptr);
 // out[0] = scale * sum of x[0..n)
 hipError_t launch_sum_scaled(const float* x, int n, float scale, float* out, hipStream_t s);
 // Cross-entropy over the rows of the positions that carry loss (t >= mask_from
@@ -133,7 +172,8 @@ hipError_t launch_sum_scaled(const float* x, int n, float scale, float* out, hip
 // p = (i / n) T + mask_from + i % n, n = T - mask_from, whose target and loss
 // are targets[p] and losses[p]; the losses of the other positions are set to 0.
 hipError_t launch_cross_entropy_masked(bf16_t* logits, const int32_t* targets, float* losses, int rows, int V, int Vp,
-                                       float grad_scale, int write_grad, int T, int mask_from, hipStream_t s);
+                                       float grad_scale, int write_grad, int T, int mask_from, hipStream_t s,
+                                       uint32_t* bad = nullptr);
 
 // ---------------------------------------------------------------- Qwen3-shaped adapter step
 hipError_t launch_embed_gather(const int32_t* ids, const bf16_t* table, bf16_t* x, long rows, int C, hipStream_t s);
@@ -166,6 +206,28 @@ hipError_t launch_scale_bf16(bf16_t* x, long rows, int cols, int ld, float sc, h
 // fp32 -> bf16 copy of n elements (n % 4 == 0)
 hipError_t launch_cast_bf16(const float* src, bf16_t* dst, long n, hipStream_t s);
 
+// Seeded initialisation of a flat fp32 parameter buffer from the counter-based
+// generator Philox4x32-10 (Salmon et al., SC 2011): element i takes counter
+// (i mod 2^32, i div 2^32, 0, 0) and key (key0, key1); its first two output
+// words give a standard normal by the Box-Muller transform (in fp64). Element
+// i of segment k (ending at end[k], exclusive) becomes std[k] * normal when
+// std[k] > 0, else fill[k]; elements in [zero_lo, zero_hi) become 0. Adam
+// moments m, v are cleared and the bf16 copy written. n % 4 == 0.
+struct InitArgs {
+  float* p;
+  float* m;
+  float* v;
+  bf16_t* p_bf16;
+  long n;
+  long end[16];
+  double std[16];
+  float fill[16];
+  int count;
+  long zero_lo, zero_hi;
+  uint32_t key0, key1;
+};
+hipError_t launch_init_params(const InitArgs& a, hipStream_t s);
+
 // ---------------------------------------------------------------- optimizer
 int sumsq_parts();
 hipError_t launch_sumsq(const float* g, long n, float* parts, hipStream_t s);
@@ -191,3 +253,4 @@ struct AdamArgs {
   AdamSegments seg;
 };
 hipError_t launch_adamw(const AdamArgs& a, hipStream_t s);
+

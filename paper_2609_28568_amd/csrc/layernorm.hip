@@ -71,12 +71,14 @@ __global__ __launch_bounds__(256) void ln_fwd_kernel(const bf16_t* __restrict__ 
 }
 
 // dx = rstd * (g - mean(g) - xhat * mean(g * xhat)), g = dy * w; the result is
-// added to the residual-stream gradient. Per-block sums of dy*xhat and dy.
+// added to the residual-stream gradient read from dres_in and written to
+// dres_out (the two may be the same buffer: each row is read before it is
+// written, by the same wave). Per-block sums of dy*xhat and dy.
 template <int MAXCH>
 __global__ __launch_bounds__(256) void ln_bwd_kernel(const bf16_t* __restrict__ dy, const bf16_t* __restrict__ x,
                                                      const float* __restrict__ mean_in,
                                                      const float* __restrict__ rstd_in, const float* __restrict__ w,
-                                                     bf16_t* __restrict__ dres, int has_res,
+                                                     const bf16_t* dres_in, bf16_t* dres_out, int has_res,
                                                      float* __restrict__ part, int rows, int C) {
   __shared__ float red[4][MAXCH * 4 * 64];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -100,7 +102,7 @@ __global__ __launch_bounds__(256) void ln_bwd_kernel(const bf16_t* __restrict__ 
     sl = rstd_in[row];
     const bf16_t* xr = x + (size_t)row * C;
     const bf16_t* dr = dy + (size_t)row * C;
-    const bf16_t* rr = dres + (size_t)row * C;
+    const bf16_t* rr = dres_in + (size_t)row * C;
     // all loads issued at once (no branch per chunk): chunks past C read the
     // row's last chunk and are never used
 #pragma unroll
@@ -138,7 +140,7 @@ __global__ __launch_bounds__(256) void ln_bwd_kernel(const bf16_t* __restrict__ 
       }
     }
     const float gm = wave_sum(s1) / C, gxm = wave_sum(s2) / C;
-    bf16_t* rr = dres + (size_t)row * C;
+    bf16_t* rr = dres_out + (size_t)row * C;
 #pragma unroll
     for (int i = 0; i < MAXCH; ++i) {
       int c = 4 * (lane + 64 * i);
@@ -193,9 +195,9 @@ hipError_t fwd_t(const bf16_t* x, const float* w, const float* b, bf16_t* y, flo
 
 template <int MAXCH>
 hipError_t bwd_t(const bf16_t* dy, const bf16_t* x, const float* mean, const float* rstd, const float* w,
-                 bf16_t* dres, int has_res, float* part, int rows, int C, hipStream_t s) {
+                 const bf16_t* dres_in, bf16_t* dres_out, int has_res, float* part, int rows, int C, hipStream_t s) {
   hipLaunchKernelGGL(ln_bwd_kernel<MAXCH>, dim3(layernorm_bwd_blocks(rows)), dim3(256), 0, s, dy, x, mean, rstd, w,
-                     dres, has_res, part, rows, C);
+                     dres_in, dres_out, has_res, part, rows, C);
   return hipGetLastError();
 }
 
@@ -222,13 +224,13 @@ int layernorm_bwd_blocks(int rows) {
 }
 
 hipError_t launch_layernorm_bwd(const bf16_t* dy, const bf16_t* x, const float* mean, const float* rstd,
-                                const float* w, bf16_t* dres, int has_res, float* part, int rows, int C,
-                                hipStream_t s) {
+                                const float* w, const bf16_t* dres_in, bf16_t* dres_out, int has_res, float* part,
+                                int rows, int C, hipStream_t s) {
   if (C % 4) return hipErrorInvalidValue;
-  if (C <= 256) return bwd_t<1>(dy, x, mean, rstd, w, dres, has_res, part, rows, C, s);
-  if (C <= 512) return bwd_t<2>(dy, x, mean, rstd, w, dres, has_res, part, rows, C, s);
-  if (C <= 768) return bwd_t<3>(dy, x, mean, rstd, w, dres, has_res, part, rows, C, s);
-  if (C <= 1024) return bwd_t<4>(dy, x, mean, rstd, w, dres, has_res, part, rows, C, s);
-  if (C <= 2048) return bwd_t<8>(dy, x, mean, rstd, w, dres, has_res, part, rows, C, s);
+  if (C <= 256) return bwd_t<1>(dy, x, mean, rstd, w, dres_in, dres_out, has_res, part, rows, C, s);
+  if (C <= 512) return bwd_t<2>(dy, x, mean, rstd, w, dres_in, dres_out, has_res, part, rows, C, s);
+  if (C <= 768) return bwd_t<3>(dy, x, mean, rstd, w, dres_in, dres_out, has_res, part, rows, C, s);
+  if (C <= 1024) return bwd_t<4>(dy, x, mean, rstd, w, dres_in, dres_out, has_res, part, rows, C, s);
+  if (C <= 2048) return bwd_t<8>(dy, x, mean, rstd, w, dres_in, dres_out, has_res, part, rows, C, s);
   return hipErrorInvalidValue;
 }

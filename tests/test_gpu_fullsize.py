@@ -8,7 +8,15 @@ configuration the benchmark times, against the oracle on sampled outputs:
   input gradient is exactly zero;
 * the full 12-layer step: per-token losses of sequences 0 and 15 against the
   one-sequence oracle; with all 16 sequences equal to sequence 0 the mean-loss
-  gradient equals the one-sequence gradient, for all 148 tensors.
+  gradient equals the one-sequence gradient, for all 148 tensors; on the
+  benchmark's 16 distinct Zipf sequences all 148 gradients against the sum of
+  16 one-sequence oracle gradients, each scaled by 1/(16*1024), and the
+  padding columns of dlogits exactly zero;
+* the embedding backward on the benchmark's 16 x 1024 Zipf ids: the set of
+  token rows touched is exactly the set of ids, and every value is within
+  the worst-case fp32 summation bound of a float64 scatter-add;
+* the accumulation configuration, including the loss of a step-2 micro-batch
+  after a full 32-micro-batch optimizer step.
 """
 import numpy as np
 import pytest
@@ -127,6 +135,85 @@ def test_gpt2_124m_gradients_replicated_batch(full_setup):
     print(f"  worst tensor rel_l2 {worst:.2e}")
 
 
+def test_gpt2_124m_gradients_distinct_sequences(full_setup):
+    """The benchmark's own batch (16 distinct Zipf sequences): the mean-loss
+    gradient is the sum over sequences of each one's gradient scaled by
+    1/(16*1024), which the oracle computes one sequence at a time. This
+    covers what a batch of equal sequences cannot: sequence offsets in the
+    split weight-gradient slices, batch offsets in the attention backward and
+    token-table scatter runs that cross wave and sort-group boundaries."""
+    w, p, ids, tgt = full_setup
+    B, T, V, Vp = w["B"], w["T"], w["vocab"], w["vocab_padded"]
+    m = _model(w)
+    m.set_params(p)
+    m.forward(torch.from_numpy(ids), torch.from_numpy(tgt))
+    loss = m.loss()
+    pad = m.activation("logits").view(B * T, Vp)[:, V:]
+    pad_nonzero = int(torch.count_nonzero(pad).item())
+    m.backward()
+    g = m.to_dict("grads")
+    m.close()
+    assert pad_nonzero == 0
+    assert np.all(g["wte"][V:] == 0.0)
+    ocfg = oracle_config(w)
+    ref = oracle.zero_grads(p)
+    losses = []
+    for b in range(B):
+        print(f"gpt2_124m: oracle forward+backward of sequence {b}", flush=True)
+        c = oracle.forward(p, ids[b:b + 1], tgt[b:b + 1], ocfg, grad_scale=1.0 / (B * T))
+        losses.append(float(c["loss"]))
+        oracle.backward(p, c, ocfg, ref)
+        del c
+    assert abs(loss - float(np.mean(losses))) < LOSS_ATOL
+    worst = 0.0
+    for k in oracle.KINDS:
+        slices = [(g[k], ref[k])] if g[k].ndim <= 1 or k in ("wte", "wpe") else list(zip(g[k], ref[k]))
+        for i, (a, r) in enumerate(slices):
+            e = rel_l2(a, r)
+            worst = max(worst, e)
+            assert e < REL_L2, (k, i, e)
+    print(f"  worst tensor rel_l2 {worst:.2e}")
+
+
+def test_gpt2_124m_embedding_backward_zipf(full_setup):
+    """Token-table scatter on the benchmark's 16 x 1024 Zipf ids (id 0 about
+    14 % of positions, so its runs cross every wave and sort group): the rows
+    touched are exactly the ids, the padding rows stay 0, and each value
+    differs from a float64 scatter-add by at most the worst-case bound of an
+    n-term fp32 sum in any order, n u / (1 - n u) times the sum of the
+    magnitudes (u = 2^-24, n the id's count)."""
+    w, p, ids, tgt = full_setup
+    B, T, C, V = w["B"], w["T"], w["d_model"], w["vocab"]
+    g = np.random.default_rng(71)
+    dx = synth.round_to_bf16(g.standard_normal((B * T, C), dtype=np.float32))
+    m = _model(w)
+    m.set_params(p)
+    m.embedding_backward(torch.from_numpy(ids), torch.from_numpy(dx).cuda().to(torch.bfloat16))
+    got = m.to_dict("grads")
+    m.close()
+    flat = ids.ravel()
+    ref = np.zeros((w["vocab_padded"], C), np.float64)
+    mag = np.zeros_like(ref)
+    np.add.at(ref, flat, dx.astype(np.float64))
+    np.add.at(mag, flat, np.abs(dx.astype(np.float64)))
+    touched = np.unique(flat)
+    rows = np.flatnonzero(np.any(got["wte"] != 0.0, axis=1))
+    assert np.array_equal(rows, touched)
+    assert np.all(got["wte"][V:] == 0.0)
+    u = 2.0 ** -24
+    n = np.bincount(flat, minlength=w["vocab_padded"]).astype(np.float64)[:, None]
+    bound = n * u / (1.0 - n * u) * mag
+    err = np.abs(got["wte"].astype(np.float64) - ref)
+    print(f"embedding backward: {touched.size} distinct ids, max count {int(n.max())}, "
+          f"max err/bound {float(np.max(err / np.maximum(bound, 1e-300))):.3f}")
+    assert np.all(err <= bound)
+    refp = dx.reshape(B, T, C).astype(np.float64).sum(axis=0)
+    magp = np.abs(dx.reshape(B, T, C).astype(np.float64)).sum(axis=0)
+    errp = np.abs(got["wpe"][:T].astype(np.float64) - refp)
+    assert np.all(errp <= B * u / (1.0 - B * u) * magp)
+    assert np.all(got["wpe"][T:] == 0.0)
+
+
 def test_gpt2_124m_evaluate_equals_forward(full_setup):
     """Forward-only evaluation at full size reuses one block's activation
     slots: its per-token losses equal the training forward's exactly."""
@@ -202,5 +289,47 @@ def test_gpt2_124m_accumulation_configuration():
         print(f"  oracle forward of sequence {b}", flush=True)
         c = oracle.forward(p, ids[b:b + 1], tgt[b:b + 1], ocfg)
         d = np.abs(losses[b] - c["losses"][0])
+        assert abs(losses[b].mean() - float(c["loss"])) < LOSS_ATOL
+        assert d.max() < 5 * LOSS_ATOL
+
+
+def test_gpt2_124m_accumulation_two_optimizer_steps():
+    """The loss trajectory of the accumulation configuration over its first
+    two optimizer steps: step 1 accumulates all 32 micro-batches, clips and
+    takes AdamW at lr_0; the first micro-batch of step 2 then runs on the
+    updated weights, and its per-position losses (sequences 0 and 15) match
+    the oracle's forward on the GPU's updated fp32 weights; step 2's rate is
+    the schedule's lr_1 = 2 lr_max / warmup."""
+    w = workload("gpt2_124m_accum32")
+    accum = w["grad_accum"]
+    p = synth.init_params(w)
+    m = _model(w)
+    m.set_params(p)
+    step_losses = []
+    for step in range(2):
+        mb = []
+        for k in range(accum):
+            ids, tgt = synth.token_batch(w, micro=step * accum + k)
+            m.forward(torch.from_numpy(ids), torch.from_numpy(tgt))
+            mb.append(m.loss())
+            if step == 1 and k == 0:
+                first = (ids, tgt, _np(m.activation("losses")).reshape(w["B"], w["T"]))
+                p1 = m.to_dict("params")
+            m.backward(accumulate=k > 0)
+        lr = m.adamw_step(step)
+        assert abs(lr - synth.OPTIM["lr_max"] * (step + 1) / synth.OPTIM["warmup_steps"]) < 1e-12
+        assert abs(lr - oracle.lr_at(oracle_config(w), step)) < 1e-12
+        step_losses.append(float(np.mean(mb)))
+    torch.cuda.synchronize()
+    m.close()
+    print(f"gpt2_124m_accum32: step losses {step_losses}", flush=True)
+    assert all(np.isfinite(step_losses))
+    ids, tgt, losses = first
+    ocfg = oracle_config(w)
+    for b in (0, 15):
+        print(f"  oracle forward of step-2 sequence {b} on the updated weights", flush=True)
+        c = oracle.forward(p1, ids[b:b + 1], tgt[b:b + 1], ocfg)
+        d = np.abs(losses[b] - c["losses"][0])
+        print(f"  seq {b}: gpu {losses[b].mean():.5f} oracle {float(c['loss']):.5f} max|d| {d.max():.3e}")
         assert abs(losses[b].mean() - float(c["loss"])) < LOSS_ATOL
         assert d.max() < 5 * LOSS_ATOL
