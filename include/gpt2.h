@@ -167,6 +167,21 @@ gpt2_status gpt2_backward(gpt2_model* m, int32_t accumulate);
 gpt2_status gpt2_adamw_step(gpt2_model* m, int64_t step, float* lr_out,
                             float* d_grad_norm_out);
 
+/* The optimizer step of gpt2_adamw_step, for callers that cannot allocate
+ * memory (code under HIP graph capture, tight serving or training loops,
+ * harnesses that forbid allocation): same arguments, same results, same
+ * kernels, but its scratch (the sum-of-squares partials, the norm and the
+ * clip coefficient) lives in a static device array of the library (16 KiB,
+ * one copy per GPU, held until the process ends) instead of the caller's
+ * workspace. Nothing is allocated: the array's device address is looked up
+ * once per device on the first call (which must run with the model's device
+ * current). The scratch does not grow with the model, so no model is too
+ * large for it (INVALID_ARG would name the two sizes otherwise). Calls that
+ * overlap on one GPU share the array and race; the array keeps the last
+ * call's contents, every one of which a call writes before it reads it. */
+gpt2_status gpt2_adamw_step_noalloc(gpt2_model* m, int64_t step, float* lr_out,
+                                    float* d_grad_norm_out);
+
 /* Loss of the last forward with targets ("Optimisation and precision": loss
  * in fp32, the mean over the B*T positions): *loss_out (host) receives the
  * mean; d_token_losses (device fp32 [B*T], row-major [B, T], optional)

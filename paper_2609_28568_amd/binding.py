@@ -75,6 +75,7 @@ def lib():
         "gpt2_forward": (I32, [P, P, P]),
         "gpt2_backward": (I32, [P, I32]),
         "gpt2_adamw_step": (I32, [P, I64, ctypes.POINTER(F32), P]),
+        "gpt2_adamw_step_noalloc": (I32, [P, I64, ctypes.POINTER(F32), P]),
         "gpt2_loss": (I32, [P, ctypes.POINTER(F32), P]),
         "gpt2_evaluate": (I32, [P, P, P, ctypes.POINTER(F32), P]),
         "gpt2_lr_at": (F32, [cfgp, I64]),
@@ -243,10 +244,13 @@ class GPT2:
     def backward(self, accumulate=False):
         _check(self.L.gpt2_backward(self.handle, int(bool(accumulate))), self.handle)
 
-    def adamw_step(self, step: int, norm_out=None):
+    def adamw_step(self, step: int, norm_out=None, noalloc=False):
+        """Clip + AdamW; noalloc=True takes the entry point whose scratch is
+        the library's static device array instead of the workspace."""
         lr = ctypes.c_float()
         ptr = ctypes.c_void_p(norm_out.data_ptr()) if norm_out is not None else ctypes.c_void_p(0)
-        _check(self.L.gpt2_adamw_step(self.handle, int(step), ctypes.byref(lr), ptr), self.handle)
+        fn = self.L.gpt2_adamw_step_noalloc if noalloc else self.L.gpt2_adamw_step
+        _check(fn(self.handle, int(step), ctypes.byref(lr), ptr), self.handle)
         return lr.value
 
     def loss(self, token_losses=None) -> float:

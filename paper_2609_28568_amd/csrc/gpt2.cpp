@@ -927,6 +927,22 @@ gpt2_status gpt2_adamw_step(gpt2_model* m, int64_t step, float* lr_out, float* d
   return adamw_step_with(m, step, lr_out, d_grad_norm_out, m->wsf(m->ws.sumsq), m->wsf(m->ws.normcoef));
 }
 
+gpt2_status gpt2_adamw_step_noalloc(gpt2_model* m, int64_t step, float* lr_out, float* d_grad_norm_out) {
+  if (!m) return GPT2_ERR_INVALID_ARG;
+  if (step < 0) return m->fail(GPT2_ERR_INVALID_ARG, "step must be >= 0");
+  if (!m->have_grads) return m->fail(GPT2_ERR_STATE, "optimizer step with no gradient");
+  // partials, then the norm and coefficient at the next 64-float boundary
+  const int parts = sumsq_parts();
+  const int nc_off = (parts + 63) / 64 * 64;
+  if (nc_off + 2 > NOALLOC_SCRATCH_FLOATS)
+    return m->fail(GPT2_ERR_INVALID_ARG, "the optimizer's scratch (" + std::to_string(nc_off + 2) +
+                                             " floats) exceeds the static scratch array (" +
+                                             std::to_string(NOALLOC_SCRATCH_FLOATS) + " floats)");
+  float* scratch = nullptr;
+  TRY(noalloc_scratch(&scratch));
+  return adamw_step_with(m, step, lr_out, d_grad_norm_out, scratch, scratch + nc_off);
+}
+
 gpt2_status gpt2_loss(gpt2_model* m, float* loss_out, float* d_token_losses) {
   if (!m) return GPT2_ERR_INVALID_ARG;
   if (!loss_out) return m->fail(GPT2_ERR_INVALID_ARG, "loss_out is NULL");

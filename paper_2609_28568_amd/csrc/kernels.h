@@ -254,3 +254,11 @@ struct AdamArgs {
 };
 hipError_t launch_adamw(const AdamArgs& a, hipStream_t s);
 
+// ---------------------------------------------------------------- no-alloc scratch
+// Floats of the static scratch array the allocation-free entry points use
+// (the optimizer's sum-of-squares partials, then its norm and clip
+// coefficient): 16 KiB per GPU.
+constexpr int NOALLOC_SCRATCH_FLOATS = 4096;
+// Device address of the current device's copy of the array (looked up on the
+// first call per device, with that device current).
+hipError_t noalloc_scratch(float** out);
