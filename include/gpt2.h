@@ -274,6 +274,25 @@ gpt2_status gpt2_block_backward(gpt2_model* m, int32_t layer,
 gpt2_status gpt2_embedding_backward(gpt2_model* m, const int32_t* d_ids,
                                     const void* d_dx, int32_t accumulate);
 
+/* Alternative kernel arrangements of the same computation, for measuring
+ * the fusions the paper reports trying (section "Speed", table of levers),
+ * each checked against the arrangement it replaces:
+ *   GPT2_FUSION_RESIDUAL_NORM, how a residual connection meets the pre-norm
+ *   after it (the paper's fused residual-and-pre-norm lever):
+ *     0 (default) the projection GEMM's epilogue adds the residual and the
+ *       LayerNorm reads the sum;
+ *     1 the projection writes its branch, one kernel forms the rounded sum
+ *       and normalises it;
+ *     2 the composed path: a separate addition kernel, then the LayerNorm.
+ *     Modes 1 and 2 give bit-identical activations (the paper's gate: the
+ *     fused residual sum must equal the composed addition exactly).
+ * The mode applies from the next forward pass on; the backward reads only the
+ * saved activations. INVALID_ARG for an unknown fusion or mode. */
+typedef enum gpt2_fusion {
+  GPT2_FUSION_RESIDUAL_NORM = 0
+} gpt2_fusion;
+gpt2_status gpt2_set_fusion(gpt2_model* m, int32_t fusion, int32_t mode);
+
 /* Kernel timing probes for measurement, per stage in the manner of the
  * paper's stage table (section "Speed"). Kernels are grouped in classes; for
  * classes in the enabled mask, every launch is bracketed by HIP events on

@@ -19,6 +19,7 @@ GPT2_OK, GPT2_ERR_INVALID_ARG, GPT2_ERR_STATE, GPT2_ERR_DEVICE = 0, 1, 2, 3
 ACT = dict(residual=0, ln1=1, ln1_mean=2, ln1_rstd=3, qkv=4, att=5, att_lse=6, x_mid=7,
            ln2=8, ln2_mean=9, ln2_rstd=10, fc=11, gelu=12, lnf=13, lnf_mean=14, lnf_rstd=15,
            logits=16, losses=17)
+FUSION = dict(residual_norm=0)
 KCLASS = dict(gemm_fwd=0, gemm_fwd_gelu=1, gemm_dx=2, gemm_dx_gelu=3, gemm_dw=4, attn_fwd=5,
               attn_bwd=6, layernorm=7, cross_entropy=8, optimizer=9, other=10)
 
@@ -86,6 +87,7 @@ def lib():
         "gpt2_block_forward": (I32, [P, I32, P, P]),
         "gpt2_block_backward": (I32, [P, I32, P, P, I32]),
         "gpt2_embedding_backward": (I32, [P, P, P, I32]),
+        "gpt2_set_fusion": (I32, [P, I32, I32]),
         "gpt2_probe_enable": (I32, [P, ctypes.c_uint32]),
         "gpt2_probe_reset": (I32, [P]),
         "gpt2_probe_read": (I32, [P, I32, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(I64),
@@ -299,6 +301,10 @@ class GPT2:
                                            ctypes.byref(dt)), self.handle)
         tdt, es = {0: (self.torch.float32, 4), 1: (self.torch.bfloat16, 2), 2: (self.torch.int32, 4)}[dt.value]
         return self.activations[off.value: off.value + n.value * es].view(tdt)
+
+    def set_fusion(self, fusion: str, mode: int):
+        """Select an alternative kernel arrangement (gpt2_set_fusion)."""
+        _check(self.L.gpt2_set_fusion(self.handle, FUSION[fusion], int(mode)), self.handle)
 
     # ---- probes -------------------------------------------------------------
     def probe_enable(self, classes):

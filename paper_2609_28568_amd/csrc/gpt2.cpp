@@ -271,6 +271,12 @@ struct gpt2_model {
   bool have_dlogits = false;   // last forward had targets
   bool have_grads = false;     // gradients hold a backward result
   bool have_loss = false;
+  // how a residual connection meets the following pre-norm (gpt2_fusion):
+  // 0 the projection's epilogue adds the residual, the LayerNorm reads the
+  // sum; 1 the projection writes its branch and one kernel adds and
+  // normalises; 2 a separate addition kernel, then the LayerNorm (the
+  // composed path that 1 must match bit for bit)
+  int residual_norm = 0;
   std::string err;
   ProbeSet<GPT2_K_COUNT> probes;
 
@@ -443,22 +449,86 @@ double attn_fwd_flops(const Dims& d) {
 // keeping the block's activations in activation slot `a`. Training uses
 // in = a = l, out = l + 1 (everything kept for the backward); evaluation
 // reuses slot 0 and two residual slots.
-gpt2_status block_fwd(Model* m, int l, int in, int out, int a) {
+// The pre-norm that follows a residual connection: xsum = bf16(res +
+// branch), y = LayerNorm(xsum), by the configured path (Model::residual_norm,
+// modes 1 and 2; branch is the projection's output without the residual).
+// With w == nullptr only the sum is formed.
+hipError_t add_norm(Model* m, const bf16_t* res, const bf16_t* branch, bf16_t* xsum, const float* w, const float* b,
+                    bf16_t* y, float* mean, float* rstd) {
+  const int BT = (int)m->d.BT, C = m->d.C;
+  if (m->residual_norm == 2 || !w) {
+    hipError_t e = m->run(GPT2_K_OTHER, 0.0, 6.0 * BT * C,
+                          [&] { return launch_residual_add(res, branch, xsum, (long)BT * C, m->stream); });
+    if (e != hipSuccess || !w) return e;
+    return ln_fwd(m, xsum, w, b, y, mean, rstd);
+  }
+  return m->run(GPT2_K_LAYERNORM, 0.0, 8.0 * BT * C + 8.0 * BT + 8.0 * C, [&] {
+    return launch_add_layernorm_fwd(branch, res, xsum, w, b, y, mean, rstd, BT, C, m->cfg.ln_eps, m->stream);
+  });
+}
+
+// The pre-norm that follows block l's output: the next block's LN1 (into
+// activation slot a_next), or the final LayerNorm after the last block.
+struct NextNorm {
+  const float *w, *b;
+  bf16_t* y;
+  float *mean, *rstd;
+};
+NextNorm next_norm(Model* m, int l, int a_next) {
+  if (l + 1 < m->d.L) {
+    const size_t oC = (size_t)(l + 1) * m->d.C;
+    return {m->pf(K_LN1W) + oC, m->pf(K_LN1B) + oC, m->ln1(a_next), m->ln1m(a_next), m->ln1r(a_next)};
+  }
+  return {m->pf(K_LNFW), m->pf(K_LNFB), m->lnf(), m->lnfm(), m->lnfr()};
+}
+
+// Forward of block l (its weights) from residual slot `in` to slot `out`,
+// keeping the block's activations in activation slot `a`. Training uses
+// in = a = l, out = l + 1 (everything kept for the backward); evaluation
+// reuses slot 0 and two residual slots. When ln1_done, the block's LN1 was
+// already computed together with the residual sum that forms its input.
+// With residual_norm 1 or 2 and next_a >= 0 the block also forms the next
+// pre-norm (next_norm) with its output and sets *next_done.
+gpt2_status block_fwd(Model* m, int l, int in, int out, int a, int next_a = -1, bool ln1_done = false,
+                      bool* next_done = nullptr) {
   const Dims& d = m->d;
   const int BT = (int)d.BT, C = d.C, F = d.F;
   const size_t oC = (size_t)l * C, o3C = (size_t)l * 3 * C, oF = (size_t)l * F;
-  TRY(ln_fwd(m, m->res(in), m->pf(K_LN1W) + oC, m->pf(K_LN1B) + oC, m->ln1(a), m->ln1m(a), m->ln1r(a)));
+  const bool fused = m->residual_norm != 0;
+  bf16_t* branch = m->wsb(m->ws.datt);   // free during the forward pass
+  if (next_done) *next_done = false;
+  if (!ln1_done)
+    TRY(ln_fwd(m, m->res(in), m->pf(K_LN1W) + oC, m->pf(K_LN1B) + oC, m->ln1(a), m->ln1m(a), m->ln1r(a)));
   TRY(gemm(m, GPT2_K_GEMM_FWD, BT, 3 * C, C, m->ln1(a), C, 0, m->pb(K_QKVW) + o3C * C, C, 0, EPI_BF16, m->qkv(a),
            3 * C, m->pf(K_QKVB) + o3C));
   AttnArgs aa = attn_args(m, a);
   TRY(m->run(GPT2_K_ATTN_FWD, attn_fwd_flops(d), 0.0, [&] { return launch_attention_fwd(aa, m->stream); }));
-  TRY(gemm(m, GPT2_K_GEMM_FWD, BT, C, C, m->att(a), C, 0, m->pb(K_ATTPROJW) + oC * C, C, 0, EPI_BF16, m->xmid(a), C,
-           m->pf(K_ATTPROJB) + oC, m->res(in)));
-  TRY(ln_fwd(m, m->xmid(a), m->pf(K_LN2W) + oC, m->pf(K_LN2B) + oC, m->ln2(a), m->ln2m(a), m->ln2r(a)));
+  if (!fused) {
+    TRY(gemm(m, GPT2_K_GEMM_FWD, BT, C, C, m->att(a), C, 0, m->pb(K_ATTPROJW) + oC * C, C, 0, EPI_BF16, m->xmid(a),
+             C, m->pf(K_ATTPROJB) + oC, m->res(in)));
+    TRY(ln_fwd(m, m->xmid(a), m->pf(K_LN2W) + oC, m->pf(K_LN2B) + oC, m->ln2(a), m->ln2m(a), m->ln2r(a)));
+  } else {
+    TRY(gemm(m, GPT2_K_GEMM_FWD, BT, C, C, m->att(a), C, 0, m->pb(K_ATTPROJW) + oC * C, C, 0, EPI_BF16, branch, C,
+             m->pf(K_ATTPROJB) + oC));
+    TRY(add_norm(m, m->res(in), branch, m->xmid(a), m->pf(K_LN2W) + oC, m->pf(K_LN2B) + oC, m->ln2(a), m->ln2m(a),
+                 m->ln2r(a)));
+  }
   TRY(gemm(m, GPT2_K_GEMM_FWD, BT, F, C, m->ln2(a), C, 0, m->pb(K_FCW) + oF * C, C, 0, EPI_GELU, m->fc(a), F,
            m->pf(K_FCB) + oF, nullptr, m->gelu(a)));
-  TRY(gemm(m, GPT2_K_GEMM_FWD, BT, C, F, m->gelu(a), F, 0, m->pb(K_FCPROJW) + oC * F, F, 0, EPI_BF16, m->res(out),
-           C, m->pf(K_FCPROJB) + oC, m->xmid(a)));
+  if (!fused) {
+    TRY(gemm(m, GPT2_K_GEMM_FWD, BT, C, F, m->gelu(a), F, 0, m->pb(K_FCPROJW) + oC * F, F, 0, EPI_BF16, m->res(out),
+             C, m->pf(K_FCPROJB) + oC, m->xmid(a)));
+  } else {
+    TRY(gemm(m, GPT2_K_GEMM_FWD, BT, C, F, m->gelu(a), F, 0, m->pb(K_FCPROJW) + oC * F, F, 0, EPI_BF16, branch, C,
+             m->pf(K_FCPROJB) + oC));
+    if (next_a >= 0) {
+      const NextNorm nn = next_norm(m, l, next_a);
+      TRY(add_norm(m, m->xmid(a), branch, m->res(out), nn.w, nn.b, nn.y, nn.mean, nn.rstd));
+      if (next_done) *next_done = true;
+    } else {
+      TRY(add_norm(m, m->xmid(a), branch, m->res(out), nullptr, nullptr, nullptr, nullptr, nullptr));
+    }
+  }
   return GPT2_OK;
 }
 
@@ -791,11 +861,12 @@ gpt2_status gpt2_forward(gpt2_model* m, const int32_t* d_inputs, const int32_t* 
                return launch_embed_fwd(d_inputs, m->pf(K_WTE), m->pf(K_WPE), m->res(0), d.B, d.T, C, d.V, m->id_flag(),
                                        m->stream);
              }));
+  bool ln_done = false;
   for (int l = 0; l < d.L; ++l) {
-    gpt2_status s = block_fwd(m, l, l, l + 1, l);
+    gpt2_status s = block_fwd(m, l, l, l + 1, l, l + 1, ln_done, &ln_done);
     if (s != GPT2_OK) return s;
   }
-  TRY(ln_fwd(m, m->res(d.L), m->pf(K_LNFW), m->pf(K_LNFB), m->lnf(), m->lnfm(), m->lnfr()));
+  if (!ln_done) TRY(ln_fwd(m, m->res(d.L), m->pf(K_LNFW), m->pf(K_LNFB), m->lnf(), m->lnfm(), m->lnfr()));
   TRY(gemm(m, GPT2_K_GEMM_FWD, BT, d.Vp, C, m->lnf(), C, 0, m->pb(K_WTE), C, 0, EPI_BF16, m->logits(), d.Vp,
            nullptr, nullptr, nullptr, nullptr, 0, 1, 0, 0, 2.0 * BT * (double)d.V * C));
   if (d_targets) {
@@ -826,11 +897,12 @@ gpt2_status gpt2_evaluate(gpt2_model* m, const int32_t* d_inputs, const int32_t*
                return launch_embed_fwd(d_inputs, m->pf(K_WTE), m->pf(K_WPE), m->res(0), d.B, d.T, C, d.V, m->id_flag(),
                                        m->stream);
              }));
+  bool ln_done = false;
   for (int l = 0; l < d.L; ++l) {
-    gpt2_status s = block_fwd(m, l, l & 1, (l + 1) & 1, 0);
+    gpt2_status s = block_fwd(m, l, l & 1, (l + 1) & 1, 0, 0, ln_done, &ln_done);
     if (s != GPT2_OK) return s;
   }
-  TRY(ln_fwd(m, m->res(d.L & 1), m->pf(K_LNFW), m->pf(K_LNFB), m->lnf(), m->lnfm(), m->lnfr()));
+  if (!ln_done) TRY(ln_fwd(m, m->res(d.L & 1), m->pf(K_LNFW), m->pf(K_LNFB), m->lnf(), m->lnfm(), m->lnfr()));
   TRY(gemm(m, GPT2_K_GEMM_FWD, BT, d.Vp, C, m->lnf(), C, 0, m->pb(K_WTE), C, 0, EPI_BF16, m->logits(), d.Vp,
            nullptr, nullptr, nullptr, nullptr, 0, 1, 0, 0, 2.0 * BT * (double)d.V * C));
   TRY(m->run(GPT2_K_CROSS_ENTROPY, 0.0, 2.0 * BT * d.Vp + 8.0 * BT, [&] {
@@ -1039,6 +1111,16 @@ gpt2_status gpt2_embedding_backward(gpt2_model* m, const int32_t* d_ids, const v
   TRY(m->run(GPT2_K_OTHER, 0.0, 2.0 * d.BT * d.C + 4.0 * d.Tmax * d.C * (1 + acc),
              [&] { return launch_embed_bwd_pos(dx, m->gf(K_WPE), d.B, d.T, d.Tmax, d.C, acc, m->stream); }));
   return GPT2_OK;
+}
+
+gpt2_status gpt2_set_fusion(gpt2_model* m, int32_t fusion, int32_t mode) {
+  if (!m) return GPT2_ERR_INVALID_ARG;
+  if (fusion == GPT2_FUSION_RESIDUAL_NORM) {
+    if (mode < 0 || mode > 2) return m->fail(GPT2_ERR_INVALID_ARG, "residual-norm mode must be 0, 1 or 2");
+    m->residual_norm = mode;
+    return GPT2_OK;
+  }
+  return m->fail(GPT2_ERR_INVALID_ARG, "unknown fusion");
 }
 
 gpt2_status gpt2_probe_enable(gpt2_model* m, uint32_t class_mask) {

@@ -119,6 +119,14 @@ hipError_t launch_attention_bwd(const AttnArgs& a, hipStream_t s);
 // ---------------------------------------------------------------- layernorm
 hipError_t launch_layernorm_fwd(const bf16_t* x, const float* w, const float* b, bf16_t* y,
                                 float* mean, float* rstd, int rows, int C, float eps, hipStream_t s);
+// The residual connection and the following pre-norm in one pass: xsum =
+// bf16(res + x) (fp32 sum, rounded to nearest even), then y = LayerNorm(xsum)
+// read from those rounded values, bit for bit what launch_residual_add
+// followed by launch_layernorm_fwd gives. res == nullptr: plain LayerNorm of x.
+hipError_t launch_add_layernorm_fwd(const bf16_t* x, const bf16_t* res, bf16_t* xsum, const float* w, const float* b,
+                                    bf16_t* y, float* mean, float* rstd, int rows, int C, float eps, hipStream_t s);
+// out = bf16(res + x) elementwise (n % 4 == 0)
+hipError_t launch_residual_add(const bf16_t* res, const bf16_t* x, bf16_t* out, long n, hipStream_t s);
 // dres_out = (has_res ? dres_in : 0) + dx (dres_in may be dres_out; it is not
 // read when has_res == 0).
 // Each block writes one row of partials part[blk][3][C]: sums over its rows of

@@ -7,9 +7,20 @@
 
 namespace {
 
-// MAXCH: 4-channel chunks per lane, C <= 256*MAXCH
-template <int MAXCH>
-__global__ __launch_bounds__(256) void ln_fwd_kernel(const bf16_t* __restrict__ x, const float* __restrict__ w,
+// Sum of two bf16 rows in fp32, rounded to bf16 (to nearest even): the
+// residual connection's addition
+DEV uint2 add_rows(uint2 r, uint2 a) {
+  return make_uint2(pack2(lo_f(r.x) + lo_f(a.x), hi_f(r.x) + hi_f(a.x)),
+                    pack2(lo_f(r.y) + lo_f(a.y), hi_f(r.y) + hi_f(a.y)));
+}
+
+// MAXCH: 4-channel chunks per lane, C <= 256*MAXCH. With RES the row is first
+// formed as the residual sum x = bf16(res + x) (stored to xsum), and the
+// normalisation then reads those rounded values, exactly as a separate
+// addition followed by this kernel would.
+template <int MAXCH, bool RES = false>
+__global__ __launch_bounds__(256) void ln_fwd_kernel(const bf16_t* __restrict__ x, const bf16_t* __restrict__ res,
+                                                     bf16_t* __restrict__ xsum, const float* __restrict__ w,
                                                      const float* __restrict__ b, bf16_t* __restrict__ y,
                                                      float* __restrict__ mean_out, float* __restrict__ rstd_out,
                                                      int rows, int C, float eps) {
@@ -20,14 +31,23 @@ __global__ __launch_bounds__(256) void ln_fwd_kernel(const bf16_t* __restrict__ 
   // Every lane issues all its loads at once: chunks past C read the row's
   // last chunk (an in-range address) and are masked out of the arithmetic,
   // so no load waits behind a branch.
-  uint2 xu[MAXCH];
+  uint2 xu[MAXCH], ru[MAXCH];
   float4 wv[MAXCH], bv[MAXCH];
 #pragma unroll
   for (int i = 0; i < MAXCH; ++i) {
     const int c = min(4 * (lane + 64 * i), C - 4);
     xu[i] = *reinterpret_cast<const uint2*>(xr + c);
+    if constexpr (RES) ru[i] = *reinterpret_cast<const uint2*>(res + (size_t)row * C + c);
     wv[i] = *reinterpret_cast<const float4*>(w + c);
     bv[i] = *reinterpret_cast<const float4*>(b + c);
+  }
+  if constexpr (RES) {
+#pragma unroll
+    for (int i = 0; i < MAXCH; ++i) {
+      xu[i] = add_rows(ru[i], xu[i]);
+      const int c = 4 * (lane + 64 * i);
+      if (c < C) *reinterpret_cast<uint2*>(xsum + (size_t)row * C + c) = xu[i];
+    }
   }
   float v[MAXCH][4];
   float s = 0.0f;
@@ -186,10 +206,24 @@ __global__ __launch_bounds__(256) void ln_bwd_kernel(const bf16_t* __restrict__ 
   }
 }
 
+// the residual addition alone: out = bf16(res + x), 4 elements per thread
+__global__ void residual_add_kernel(const bf16_t* __restrict__ res, const bf16_t* __restrict__ x,
+                                    bf16_t* __restrict__ out, long n) {
+  const long i = ((long)blockIdx.x * blockDim.x + threadIdx.x) * 4;
+  if (i >= n) return;
+  *reinterpret_cast<uint2*>(out + i) =
+      add_rows(*reinterpret_cast<const uint2*>(res + i), *reinterpret_cast<const uint2*>(x + i));
+}
+
 template <int MAXCH>
-hipError_t fwd_t(const bf16_t* x, const float* w, const float* b, bf16_t* y, float* mean, float* rstd, int rows,
-                 int C, float eps, hipStream_t s) {
-  hipLaunchKernelGGL(ln_fwd_kernel<MAXCH>, dim3((rows + 3) / 4), dim3(256), 0, s, x, w, b, y, mean, rstd, rows, C, eps);
+hipError_t fwd_t(const bf16_t* x, const bf16_t* res, bf16_t* xsum, const float* w, const float* b, bf16_t* y,
+                 float* mean, float* rstd, int rows, int C, float eps, hipStream_t s) {
+  if (res)
+    hipLaunchKernelGGL((ln_fwd_kernel<MAXCH, true>), dim3((rows + 3) / 4), dim3(256), 0, s, x, res, xsum, w, b, y,
+                       mean, rstd, rows, C, eps);
+  else
+    hipLaunchKernelGGL((ln_fwd_kernel<MAXCH, false>), dim3((rows + 3) / 4), dim3(256), 0, s, x, nullptr, nullptr, w,
+                       b, y, mean, rstd, rows, C, eps);
   return hipGetLastError();
 }
 
@@ -203,15 +237,26 @@ hipError_t bwd_t(const bf16_t* dy, const bf16_t* x, const float* mean, const flo
 
 }  // namespace
 
+hipError_t launch_add_layernorm_fwd(const bf16_t* x, const bf16_t* res, bf16_t* xsum, const float* w, const float* b,
+                                    bf16_t* y, float* mean, float* rstd, int rows, int C, float eps, hipStream_t s) {
+  if (C % 4 || (res && !xsum)) return hipErrorInvalidValue;
+  if (C <= 256) return fwd_t<1>(x, res, xsum, w, b, y, mean, rstd, rows, C, eps, s);
+  if (C <= 512) return fwd_t<2>(x, res, xsum, w, b, y, mean, rstd, rows, C, eps, s);
+  if (C <= 768) return fwd_t<3>(x, res, xsum, w, b, y, mean, rstd, rows, C, eps, s);
+  if (C <= 1024) return fwd_t<4>(x, res, xsum, w, b, y, mean, rstd, rows, C, eps, s);
+  if (C <= 2048) return fwd_t<8>(x, res, xsum, w, b, y, mean, rstd, rows, C, eps, s);
+  return hipErrorInvalidValue;
+}
+
 hipError_t launch_layernorm_fwd(const bf16_t* x, const float* w, const float* b, bf16_t* y, float* mean,
                                 float* rstd, int rows, int C, float eps, hipStream_t s) {
-  if (C % 4) return hipErrorInvalidValue;
-  if (C <= 256) return fwd_t<1>(x, w, b, y, mean, rstd, rows, C, eps, s);
-  if (C <= 512) return fwd_t<2>(x, w, b, y, mean, rstd, rows, C, eps, s);
-  if (C <= 768) return fwd_t<3>(x, w, b, y, mean, rstd, rows, C, eps, s);
-  if (C <= 1024) return fwd_t<4>(x, w, b, y, mean, rstd, rows, C, eps, s);
-  if (C <= 2048) return fwd_t<8>(x, w, b, y, mean, rstd, rows, C, eps, s);
-  return hipErrorInvalidValue;
+  return launch_add_layernorm_fwd(x, nullptr, nullptr, w, b, y, mean, rstd, rows, C, eps, s);
+}
+
+hipError_t launch_residual_add(const bf16_t* res, const bf16_t* x, bf16_t* out, long n, hipStream_t s) {
+  if (n % 4) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(residual_add_kernel, dim3((unsigned)((n / 4 + 255) / 256)), dim3(256), 0, s, res, x, out, n);
+  return hipGetLastError();
 }
 
 // At least 4 rows per wave, 4 waves per block, each block writing one row of
