@@ -321,6 +321,9 @@ def main():
     ap.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="write profiles/<probe>_<workload>_traffic.json from two rocprofv3 counter passes and exit")
     ap.add_argument("--pmc-command", default="", help="the profiling command, recorded with --pmc-summary")
+    ap.add_argument("--head-ce", type=int, default=0,
+                    help="LM head and cross-entropy: 0 logits stored and one cross-entropy kernel, 1 two head "
+                         "GEMM passes (softmax statistics, then dlogits) with the logits never stored")
     ap.add_argument("--residual-norm", type=int, default=0,
                     help="how residual connections meet the following pre-norm: 0 in the projection's epilogue, "
                          "1 the fused add + LayerNorm kernel, 2 separate add and LayerNorm kernels")
@@ -352,6 +355,7 @@ def main():
     m = binding.GPT2(cfg)
     m.set_params(params)
     m.set_fusion("residual_norm", args.residual_norm)
+    m.set_fusion("head_ce", args.head_ce)
     dev = [(torch.from_numpy(a).cuda(), torch.from_numpy(b).cuda()) for a, b in batches]
     torch.cuda.synchronize()
 
@@ -464,7 +468,7 @@ def main():
                    "n_layer": w["n_layer"], "d_model": w["d_model"], "n_head": w["n_head"],
                    "vocab": w["vocab"], "vocab_padded": w["vocab_padded"], "global_batch": w["B"],
                    "seq_len": w["T"], "grad_accum": w.get("grad_accum", 1), "tokens_per_step": tokens,
-                   "token_dist": "zipf(1.1)", "parallelism": "none", "residual_norm": args.residual_norm},
+                   "token_dist": "zipf(1.1)", "parallelism": "none", "residual_norm": args.residual_norm, "head_ce": args.head_ce},
         "mfu": round(mfu, 4),
         "flops_per_token": f_tok,
         "flops_per_token_6n_12lct": flops_per_token_palm(w, m.n_params - (w["vocab_padded"] - w["vocab"]) * w["d_model"]),

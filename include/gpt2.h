@@ -191,9 +191,12 @@ gpt2_status gpt2_adamw_step_noalloc(gpt2_model* m, int64_t step, float* lr_out,
 gpt2_status gpt2_loss(gpt2_model* m, float* loss_out, float* d_token_losses);
 
 /* Forward-only evaluation of held-out tokens (the held-out loss of section
- * "Batch geometry" and the evaluation cadence of "Method"): the same forward
- * as gpt2_forward, with the same kernels and the same per-token losses, but
- * keeping one block's activations at a time and not writing dlogits.
+ * "Batch geometry" and the evaluation cadence of "Method"): the same blocks
+ * as gpt2_forward, keeping one block's activations at a time, and the head
+ * and cross-entropy of GPT2_FUSION_HEAD_CE mode 1 without its gradient pass:
+ * the logits are never stored, only each row's softmax statistics. Its
+ * per-token losses equal those of a training forward in that mode bit for
+ * bit (mode 0 works from bf16-rounded logits instead of fp32 ones).
  * d_inputs, d_targets: int32 [B*T] as for gpt2_forward (targets required).
  * *loss_out (host) receives the mean loss; d_token_losses (device fp32
  * [B*T], optional) the per-token losses. It reuses the activation buffer, so
@@ -286,10 +289,19 @@ gpt2_status gpt2_embedding_backward(gpt2_model* m, const int32_t* d_ids,
  *     2 the composed path: a separate addition kernel, then the LayerNorm.
  *     Modes 1 and 2 give bit-identical activations (the paper's gate: the
  *     fused residual sum must equal the composed addition exactly).
+ *   GPT2_FUSION_HEAD_CE, the tied LM head and the cross-entropy (the stage
+ *   table's cross-entropy row, section "Speed"):
+ *     0 (default) the head GEMM writes the bf16 logits, one kernel reads
+ *       them and writes loss and dlogits;
+ *     1 the logits are never stored: a first head GEMM writes only each
+ *       row's softmax statistics per tile slice and its target logit, a
+ *       kernel combines them into the log-sum-exp and the loss, and a second
+ *       head GEMM's epilogue writes dlogits from the fp32 logits.
  * The mode applies from the next forward pass on; the backward reads only the
  * saved activations. INVALID_ARG for an unknown fusion or mode. */
 typedef enum gpt2_fusion {
-  GPT2_FUSION_RESIDUAL_NORM = 0
+  GPT2_FUSION_RESIDUAL_NORM = 0,
+  GPT2_FUSION_HEAD_CE = 1
 } gpt2_fusion;
 gpt2_status gpt2_set_fusion(gpt2_model* m, int32_t fusion, int32_t mode);
 

@@ -19,7 +19,7 @@ GPT2_OK, GPT2_ERR_INVALID_ARG, GPT2_ERR_STATE, GPT2_ERR_DEVICE = 0, 1, 2, 3
 ACT = dict(residual=0, ln1=1, ln1_mean=2, ln1_rstd=3, qkv=4, att=5, att_lse=6, x_mid=7,
            ln2=8, ln2_mean=9, ln2_rstd=10, fc=11, gelu=12, lnf=13, lnf_mean=14, lnf_rstd=15,
            logits=16, losses=17)
-FUSION = dict(residual_norm=0)
+FUSION = dict(residual_norm=0, head_ce=1)
 KCLASS = dict(gemm_fwd=0, gemm_fwd_gelu=1, gemm_dx=2, gemm_dx_gelu=3, gemm_dw=4, attn_fwd=5,
               attn_bwd=6, layernorm=7, cross_entropy=8, optimizer=9, other=10)
 

@@ -373,6 +373,41 @@ __global__ __launch_bounds__(NT) void cross_entropy_kernel(bf16_t* __restrict__ 
   if (tid == 0) losses[pos] = mx + logf(sum) - bf2f(xt_raw);
 }
 
+// Combine the per-slice softmax statistics of each row (written by the head
+// GEMM's statistics epilogue): one wave per row, each lane merging every 64th
+// slice (max, sum of exponentials) pair, then the lanes merged in a fixed
+// butterfly order.
+DEV void merge_ms(float& m, float& s, float m2, float s2) {
+  const float mn = fmaxf(m, m2);
+  s = (m == -INFINITY ? 0.0f : s * __expf(m - mn)) + (m2 == -INFINITY ? 0.0f : s2 * __expf(m2 - mn));
+  m = mn;
+}
+
+__global__ __launch_bounds__(256) void ce_combine_kernel(const float2* __restrict__ stats, int nparts,
+                                                         const float* __restrict__ tlogit,
+                                                         const int32_t* __restrict__ targets, int V,
+                                                         float* __restrict__ lse, float* __restrict__ losses, int rows,
+                                                         uint32_t* __restrict__ bad) {
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (row >= rows) return;
+  float m = -INFINITY, sum = 0.0f;
+  for (int k = lane; k < nparts; k += 64) {
+    const float2 p = stats[(size_t)row * nparts + k];
+    merge_ms(m, sum, p.x, p.y);
+  }
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) {
+    const float m2 = __shfl_xor(m, o, WAVE), s2 = __shfl_xor(sum, o, WAVE);
+    merge_ms(m, sum, m2, s2);
+  }
+  if (lane == 0) {
+    const float l = m + logf(sum);
+    lse[row] = l;
+    losses[row] = l - tlogit[row];
+    if ((unsigned)targets[row] >= (unsigned)V && bad) atomicOr(bad, ID_BAD_TARGET);
+  }
+}
+
 // ------------------------------------------------------------ casts
 
 __global__ void cast_bf16_kernel(const float* __restrict__ src, bf16_t* __restrict__ dst, long n) {
@@ -643,5 +678,13 @@ hipError_t launch_init_params(const InitArgs& a, hipStream_t s) {
   unsigned blocks = blocks_for(a.n / 4, 256);
   if (blocks > 8192) blocks = 8192;
   hipLaunchKernelGGL(init_params_kernel, dim3(blocks), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_ce_combine(const float* stats, int nparts, const float* tlogit, const int32_t* targets, int V,
+                             float* lse, float* losses, int rows, uint32_t* bad, hipStream_t s) {
+  if (nparts < 1 || rows < 1) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(ce_combine_kernel, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, s,
+                     reinterpret_cast<const float2*>(stats), nparts, tlogit, targets, V, lse, losses, rows, bad);
   return hipGetLastError();
 }

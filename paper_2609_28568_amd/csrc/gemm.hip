@@ -396,6 +396,58 @@ __global__ __launch_bounds__(64 * gemm_waves(BM, BK), (NS <= 2 ? 2 : 1)) void ge
     }
   }
 
+  // ---------------------------------------------------------------- softmax cross-entropy
+  // Lane l holds row l%32 of each 32-row block i and, of fragment j, the
+  // columns 32j + 8q + 4(l/32) + e (acc[i][j][4q + e]), so a row's values sit
+  // in lanes l and l^32 only.
+  if constexpr (EPI == EPI_CE_STATS || EPI == EPI_CE_GRAD) {
+    const int lg = lane >> 5;
+    const int nb = n0 + wn * WTN + 4 * lg;
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+      const int mrow = m0 + wm * WTM + 32 * i + (lane & 31);
+      const bool row_ok = mrow < g.M;
+      int t = row_ok ? g.ce_targets[mrow] : 0;
+      if ((unsigned)t >= (unsigned)g.ce_V) t = 0;
+      if constexpr (EPI == EPI_CE_STATS) {
+        float mx = -INFINITY;
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+            if (nb + 32 * j + 8 * (r >> 2) + (r & 3) < g.ce_V) mx = fmaxf(mx, acc[i][j][r]);
+        float se = 0.0f;
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int n = nb + 32 * j + 8 * (r >> 2) + (r & 3);
+            if (n < g.ce_V) se += __expf(acc[i][j][r] - mx);
+            if (n == t && row_ok) g.ce_tlogit[mrow] = acc[i][j][r];
+          }
+        const float m2 = __shfl_xor(mx, 32, WAVE), s2 = __shfl_xor(se, 32, WAVE);
+        const float mn = fmaxf(mx, m2);
+        se = (mx == -INFINITY ? 0.0f : se * __expf(mx - mn)) + (m2 == -INFINITY ? 0.0f : s2 * __expf(m2 - mn));
+        if (lg == 0 && row_ok) {
+          const int parts = ((g.N + BN - 1) / BN) * 2;
+          reinterpret_cast<float2*>(g.ce_stats)[(size_t)mrow * parts + (n0 / BN) * 2 + wn] = make_float2(mn, se);
+        }
+      } else {
+        const float lse = row_ok ? g.ce_lse[mrow] : 0.0f;
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int n = nb + 32 * j + 8 * (r >> 2) + (r & 3);
+            float v = n < g.ce_V ? __expf(acc[i][j][r] - lse) * g.ce_scale : 0.0f;
+            if (n == t) v -= g.ce_scale;
+            acc[i][j][r] = v;
+          }
+      }
+    }
+    if constexpr (EPI == EPI_CE_STATS) return;
+  }
+
   // ---------------------------------------------------------------- epilogue
   // Each wave writes its tile 32 rows at a time: accumulators go to LDS, come
   // back as whole row segments, and are stored with the bias, residual,
@@ -416,7 +468,8 @@ __global__ __launch_bounds__(64 * gemm_waves(BM, BK), (NS <= 2 ? 2 : 1)) void ge
   bf16_t* Cb = static_cast<bf16_t*>(g.C);
   const int ncol0 = n0 + wn * WTN;
   float4 bias4[NB];
-  if constexpr (EPI == EPI_BF16 || EPI == EPI_BF16_RES || EPI == EPI_GELU || EPI == EPI_BF16_SCALE) {
+  if constexpr (EPI == EPI_BF16 || EPI == EPI_BF16_RES || EPI == EPI_GELU || EPI == EPI_BF16_SCALE ||
+                EPI == EPI_CE_GRAD) {
 #pragma unroll
     for (int q = 0; q < NB; ++q) {
       const int n = ncol0 + ((lane + 64 * q) % CPR) * 4;
@@ -581,6 +634,8 @@ hipError_t launch_cfg(const GemmArgs& g, int a_t, int b_t, int epi, hipStream_t 
   if (g.K2 > 0 && (a_t || epi != EPI_BF16)) return hipErrorInvalidValue;
   if (!a_t && !b_t && epi == EPI_BF16) return launch_bf16<BM, BN, BK, false>(g, s);
   if (!a_t && !b_t && epi == EPI_GELU) return launch_t<BM, BN, BK, 2, false, false, EPI_GELU>(g, s);
+  if (!a_t && !b_t && epi == EPI_CE_STATS) return launch_t<BM, BN, BK, 2, false, false, EPI_CE_STATS>(g, s);
+  if (!a_t && !b_t && epi == EPI_CE_GRAD) return launch_t<BM, BN, BK, 2, false, false, EPI_CE_GRAD>(g, s);
   if (!a_t && b_t && epi == EPI_BF16) return launch_bf16<BM, BN, BK, true>(g, s);
   if (!a_t && b_t && epi == EPI_GELU_BWD) return launch_t<BM, BN, BK, 2, false, true, EPI_GELU_BWD>(g, s);
   // products with few output tiles and a long contraction, split into fp32 slices
@@ -629,6 +684,11 @@ GemmConfig gemm_config(int M, int N, int a_t, int b_t, int epi) {
   // workgroup alone on a CU keeps its MFMA pipe about half busy)
   if (M >= 256 && N >= 128 && N % 128 == 0 && (long)((M + 255) / 256) * (N / 128) >= 512) return {256, 128, 32};
   return {128, 128, a_t ? 32 : 64};
+}
+
+int gemm_ce_parts(int M, int N) {
+  const GemmConfig c = gemm_config(M, N, 0, 0, EPI_CE_STATS);
+  return ((N + c.bn - 1) / c.bn) * 2;
 }
 
 int gemm_bias_parts(int M, int N, int splits) {

@@ -161,6 +161,9 @@ struct WsLayout {
   // groups
   size_t dres_l, dfc_l, dqkv_l, gbs_qkv, gbs_fc;
   size_t s_dres, s_dfc, s_dqkv;
+  // the two-pass head + cross-entropy: per-row softmax statistics of every
+  // head tile slice, the target logits and the log-sum-exp of each row
+  size_t ce_stats, ce_tlogit, ce_lse;
 };
 
 ActLayout act_layout(const Dims& d) {
@@ -254,6 +257,9 @@ WsLayout ws_layout(const Dims& d) {
   const GemmGroupedArgs gg = dw_groups(d);
   w.gbs_qkv = o; o += align_up((size_t)gemm_grouped_bias_parts(gg, G_QKV) * d.L * 3 * C * 4);
   w.gbs_fc = o; o += align_up((size_t)gemm_grouped_bias_parts(gg, G_FC) * d.L * F * 4);
+  w.ce_stats = o; o += align_up(BT * (size_t)gemm_ce_parts((int)BT, d.Vp) * 8);
+  w.ce_tlogit = o; o += align_up(BT * 4);
+  w.ce_lse = o; o += align_up(BT * 4);
   w.total = o;
   return w;
 }
@@ -277,6 +283,11 @@ struct gpt2_model {
   // normalises; 2 a separate addition kernel, then the LayerNorm (the
   // composed path that 1 must match bit for bit)
   int residual_norm = 0;
+  // the LM head and the cross-entropy (gpt2_fusion): 0 the head GEMM writes
+  // the logits and one kernel computes loss and dlogits over them; 1 the head
+  // GEMM runs twice, first writing only each row's softmax statistics and
+  // target logit, then writing dlogits from the combined log-sum-exp
+  int head_ce = 0;
   std::string err;
   ProbeSet<GPT2_K_COUNT> probes;
 
@@ -445,10 +456,46 @@ double attn_fwd_flops(const Dims& d) {
   return 4.0 * d.B * d.H * d.hd * ((double)d.T * (d.T + 1) / 2.0);
 }
 
-// Forward of block l (its weights) from residual slot `in` to slot `out`,
-// keeping the block's activations in activation slot `a`. Training uses
-// in = a = l, out = l + 1 (everything kept for the backward); evaluation
-// reuses slot 0 and two residual slots.
+// The tied LM head and the softmax cross-entropy over the real vocabulary
+// (sections "Model" and "Optimisation and precision"), with targets:
+// per-token losses, and (write_grad) dlogits scaled by grad_scale in the
+// logits buffer. mode 0: the head writes the logits, the cross-entropy
+// kernel reads them and writes dlogits over them; mode 1: a statistics pass
+// of the head GEMM, a combine kernel, and (write_grad) a second head GEMM
+// whose epilogue writes dlogits; the logits are never stored. Training takes
+// the configured head_ce; the forward-only evaluation always takes mode 1,
+// which needs only the statistics pass there.
+gpt2_status head_and_loss(Model* m, const int32_t* d_targets, float grad_scale, int write_grad, int mode) {
+  const Dims& d = m->d;
+  const int BT = (int)d.BT, C = d.C;
+  const double head_fl = 2.0 * BT * (double)d.V * C;
+  if (mode == 0) {
+    TRY(gemm(m, GPT2_K_GEMM_FWD, BT, d.Vp, C, m->lnf(), C, 0, m->pb(K_WTE), C, 0, EPI_BF16, m->logits(), d.Vp,
+             nullptr, nullptr, nullptr, nullptr, 0, 1, 0, 0, head_fl));
+    TRY(m->run(GPT2_K_CROSS_ENTROPY, 0.0, (2.0 + 2.0 * write_grad) * BT * d.Vp + 8.0 * BT, [&] {
+      return launch_cross_entropy(m->logits(), d_targets, m->losses(), BT, d.V, d.Vp, grad_scale, write_grad,
+                                  m->id_flag(), m->stream);
+    }));
+  } else {
+    GemmArgs g{};
+    g.A = m->lnf(); g.B = m->pb(K_WTE); g.M = BT; g.N = d.Vp; g.K = C; g.lda = C; g.ldb = C;
+    g.C = m->logits(); g.ldc = d.Vp;
+    g.ce_targets = d_targets; g.ce_stats = m->wsf(m->ws.ce_stats); g.ce_tlogit = m->wsf(m->ws.ce_tlogit);
+    g.ce_lse = m->wsf(m->ws.ce_lse); g.ce_V = d.V; g.ce_scale = grad_scale;
+    TRY(m->run(GPT2_K_GEMM_FWD, head_fl, 0.0, [&] { return launch_gemm(g, 0, 0, EPI_CE_STATS, m->stream); }));
+    const int parts = gemm_ce_parts(BT, d.Vp);
+    TRY(m->run(GPT2_K_CROSS_ENTROPY, 0.0, 8.0 * BT * parts + 16.0 * BT, [&] {
+      return launch_ce_combine(g.ce_stats, parts, g.ce_tlogit, d_targets, d.V, m->wsf(m->ws.ce_lse), m->losses(), BT,
+                               m->id_flag(), m->stream);
+    }));
+    if (write_grad)
+      TRY(m->run(GPT2_K_GEMM_FWD, head_fl, 0.0, [&] { return launch_gemm(g, 0, 0, EPI_CE_GRAD, m->stream); }));
+  }
+  TRY(m->run(GPT2_K_OTHER, 0.0, 4.0 * BT,
+             [&] { return launch_mean(m->losses(), BT, m->loss_mean(), m->stream, m->id_flag()); }));
+  return GPT2_OK;
+}
+
 // The pre-norm that follows a residual connection: xsum = bf16(res +
 // branch), y = LayerNorm(xsum), by the configured path (Model::residual_norm,
 // modes 1 and 2; branch is the projection's output without the residual).
@@ -867,19 +914,18 @@ gpt2_status gpt2_forward(gpt2_model* m, const int32_t* d_inputs, const int32_t* 
     if (s != GPT2_OK) return s;
   }
   if (!ln_done) TRY(ln_fwd(m, m->res(d.L), m->pf(K_LNFW), m->pf(K_LNFB), m->lnf(), m->lnfm(), m->lnfr()));
-  TRY(gemm(m, GPT2_K_GEMM_FWD, BT, d.Vp, C, m->lnf(), C, 0, m->pb(K_WTE), C, 0, EPI_BF16, m->logits(), d.Vp,
-           nullptr, nullptr, nullptr, nullptr, 0, 1, 0, 0, 2.0 * BT * (double)d.V * C));
-  if (d_targets) {
-    const float scale = (float)(1.0 / ((double)BT * d.accum));
-    TRY(m->run(GPT2_K_CROSS_ENTROPY, 0.0, 4.0 * BT * d.Vp + 8.0 * BT, [&] {
-      return launch_cross_entropy(m->logits(), d_targets, m->losses(), BT, d.V, d.Vp, scale, 1, m->id_flag(),
-                                  m->stream);
-    }));
-    TRY(m->run(GPT2_K_OTHER, 0.0, 4.0 * BT,
-               [&] { return launch_mean(m->losses(), BT, m->loss_mean(), m->stream, m->id_flag()); }));
-    m->have_dlogits = true;
-    m->have_loss = true;
+  if (!d_targets) {
+    // logits only
+    TRY(gemm(m, GPT2_K_GEMM_FWD, BT, d.Vp, C, m->lnf(), C, 0, m->pb(K_WTE), C, 0, EPI_BF16, m->logits(), d.Vp,
+             nullptr, nullptr, nullptr, nullptr, 0, 1, 0, 0, 2.0 * BT * (double)d.V * C));
+    return GPT2_OK;
   }
+  {
+    gpt2_status st = head_and_loss(m, d_targets, (float)(1.0 / ((double)BT * d.accum)), 1, m->head_ce);
+    if (st != GPT2_OK) return st;
+  }
+  m->have_dlogits = true;
+  m->have_loss = true;
   return GPT2_OK;
 }
 
@@ -903,13 +949,10 @@ gpt2_status gpt2_evaluate(gpt2_model* m, const int32_t* d_inputs, const int32_t*
     if (s != GPT2_OK) return s;
   }
   if (!ln_done) TRY(ln_fwd(m, m->res(d.L & 1), m->pf(K_LNFW), m->pf(K_LNFB), m->lnf(), m->lnfm(), m->lnfr()));
-  TRY(gemm(m, GPT2_K_GEMM_FWD, BT, d.Vp, C, m->lnf(), C, 0, m->pb(K_WTE), C, 0, EPI_BF16, m->logits(), d.Vp,
-           nullptr, nullptr, nullptr, nullptr, 0, 1, 0, 0, 2.0 * BT * (double)d.V * C));
-  TRY(m->run(GPT2_K_CROSS_ENTROPY, 0.0, 2.0 * BT * d.Vp + 8.0 * BT, [&] {
-    return launch_cross_entropy(m->logits(), d_targets, m->losses(), BT, d.V, d.Vp, 0.0f, 0, m->id_flag(), m->stream);
-  }));
-  TRY(m->run(GPT2_K_OTHER, 0.0, 4.0 * BT,
-             [&] { return launch_mean(m->losses(), BT, m->loss_mean(), m->stream, m->id_flag()); }));
+  {
+    gpt2_status st = head_and_loss(m, d_targets, 0.0f, 0, 1);
+    if (st != GPT2_OK) return st;
+  }
   if (d_token_losses)
     TRY(hipMemcpyAsync(d_token_losses, m->losses(), (size_t)BT * 4, hipMemcpyDeviceToDevice, m->stream));
   return read_loss(m, loss_out);
@@ -1118,6 +1161,11 @@ gpt2_status gpt2_set_fusion(gpt2_model* m, int32_t fusion, int32_t mode) {
   if (fusion == GPT2_FUSION_RESIDUAL_NORM) {
     if (mode < 0 || mode > 2) return m->fail(GPT2_ERR_INVALID_ARG, "residual-norm mode must be 0, 1 or 2");
     m->residual_norm = mode;
+    return GPT2_OK;
+  }
+  if (fusion == GPT2_FUSION_HEAD_CE) {
+    if (mode < 0 || mode > 1) return m->fail(GPT2_ERR_INVALID_ARG, "head-cross-entropy mode must be 0 or 1");
+    m->head_ce = mode;
     return GPT2_OK;
   }
   return m->fail(GPT2_ERR_INVALID_ARG, "unknown fusion");

@@ -12,7 +12,9 @@ enum GemmEpilogue {
   EPI_BF16 = 0,      // C = bf16(acc + bias? + residual?)
   EPI_GELU = 1,      // C = bf16(acc + bias) (pre-activation), C2 = bf16(gelu(acc + bias))
   EPI_GELU_BWD = 2,  // C = bf16(acc * gelu'(aux))
-  EPI_F32 = 3        // C (fp32, one slice per split) = acc (+ C if accumulate)
+  EPI_F32 = 3,       // C (fp32, one slice per split) = acc (+ C if accumulate)
+  EPI_CE_STATS = 7,  // softmax statistics of each row, see GemmArgs
+  EPI_CE_GRAD = 8    // softmax cross-entropy gradient of each row, see GemmArgs
 };
 
 struct GemmArgs {
@@ -54,6 +56,21 @@ struct GemmArgs {
   int b_bound[2], b_step;
   // row stride of the bsum partial rows (0: M)
   int bsum_ld;
+  // Softmax cross-entropy over the output rows (the tied LM head, rows =
+  // token positions, columns = vocabulary entries; only columns < ce_V count,
+  // targets outside [0, ce_V) read column 0):
+  //   EPI_CE_STATS writes no C: for each row, per wave-column slice of each
+  //     tile, the max and the sum of exp(logit - max) over its real columns
+  //     into ce_stats [M][gemm_ce_parts(N)] (float2), and the target's logit
+  //     into ce_tlogit [M];
+  //   EPI_CE_GRAD writes C = bf16((exp(logit - ce_lse[m]) - [n == target])
+  //     * ce_scale) on real columns, 0 on the others.
+  const int32_t* ce_targets;
+  float* ce_stats;
+  float* ce_tlogit;
+  const float* ce_lse;
+  int ce_V;
+  float ce_scale;
 };
 
 // Grouped weight gradients: launch_gemm_grouped runs, in one launch, every
@@ -96,6 +113,13 @@ int gemm_split_plan(int K, int want, int* k_chunk);
 // Partial rows a weight-gradient GEMM writes into GemmArgs::bsum
 int gemm_bias_parts(int M, int N, int splits);
 hipError_t launch_gemm(const GemmArgs& g, int a_t, int b_t, int epi, hipStream_t s);
+// float2 partials per row that EPI_CE_STATS writes for an M x N product
+int gemm_ce_parts(int M, int N);
+// Combine the EPI_CE_STATS partials of each row: lse[r] = log-sum-exp of the
+// real columns, losses[r] = lse[r] - tlogit[r]; targets outside [0, V) set
+// bit ID_BAD_TARGET of *bad (when not null).
+hipError_t launch_ce_combine(const float* stats, int nparts, const float* tlogit, const int32_t* targets, int V,
+                             float* lse, float* losses, int rows, uint32_t* bad, hipStream_t s);
 
 // ---------------------------------------------------------------- attention
 // Grouped-query attention: H query heads, Hkv key/value heads (0: Hkv = H),

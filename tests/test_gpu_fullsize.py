@@ -216,10 +216,15 @@ def test_gpt2_124m_embedding_backward_zipf(full_setup):
 
 def test_gpt2_124m_evaluate_equals_forward(full_setup):
     """Forward-only evaluation at full size reuses one block's activation
-    slots: its per-token losses equal the training forward's exactly."""
+    slots and never stores the logits: its per-token losses equal a training
+    forward's with the two-pass head exactly, and the default forward's
+    within tolerance."""
     w, p, ids, tgt = full_setup
     m = _model(w)
     m.set_params(p)
+    m.forward(torch.from_numpy(ids), torch.from_numpy(tgt))
+    ref0 = _np(m.activation("losses")).copy()
+    m.set_fusion("head_ce", 1)
     m.forward(torch.from_numpy(ids), torch.from_numpy(tgt))
     loss = m.loss()
     ref = _np(m.activation("losses")).copy()
@@ -229,6 +234,7 @@ def test_gpt2_124m_evaluate_equals_forward(full_setup):
     m.close()
     assert np.array_equal(got, ref)
     assert ev == loss
+    assert np.max(np.abs(got - ref0)) < LOSS_ATOL
 
 
 def test_gpt2_124m_accumulation_configuration():

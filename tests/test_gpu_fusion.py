@@ -100,3 +100,72 @@ def test_fused_residual_norm_bit_identical_at_full_size():
     for name, xs in out[1][1].items():
         for l, (a, b) in enumerate(zip(xs, out[2][1][name])):
             assert torch.equal(a, b), (name, l)
+
+
+def _head_ce_run(w, p, ids, tgt, mode):
+    from paper_2609_28568_amd import binding
+    m = binding.GPT2(binding.make_config(w, synth.OPTIM))
+    m.set_params(p)
+    m.set_fusion("head_ce", mode)
+    m.forward(torch.from_numpy(ids), torch.from_numpy(tgt))
+    loss = m.loss()
+    losses = m.activation("losses").clone()
+    dlogits = m.activation("logits").clone()
+    m.backward()
+    g = m.to_dict("grads")
+    ev_losses = torch.zeros_like(losses)
+    ev = m.evaluate(torch.from_numpy(ids), torch.from_numpy(tgt), ev_losses)
+    m.close()
+    return dict(loss=loss, losses=losses, dlogits=dlogits, grads=g, ev=ev, ev_losses=ev_losses)
+
+
+@pytest.mark.parametrize("case", list(CASES) + ["single_token"])
+def test_two_pass_head_cross_entropy_meets_the_oracle(case):
+    """Head + cross-entropy without stored logits (mode 1): loss, per-token
+    losses and all gradients against the oracle; padding columns of dlogits
+    exactly 0; the forward-only evaluation gives the training forward's
+    per-token losses bit for bit."""
+    if case == "single_token":
+        w = workload("tiny", B=5, T=1)
+        p = synth.perturb_params(synth.init_params(w, seed=101), seed=102)
+        ids, tgt = synth.token_batch(w, seed=103)
+    else:
+        w, p, ids, tgt = _case(case)
+    r = _head_ce_run(w, p, ids, tgt, 1)
+    ocfg = oracle_config(w)
+    cache = oracle.forward(p, ids, tgt, ocfg)
+    ref = oracle.backward(p, cache, ocfg)
+    assert abs(r["loss"] - float(cache["loss"])) < LOSS_ATOL
+    got = r["losses"].cpu().numpy()
+    assert np.max(np.abs(got - cache["losses"].ravel())) < 5 * LOSS_ATOL
+    assert rel_l2(got, cache["losses"].ravel()) < REL_L2
+    Vp, V = w["vocab_padded"], w["vocab"]
+    dl = r["dlogits"].view(-1, Vp)
+    assert int(torch.count_nonzero(dl[:, V:]).item()) == 0
+    assert rel_l2(dl.float().cpu().numpy(), cache["dlogits"]) < REL_L2
+    for k in oracle.KINDS:
+        assert rel_l2(r["grads"][k], ref[k]) < REL_L2, k
+    assert torch.equal(r["ev_losses"], r["losses"])
+    assert r["ev"] == r["loss"]
+
+
+def test_two_pass_head_cross_entropy_full_size():
+    """GPT-2 124M, the benchmark's batch: the two arrangements' losses,
+    dlogits and gradients agree (the second works from fp32 logits, the first
+    from bf16 ones), and the padding columns are exactly 0."""
+    w = workload("gpt2_124m")
+    p = synth.init_params(w)
+    ids, tgt = synth.token_batch(w)
+    a = _head_ce_run(w, p, ids, tgt, 0)
+    b = _head_ce_run(w, p, ids, tgt, 1)
+    V, Vp = w["vocab"], w["vocab_padded"]
+    assert abs(a["loss"] - b["loss"]) < 1e-3
+    assert float((a["losses"] - b["losses"]).abs().max()) < 2e-2
+    dla, dlb = a["dlogits"].view(-1, Vp), b["dlogits"].view(-1, Vp)
+    assert int(torch.count_nonzero(dlb[:, V:]).item()) == 0
+    e = float(torch.linalg.norm((dla.float() - dlb.float())) / torch.linalg.norm(dla.float()))
+    print(f"head_ce full size: dlogits rel_l2 {e:.2e}, loss {a['loss']:.5f} vs {b['loss']:.5f}")
+    assert e < 1e-2
+    for k in oracle.KINDS:
+        assert rel_l2(b["grads"][k], a["grads"][k]) < 1e-2, k
+    assert torch.equal(b["ev_losses"], b["losses"])

@@ -187,15 +187,19 @@ def test_per_token_losses_at_their_positions():
 
 @pytest.mark.parametrize("case", list(CASES))
 def test_evaluate_equals_the_training_forward(case):
-    """The forward-only evaluation runs the same kernels on the same inputs:
-    per-token losses equal the training forward's bit for bit (so they match
-    the oracle as that forward does), and it leaves no state to backward
-    from."""
+    """The forward-only evaluation runs the training forward's kernels (the
+    head and cross-entropy as the two-pass arrangement's statistics pass): its
+    per-token losses equal a training forward's in that arrangement bit for
+    bit, are within tolerance of the oracle and of the default arrangement's,
+    and it leaves no state to backward from."""
     w = workload("tiny", **CASES[case])
     p = synth.perturb_params(synth.init_params(w, seed=41), seed=42)
     ids, tgt = synth.token_batch(w, seed=43)
     m = _model(w)
     m.set_params(p)
+    m.forward(torch.from_numpy(ids), torch.from_numpy(tgt))
+    ref0 = _np(m.activation("losses")).copy()
+    m.set_fusion("head_ce", 1)
     m.forward(torch.from_numpy(ids), torch.from_numpy(tgt))
     loss = m.loss()
     ref = _np(m.activation("losses")).copy()
@@ -204,8 +208,10 @@ def test_evaluate_equals_the_training_forward(case):
     got = tl.cpu().numpy()
     assert np.array_equal(got, ref)
     assert ev == loss
+    assert np.max(np.abs(got - ref0)) < LOSS_ATOL
     cache = oracle.forward(p, ids, tgt, oracle_config(w))
     assert abs(ev - float(cache["loss"])) < LOSS_ATOL
+    assert np.max(np.abs(got - cache["losses"].ravel())) < 5 * LOSS_ATOL
     from paper_2609_28568_amd import binding
     with pytest.raises(binding.LibError):
         m.backward()
