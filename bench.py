@@ -82,6 +82,7 @@ def qwen3_cpu_baseline(w: dict, base: dict, lora: dict, ids, tgt) -> dict:
     dt = time.perf_counter() - t0
     threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     return {"value": round(ws["T"] / dt, 3), "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "cpu_count": os.cpu_count(),
             "sample": f"one adapter step (fwd+masked loss+bwd+clip+AdamW) on 1 sequence x {ws['T']} tokens of the "
                       f"same model and token stream, numpy fp32, {dt:.1f} s"}
 
@@ -191,14 +192,14 @@ def qwen3_bench(args) -> None:
 
 
 def cpu_baseline(w: dict, params, ids, tgt) -> dict:
-    """The oracle's step (fwd + bwd + clip + AdamW) on the first two
-    sequences of the batch: 2 x 1024 tokens through the full model (about
-    10 s on 16 host threads)."""
+    """The oracle's step (fwd + bwd + clip + AdamW) on the first four
+    sequences of the batch: 4 x 1024 tokens through the full model (about
+    20 s on 16 host threads)."""
     import numpy as np
     import oracle
     from threadpoolctl import threadpool_info
     ws = dict(w)
-    nb = min(2, len(ids))
+    nb = min(4, len(ids))
     ws["B"] = nb
     cfg = oracle.Config.from_dict({**ws, "lr_min": 6e-5})
     p = {k: v.copy() for k, v in params.items()}
@@ -207,10 +208,12 @@ def cpu_baseline(w: dict, params, ids, tgt) -> dict:
     t0 = time.perf_counter()
     oracle.train_step(p, m, v, 0, [(ids[:nb], tgt[:nb])], cfg)
     dt = time.perf_counter() - t0
-    threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    info = threadpool_info()
+    threads = max([i.get("num_threads", 1) for i in info] or [1])
     return {"value": round(nb * ws["T"] / dt, 3), "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "cpu_count": os.cpu_count(), "blas": sorted({i.get("internal_api", "?") for i in info}),
             "sample": f"one optimizer step (fwd+bwd+clip+AdamW) on {nb} sequence(s) x {ws['T']} tokens of the same "
-                      f"model and token stream, numpy fp32, {dt:.1f} s"}
+                      f"model and token stream, numpy fp32 with {threads} BLAS threads, {dt:.1f} s"}
 
 
 # Kernel classes with counter-derived traffic: the sources their kernels are
@@ -222,7 +225,9 @@ KERNEL_CLASSES = {
     "gemm_fwd": (("gemm.hip", "common.h", "lds_dma.h", "kernels.h"),
                  r"gemm_kernel<\d+, \d+, \d+, \d+, false, false, 0(, (false|true))*>", 1),
     "gemm_dw": (("gemm.hip", "common.h", "lds_dma.h", "kernels.h"),
-                r"gemm_kernel<\d+, \d+, \d+, \d+, true, true, [35](, (false|true))*>", 1),
+                r"gemm_kernel<\d+, \d+, \d+, \d+, true, true, [35](, false)?(, false)?>", 1),
+    "gemm_dw_grouped": (("gemm.hip", "common.h", "lds_dma.h", "kernels.h"),
+                        r"gemm_kernel<\d+, \d+, \d+, \d+, true, true, [35], false, true>", 1),
     "attn_bwd": (("attention.hip", "common.h", "lds_dma.h", "kernels.h"), r"attn_bwd", 2),
 }
 
@@ -307,13 +312,85 @@ def pmc_summary(kernel_tag: str, workload: str, fetch_csv: str, write_csv: str, 
             "source_sha256": kernel_source_hash(kernel_tag, workload), "command": command}
 
 
+def pmc_report(workload: str, stats_csv: str, fetch_csv: str, write_csv: str, mfma_csv: str, command: str) -> None:
+    """Per-kernel counter summary of one benchmark command: average duration
+    (kernel-statistics run), HBM bytes per dispatch from FETCH_SIZE and
+    WRITE_SIZE (each scaled by its reading for a device-to-device copy of
+    CALIBRATION_BYTES), the bandwidth they make over the average duration,
+    and the MFMA busy fraction (rocprofv3's MfmaUtil: MFMA-busy cycles over
+    active cycles times SIMDs), written to profiles/<workload>_kernel_counters.md."""
+    import csv
+    from collections import defaultdict
+
+    def counters(path, name):
+        vals, copy = defaultdict(list), []
+        for r in csv.DictReader(open(path)):
+            if r["Counter_Name"] != name:
+                continue
+            v = float(r["Counter_Value"])
+            if "copyBuffer" in r["Kernel_Name"]:
+                if int(r["Grid_Size"]) >= 1 << 16:
+                    copy.append(v)
+            else:
+                vals[r["Kernel_Name"]].append(v)
+        return vals, (max(copy) if copy else None)
+
+    stats = {}
+    for r in csv.DictReader(open(stats_csv)):
+        stats[r["Name"]] = (int(r["Calls"]), float(r["AverageNs"]) / 1e3, float(r["TotalDurationNs"]) / 1e6)
+    fetch, fcopy = counters(fetch_csv, "FETCH_SIZE")
+    write, wcopy = counters(write_csv, "WRITE_SIZE")
+    mfma, _ = counters(mfma_csv, "MfmaUtil")
+    fs = CALIBRATION_BYTES / (fcopy * 1024.0) if fcopy else None
+    ws = CALIBRATION_BYTES / (wcopy * 1024.0) if wcopy else None
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2609_28568_amd", "csrc")
+    for f in sorted(os.listdir(csrc)):
+        h.update(open(os.path.join(csrc, f), "rb").read())
+    total = sum(t for _, _, t in stats.values())
+    lines = [f"# rocprofv3 kernel counters: {workload}", "",
+             "Commands (from the repository root, `R` = its absolute path, each after "
+             "`cd /tmp && export TMPDIR=/tmp`):", "", "```", command, "```", "",
+             f"Source hash (all of `paper_2609_28568_amd/csrc`): `{h.hexdigest()}`.", "",
+             f"Counter scale factors from the 1 GiB device-to-device copy: FETCH_SIZE x {fs:.3f}, "
+             f"WRITE_SIZE x {ws:.3f} (KiB per dispatch to bytes).", "",
+             "| kernel | calls | avg us | % time | HBM read MB | HBM write MB | HBM GB/s | MFMA busy % |",
+             "|---|---:|---:|---:|---:|---:|---:|---:|"]
+    for name, (calls, avg, tot) in sorted(stats.items(), key=lambda kv: -kv[1][2]):
+        if tot < 0.002 * total:
+            continue
+        fb = sum(fetch[name]) / len(fetch[name]) * 1024.0 * fs if fetch.get(name) and fs else None
+        wb = sum(write[name]) / len(write[name]) * 1024.0 * ws if write.get(name) and ws else None
+        mu = sum(mfma[name]) / len(mfma[name]) if mfma.get(name) else None
+        gbs = (fb + wb) / (avg * 1e-6) / 1e9 if fb is not None and wb is not None else None
+        f = lambda x, d: "" if x is None else f"{x:.{d}f}"
+        short = name.replace("void ", "").replace("(anonymous namespace)::", "")
+        short = short[:short.index("(")] if "(" in short else short
+        lines.append(f"| `{short}` | {calls} | {avg:.1f} | {100 * tot / total:.1f} | {f(fb and fb / 1e6, 1)} | "
+                     f"{f(wb and wb / 1e6, 1)} | {f(gbs, 0)} | {f(mu, 1)} |")
+    lines += ["", "`gemm_kernel<BM, BN, BK, NS, A_T, B_T, EPI, SEG2, GROUPED>`: block tile BM x BN, contraction "
+              "step BK, NS-stage LDS ring, A and B read transposed, epilogue (0 bf16 with optional bias, 1 bias + "
+              "GELU storing the pre-activation too, 2 GELU derivative, 3 fp32, 4 bf16 with bias and residual, "
+              "5 fp32 accumulate, 7 and 8 the two-pass head's softmax statistics and gradient), a second "
+              "contraction segment (adapters), the grouped weight-gradient launch. Calls cover the warm-up and "
+              "timed steps of the profiled command (no evaluation passes); HBM bytes are per dispatch."]
+    out = os.path.join(ROOT, "profiles", f"{workload}_kernel_counters.md")
+    open(out, "w").write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="gpt2_124m")
-    ap.add_argument("--probe", default="gemm_dw", help="kernel class timed for the roofline entry")
+    ap.add_argument("--probe", default=None, help="kernel class timed for the roofline entry (default: the "
+                    "grouped weight-gradient launch for GPT-2, the attention backward for the adapter step)")
+    ap.add_argument("--no-eval", action="store_true", help="skip the forward-only evaluation passes")
+    ap.add_argument("--pmc-report", nargs=4, metavar=("STATS_CSV", "FETCH_CSV", "WRITE_CSV", "MFMA_CSV"),
+                    help="write profiles/<workload>_kernel_counters.md from a rocprofv3 kernel-statistics run and "
+                         "three counter passes (FETCH_SIZE, WRITE_SIZE, MfmaUtil) and exit")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--classes", action="store_true", help="also report every kernel class (extra pass)")
     ap.add_argument("--calibration-copy", action="store_true",
@@ -328,6 +405,11 @@ def main():
                     help="how residual connections meet the following pre-norm: 0 in the projection's epilogue, "
                          "1 the fused add + LayerNorm kernel, 2 separate add and LayerNorm kernels")
     args = ap.parse_args()
+    if args.probe is None:
+        args.probe = "attn_bwd" if args.workload.startswith("qwen3") else "gemm_dw_grouped"
+    if args.pmc_report:
+        pmc_report(args.workload, *args.pmc_report, args.pmc_command)
+        return
     if args.pmc_summary:
         d = pmc_summary(args.probe, args.workload, *args.pmc_summary, args.pmc_command)
         d["workload"] = args.workload
@@ -399,17 +481,19 @@ def main():
           file=sys.stderr, flush=True)
 
     # forward-only evaluation of the same batch (held-out loss path)
-    ev_ids, ev_tgt = dev[0]
-    for _ in range(2):
-        m.evaluate(ev_ids, ev_tgt)
-    n_eval = 10
-    t_ev = time.perf_counter()
-    for _ in range(n_eval):
-        m.evaluate(ev_ids, ev_tgt)
-    ev_ms = (time.perf_counter() - t_ev) * 1e3 / n_eval
-    eval_out = {"tokens_per_s": round(w["B"] * w["T"] / (ev_ms * 1e-3), 1), "ms_per_pass": round(ev_ms, 3),
-                "passes": n_eval, "note": "forward only, one block's activations kept, no dlogits; each pass "
-                                          "synchronises to return its loss"}
+    eval_out = None
+    if not args.no_eval:
+        ev_ids, ev_tgt = dev[0]
+        for _ in range(2):
+            m.evaluate(ev_ids, ev_tgt)
+        n_eval = 10
+        t_ev = time.perf_counter()
+        for _ in range(n_eval):
+            m.evaluate(ev_ids, ev_tgt)
+        ev_ms = (time.perf_counter() - t_ev) * 1e3 / n_eval
+        eval_out = {"tokens_per_s": round(w["B"] * w["T"] / (ev_ms * 1e-3), 1), "ms_per_pass": round(ev_ms, 3),
+                    "passes": n_eval, "note": "forward only, one block's activations kept, logits never stored, "
+                                              "no dlogits; each pass synchronises to return its loss"}
 
     tokens = w["B"] * w["T"] * w.get("grad_accum", 1)
     ms_step = wall * 1e3 / args.steps

@@ -316,14 +316,17 @@ typedef enum gpt2_kclass {
   GPT2_K_GEMM_FWD_GELU = 1,  /* x W^T + bias with the GELU epilogue */
   GPT2_K_GEMM_DX = 2,        /* dY W */
   GPT2_K_GEMM_DX_GELU = 3,   /* dY W times GELU'(pre-activation) */
-  GPT2_K_GEMM_DW = 4,        /* dY^T X into fp32 gradients (or split slices) */
+  GPT2_K_GEMM_DW = 4,        /* dY^T X into fp32 gradients (or split slices);
+                                the LM head's, and the single-block path's */
   GPT2_K_ATTN_FWD = 5,
   GPT2_K_ATTN_BWD = 6,       /* dQ (which also computes D), then dK/dV */
   GPT2_K_LAYERNORM = 7,      /* forward and backward */
   GPT2_K_CROSS_ENTROPY = 8,
   GPT2_K_OPTIMIZER = 9,      /* norm, clip coefficient and AdamW */
   GPT2_K_OTHER = 10,         /* embedding, reductions, casts */
-  GPT2_K_COUNT = 11
+  GPT2_K_GEMM_DW_GROUPED = 11, /* every block weight gradient of a backward
+                                  pass in one grouped launch */
+  GPT2_K_COUNT = 12
 } gpt2_kclass;
 
 gpt2_status gpt2_probe_enable(gpt2_model* m, uint32_t class_mask);

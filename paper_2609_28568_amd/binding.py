@@ -21,7 +21,7 @@ ACT = dict(residual=0, ln1=1, ln1_mean=2, ln1_rstd=3, qkv=4, att=5, att_lse=6, x
            logits=16, losses=17)
 FUSION = dict(residual_norm=0, head_ce=1)
 KCLASS = dict(gemm_fwd=0, gemm_fwd_gelu=1, gemm_dx=2, gemm_dx_gelu=3, gemm_dw=4, attn_fwd=5,
-              attn_bwd=6, layernorm=7, cross_entropy=8, optimizer=9, other=10)
+              attn_bwd=6, layernorm=7, cross_entropy=8, optimizer=9, other=10, gemm_dw_grouped=11)
 
 # parameter kinds of the flat buffer, in order, with the per-layer tensor
 # name each stacked kind is made of

@@ -672,7 +672,7 @@ gpt2_status grouped_weight_grads(Model* m, int acc) {
   fp->C = m->gf(K_FCPROJW); fp->c_stride = (long)(C * F);
   double fl = 0.0;
   for (int i = 0; i < g.ngroups; ++i) fl += 2.0 * g.grp[i].M * (double)g.grp[i].N * d.BT * g.grp[i].count;
-  TRY(m->run(GPT2_K_GEMM_DW, fl, 0.0, [&] { return launch_gemm_grouped(g, m->stream); }));
+  TRY(m->run(GPT2_K_GEMM_DW_GROUPED, fl, 0.0, [&] { return launch_gemm_grouped(g, m->stream); }));
   const int pq = gemm_grouped_bias_parts(g, G_QKV), pf = gemm_grouped_bias_parts(g, G_FC);
   const long nq = (long)d.L * 3 * C, nf = (long)d.L * F;
   TRY(m->run(GPT2_K_OTHER, 0.0, 4.0 * nq * (pq + 1 + acc), [&] {

@@ -78,14 +78,16 @@ def test_every_position_loss(run):
         assert rel_l2(got, ref) < REL_L2
 
 
-# Per-layer slices of the adapter gradients: bf16 activations already differ
-# from the fp32 oracle by 0.5-1 % relative L2 one layer in (measured: the
-# q/k/v projections 0.3 %, the attention output 0.5 %, the SwiGLU output
-# 0.9 %), and the gradient of a 28-layer model through the q/k head norms
-# sits at 1.4 % on average with single layers up to 2.6 %; the bar for a
-# single layer's slice is therefore 3e-2, while every adapter tensor of the
-# library's layout (stacked over the layers) stays within the 2e-2 bar.
-LAYER_REL_L2 = 3e-2
+# Per-layer slices of the adapter gradients meet the same 2e-2 bar as the
+# whole tensors. It is the tightest parity of the suite: the adapter
+# gradient dA = du^T h contracts 2,048 positions with strong cancellation,
+# which amplifies the bf16 rounding of stored activations that the paper's
+# precision prescribes. Emulating that storage alone on the CPU (every
+# tensor this path stores in bf16 rounded inside the oracle's composition,
+# and attention's bf16 probabilities and score gradients) already moves
+# single q/k layers by up to 1.5e-2 from the fp32 oracle (mean 1.1e-2); this
+# path measures up to 1.95e-2 (mean 1.55e-2).
+LAYER_REL_L2 = REL_L2
 
 
 def test_adapter_gradients(run):
