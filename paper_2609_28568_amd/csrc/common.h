@@ -55,16 +55,24 @@ DEV uint32_t hi_pair(uint32_t r0, uint32_t r1) { return (r0 >> 16) | (r1 & 0xfff
 
 // GELU, tanh form: 0.5 u (1 + tanh(y)) with y = sqrt(2/pi) (u + 0.044715 u^3).
 // Evaluated as u * sigmoid(2y) (the same function, since 0.5 (1 + tanh(y)) =
-// 1 / (1 + exp(-2y))) with one exponential and a fast reciprocal.
-DEV float gelu_tanh(float u) {
-  const float k2 = 2.0f * 0.7978845608028654f, a = 0.044715f;
-  const float e = __expf(-k2 * (u + a * u * u * u));
-  return __fdividef(u, 1.0f + e);
+// 1 / (1 + exp(-2y))): exp(-2y) = 2^z with z = -2 y log2(e) = u (G1 + G3 u^2),
+// one hardware base-2 exponential (v_exp_f32) and one hardware reciprocal
+// (v_rcp_f32), both within 1 ulp. An IEEE division here would cost ten
+// instructions more per element of a GEMM epilogue. Large |u| saturate
+// cleanly: 2^z overflows to inf (reciprocal 0) or underflows to 0.
+constexpr float GELU_G1 = -2.0f * 0.7978845608028654f * 1.4426950408889634f;
+constexpr float GELU_G3 = GELU_G1 * 0.044715f;
+DEV float gelu_sigmoid2y(float u, float u2) {
+  const float e = __builtin_amdgcn_exp2f(u * fmaf(GELU_G3, u2, GELU_G1));
+  return __builtin_amdgcn_rcpf(1.0f + e);
 }
-// d/du: s + 2 u s (1 - s) sqrt(2/pi) (1 + 3*0.044715 u^2), s = sigmoid(2y)
+DEV float gelu_tanh(float u) { return u * gelu_sigmoid2y(u, u * u); }
+// d/du = s + u s (1 - s) 2 sqrt(2/pi) (1 + 3*0.044715 u^2) with s = sigmoid(2y),
+// evaluated as s (1 + q), q = u (1 - s) (D0 + D2 u^2)
 DEV float gelu_tanh_grad(float u) {
-  const float k = 0.7978845608028654f, a = 0.044715f;
-  const float e = __expf(-2.0f * k * (u + a * u * u * u));
-  const float s = __fdividef(1.0f, 1.0f + e);
-  return s + 2.0f * u * s * (1.0f - s) * k * (1.0f + 3.0f * a * u * u);
+  constexpr float D0 = 2.0f * 0.7978845608028654f, D2 = D0 * 3.0f * 0.044715f;
+  const float u2 = u * u;
+  const float s = gelu_sigmoid2y(u, u2);
+  const float q = (u * (1.0f - s)) * fmaf(D2, u2, D0);
+  return fmaf(s, q, s);
 }

@@ -454,7 +454,10 @@ __global__ __launch_bounds__(64 * gemm_waves(BM, BK), (NS <= 2 ? 2 : 1)) void ge
   // GELU, GELU derivative or fp32 accumulation applied. Every global read an
   // output block needs (residual, pre-activation, previous fp32 value) is
   // issued before its LDS round trip, so its latency is paid once per block
-  // of 32 rows instead of once per chunk.
+  // of 32 rows instead of once per chunk. Addresses are the block's origin
+  // (uniform across the wave) plus a per-lane 32-bit offset computed once;
+  // a tile lying wholly inside C (every tile when M and N are multiples of
+  // the tile) runs a copy of the loop without bounds checks.
   constexpr int CPR = WTN / 4;                 // 4-column chunks per row
   constexpr int CHUNKS = 32 * CPR / 64;        // chunks per lane per 32-row block
   static_assert((32 * CPR) % 64 == 0, "epilogue chunking");
@@ -476,6 +479,20 @@ __global__ __launch_bounds__(64 * gemm_waves(BM, BK), (NS <= 2 ? 2 : 1)) void ge
       bias4[q] = (g.bias && n < g.N) ? *reinterpret_cast<const float4*>(g.bias + n) : make_float4(0.f, 0.f, 0.f, 0.f);
     }
   }
+  // chunk cc of this lane: row idx / CPR of a 32-row block, columns
+  // (idx % CPR) * 4 .. +3 of the wave's WTN, idx = lane + 64 cc; its offset
+  // from the block's origin (computed where used: kept in registers across
+  // the blocks it would cost the largest tiles spills)
+  auto co = [&](int cc) -> uint32_t {
+    const int idx = lane + 64 * cc;
+    return (uint32_t)(idx / CPR) * (uint32_t)g.ldc + (uint32_t)((idx % CPR) * 4);
+  };
+  const bool interior = m0 + BM <= g.M && n0 + BN <= g.N;
+  auto in_c = [&](auto checked, int mrow0, int cc) -> bool {
+    if constexpr (!decltype(checked)::value) return true;
+    const int idx = lane + 64 * cc;
+    return mrow0 + idx / CPR < g.M && ncol0 + (idx % CPR) * 4 < g.N;
+  };
 
   // every wave is done with the ring before it is reused for staging
   block_barrier();
@@ -491,95 +508,96 @@ __global__ __launch_bounds__(64 * gemm_waves(BM, BK), (NS <= 2 ? 2 : 1)) void ge
   constexpr int RD_AHEAD = TM <= 2 ? TM : 1;
   const bf16_t* rd_src = EPI == EPI_GELU_BWD ? g.aux : g.residual;
   uint2 rd_all[RD16 ? TM : 1][RD16 ? CHUNKS : 1];
-  auto read_block = [&](int i) {
+  auto read_block = [&](int i, auto checked) {
     const int mrow0 = m0 + wm * WTM + i * 32;
+    const bf16_t* src = rd_src + ((size_t)mrow0 * g.ldc + ncol0);
 #pragma unroll
-    for (int cc = 0; cc < CHUNKS; ++cc) {
-      const int idx = lane + 64 * cc;
-      const int m = mrow0 + idx / CPR, n = ncol0 + (idx % CPR) * 4;
-      rd_all[i][cc] = (m < g.M && n < g.N) ? *reinterpret_cast<const uint2*>(rd_src + (size_t)m * g.ldc + n)
-                                           : make_uint2(0, 0);
+    for (int cc = 0; cc < CHUNKS; ++cc)
+      rd_all[i][cc] = in_c(checked, mrow0, cc) ? *reinterpret_cast<const uint2*>(src + co(cc)) : make_uint2(0, 0);
+  };
+  auto store_tile = [&](auto checked) {
+    if constexpr (RD16) {
+#pragma unroll
+      for (int i = 0; i < RD_AHEAD; ++i) read_block(i, checked);
+    }
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+      const int mrow0 = m0 + wm * WTM + i * 32;
+      if constexpr (RD16) {
+        if (i >= RD_AHEAD) read_block(i, checked);
+      }
+      uint2 (&rd)[RD16 ? CHUNKS : 1] = rd_all[RD16 ? i : 0];
+      // lane holds, for row lrow of this 32-row block, columns
+      // 32j + 8q + 4*lg .. +3 of the wave's WTN columns
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int col = 32 * j + 8 * q + 4 * lg;
+          const v4f32_t v = {acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
+          *reinterpret_cast<lds_v4f32_t*>(ep + lrow * EP_LD + col) = v;
+        }
+      __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0): this wave's LDS writes are done
+      __builtin_amdgcn_wave_barrier();
+      // the bias and bf16 inputs read above have landed: one explicit wait here
+      // (otherwise the compiler waits before every store that follows a read)
+      if (i == 0 || (RD16 && i >= RD_AHEAD)) wait_vmcnt<0>();
+      const size_t bo = (size_t)mrow0 * g.ldc + ncol0;
+      float* Cfi = Cf + bo;
+      bf16_t* Cbi = Cb + bo;
+      // read back row segments a group at a time, apply and store
+#pragma unroll
+      for (int c0 = 0; c0 < CHUNKS; c0 += CG) {
+        v4f32_t vals[CG];
+        float4 prev[EPI == EPI_F32_ACC ? CG : 1];
+#pragma unroll
+        for (int c = 0; c < CG; ++c) {
+          const int idx = lane + 64 * (c0 + c);
+          if constexpr (EPI == EPI_F32_ACC)
+            prev[c] = in_c(checked, mrow0, c0 + c) ? *reinterpret_cast<const float4*>(Cfi + co(c0 + c))
+                                                   : make_float4(0.f, 0.f, 0.f, 0.f);
+          vals[c] = *reinterpret_cast<const lds_v4f32_t*>(ep + (idx / CPR) * EP_LD + (idx % CPR) * 4);
+        }
+#pragma unroll
+        for (int c = 0; c < CG; ++c) {
+          const int cc = c0 + c;
+          if (!in_c(checked, mrow0, cc)) continue;
+          float v0 = vals[c].x, v1 = vals[c].y, v2 = vals[c].z, v3 = vals[c].w;
+          const uint32_t off = co(cc);
+          if constexpr (EPI == EPI_F32 || EPI == EPI_F32_ACC) {
+            if constexpr (EPI == EPI_F32_ACC) {
+              v0 += prev[c].x; v1 += prev[c].y; v2 += prev[c].z; v3 += prev[c].w;
+            }
+            *reinterpret_cast<float4*>(Cfi + off) = make_float4(v0, v1, v2, v3);
+          } else if constexpr (EPI == EPI_GELU_BWD) {
+            v0 *= gelu_tanh_grad(lo_f(rd[cc].x)); v1 *= gelu_tanh_grad(hi_f(rd[cc].x));
+            v2 *= gelu_tanh_grad(lo_f(rd[cc].y)); v3 *= gelu_tanh_grad(hi_f(rd[cc].y));
+            *reinterpret_cast<uint2*>(Cbi + off) = make_uint2(pack2(v0, v1), pack2(v2, v3));
+          } else {
+            if constexpr (EPI == EPI_BF16_SCALE) {
+              v0 *= g.alpha; v1 *= g.alpha; v2 *= g.alpha; v3 *= g.alpha;
+            }
+            const float4 bb = bias4[cc % NB];
+            v0 += bb.x; v1 += bb.y; v2 += bb.z; v3 += bb.w;
+            if constexpr (EPI == EPI_GELU) {
+              *reinterpret_cast<uint2*>(Cbi + off) = make_uint2(pack2(v0, v1), pack2(v2, v3));
+              *reinterpret_cast<uint2*>(g.C2 + bo + off) =
+                  make_uint2(pack2(gelu_tanh(v0), gelu_tanh(v1)), pack2(gelu_tanh(v2), gelu_tanh(v3)));
+            } else {
+              if constexpr (EPI == EPI_BF16_RES) {
+                v0 += lo_f(rd[cc].x); v1 += hi_f(rd[cc].x); v2 += lo_f(rd[cc].y); v3 += hi_f(rd[cc].y);
+              }
+              *reinterpret_cast<uint2*>(Cbi + off) = make_uint2(pack2(v0, v1), pack2(v2, v3));
+            }
+          }
+        }
+      }
+      __builtin_amdgcn_s_waitcnt(0xC07F);   // reads done before the next block overwrites
+      __builtin_amdgcn_wave_barrier();
     }
   };
-  if constexpr (RD16) {
-#pragma unroll
-    for (int i = 0; i < RD_AHEAD; ++i) read_block(i);
-  }
-#pragma unroll
-  for (int i = 0; i < TM; ++i) {
-    const int mrow0 = m0 + wm * WTM + i * 32;
-    if constexpr (RD16) {
-      if (i >= RD_AHEAD) read_block(i);
-    }
-    uint2 (&rd)[RD16 ? CHUNKS : 1] = rd_all[RD16 ? i : 0];
-    // lane holds, for row lrow of this 32-row block, columns
-    // 32j + 8q + 4*lg .. +3 of the wave's WTN columns
-#pragma unroll
-    for (int j = 0; j < TN; ++j)
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int col = 32 * j + 8 * q + 4 * lg;
-        const v4f32_t v = {acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
-        *reinterpret_cast<lds_v4f32_t*>(ep + lrow * EP_LD + col) = v;
-      }
-    __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0): this wave's LDS writes are done
-    __builtin_amdgcn_wave_barrier();
-    // the bias and bf16 inputs read above have landed: one explicit wait here
-    // (otherwise the compiler waits before every store that follows a read)
-    if (i == 0 || (RD16 && i >= RD_AHEAD)) wait_vmcnt<0>();
-    // read back row segments a group at a time, apply and store
-#pragma unroll
-    for (int c0 = 0; c0 < CHUNKS; c0 += CG) {
-      v4f32_t vals[CG];
-      float4 prev[EPI == EPI_F32_ACC ? CG : 1];
-#pragma unroll
-      for (int c = 0; c < CG; ++c) {
-        const int idx = lane + 64 * (c0 + c);
-        if constexpr (EPI == EPI_F32_ACC) {
-          const int m = mrow0 + idx / CPR, n = ncol0 + (idx % CPR) * 4;
-          prev[c] = (m < g.M && n < g.N) ? *reinterpret_cast<const float4*>(Cf + (size_t)m * g.ldc + n)
-                                         : make_float4(0.f, 0.f, 0.f, 0.f);
-        }
-        vals[c] = *reinterpret_cast<const lds_v4f32_t*>(ep + (idx / CPR) * EP_LD + (idx % CPR) * 4);
-      }
-#pragma unroll
-      for (int c = 0; c < CG; ++c) {
-        const int cc = c0 + c, idx = lane + 64 * cc;
-        const int m = mrow0 + idx / CPR, n = ncol0 + (idx % CPR) * 4;
-        if (m >= g.M || n >= g.N) continue;
-        float v0 = vals[c].x, v1 = vals[c].y, v2 = vals[c].z, v3 = vals[c].w;
-        const size_t off = (size_t)m * g.ldc + n;
-        if constexpr (EPI == EPI_F32 || EPI == EPI_F32_ACC) {
-          if constexpr (EPI == EPI_F32_ACC) {
-            v0 += prev[c].x; v1 += prev[c].y; v2 += prev[c].z; v3 += prev[c].w;
-          }
-          *reinterpret_cast<float4*>(Cf + off) = make_float4(v0, v1, v2, v3);
-        } else if constexpr (EPI == EPI_GELU_BWD) {
-          v0 *= gelu_tanh_grad(lo_f(rd[cc].x)); v1 *= gelu_tanh_grad(hi_f(rd[cc].x));
-          v2 *= gelu_tanh_grad(lo_f(rd[cc].y)); v3 *= gelu_tanh_grad(hi_f(rd[cc].y));
-          *reinterpret_cast<uint2*>(Cb + off) = make_uint2(pack2(v0, v1), pack2(v2, v3));
-        } else {
-          if constexpr (EPI == EPI_BF16_SCALE) {
-            v0 *= g.alpha; v1 *= g.alpha; v2 *= g.alpha; v3 *= g.alpha;
-          }
-          const float4 bb = bias4[cc % NB];
-          v0 += bb.x; v1 += bb.y; v2 += bb.z; v3 += bb.w;
-          if constexpr (EPI == EPI_GELU) {
-            *reinterpret_cast<uint2*>(Cb + off) = make_uint2(pack2(v0, v1), pack2(v2, v3));
-            *reinterpret_cast<uint2*>(g.C2 + off) =
-                make_uint2(pack2(gelu_tanh(v0), gelu_tanh(v1)), pack2(gelu_tanh(v2), gelu_tanh(v3)));
-          } else {
-            if constexpr (EPI == EPI_BF16_RES) {
-              v0 += lo_f(rd[cc].x); v1 += hi_f(rd[cc].x); v2 += lo_f(rd[cc].y); v3 += hi_f(rd[cc].y);
-            }
-            *reinterpret_cast<uint2*>(Cb + off) = make_uint2(pack2(v0, v1), pack2(v2, v3));
-          }
-        }
-      }
-    }
-    __builtin_amdgcn_s_waitcnt(0xC07F);   // reads done before the next block overwrites
-    __builtin_amdgcn_wave_barrier();
-  }
+  if (interior) store_tile(std::false_type{});
+  else store_tile(std::true_type{});
 }
 
 template <int BM, int BN, int BK, int NS, bool A_T, bool B_T, int EPI, bool SEG2 = false>
