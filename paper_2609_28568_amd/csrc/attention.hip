@@ -19,7 +19,13 @@
 //
 //   forward: per 128 queries (4 waves x 32), walk key tiles: S^T = K Q^T
 //            (one query per lane, so the running max and sum are lane-local up
-//            to an exchange with lane^32), O^T += V^T P^T.
+//            to an exchange with lane^32), O^T += V^T P^T. The softmax takes
+//            the max over the raw scores and folds the scale into the
+//            exponential's argument (one fma, one exp2 per score); the shift
+//            it subtracts only moves when a lane's tile max exceeds it by more
+//            than RESCALE_SLACK (log2 units), so the output accumulators are
+//            rescaled on few tiles. Softmax does not depend on the shift, and
+//            probabilities stay below 2^RESCALE_SLACK.
 //   dQ:      per 128 queries, walk key tiles: recompute P^T, dP^T = V dO^T,
 //            dS^T = P^T (dP^T - D), dQ^T += K^T dS^T. D = rowsum(dO * O) is
 //            computed here from the query's dO and O rows and stored.
@@ -43,9 +49,11 @@ typedef LDS_AS v4f32 lds_v4f32_t;
 constexpr int BQ = 128;     // rows owned by one workgroup (4 waves x 32)
 constexpr float LOG2E = 1.4426950408889634f;
 constexpr float LN2 = 0.6931471805599453f;
+constexpr float RESCALE_SLACK = 8.0f;
 
-// 2^x with the bare hardware instruction: softmax arguments are <= 0 and
-// results below 2^-126 are negligible against the row maximum's 1
+// 2^x with the bare hardware instruction: softmax arguments are at most
+// RESCALE_SLACK (forward) or 0 (backward), and results below 2^-126 are
+// negligible against the row maximum's term of at least 1
 DEV float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
 DEV int bitrev3(int x) { return ((x & 1) << 2) | (x & 2) | ((x >> 2) & 1); }
@@ -234,39 +242,42 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(AttnArgs a) {
     // only tiles that straddle the diagonal or the sequence end are masked
     const bool diag = kv0 + TILE - 1 > q0w || kv0 + TILE > T;
     float mt = -INFINITY;
-    auto scale_mask = [&](auto masked) {
+    auto mask_max = [&](auto masked) {
       const int jmax = min(q, T - 1) - kv0 - 4 * g;   // key j = kv0 + 4g + offset is kept if offset <= jmax
 #pragma unroll
       for (int t = 0; t < 2; ++t)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          float x = s[t][r] * sc;
+          float x = s[t][r];
           if constexpr (decltype(masked)::value) x = (32 * t + acc_row(r, 0) <= jmax) ? x : -INFINITY;
           s[t][r] = x;
           mt = fmaxf(mt, x);
         }
     };
-    if (diag) scale_mask(std::true_type{});
-    else scale_mask(std::false_type{});
-    mt = fmaxf(mt, __shfl_xor(mt, 32, WAVE));
-    const float m_new = fmaxf(m_run, mt);
-    const float alpha = fast_exp2(m_run - m_new);
+    if (diag) mask_max(std::true_type{});
+    else mask_max(std::false_type{});
+    mt = fmaxf(mt, __shfl_xor(mt, 32, WAVE)) * sc;
+    // key 0 is visible to every query, so after tile 0 the shift is finite
+    const bool grow = mt > m_run + RESCALE_SLACK;
+    if (__ballot(grow) != 0) {
+      const float alpha = grow ? fast_exp2(m_run - mt) : 1.0f;
+      m_run = grow ? mt : m_run;
+      l_run *= alpha;
+#pragma unroll
+      for (int d = 0; d < S::DT; ++d)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) o[d][r] *= alpha;
+    }
     float rsum = 0.0f;
 #pragma unroll
     for (int t = 0; t < 2; ++t)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const float p = fast_exp2(s[t][r] - m_new);
+        const float p = fast_exp2(fmaf(s[t][r], sc, -m_run));
         s[t][r] = p;
         rsum += p;
       }
-    rsum += __shfl_xor(rsum, 32, WAVE);
-    l_run = l_run * alpha + rsum;
-    m_run = m_new;
-#pragma unroll
-    for (int d = 0; d < S::DT; ++d)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) o[d][r] *= alpha;
+    l_run += rsum + __shfl_xor(rsum, 32, WAVE);
 #pragma unroll
     for (int t = 0; t < 2; ++t)
 #pragma unroll
