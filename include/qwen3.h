@@ -108,6 +108,20 @@ gpt2_status qwen3_adamw_step(qwen3_model* m, int64_t step, float* d_grad_norm_ou
  * d_token_losses if given. */
 gpt2_status qwen3_loss(qwen3_model* m, float* loss_out, float* d_token_losses);
 
+/* Alternative kernel arrangements, for measurement and for the tests that
+ * compare them (the paper's fusion levers, section "Speed"):
+ *   QWEN3_FUSION_SWIGLU, where the SwiGLU of the MLP runs:
+ *     1 (default) in the GEMM epilogues: the gate|up projection writes its
+ *       pre-activation and silu(gate) up; the input gradient of the down
+ *       projection writes the gate and up gradients from the saved
+ *       pre-activation, and its own output is never stored (a projection
+ *       with an adapter keeps the separate kernels);
+ *     0 separate SwiGLU forward and backward kernels between the GEMMs.
+ *   Both compute the same bits. GPT2_ERR_INVALID_ARG for an unknown
+ *   arrangement or mode. */
+enum { QWEN3_FUSION_SWIGLU = 0 };
+gpt2_status qwen3_set_fusion(qwen3_model* m, int32_t fusion, int32_t mode);
+
 void qwen3_destroy(qwen3_model* m);
 const char* qwen3_last_error(const qwen3_model* m);
 

@@ -76,3 +76,16 @@ DEV float gelu_tanh_grad(float u) {
   const float q = (u * (1.0f - s)) * fmaf(D2, u2, D0);
   return fmaf(s, q, s);
 }
+
+// SwiGLU of one (gate g, up u) pair, silu(g) u with silu(g) = g sigmoid(g),
+// and its gradients given the output gradient d: dg = d u s (1 + g (1 - s)),
+// du = d g s with s = sigmoid(g) = 1 / (1 + e^-g), the division correctly
+// rounded. Shared by the separate SwiGLU kernels and the GEMM epilogues that
+// fuse them, so the two arrangements compute the same bits.
+DEV float sigmoid_f(float x) { return 1.0f / (1.0f + __expf(-x)); }
+DEV float swiglu1(float g, float u) { return g * sigmoid_f(g) * u; }
+DEV void swiglu1_bwd(float d, float g, float u, float& dg, float& du) {
+  const float s = sigmoid_f(g);
+  dg = d * u * s * (1.0f + g * (1.0f - s));
+  du = d * g * s;
+}

@@ -81,8 +81,13 @@ constexpr int gemm_waves(int bm, int bk) { return bm >= 256 && bk >= 64 ? 8 : 4;
 // BK contraction steps starting at k0) into the stage at `dst`. Wave w of NW
 // issues instructions w, w+NW, ...; each instruction moves 64 units (1 KB),
 // unit u of the tile going to byte 16*u.
-template <int R, int BK, bool TR, int NW>
-DEV void issue_tile(v4i32 rs, int ld, int r0, int k0, lds_char_t* dst, int wave, int lane) {
+// With PAIRS (a contraction-contiguous operand only), tile row r reads
+// operand row r0 + 32 (r / 64) + r % 32, plus alt for the odd 32-row groups:
+// 32 rows of one block of the operand, then the same 32 rows of the block
+// alt rows further on, and so on.
+template <int R, int BK, bool TR, int NW, bool PAIRS = false>
+DEV void issue_tile(v4i32 rs, int ld, int r0, int k0, lds_char_t* dst, int wave, int lane, int alt = 0) {
+  static_assert(!PAIRS || (!TR && R % 64 == 0), "paired rows: contraction-contiguous tiles of whole 64-row pairs");
   constexpr int UNITS = R * BK / 8;
   constexpr int INSTR = UNITS / 64;
   static_assert(UNITS % (64 * NW) == 0, "tile must split evenly over the waves");
@@ -95,7 +100,8 @@ DEV void issue_tile(v4i32 rs, int ld, int r0, int k0, lds_char_t* dst, int wave,
       constexpr int U = BK / 8;
       const int row = u / U, p = u % U;
       const int c = unit_n<BK>(row, p) - row * U;   // the XOR is its own inverse
-      off = ((uint32_t)(r0 + row) * (uint32_t)ld + (uint32_t)(k0 + c * 8)) * 2u;
+      const int grow = PAIRS ? r0 + 32 * (row >> 6) + (row & 31) + ((row >> 5) & 1) * alt : r0 + row;
+      off = ((uint32_t)grow * (uint32_t)ld + (uint32_t)(k0 + c * 8)) * 2u;
     } else {
       const int k = u / (R / 8), p = u % (R / 8);
       const int c = unit_t<R>(k, p) - k * (R / 8);
@@ -253,7 +259,10 @@ __global__ __launch_bounds__(64 * gemm_waves(BM, BK), (NS <= 2 ? 2 : 1)) void ge
     if (!SEG2 || kt < nk1) {
       const int k0 = kbeg + kt * BK;
       issue_tile<BM, BK, A_T, NW>(ra, g.lda, m0, k0, st, wave, lane);
-      issue_tile<BN, BK, B_T, NW>(rb, g.ldb, n0 + bcol, k0, st + A_BYTES, wave, lane);
+      if constexpr (EPI == EPI_SWIGLU)
+        issue_tile<BN, BK, B_T, NW, true>(rb, g.ldb, n0 / 2, k0, st + A_BYTES, wave, lane, g.N / 2);
+      else
+        issue_tile<BN, BK, B_T, NW>(rb, g.ldb, n0 + bcol, k0, st + A_BYTES, wave, lane);
     } else {
       const int k2 = (kt - nk1) * BK;
       issue_tile<BM, BK, A_T, NW>(ra2, g.lda2, m0, a2col + k2, st, wave, lane);
@@ -506,7 +515,7 @@ __global__ __launch_bounds__(64 * gemm_waves(BM, BK), (NS <= 2 ? 2 : 1)) void ge
   // with at most two 32-row blocks per wave the bf16 inputs of the whole tile
   // are read up front; otherwise block by block
   constexpr int RD_AHEAD = TM <= 2 ? TM : 1;
-  const bf16_t* rd_src = EPI == EPI_GELU_BWD ? g.aux : g.residual;
+  const bf16_t* rd_src = (EPI == EPI_GELU_BWD || EPI == EPI_SWIGLU_BWD) ? g.aux : g.residual;
   uint2 rd_all[RD16 ? TM : 1][RD16 ? CHUNKS : 1];
   auto read_block = [&](int i, auto checked) {
     const int mrow0 = m0 + wm * WTM + i * 32;
@@ -545,17 +554,52 @@ __global__ __launch_bounds__(64 * gemm_waves(BM, BK), (NS <= 2 ? 2 : 1)) void ge
       const size_t bo = (size_t)mrow0 * g.ldc + ncol0;
       float* Cfi = Cf + bo;
       bf16_t* Cbi = Cb + bo;
+      if constexpr (EPI == EPI_SWIGLU) {
+        // The wave's 64 staged columns are the gate values of features
+        // f0..f0+31, then the up values of the same features (the B rows were
+        // loaded in such pairs). Lane slot pi = lane + 64 pp takes row pi / 8
+        // and features f0 + 4 (pi % 8) .. +3 of both halves: the
+        // pre-activation (gate columns, then up columns) and silu(gate) up,
+        // from the bf16-rounded values as the separate kernel computes it;
+        // eight lanes write 64 contiguous bytes of a row.
+        static_assert(TN == 2 && !A_T && !B_T && !SEG2, "SwiGLU: 64 columns per wave, no second segment");
+        const int F = g.N / 2, f0 = ncol0 / 2;
+#pragma unroll
+        for (int pp = 0; pp < 4; ++pp) {
+          const int pi = lane + 64 * pp, row = pi >> 3, k = pi & 7;
+          const int m = mrow0 + row, f = f0 + 4 * k;
+          const v4f32_t gv = *reinterpret_cast<const lds_v4f32_t*>(ep + row * EP_LD + 4 * k);
+          const v4f32_t uv = *reinterpret_cast<const lds_v4f32_t*>(ep + row * EP_LD + 32 + 4 * k);
+          if (decltype(checked)::value && (m >= g.M || f >= F)) continue;
+          const uint2 gw = make_uint2(pack2(gv.x, gv.y), pack2(gv.z, gv.w));
+          const uint2 uw = make_uint2(pack2(uv.x, uv.y), pack2(uv.z, uv.w));
+          bf16_t* pre = Cb + (size_t)m * g.ldc;
+          *reinterpret_cast<uint2*>(pre + f) = gw;
+          *reinterpret_cast<uint2*>(pre + F + f) = uw;
+          *reinterpret_cast<uint2*>(g.C2 + (size_t)m * F + f) =
+              make_uint2(pack2(swiglu1(lo_f(gw.x), lo_f(uw.x)), swiglu1(hi_f(gw.x), hi_f(uw.x))),
+                         pack2(swiglu1(lo_f(gw.y), lo_f(uw.y)), swiglu1(hi_f(gw.y), hi_f(uw.y))));
+        }
+      } else {
       // read back row segments a group at a time, apply and store
 #pragma unroll
       for (int c0 = 0; c0 < CHUNKS; c0 += CG) {
         v4f32_t vals[CG];
         float4 prev[EPI == EPI_F32_ACC ? CG : 1];
+        // SwiGLU backward: the saved gate and up values of the chunk's features
+        uint2 gx[EPI == EPI_SWIGLU_BWD ? CG : 1], ux[EPI == EPI_SWIGLU_BWD ? CG : 1];
 #pragma unroll
         for (int c = 0; c < CG; ++c) {
           const int idx = lane + 64 * (c0 + c);
           if constexpr (EPI == EPI_F32_ACC)
             prev[c] = in_c(checked, mrow0, c0 + c) ? *reinterpret_cast<const float4*>(Cfi + co(c0 + c))
                                                    : make_float4(0.f, 0.f, 0.f, 0.f);
+          if constexpr (EPI == EPI_SWIGLU_BWD) {
+            const bool ok = in_c(checked, mrow0, c0 + c);
+            const bf16_t* src = rd_src + bo + co(c0 + c);
+            gx[c] = ok ? *reinterpret_cast<const uint2*>(src) : make_uint2(0, 0);
+            ux[c] = ok ? *reinterpret_cast<const uint2*>(src + g.N) : make_uint2(0, 0);
+          }
           vals[c] = *reinterpret_cast<const lds_v4f32_t*>(ep + (idx / CPR) * EP_LD + (idx % CPR) * 4);
         }
 #pragma unroll
@@ -569,6 +613,16 @@ __global__ __launch_bounds__(64 * gemm_waves(BM, BK), (NS <= 2 ? 2 : 1)) void ge
               v0 += prev[c].x; v1 += prev[c].y; v2 += prev[c].z; v3 += prev[c].w;
             }
             *reinterpret_cast<float4*>(Cfi + off) = make_float4(v0, v1, v2, v3);
+          } else if constexpr (EPI == EPI_SWIGLU_BWD) {
+            // the output gradient rounded to bf16, as the separate kernel reads it
+            const uint32_t d01 = pack2(v0, v1), d23 = pack2(v2, v3);
+            float dg[4], du[4];
+            swiglu1_bwd(lo_f(d01), lo_f(gx[c].x), lo_f(ux[c].x), dg[0], du[0]);
+            swiglu1_bwd(hi_f(d01), hi_f(gx[c].x), hi_f(ux[c].x), dg[1], du[1]);
+            swiglu1_bwd(lo_f(d23), lo_f(gx[c].y), lo_f(ux[c].y), dg[2], du[2]);
+            swiglu1_bwd(hi_f(d23), hi_f(gx[c].y), hi_f(ux[c].y), dg[3], du[3]);
+            *reinterpret_cast<uint2*>(Cbi + off) = make_uint2(pack2(dg[0], dg[1]), pack2(dg[2], dg[3]));
+            *reinterpret_cast<uint2*>(Cbi + off + g.N) = make_uint2(pack2(du[0], du[1]), pack2(du[2], du[3]));
           } else if constexpr (EPI == EPI_GELU_BWD) {
             v0 *= gelu_tanh_grad(lo_f(rd[cc].x)); v1 *= gelu_tanh_grad(hi_f(rd[cc].x));
             v2 *= gelu_tanh_grad(lo_f(rd[cc].y)); v3 *= gelu_tanh_grad(hi_f(rd[cc].y));
@@ -591,6 +645,7 @@ __global__ __launch_bounds__(64 * gemm_waves(BM, BK), (NS <= 2 ? 2 : 1)) void ge
             }
           }
         }
+      }
       }
       __builtin_amdgcn_s_waitcnt(0xC07F);   // reads done before the next block overwrites
       __builtin_amdgcn_wave_barrier();
@@ -656,6 +711,11 @@ hipError_t launch_cfg(const GemmArgs& g, int a_t, int b_t, int epi, hipStream_t 
   if (!a_t && !b_t && epi == EPI_CE_GRAD) return launch_t<BM, BN, BK, 2, false, false, EPI_CE_GRAD>(g, s);
   if (!a_t && b_t && epi == EPI_BF16) return launch_bf16<BM, BN, BK, true>(g, s);
   if (!a_t && b_t && epi == EPI_GELU_BWD) return launch_t<BM, BN, BK, 2, false, true, EPI_GELU_BWD>(g, s);
+  if (!a_t && b_t && epi == EPI_SWIGLU_BWD) return launch_t<BM, BN, BK, 2, false, true, EPI_SWIGLU_BWD>(g, s);
+  if (!a_t && !b_t && epi == EPI_SWIGLU) {
+    if constexpr (BN == 128) return launch_t<BM, BN, BK, 2, false, false, EPI_SWIGLU>(g, s);
+    return hipErrorInvalidValue;
+  }
   // products with few output tiles and a long contraction, split into fp32 slices
   if (!a_t && b_t && epi == EPI_F32 && !g.accumulate) return launch_t<BM, BN, BK, 2, false, true, EPI_F32>(g, s);
   if (!a_t && !b_t && epi == EPI_F32 && !g.accumulate) return launch_t<BM, BN, BK, 2, false, false, EPI_F32>(g, s);
@@ -686,6 +746,9 @@ hipError_t launch_cfg(const GemmArgs& g, int a_t, int b_t, int epi, hipStream_t 
 // 128 x 128, 64-deep except for weight gradients (the Qwen3-shaped step:
 // input gradients -17 %, forward products -4 % against 32-deep stages).
 GemmConfig gemm_config(int M, int N, int a_t, int b_t, int epi) {
+  // the fused SwiGLU pairs the two 32-column fragments of a wave: 128-wide tiles
+  if (epi == EPI_SWIGLU)
+    return (M >= 256 && (long)((M + 255) / 256) * (N / 128) >= 512) ? GemmConfig{256, 128, 32} : GemmConfig{128, 128, 64};
   if (N >= 192 && N % 192 == 0) {
     if (a_t) {
       if (M >= 192 && M % 192 == 0) return {192, 192, 32};
@@ -740,6 +803,14 @@ hipError_t launch_gemm(const GemmArgs& g0, int a_t, int b_t, int epi, hipStream_
     if (g.k_chunk % 64 || (long)g.k_chunk * g.splits < g.K || (long)g.k_chunk * (g.splits - 1) >= g.K)
       return hipErrorInvalidValue;
     if (epi != EPI_F32) return hipErrorInvalidValue;
+  }
+  if (epi == EPI_SWIGLU || epi == EPI_SWIGLU_BWD) {
+    // one contraction, A not transposed; SwiGLU: B not transposed, gate and up
+    // rows in 64-row pairs of tiles, both outputs given; its backward: the
+    // pre-activation to read and room for both gradients in each row
+    if (a_t || g.K2 > 0 || g.splits > 1 || g.bias || g.residual) return hipErrorInvalidValue;
+    if (epi == EPI_SWIGLU && (b_t || g.N % 128 || !g.C2 || g.ldc < g.N)) return hipErrorInvalidValue;
+    if (epi == EPI_SWIGLU_BWD && (!b_t || g.N % 4 || !g.aux || g.ldc < 2 * g.N)) return hipErrorInvalidValue;
   }
   if (g.K2 > 0) {
     if (g.splits > 1 || g.K % 64 || g.K2 % 64 || !g.A2 || !g.B2 || a_t) return hipErrorInvalidValue;

@@ -14,7 +14,19 @@ enum GemmEpilogue {
   EPI_GELU_BWD = 2,  // C = bf16(acc * gelu'(aux))
   EPI_F32 = 3,       // C (fp32, one slice per split) = acc (+ C if accumulate)
   EPI_CE_STATS = 7,  // softmax statistics of each row, see GemmArgs
-  EPI_CE_GRAD = 8    // softmax cross-entropy gradient of each row, see GemmArgs
+  EPI_CE_GRAD = 8,   // softmax cross-entropy gradient of each row, see GemmArgs
+  // SwiGLU fused into the gate|up projection (B = [gate rows; up rows], N =
+  // 2F output columns, no second segment, tiles 128 columns wide): a tile's
+  // B rows alternate 32 gate rows and the 32 up rows of the same features, so
+  // C = the pre-activation [M][2F] (gate columns, then up columns, row stride
+  // ldc) and C2 = silu(gate) up [M][F] (row stride F), computed from the
+  // bf16-rounded pre-activation as the separate kernel does
+  EPI_SWIGLU = 9,
+  // SwiGLU backward fused into the input gradient of the down projection
+  // (N = F): the product, rounded to bf16, is the gradient of silu(gate) up;
+  // with aux = the saved pre-activation [M][2F] (row stride ldc) the epilogue
+  // writes C = [gate gradient | up gradient] [M][2F] (row stride ldc)
+  EPI_SWIGLU_BWD = 10
 };
 
 struct GemmArgs {

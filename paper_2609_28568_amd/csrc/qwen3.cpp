@@ -250,6 +250,7 @@ struct qwen3_model {
   size_t n_lora;
   size_t base_off[B_NKIND];
   bool have_targets = false, have_grads = false;
+  int swiglu_fused = 1;   // QWEN3_FUSION_SWIGLU mode
   std::string err;
   ProbeSet<QWEN3_K_COUNT> probes;
 
@@ -605,8 +606,17 @@ gpt2_status qwen3_forward(qwen3_model* m, const int32_t* d_inputs, const int32_t
       return launch_rmsnorm_fwd(xmid, m->base(B_POST_NORM) + (size_t)l * d.C, h2, r2, BT, d.C, m->cfg.rms_eps, 1, 0,
                                 m->stream);
     }));
-    TRY(proj_fwd(m, G_GU, l, h2, m->base(B_GU) + (size_t)l * 2 * d.F * d.C, gu, 2 * d.F, nullptr));
-    TRY(m->run(OTHER, 0.0, 6.0 * d.BT * d.F, [&] { return launch_swiglu_fwd(gu, mm, d.BT, d.F, m->stream); }));
+    if (m->swiglu_fused && !m->has(G_GU)) {
+      // gate|up projection with the SwiGLU in its epilogue: writes the
+      // pre-activation (kept for the backward) and the output
+      GemmArgs a{};
+      a.A = h2; a.lda = d.C; a.B = m->base(B_GU) + (size_t)l * 2 * d.F * d.C; a.ldb = d.C;
+      a.M = BT; a.N = 2 * d.F; a.K = d.C; a.C = gu; a.ldc = 2 * d.F; a.C2 = mm;
+      TRY(run_gemm(m, FWD, mnk2(d.BT, 2 * d.F, d.C), a, 0, 0, EPI_SWIGLU));
+    } else {
+      TRY(proj_fwd(m, G_GU, l, h2, m->base(B_GU) + (size_t)l * 2 * d.F * d.C, gu, 2 * d.F, nullptr));
+      TRY(m->run(OTHER, 0.0, 6.0 * d.BT * d.F, [&] { return launch_swiglu_fwd(gu, mm, d.BT, d.F, m->stream); }));
+    }
     TRY(proj_fwd(m, G_DN, l, mm, m->base(B_DOWN) + (size_t)l * d.C * d.F, m->res(l + 1), d.C, xmid));
   }
   // final norm and LM head on the positions that carry loss (compacted rows)
@@ -667,9 +677,18 @@ gpt2_status qwen3_backward(qwen3_model* m) {
     bf16_t* dm = m->wb(m->ws.dm);
     bf16_t* dgu = m->wb(m->ws.dgu);
     // down projection: res(l+1) = xmid + m down^T (+ adapter)
-    TRY(proj_bwd(m, G_DN, l, dres, d.C, mm, m->base(B_DOWN) + (size_t)l * d.C * d.F, dm));
-    TRY(m->run(QWEN3_K_OTHER, 0.0, 10.0 * d.BT * d.F,
-               [&] { return launch_swiglu_bwd(dm, gu, dgu, d.BT, d.F, m->stream); }));
+    if (m->swiglu_fused && !m->has(G_DN)) {
+      // no adapter: only its input gradient, with the SwiGLU backward in the
+      // epilogue (dgu from the gradient of m and the saved pre-activation)
+      GemmArgs a{};
+      a.A = dres; a.lda = d.C; a.B = m->base(B_DOWN) + (size_t)l * d.C * d.F; a.ldb = d.F;
+      a.M = BT; a.N = d.F; a.K = d.C; a.C = dgu; a.ldc = 2 * d.F; a.aux = gu;
+      TRY(run_gemm(m, DX, mnk2(d.BT, d.F, d.C), a, 0, 1, EPI_SWIGLU_BWD));
+    } else {
+      TRY(proj_bwd(m, G_DN, l, dres, d.C, mm, m->base(B_DOWN) + (size_t)l * d.C * d.F, dm));
+      TRY(m->run(QWEN3_K_OTHER, 0.0, 10.0 * d.BT * d.F,
+                 [&] { return launch_swiglu_bwd(dm, gu, dgu, d.BT, d.F, m->stream); }));
+    }
     TRY(proj_bwd(m, G_GU, l, dgu, 2 * d.F, h2, m->base(B_GU) + (size_t)l * 2 * d.F * d.C, dh));
     TRY(m->run(NORM, 0.0, 4.0 * rowb + 4.0 * d.BT, [&] {
       return launch_rmsnorm_bwd(dh, xmid, r2, m->base(B_POST_NORM) + (size_t)l * d.C, dres, 1, BT, d.C, 1, 0,
@@ -744,6 +763,16 @@ gpt2_status qwen3_loss(qwen3_model* m, float* loss_out, float* d_token_losses) {
   TRY(hipMemcpyAsync(loss_out, m->af(m->act.loss), 4, hipMemcpyDeviceToHost, m->stream));
   TRY(hipStreamSynchronize(m->stream));
   return GPT2_OK;
+}
+
+gpt2_status qwen3_set_fusion(qwen3_model* m, int32_t fusion, int32_t mode) {
+  if (!m) return GPT2_ERR_INVALID_ARG;
+  if (fusion == QWEN3_FUSION_SWIGLU) {
+    if (mode < 0 || mode > 1) return fail(m, GPT2_ERR_INVALID_ARG, "SwiGLU mode must be 0 or 1");
+    m->swiglu_fused = mode;
+    return GPT2_OK;
+  }
+  return fail(m, GPT2_ERR_INVALID_ARG, "unknown fusion");
 }
 
 void qwen3_destroy(qwen3_model* m) { delete m; }

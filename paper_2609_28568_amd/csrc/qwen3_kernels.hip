@@ -266,7 +266,6 @@ __global__ __launch_bounds__(256) void qknorm_rope_bwd_kernel(const bf16_t* __re
   *reinterpret_cast<uint4*>(draw + off) = pack8(o);
 }
 
-DEV float sigmoid_f(float x) { return 1.0f / (1.0f + __expf(-x)); }
 
 // m[r][c] = silu(gu[r][c]) * gu[r][F + c]; 4 columns per thread
 __global__ void swiglu_fwd_kernel(const bf16_t* __restrict__ gu, bf16_t* __restrict__ m, long rows, int F) {
@@ -280,7 +279,7 @@ __global__ void swiglu_fwd_kernel(const bf16_t* __restrict__ gu, bf16_t* __restr
   const float uv[4] = {lo_f(u.x), hi_f(u.x), lo_f(u.y), hi_f(u.y)};
   float o[4];
 #pragma unroll
-  for (int e = 0; e < 4; ++e) o[e] = gv[e] * sigmoid_f(gv[e]) * uv[e];
+  for (int e = 0; e < 4; ++e) o[e] = swiglu1(gv[e], uv[e]);
   *reinterpret_cast<uint2*>(m + i) = make_uint2(pack2(o[0], o[1]), pack2(o[2], o[3]));
 }
 
@@ -300,9 +299,7 @@ __global__ void swiglu_bwd_kernel(const bf16_t* __restrict__ dm, const bf16_t* _
   float dg[4], du[4];
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
-    const float s = sigmoid_f(gv[e]);
-    dg[e] = dv[e] * uv[e] * s * (1.0f + gv[e] * (1.0f - s));
-    du[e] = dv[e] * gv[e] * s;
+    swiglu1_bwd(dv[e], gv[e], uv[e], dg[e], du[e]);
   }
   *reinterpret_cast<uint2*>(dgu + (size_t)r * 2 * F + c) = make_uint2(pack2(dg[0], dg[1]), pack2(dg[2], dg[3]));
   *reinterpret_cast<uint2*>(dgu + (size_t)r * 2 * F + F + c) = make_uint2(pack2(du[0], du[1]), pack2(du[2], du[3]));

@@ -16,6 +16,7 @@ from .binding import LibError, lib as _lib_gpt2
 
 RP = 64   # padded adapter rank of the library
 # kernel classes of the timing probes (QWEN3_K_* in include/qwen3.h)
+FUSION = dict(swiglu=0)
 KCLASS = dict(gemm_fwd=0, gemm_dx=1, gemm_adapter=2, attn_fwd=3, attn_bwd=4, norm=5, cross_entropy=6, optimizer=7,
               other=8)
 GROUPS = {"qkv": 1, "o": 2, "gate_up": 4, "down": 8}
@@ -62,6 +63,7 @@ def lib():
         "qwen3_backward": (I32, [P]),
         "qwen3_adamw_step": (I32, [P, ctypes.c_int64, P]),
         "qwen3_loss": (I32, [P, ctypes.POINTER(F32), P]),
+        "qwen3_set_fusion": (I32, [P, I32, I32]),
         "qwen3_destroy": (None, [P]),
         "qwen3_last_error": (ctypes.c_char_p, [P]),
         "qwen3_probe_enable": (I32, [P, ctypes.c_uint32]),
@@ -268,6 +270,10 @@ class Qwen3:
         return v.value
 
     # ---- probes -------------------------------------------------------------
+    def set_fusion(self, fusion: str, mode: int):
+        """Select an alternative kernel arrangement (qwen3_set_fusion)."""
+        _check(lib().qwen3_set_fusion(self.h, FUSION[fusion], int(mode)), self.h)
+
     def probe_enable(self, classes):
         mask = 0
         for c in classes:

@@ -28,7 +28,7 @@ def _cfg(name="qwen3_tiny", **over):
 
 def test_library_exports_every_declared_function():
     names = header_functions()
-    assert len(names) == 13
+    assert len(names) == 14
     L = qb.lib()
     for n in names:
         assert hasattr(L, n), n
@@ -127,6 +127,7 @@ def test_null_arguments_are_rejected():
     assert L.qwen3_query_sizes(None, None) == binding.GPT2_ERR_INVALID_ARG
     assert L.qwen3_forward(None, None, None) == binding.GPT2_ERR_INVALID_ARG
     assert L.qwen3_backward(None) == binding.GPT2_ERR_INVALID_ARG
+    assert L.qwen3_set_fusion(None, 0, 1) == binding.GPT2_ERR_INVALID_ARG
     assert L.qwen3_adamw_step(None, 0, None) == binding.GPT2_ERR_INVALID_ARG
     w, cfg = _cfg()
     assert L.qwen3_init(ctypes.byref(cfg), None, None, None) == binding.GPT2_ERR_INVALID_ARG
