@@ -100,6 +100,7 @@ def qwen3_bench(args) -> None:
     base, lora = synth.init_qwen3(w)
     ids, tgt = synth.token_batch(w)
     m = qb.Qwen3(qb.make_config(w, synth.QWEN3_OPTIM))
+    m.set_fusion("swiglu", args.swiglu)
     m.set_base(base)
     m.set_lora(lora)
     dev_ids, dev_tgt = torch.from_numpy(ids).cuda(), torch.from_numpy(tgt).cuda()
@@ -176,7 +177,8 @@ def qwen3_bench(args) -> None:
                    "n_kv_head": w["n_kv_head"], "head_dim": w["head_dim"], "d_ff": w["d_ff"], "vocab": w["vocab"],
                    "global_batch": w["B"], "seq_len": w["T"], "lora_rank": w["lora_rank"],
                    "lora_targets": list(w["lora_targets"]), "loss_from": w["loss_from"],
-                   "tokens_per_step": tokens, "token_dist": "zipf(1.1)", "parallelism": "none"},
+                   "tokens_per_step": tokens, "token_dist": "zipf(1.1)", "parallelism": "none",
+                   "swiglu_fused": args.swiglu},
         "mfu": round(tok_s * f_tok / (PEAK_BF16_TFLOPS * 1e12), 4),
         "flops_per_token": f_tok,
         "peak_tflops": PEAK_BF16_TFLOPS,
@@ -404,6 +406,8 @@ def main():
     ap.add_argument("--residual-norm", type=int, default=0,
                     help="how residual connections meet the following pre-norm: 0 in the projection's epilogue, "
                          "1 the fused add + LayerNorm kernel, 2 separate add and LayerNorm kernels")
+    ap.add_argument("--swiglu", type=int, default=1,
+                    help="Qwen3-shaped workload: 1 SwiGLU in the GEMM epilogues, 0 separate SwiGLU kernels")
     args = ap.parse_args()
     if args.probe is None:
         args.probe = "attn_bwd" if args.workload.startswith("qwen3") else "gemm_dw_grouped"
