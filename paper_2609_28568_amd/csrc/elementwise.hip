@@ -165,20 +165,21 @@ __global__ void embed_fwd_kernel(const int32_t* __restrict__ ids, const float* _
 }
 
 // token table: scatter-add of each position's gradient into its id's row.
-// A workgroup takes EMB_P consecutive positions and one 256-column slice of
-// the row; it sorts the positions by (id, position) in LDS, and each wave
+// A workgroup takes EMB_P consecutive positions and one EMB_C-column slice of
+// the row (two columns per lane: at C = 768, 16,384 positions make 384
+// workgroups); it sorts the positions by (id, position) in LDS, and each wave
 // walks 64 of the sorted positions, summing runs of equal ids in registers
 // and adding each run once with fp32 atomics. Frequent ids (the token
 // distribution is Zipf-like) then cost one atomic per workgroup instead of
 // one per occurrence.
-constexpr int EMB_P = 256;
+constexpr int EMB_P = 256, EMB_C = 128;
 __global__ __launch_bounds__(256) void embed_bwd_wte_kernel(const int32_t* __restrict__ ids,
                                                             const bf16_t* __restrict__ dx, float* __restrict__ dwte,
                                                             int BT, int C, int V) {
   __shared__ unsigned long long key[EMB_P];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int p0 = blockIdx.x * EMB_P;
-  const int c = blockIdx.y * 256 + 4 * lane;
+  const int c = blockIdx.y * EMB_C + 2 * lane;
   {
     // positions past the end and ids outside [0, V) (a contract violation,
     // reported by the forward pass) take the key that sorts last and is skipped
@@ -202,24 +203,24 @@ __global__ __launch_bounds__(256) void embed_bwd_wte_kernel(const int32_t* __res
       __syncthreads();
     }
   const bool col_ok = c < C;
-  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+  float2 acc = make_float2(0.f, 0.f);
   constexpr int BATCH = 8;
   for (int k0 = 0; k0 < 64; k0 += BATCH) {
     unsigned long long kk[BATCH];
-    uint2 u[BATCH];
+    uint32_t u[BATCH];
 #pragma unroll
     for (int q = 0; q < BATCH; ++q) {
       kk[q] = key[64 * w + k0 + q];
-      u[q] = make_uint2(0, 0);
+      u[q] = 0;
       if (kk[q] != ~0ull && col_ok) {
         const uint32_t pos = (uint32_t)kk[q];
-        u[q] = *reinterpret_cast<const uint2*>(dx + (size_t)pos * C + c);
+        u[q] = *reinterpret_cast<const uint32_t*>(dx + (size_t)pos * C + c);
       }
     }
 #pragma unroll
     for (int q = 0; q < BATCH; ++q) {
       if (kk[q] == ~0ull) continue;
-      acc.x += lo_f(u[q].x); acc.y += hi_f(u[q].x); acc.z += lo_f(u[q].y); acc.w += hi_f(u[q].y);
+      acc.x += lo_f(u[q]); acc.y += hi_f(u[q]);
       const int kn = k0 + q + 1;
       const unsigned long long nxt = kn < 64 ? key[64 * w + kn] : ~0ull;
       const uint32_t id = (uint32_t)(kk[q] >> 32);
@@ -228,10 +229,8 @@ __global__ __launch_bounds__(256) void embed_bwd_wte_kernel(const int32_t* __res
           float* d = dwte + (size_t)id * C + c;
           atomicAdd(d + 0, acc.x);
           atomicAdd(d + 1, acc.y);
-          atomicAdd(d + 2, acc.z);
-          atomicAdd(d + 3, acc.w);
         }
-        acc = make_float4(0.f, 0.f, 0.f, 0.f);
+        acc = make_float2(0.f, 0.f);
       }
     }
   }
@@ -594,7 +593,7 @@ hipError_t launch_embed_bwd(const int32_t* ids, const bf16_t* dx, float* dwte, i
                             hipStream_t s) {
   if (C % 4) return hipErrorInvalidValue;
   const int BT = B * T;
-  dim3 grid((BT + EMB_P - 1) / EMB_P, (C + 255) / 256);
+  dim3 grid((BT + EMB_P - 1) / EMB_P, (C + EMB_C - 1) / EMB_C);
   hipLaunchKernelGGL(embed_bwd_wte_kernel, grid, dim3(256), 0, s, ids, dx, dwte, BT, C, V);
   return hipGetLastError();
 }
