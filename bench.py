@@ -218,6 +218,64 @@ def cpu_baseline(w: dict, params, ids, tgt) -> dict:
                       f"model and token stream, numpy fp32 with {threads} BLAS threads, {dt:.1f} s"}
 
 
+def block_measure(with_cpu: bool) -> dict:
+    """The single-block configuration: one GPT-2 124M block on 16 sequences of
+    1024 tokens (bf16 input ~ N(0,1), upstream gradient ~ N(0, 1e-3)), forward
+    and then backward to the block's weight gradients and its input gradient.
+    GPU: 20 passes after 3 untimed ones, timed with HIP events on the stream;
+    with_cpu, the oracle's block forward and backward over the same 16
+    sequences on the host."""
+    import torch
+    from paper_2609_28568_amd import binding, synth
+    w = dict(synth.WORKLOADS["block124m"])
+    B, T, C, F, H = w["B"], w["T"], w["d_model"], w["d_ff"], w["n_head"]
+    p = synth.init_params(w)
+    x, dy = synth.block_inputs(w)
+    m = binding.GPT2(binding.make_config(w, synth.OPTIM))
+    m.set_params(p)
+    tx = torch.from_numpy(x).cuda().to(torch.bfloat16)
+    tdy = torch.from_numpy(dy).cuda().to(torch.bfloat16)
+    out, dxin = torch.empty_like(tx), torch.empty_like(tx)
+
+    def one():
+        m.block_forward(0, tx, out)
+        m.block_backward(0, tdy, dxin)
+
+    for _ in range(3):
+        one()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    n = 20
+    e0.record(stream)
+    for _ in range(n):
+        one()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / n
+    m.close()
+    # forward: the four products 2 BT (4 C^2 + 2 C F) and causal attention
+    # 4 hd T(T+1)/2 per (sequence, head); the backward twice the forward
+    fwd = 2.0 * B * T * (4 * C * C + 2 * C * F) + 4.0 * (C // H) * T * (T + 1) / 2 * B * H
+    res = {"workload": "one GPT-2 124M block, 16 x 1024 tokens: forward, then backward to its weight and input "
+                       "gradients (block124m)",
+           "gpu_ms": round(ms, 3), "gpu_tokens_per_s": round(B * T / (ms * 1e-3), 1),
+           "gpu_tflops": round(3 * fwd / (ms * 1e-3) / 1e12, 1), "flops_per_pass": 3 * fwd, "passes": n}
+    if with_cpu:
+        import oracle
+        print("bench: timing the CPU oracle on the single block", file=sys.stderr, flush=True)
+        ocfg = oracle.Config.from_dict({**w, "lr_min": 6e-5})
+        t0 = time.perf_counter()
+        _, cache = oracle.block_forward(x.reshape(B, T, C), p, 0, ocfg)
+        grads = oracle.zero_grads(p)
+        oracle.block_backward(dy.reshape(B, T, C), cache, p, 0, ocfg, grads)
+        dt = time.perf_counter() - t0
+        res["cpu_oracle"] = {"value": round(B * T / dt, 1), "unit": "tokens/s", "seconds": round(dt, 2),
+                             "kind": "oracle", "cpu_count": os.cpu_count(),
+                             "sample": "the same 16 x 1024 tokens through the block, numpy fp32"}
+    return res
+
+
 # Kernel classes with counter-derived traffic: the sources their kernels are
 # built from, the pattern of their kernel names in rocprofv3 output, and how
 # many kernels one launch of the class runs (the attention backward is the
@@ -406,6 +464,8 @@ def main():
     ap.add_argument("--residual-norm", type=int, default=0,
                     help="how residual connections meet the following pre-norm: 0 in the projection's epilogue, "
                          "1 the fused add + LayerNorm kernel, 2 separate add and LayerNorm kernels")
+    ap.add_argument("--no-block", action="store_true",
+                    help="skip the single-block (16 x 1024 tokens through one block) measurement")
     ap.add_argument("--swiglu", type=int, default=1,
                     help="Qwen3-shaped workload: 1 SwiGLU in the GEMM epilogues, 0 separate SwiGLU kernels")
     args = ap.parse_args()
@@ -536,8 +596,12 @@ def main():
 
     cpu = None
     if not args.no_cpu_baseline:
-        print("bench: timing the CPU oracle on a 1-sequence sample", file=sys.stderr, flush=True)
+        print("bench: timing the CPU oracle on a 4-sequence sample", file=sys.stderr, flush=True)
         cpu = cpu_baseline(w, params, *batches[0])
+
+    block = None
+    if not args.no_block and args.workload == "gpt2_124m":
+        block = block_measure(not args.no_cpu_baseline)
 
     out = {
         "metric": "training tokens/sec on 1 MI355X at GPT-2 124M; bf16 MFMA model-FLOPs util",
@@ -566,6 +630,7 @@ def main():
         "roofline": roofline,
         "cpu_baseline": cpu,
         "eval": eval_out,
+        "block": block,
     }
     if extra:
         out["classes"] = extra
