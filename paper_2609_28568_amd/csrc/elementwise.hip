@@ -173,6 +173,7 @@ __global__ void embed_fwd_kernel(const int32_t* __restrict__ ids, const float* _
 // distribution is Zipf-like) then cost one atomic per workgroup instead of
 // one per occurrence.
 constexpr int EMB_P = 256, EMB_C = 128;
+constexpr float LOG2E_F = 1.4426950408889634f;
 __global__ __launch_bounds__(256) void embed_bwd_wte_kernel(const int32_t* __restrict__ ids,
                                                             const bf16_t* __restrict__ dx, float* __restrict__ dwte,
                                                             int BT, int C, int V) {
@@ -309,13 +310,21 @@ __global__ __launch_bounds__(NT) void cross_entropy_kernel(bf16_t* __restrict__ 
     const uint32_t wd = e < 2 ? q.x : e < 4 ? q.y : e < 6 ? q.z : q.w;
     return (e & 1) ? hi_f(wd) : lo_f(wd);
   };
+  // Only the chunk that holds column V-1 mixes real and padding columns:
+  // whole chunks below it skip the per-element test, those past it count
+  // nothing.
   float m = -INFINITY;
 #pragma unroll
   for (int i = 0; i < MAXCH; ++i) {
     const int c = tid + NT * i;
+    if (c * 8 + 8 <= V) {
 #pragma unroll
-    for (int e = 0; e < 8; ++e)
-      if (c * 8 + e < V) m = fmaxf(m, elem(v[i], e));
+      for (int e = 0; e < 8; ++e) m = fmaxf(m, elem(v[i], e));
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        if (c * 8 + e < V) m = fmaxf(m, elem(v[i], e));
+    }
   }
   // the packed row is all that stays live between passes (otherwise the
   // compiler keeps every unpacked fp32 value in registers)
@@ -324,13 +333,20 @@ __global__ __launch_bounds__(NT) void cross_entropy_kernel(bf16_t* __restrict__ 
     for (int i = 0; i < MAXCH; ++i) asm volatile("" : "+v"(v[i].x), "+v"(v[i].y), "+v"(v[i].z), "+v"(v[i].w));
   };
   opaque();
+  // exp(x - m) = 2^(x log2(e) - m log2(e)): one fma and one exponential
+  const float ml = m == -INFINITY ? 0.0f : m * LOG2E_F;
   float se = 0.0f;
 #pragma unroll
   for (int i = 0; i < MAXCH; ++i) {
     const int c = tid + NT * i;
+    if (c * 8 + 8 <= V) {
 #pragma unroll
-    for (int e = 0; e < 8; ++e)
-      if (c * 8 + e < V) se += __expf(elem(v[i], e) - m);
+      for (int e = 0; e < 8; ++e) se += __builtin_amdgcn_exp2f(fmaf(elem(v[i], e), LOG2E_F, -ml));
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        if (c * 8 + e < V) se += __builtin_amdgcn_exp2f(fmaf(elem(v[i], e), LOG2E_F, -ml));
+    }
   }
   opaque();
   // combine (m, se) over the wave, then over the waves
@@ -352,18 +368,26 @@ __global__ __launch_bounds__(NT) void cross_entropy_kernel(bf16_t* __restrict__ 
   float sum = 0.0f;
 #pragma unroll
   for (int k = 0; k < NW; ++k) sum += shm[k] == -INFINITY ? 0.0f : shs[k] * __expf(shm[k] - mx);
-  const float inv = 1.0f / sum;
+  // dlogits = (softmax - onehot(target)) * grad_scale: 2^(x log2(e) - mx
+  // log2(e)) times grad_scale / sum, the target's column less grad_scale
+  const float mxl = mx * LOG2E_F, k = grad_scale / sum;
 #pragma unroll
   for (int i = 0; i < MAXCH; ++i) {
     const int c = tid + NT * i;
     if (GRAD && c < nch) {
       float d[8];
+      if (c * 8 + 8 <= V) {
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const int j = c * 8 + e;
-        float p = j < V ? __expf(elem(v[i], e) - mx) * inv : 0.0f;
-        if (j == tgt) p -= 1.0f;
-        d[e] = p * grad_scale;
+        for (int e = 0; e < 8; ++e) d[e] = __builtin_amdgcn_exp2f(fmaf(elem(v[i], e), LOG2E_F, -mxl)) * k;
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          d[e] = c * 8 + e < V ? __builtin_amdgcn_exp2f(fmaf(elem(v[i], e), LOG2E_F, -mxl)) * k : 0.0f;
+      }
+      if (c == (tgt >> 3)) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          if (e == (tgt & 7)) d[e] -= grad_scale;
       }
       *reinterpret_cast<uint4*>(lr + c * 8) =
           make_uint4(pack2(d[0], d[1]), pack2(d[2], d[3]), pack2(d[4], d[5]), pack2(d[6], d[7]));
