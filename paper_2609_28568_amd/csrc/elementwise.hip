@@ -60,10 +60,8 @@ __global__ void reduce_slices2_kernel(const float* __restrict__ src, int nslices
 
 // 16 waves per block, 64 columns per block: wave w sums slices w, w+16, ...
 // sixteen loads at a time, then the waves are combined in order.
-__global__ __launch_bounds__(1024) void reduce_parts_kernel(const float* __restrict__ part, int S, long stride,
-                                                            int n, int nd, float* __restrict__ d0,
-                                                            float* __restrict__ d1, float* __restrict__ d2,
-                                                            int accumulate) {
+DEV void reduce_parts_block(const float* __restrict__ part, int S, long stride, int n, int nd, float* __restrict__ d0,
+                            float* __restrict__ d1, float* __restrict__ d2, int accumulate) {
   __shared__ float red[16][64];
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int col = blockIdx.x * 64 + lane;
@@ -92,6 +90,21 @@ __global__ __launch_bounds__(1024) void reduce_parts_kernel(const float* __restr
     float* d = j == 0 ? d0 : (j == 1 ? d1 : d2);
     if (d) d[c] = (accumulate ? d[c] : 0.0f) + t;
   }
+}
+
+__global__ __launch_bounds__(1024) void reduce_parts_kernel(const float* __restrict__ part, int S, long stride,
+                                                            int n, int nd, float* __restrict__ d0,
+                                                            float* __restrict__ d1, float* __restrict__ d2,
+                                                            int accumulate) {
+  reduce_parts_block(part, S, stride, n, nd, d0, d1, d2, accumulate);
+}
+
+// The same reduction for several partial-sum arrays of one shape at once:
+// blockIdx.y picks the array and its destinations.
+__global__ __launch_bounds__(1024) void reduce_parts_multi_kernel(ReducePartsJobs J, int S, long stride, int n, int nd,
+                                                                  int accumulate) {
+  const int j = blockIdx.y;
+  reduce_parts_block(J.part[j], S, stride, n, nd, J.d[j][0], J.d[j][1], J.d[j][2], accumulate);
 }
 
 template <int NT>
@@ -583,6 +596,14 @@ hipError_t launch_reduce_slices2(const float* src, int nslices, long n, float* d
   const long nmax = n > n2 ? n : n2;
   hipLaunchKernelGGL(reduce_slices2_kernel, dim3(blocks_for(nmax / 4, 256), 2), dim3(256), 0, s, src, nslices, n, dst,
                      src2, nslices2, n2, dst2, accumulate);
+  return hipGetLastError();
+}
+
+hipError_t launch_reduce_parts_multi(const ReducePartsJobs& J, int S, long stride, int n, int nd, int accumulate,
+                                     hipStream_t s) {
+  if (nd < 1 || nd > 3 || J.count < 1 || J.count > REDUCE_JOBS) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(reduce_parts_multi_kernel, dim3((unsigned)((n * nd + 63) / 64), (unsigned)J.count), dim3(1024), 0,
+                     s, J, S, stride, n, nd, accumulate);
   return hipGetLastError();
 }
 

@@ -152,7 +152,7 @@ struct ActLayout {
 
 struct WsLayout {
   size_t dres, dh, datt, dbig, dsum, splitk, bsum, lnpart, sumsq, normcoef, total;
-  size_t splitk_elems, bsum_elems;
+  size_t splitk_elems, bsum_elems, s_lnpart;
   // the training backward keeps every layer's output gradients until one
   // grouped launch computes all block weight gradients: residual-stream
   // gradients [2L+1][BT][C] (slot 2l+2 enters block l, 2l+1 is after its MLP
@@ -245,7 +245,10 @@ WsLayout ws_layout(const Dims& d) {
   w.dsum = o; o += align_up((size_t)d.B * d.H * d.T * 4);
   w.splitk = o; o += align_up(sk * 4);
   w.bsum = o; o += align_up(w.bsum_elems * 4);
-  w.lnpart = o; o += align_up((size_t)layernorm_bwd_blocks((int)BT) * 3 * C * 4);
+  // LayerNorm backward partial sums: one slot per LayerNorm of the model
+  // (2L + 1), so that the training backward reduces them all in one launch
+  w.s_lnpart = align_up((size_t)layernorm_bwd_blocks((int)BT) * 3 * C * 4);
+  w.lnpart = o; o += (2 * (size_t)d.L + 1) * w.s_lnpart;
   w.sumsq = o; o += align_up((size_t)sumsq_parts() * 4);
   w.normcoef = o; o += ALIGN;
   w.s_dres = align_up(BT * C * 2);
@@ -288,6 +291,10 @@ struct gpt2_model {
   // GEMM runs twice, first writing only each row's softmax statistics and
   // target logit, then writing dlogits from the combined log-sum-exp
   int head_ce = 0;
+  // LayerNorm backward reductions left for one launch at the end of the
+  // training backward (their partial sums each in a slot of their own)
+  ReducePartsJobs ln_jobs{};
+  int ln_jobs_acc = 0;
   std::string err;
   ProbeSet<GPT2_K_COUNT> probes;
 
@@ -428,20 +435,49 @@ hipError_t ln_fwd(Model* m, const bf16_t* x, const float* w, const float* b, bf1
 // dres_in : 0) + dx; also writes the gain and shift gradients and, when dbias
 // is given, the column sum of the new residual gradient (the bias gradient of
 // the projection that produced it).
+// The queued LayerNorm backward reductions, in one launch.
+hipError_t reduce_ln_parts(Model* m) {
+  ReducePartsJobs& J = m->ln_jobs;
+  if (J.count == 0) return hipSuccess;
+  const int C = m->d.C, nb = layernorm_bwd_blocks((int)m->d.BT), acc = m->ln_jobs_acc;
+  hipError_t e = m->run(GPT2_K_OTHER, 0.0, 4.0 * 3 * C * (double)J.count * (nb + 1 + acc), [&] {
+    return launch_reduce_parts_multi(J, nb, 3L * C, C, 3, acc, m->stream);
+  });
+  J.count = 0;
+  return e;
+}
+
+// With slot >= 0 the partial sums go to that slot and their reduction is
+// queued for reduce_ln_parts; otherwise they are reduced at once.
 hipError_t ln_bwd(Model* m, const bf16_t* dy, const bf16_t* x, const float* mean, const float* rstd, const float* w,
                   const bf16_t* dres_in, bf16_t* dres_out, int has_res, float* dw, float* db, float* dbias,
-                  int accumulate) {
+                  int accumulate, int slot = -1) {
   const int BT = (int)m->d.BT, C = m->d.C;
-  float* part = m->wsf(m->ws.lnpart);
+  float* part = m->wsf(m->ws.lnpart + (size_t)(slot < 0 ? 0 : slot) * m->ws.s_lnpart);
   hipError_t e = m->run(GPT2_K_LAYERNORM, 0.0, 2.0 * BT * C * (3 + has_res) + 8.0 * BT, [&] {
     return launch_layernorm_bwd(dy, x, mean, rstd, w, dres_in, dres_out, has_res, part, BT, C, m->stream);
   });
   if (e != hipSuccess) return e;
+  if (slot >= 0) {
+    ReducePartsJobs& J = m->ln_jobs;
+    if (J.count == REDUCE_JOBS || (J.count > 0 && m->ln_jobs_acc != accumulate)) {
+      e = reduce_ln_parts(m);
+      if (e != hipSuccess) return e;
+    }
+    J.part[J.count] = part;
+    J.d[J.count][0] = dw;
+    J.d[J.count][1] = db;
+    J.d[J.count][2] = dbias;
+    ++J.count;
+    m->ln_jobs_acc = accumulate;
+    return hipSuccess;
+  }
   int nb = layernorm_bwd_blocks(BT);
   return m->run(GPT2_K_OTHER, 0.0, 4.0 * 3 * C * (nb + 1 + accumulate), [&] {
     return launch_reduce_parts(part, nb, 3L * C, C, 3, dw, db, dbias, accumulate, m->stream);
   });
 }
+
 
 AttnArgs attn_args(Model* m, int slot, bf16_t* dqkv = nullptr) {
   AttnArgs a{};
@@ -625,7 +661,7 @@ gpt2_status block_bwd(Model* m, int l, int acc, bool fcproj_bias_done, bool writ
   TRY(gemm(m, GPT2_K_GEMM_DX, BT, C, F, gb.dfc, F, 0, m->pb(K_FCW) + oF * C, C, 1, EPI_BF16, dh, C));
   if (!defer_dw) TRY(weight_grad(m, F, C, gb.dfc, m->ln2(l), m->gf(K_FCW) + oF * C, acc, 0, m->gf(K_FCB) + oF));
   TRY(ln_bwd(m, dh, m->xmid(l), m->ln2m(l), m->ln2r(l), m->pf(K_LN2W) + oC, gb.dres_out, gb.dres_mid, 1,
-             m->gf(K_LN2W) + oC, m->gf(K_LN2B) + oC, m->gf(K_ATTPROJB) + oC, acc));
+             m->gf(K_LN2W) + oC, m->gf(K_LN2B) + oC, m->gf(K_ATTPROJB) + oC, acc, defer_dw ? 2 * l + 1 : -1));
   // attention output projection (its bias gradient came from the LayerNorm above)
   TRY(gemm(m, GPT2_K_GEMM_DX, BT, C, C, gb.dres_mid, C, 0, m->pb(K_ATTPROJW) + oC * C, C, 1, EPI_BF16, datt, C));
   if (!defer_dw) TRY(weight_grad(m, C, C, gb.dres_mid, m->att(l), m->gf(K_ATTPROJW) + oC * C, acc));
@@ -638,7 +674,7 @@ gpt2_status block_bwd(Model* m, int l, int acc, bool fcproj_bias_done, bool writ
     TRY(weight_grad(m, 3 * C, C, gb.dqkv, m->ln1(l), m->gf(K_QKVW) + o3C * C, acc, 0, m->gf(K_QKVB) + o3C));
   float* prev_bias = (write_prev_bias && l > 0) ? m->gf(K_FCPROJB) + (size_t)(l - 1) * C : nullptr;
   TRY(ln_bwd(m, dh, m->res(l), m->ln1m(l), m->ln1r(l), m->pf(K_LN1W) + oC, gb.dres_mid, gb.dres_in, 1,
-             m->gf(K_LN1W) + oC, m->gf(K_LN1B) + oC, prev_bias, acc));
+             m->gf(K_LN1W) + oC, m->gf(K_LN1B) + oC, prev_bias, acc, defer_dw ? 2 * l : -1));
   return GPT2_OK;
 }
 
@@ -966,13 +1002,14 @@ gpt2_status gpt2_backward(gpt2_model* m, int32_t accumulate) {
   const int BT = (int)d.BT, C = d.C;
   const int acc = accumulate ? 1 : 0;
   bf16_t* dh = m->wsb(m->ws.dh);
+  m->ln_jobs.count = 0;   // nothing queued from a pass that failed part-way
   // tied LM head: input gradient and the head's share of the token-table gradient
   TRY(gemm(m, GPT2_K_GEMM_DX, BT, C, d.Vp, m->logits(), d.Vp, 0, m->pb(K_WTE), C, 1, EPI_BF16, dh, C, nullptr,
            nullptr, nullptr, nullptr, 0, 1, 0, 0, 2.0 * BT * (double)d.V * C));
   TRY(weight_grad(m, d.Vp, C, m->logits(), m->lnf(), m->gf(K_WTE), acc, d.V));
   bf16_t* dres_top = grads_of_layer(m, d.L - 1).dres_out;   // written, not read (has_res 0)
   TRY(ln_bwd(m, dh, m->res(d.L), m->lnfm(), m->lnfr(), m->pf(K_LNFW), dres_top, dres_top, 0, m->gf(K_LNFW),
-             m->gf(K_LNFB), m->gf(K_FCPROJB) + (size_t)(d.L - 1) * C, acc));
+             m->gf(K_LNFB), m->gf(K_FCPROJB) + (size_t)(d.L - 1) * C, acc, 2 * d.L));
   for (int l = d.L - 1; l >= 0; --l) {
     gpt2_status s = block_bwd(m, l, acc, true, true, grads_of_layer(m, l), true);
     if (s != GPT2_OK) return s;
@@ -987,6 +1024,8 @@ gpt2_status gpt2_backward(gpt2_model* m, int32_t accumulate) {
     gpt2_status s = grouped_weight_grads(m, acc);
     if (s != GPT2_OK) return s;
   }
+  // every LayerNorm's gain, shift and following-bias gradients
+  TRY(reduce_ln_parts(m));
   m->have_grads = true;
   return GPT2_OK;
 }

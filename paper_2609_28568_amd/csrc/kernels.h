@@ -187,6 +187,17 @@ hipError_t launch_reduce_slices2(const float* src, int nslices, long n, float* d
 // destinations, null ones skipped) and c < n. Fixed summation order.
 hipError_t launch_reduce_parts(const float* part, int S, long stride, int n, int nd, float* d0, float* d1,
                                float* d2, int accumulate, hipStream_t s);
+// Up to REDUCE_JOBS such reductions of one shape (S slices of stride floats,
+// nd outputs of n) in one launch: job j sums part[j] into d[j][0..nd-1]
+// (null destinations skipped).
+constexpr int REDUCE_JOBS = 32;
+struct ReducePartsJobs {
+  int count;
+  const float* part[REDUCE_JOBS];
+  float* d[REDUCE_JOBS][3];
+};
+hipError_t launch_reduce_parts_multi(const ReducePartsJobs& J, int S, long stride, int n, int nd, int accumulate,
+                                     hipStream_t s);
 // Token ids outside [0, V) are a caller's contract violation: the kernels
 // that read ids (embedding forward, cross-entropy target gather) read row 0
 // in their place and set bit ID_BAD_INPUT or ID_BAD_TARGET of *bad (when bad
