@@ -184,12 +184,20 @@ __global__ __launch_bounds__(64 * gemm_waves(BM, BK), (NS <= 2 ? 2 : 1)) void ge
     // groups in order, each group's products in order, each product's tiles
     // n fastest; every XCD takes a contiguous run of that order
     int b = blockIdx.x;
-    const int tot = gridDim.x;
-    if ((tot & 7) == 0) b = (b & 7) * (tot >> 3) + (b >> 3);
+    const int tot = gridDim.x, nfull = P.gg.nfull;
+    if (nfull > 0) {
+      // XCD x takes full tiles [x nfull/8, (x+1) nfull/8), then its eighth
+      // of the last group's tiles
+      const int f8 = nfull >> 3, x = b & 7, loc = b >> 3;
+      b = loc < f8 ? x * f8 + loc : nfull + x * ((tot - nfull) >> 3) + (loc - f8);
+    } else if ((tot & 7) == 0) {
+      b = (b & 7) * (tot >> 3) + (b >> 3);
+    }
     int k = 0;
 #pragma unroll
     for (int i = 0; i + 1 < GEMM_GROUPS; ++i) {
-      const int t = group_tiles<BM, BN>(P.gg.grp[i]) * P.gg.grp[i].count;
+      const GemmGroup& gr = P.gg.grp[i];
+      const int t = group_tiles<BM, BN>(gr) * gr.count * (gr.splits > 1 ? gr.splits : 1);
       if (k == i && i + 1 < P.gg.ngroups && b >= t) {
         b -= t;
         k = i + 1;
@@ -200,8 +208,12 @@ __global__ __launch_bounds__(64 * gemm_waves(BM, BK), (NS <= 2 ? 2 : 1)) void ge
       if (i == k) {
         const GemmGroup& gr = P.gg.grp[i];
         const int tpp = group_tiles<BM, BN>(gr);
-        const int pidx = b / tpp;
-        bid = b - pidx * tpp;
+        // a product's tiles, each tile's contraction chunks adjacent
+        const int sp = gr.splits > 1 ? gr.splits : 1;
+        const int pidx = b / (tpp * sp);
+        const int rem = b - pidx * tpp * sp;
+        bid = rem / sp;
+        split = rem - bid * sp;
         g.A = gr.A + (size_t)pidx * gr.a_stride;
         g.B = gr.B + (size_t)pidx * gr.b_stride;
         g.C = gr.C + (size_t)pidx * gr.c_stride;
@@ -212,9 +224,13 @@ __global__ __launch_bounds__(64 * gemm_waves(BM, BK), (NS <= 2 ? 2 : 1)) void ge
         g.ldc = gr.N;
         g.bsum = gr.bsum ? gr.bsum + (size_t)pidx * gr.M : nullptr;
         g.bsum_ld = gr.count * gr.M;
+        if (sp > 1) {
+          g.k_chunk = gr.k_chunk;
+          g.split_stride = gr.split_stride;
+          g.accumulate = 0;   // slices hold plain sums
+        }
       }
     }
-    split = 0;
   }
   const int ntn = (g.N + BN - 1) / BN, ntiles = ntn * ((g.M + BM - 1) / BM);
   if constexpr (GROUPED) {
@@ -592,8 +608,9 @@ __global__ __launch_bounds__(64 * gemm_waves(BM, BK), (NS <= 2 ? 2 : 1)) void ge
         for (int c = 0; c < CG; ++c) {
           const int idx = lane + 64 * (c0 + c);
           if constexpr (EPI == EPI_F32_ACC)
-            prev[c] = in_c(checked, mrow0, c0 + c) ? *reinterpret_cast<const float4*>(Cfi + co(c0 + c))
-                                                   : make_float4(0.f, 0.f, 0.f, 0.f);
+            prev[c] = (g.accumulate && in_c(checked, mrow0, c0 + c))
+                          ? *reinterpret_cast<const float4*>(Cfi + co(c0 + c))
+                          : make_float4(0.f, 0.f, 0.f, 0.f);
           if constexpr (EPI == EPI_SWIGLU_BWD) {
             const bool ok = in_c(checked, mrow0, c0 + c);
             const bf16_t* src = rd_src + bo + co(c0 + c);
@@ -677,7 +694,8 @@ hipError_t launch_grouped_t(const GemmGroupedArgs& gg, hipStream_t s) {
   g.A = gg.grp[0].A; g.B = gg.grp[0].B; g.C = gg.grp[0].C; g.M = gg.grp[0].M; g.N = gg.grp[0].N;
   long tiles = 0;
   for (int i = 0; i < gg.ngroups; ++i)
-    tiles += (long)((gg.grp[i].M + BM - 1) / BM) * ((gg.grp[i].N + BN - 1) / BN) * gg.grp[i].count;
+    tiles += (long)((gg.grp[i].M + BM - 1) / BM) * ((gg.grp[i].N + BN - 1) / BN) * gg.grp[i].count *
+             (gg.grp[i].splits > 1 ? gg.grp[i].splits : 1);
   if (tiles < 1 || tiles > (1L << 30)) return hipErrorInvalidValue;
   if (gg.accumulate)
     hipLaunchKernelGGL((gemm_kernel<BM, BN, BK, 2, true, true, EPI_F32_ACC, false, true>), dim3((unsigned)tiles),
@@ -867,11 +885,23 @@ int gemm_grouped_bias_parts(const GemmGroupedArgs& gg, int i) {
 
 hipError_t launch_gemm_grouped(const GemmGroupedArgs& gg, hipStream_t s) {
   if (gg.ngroups < 1 || gg.ngroups > GEMM_GROUPS || gg.K < 1) return hipErrorInvalidValue;
+  long tiles = 0, last = 0;
+  const bool g192 = grouped_uses_192(gg);
   for (int i = 0; i < gg.ngroups; ++i) {
     const GemmGroup& gr = gg.grp[i];
     if (!gr.A || !gr.B || !gr.C || gr.M < 1 || gr.N < 1 || gr.count < 1 || gr.N % 4) return hipErrorInvalidValue;
+    if (gr.splits > 1) {
+      // chunks of whole 64-token steps covering K; slices of plain sums
+      if (gr.bsum || gr.k_chunk < 64 || gr.k_chunk % 64 || (long)gr.k_chunk * gr.splits < gg.K ||
+          (long)gr.k_chunk * (gr.splits - 1) >= gg.K || gr.split_stride < (long)gr.count * gr.c_stride)
+        return hipErrorInvalidValue;
+    }
+    const int bm = g192 ? 192 : 128;
+    last = (long)((gr.M + bm - 1) / bm) * ((gr.N + bm - 1) / bm) * gr.count * (gr.splits > 1 ? gr.splits : 1);
+    tiles += last;
     if ((size_t)(gg.K + 256) * gr.lda * 2 >= (1ull << 32) || (size_t)(gg.K + 256) * gr.ldb * 2 >= (1ull << 32))
       return hipErrorInvalidValue;
   }
-  return grouped_uses_192(gg) ? launch_grouped_t<192, 192, 32>(gg, s) : launch_grouped_t<128, 128, 32>(gg, s);
+  if (gg.nfull != 0 && (gg.nfull < 0 || gg.nfull % 8 || gg.nfull != tiles - last || last % 8)) return hipErrorInvalidValue;
+  return g192 ? launch_grouped_t<192, 192, 32>(gg, s) : launch_grouped_t<128, 128, 32>(gg, s);
 }

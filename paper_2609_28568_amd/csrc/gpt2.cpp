@@ -216,6 +216,42 @@ GemmGroupedArgs dw_groups(const Dims& d) {
   return g;
 }
 
+// The grouped weight-gradient launch runs in rounds of 512 tiles (two
+// workgroups on each of the 256 CUs). When its last round would be at most
+// half full and consists of whole MLP-down products (the last group), those
+// products split their token contraction into `splits` chunks, so that the
+// final round is full of shorter work items; their fp32 slices are reduced
+// afterwards. np = 0: no such plan.
+struct DwGroupedTail {
+  int np = 0, splits = 1, chunk = 0;
+  long nfull = 0;
+};
+
+DwGroupedTail dw_grouped_tail(const Dims& d) {
+  DwGroupedTail t;
+  constexpr long ROUND = 512;
+  const GemmGroupedArgs g = dw_groups(d);
+  int bm = 192;
+  for (int i = 0; i < g.ngroups; ++i)
+    if (g.grp[i].M % 192 || g.grp[i].N % 192) bm = 128;
+  long total = 0;
+  for (int i = 0; i < g.ngroups; ++i) total += (long)((g.grp[i].M + bm - 1) / bm) * ((g.grp[i].N + bm - 1) / bm) * g.grp[i].count;
+  const GemmGroup& last = g.grp[G_FCPROJ];
+  const long tpp = (long)((last.M + bm - 1) / bm) * ((last.N + bm - 1) / bm);
+  const long tail = total % ROUND;
+  if (total < ROUND || tail == 0 || tail > ROUND / 2 || tail % tpp || tail / tpp > last.count) return t;
+  int splits = (int)(ROUND / tail);
+  if (splits > 4) splits = 4;
+  int chunk = 0;
+  splits = gemm_split_plan((int)d.BT, splits, &chunk);
+  if (splits < 2 || ((tail * splits) % 8) != 0) return t;
+  t.np = (int)(tail / tpp);
+  t.splits = splits;
+  t.chunk = chunk;
+  t.nfull = total - tail;
+  return t;
+}
+
 WsLayout ws_layout(const Dims& d) {
   WsLayout w{};
   const size_t BT = d.BT, C = d.C, F = d.F;
@@ -228,6 +264,8 @@ WsLayout ws_layout(const Dims& d) {
     if (t.splits > 1) sk = std::max(sk, (size_t)t.splits * (M - t.m_main) * N);
   };
   upd(3 * d.C, d.C); upd(d.C, d.C); upd(d.F, d.C); upd(d.C, d.F); upd(d.Vp, d.C);
+  const DwGroupedTail gt = dw_grouped_tail(d);
+  if (gt.np > 0) sk = std::max(sk, (size_t)gt.splits * gt.np * d.C * d.F);
   w.splitk_elems = sk;
   // bias partial sums of the weight gradients that carry a bias gradient
   size_t bs = 0;
@@ -706,9 +744,34 @@ gpt2_status grouped_weight_grads(Model* m, int acc) {
   fp->A = m->wsb(w.dres_l + 2 * w.s_dres); fp->a_stride = (long)(w.s_dres); fp->lda = (int)C;   // slots 2l+2
   fp->B = m->gelu(0); fp->b_stride = (long)(a.s_ff / 2); fp->ldb = (int)F;
   fp->C = m->gf(K_FCPROJW); fp->c_stride = (long)(C * F);
+  // the last np MLP-down products as a fifth group with a split contraction
+  // (slices in the split-K buffer)
+  const DwGroupedTail gt = dw_grouped_tail(d);
+  float* tail_dst = nullptr;
+  if (gt.np > 0) {
+    const int keep = (int)d.L - gt.np;
+    GemmGroup* tl = &g.grp[g.ngroups++];
+    *tl = *fp;
+    fp->count = keep;
+    tl->count = gt.np;
+    tl->A = fp->A + (size_t)keep * fp->a_stride;
+    tl->B = fp->B + (size_t)keep * fp->b_stride;
+    tl->C = m->wsf(w.splitk);
+    tl->splits = gt.splits;
+    tl->k_chunk = gt.chunk;
+    tl->split_stride = (long)gt.np * (long)(C * F);
+    g.nfull = gt.nfull;
+    tail_dst = m->gf(K_FCPROJW) + (size_t)keep * C * F;
+  }
   double fl = 0.0;
   for (int i = 0; i < g.ngroups; ++i) fl += 2.0 * g.grp[i].M * (double)g.grp[i].N * d.BT * g.grp[i].count;
   TRY(m->run(GPT2_K_GEMM_DW_GROUPED, fl, 0.0, [&] { return launch_gemm_grouped(g, m->stream); }));
+  if (tail_dst) {
+    const long n = (long)gt.np * (long)(C * F);
+    TRY(m->run(GPT2_K_GEMM_DW_GROUPED, 0.0, 4.0 * n * (gt.splits + 1 + acc), [&] {
+      return launch_reduce_slices2(m->wsf(w.splitk), gt.splits, n, tail_dst, nullptr, 0, 0, nullptr, acc, m->stream);
+    }));
+  }
   const int pq = gemm_grouped_bias_parts(g, G_QKV), pf = gemm_grouped_bias_parts(g, G_FC);
   const long nq = (long)d.L * 3 * C, nf = (long)d.L * F;
   TRY(m->run(GPT2_K_OTHER, 0.0, 4.0 * nq * (pq + 1 + acc), [&] {

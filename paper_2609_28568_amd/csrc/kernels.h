@@ -94,7 +94,14 @@ struct GemmArgs {
 // A_p's rows (its bias gradient) into rows [slot][p][M] of bsum, slot <
 // gemm_bias_parts(M, N, 1); summing over slots gives the bias gradients of
 // the group's products, stored one after another.
-constexpr int GEMM_GROUPS = 4;
+// A group with splits > 1 divides its contraction into `splits` chunks of
+// k_chunk tokens (a multiple of 64): product p's chunk z writes the plain sum
+// (never accumulating) to C_p + z * split_stride, for the caller to reduce;
+// such a group carries no bsum. With nfull > 0 the groups before the last
+// one hold nfull tiles and the last one the rest (both multiples of 8), and
+// each of the 8 XCDs takes an equal share of both (the last group's tiles
+// filling the final round).
+constexpr int GEMM_GROUPS = 5;
 struct GemmGroup {
   const bf16_t* A;
   const bf16_t* B;
@@ -103,12 +110,15 @@ struct GemmGroup {
   long a_stride, b_stride, c_stride;
   int M, N, lda, ldb;
   int count;
+  int splits, k_chunk;   // contraction split (splits <= 1: none)
+  long split_stride;
 };
 struct GemmGroupedArgs {
   GemmGroup grp[GEMM_GROUPS];
   int ngroups;
   int K;
   int accumulate;
+  int nfull;   // tiles before the last group when its tiles fill the final round (0: no such plan)
 };
 hipError_t launch_gemm_grouped(const GemmGroupedArgs& g, hipStream_t s);
 // Partial rows (slots) a grouped launch writes for group i's bias sums; it
