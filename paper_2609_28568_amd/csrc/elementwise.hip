@@ -488,7 +488,12 @@ __global__ __launch_bounds__(256) void clip_coef_kernel(const float* __restrict_
 __global__ __launch_bounds__(256) void adamw_kernel(AdamArgs a) {
   const float coef = a.norm_coef[1];
   const long stride = (long)gridDim.x * 256 * 4;
+  // Every rounding of the update is written out (no implicit contraction):
+  // the compiler could otherwise fuse the multiply-adds differently in the
+  // inlined copies below, and an element's bits would depend on which copy,
+  // grid size or segment split handles it.
   auto update = [&](long i, float wd) {
+#pragma clang fp contract(off)
     float4 p = *reinterpret_cast<const float4*>(a.p + i);
     float4 g = *reinterpret_cast<const float4*>(a.g + i);
     float4 m = *reinterpret_cast<const float4*>(a.m + i);
@@ -497,11 +502,12 @@ __global__ __launch_bounds__(256) void adamw_kernel(AdamArgs a) {
     float mv[4] = {m.x, m.y, m.z, m.w}, vv[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      float gg = gv[e] * coef;
-      mv[e] = a.beta1 * mv[e] + (1.0f - a.beta1) * gg;
-      vv[e] = a.beta2 * vv[e] + (1.0f - a.beta2) * gg * gg;
-      float mhat = mv[e] / a.bc1, vhat = vv[e] / a.bc2;
-      pv[e] -= a.lr * (mhat / (sqrtf(vhat) + a.eps) + wd * pv[e]);
+      const float gg = gv[e] * coef;
+      mv[e] = fmaf(a.beta1, mv[e], (1.0f - a.beta1) * gg);
+      vv[e] = fmaf(a.beta2, vv[e], ((1.0f - a.beta2) * gg) * gg);
+      const float mhat = mv[e] / a.bc1, vhat = vv[e] / a.bc2;
+      const float upd = fmaf(wd, pv[e], mhat / (sqrtf(vhat) + a.eps));
+      pv[e] = fmaf(-a.lr, upd, pv[e]);
     }
     *reinterpret_cast<float4*>(a.p + i) = make_float4(pv[0], pv[1], pv[2], pv[3]);
     *reinterpret_cast<float4*>(a.m + i) = make_float4(mv[0], mv[1], mv[2], mv[3]);
