@@ -768,7 +768,7 @@ gpt2_status grouped_weight_grads(Model* m, int acc) {
   TRY(m->run(GPT2_K_GEMM_DW_GROUPED, fl, 0.0, [&] { return launch_gemm_grouped(g, m->stream); }));
   if (tail_dst) {
     const long n = (long)gt.np * (long)(C * F);
-    TRY(m->run(GPT2_K_GEMM_DW_GROUPED, 0.0, 4.0 * n * (gt.splits + 1 + acc), [&] {
+    TRY(m->run(GPT2_K_OTHER, 0.0, 4.0 * n * (gt.splits + 1 + acc), [&] {
       return launch_reduce_slices2(m->wsf(w.splitk), gt.splits, n, tail_dst, nullptr, 0, 0, nullptr, acc, m->stream);
     }));
   }
