@@ -218,6 +218,72 @@ def cpu_baseline(w: dict, params, ids, tgt) -> dict:
                       f"model and token stream, numpy fp32 with {threads} BLAS threads, {dt:.1f} s"}
 
 
+def accum_measure(steps: int = 20) -> dict:
+    """The accumulation configuration: GPT-2 124M with 32 micro-batches of
+    16 x 1024 tokens per optimizer step (524,288 tokens; forward and backward
+    accumulating into the fp32 gradients, then clip and AdamW on the
+    scheduled rate), one untimed optimizer step, then `steps` consecutive ones
+    between two synchronised points, on Zipf-distributed synthetic tokens."""
+    import torch
+    from paper_2609_28568_amd import binding, synth
+    w = dict(synth.WORKLOADS["gpt2_124m_accum32"])
+    accum = w["grad_accum"]
+    m = binding.GPT2(binding.make_config(w, synth.OPTIM))
+    m.set_params(synth.init_params(w))
+    dev = [tuple(torch.from_numpy(a).cuda() for a in synth.token_batch(w, micro=i)) for i in range(4)]
+
+    def opt_step(i):
+        for k in range(accum):
+            ids, tgt = dev[(i * accum + k) % len(dev)]
+            m.forward(ids, tgt)
+            m.backward(accumulate=k > 0)
+        m.adamw_step(i)
+
+    opt_step(0)
+    first = m.loss()
+    stream = torch.cuda.current_stream()
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    evs[0].record(stream)
+    for i in range(steps):
+        opt_step(1 + i)
+        evs[i + 1].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    per_step = [evs[i].elapsed_time(evs[i + 1]) for i in range(steps)]
+    last = m.loss()
+    m.close()
+    tokens = w["B"] * w["T"] * accum
+    tok_s = tokens * steps / wall
+    return {"workload": "GPT-2 124M, 32 micro-batches of 16 x 1024 tokens per optimizer step (gpt2_124m_accum32)",
+            "optimizer_steps": steps, "tokens_per_step": tokens, "ms_per_step": round(wall * 1e3 / steps, 2),
+            "tokens_per_s": round(tok_s, 1),
+            "mfu": round(tok_s * flops_per_token(w) / (PEAK_BF16_TFLOPS * 1e12), 4),
+            "gpu_event_ms_step_stats": {"median": round(float(np.median(per_step)), 2),
+                                        "min": round(min(per_step), 2), "max": round(max(per_step), 2)},
+            "loss_after_first_step": round(first, 4), "loss_last": round(last, 4)}
+
+
+def device_info() -> dict:
+    """The GPU the run used: name, architecture, compute units and peak
+    shader clock (hipDeviceGetAttribute), beside the peaks the roofline uses."""
+    import ctypes
+    import torch
+    props = torch.cuda.get_device_properties(0)
+    out = {"name": props.name, "arch": getattr(props, "gcnArchName", ""), "compute_units": props.multi_processor_count,
+           "peak_bf16_tflops_used": PEAK_BF16_TFLOPS, "peak_hbm_gbs_used": 8000.0}
+    try:
+        hip = ctypes.CDLL("libamdhip64.so")
+        v = ctypes.c_int()
+        # hipDeviceAttributeClockRate (5): peak clock in kHz
+        if hip.hipDeviceGetAttribute(ctypes.byref(v), 5, 0) == 0:
+            out["clock_mhz_max"] = v.value / 1000.0
+    except OSError:
+        pass
+    return out
+
+
 def block_measure(with_cpu: bool) -> dict:
     """The single-block configuration: one GPT-2 124M block on 16 sequences of
     1024 tokens (bf16 input ~ N(0,1), upstream gradient ~ N(0, 1e-3)), forward
@@ -464,6 +530,8 @@ def main():
     ap.add_argument("--residual-norm", type=int, default=0,
                     help="how residual connections meet the following pre-norm: 0 in the projection's epilogue, "
                          "1 the fused add + LayerNorm kernel, 2 separate add and LayerNorm kernels")
+    ap.add_argument("--no-accum", action="store_true",
+                    help="skip the accumulation configuration (20 optimizer steps of 32 micro-batches)")
     ap.add_argument("--no-block", action="store_true",
                     help="skip the single-block (16 x 1024 tokens through one block) measurement")
     ap.add_argument("--swiglu", type=int, default=1,
@@ -530,14 +598,22 @@ def main():
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     ev0.record(stream)
+    ev_step = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
     for i in range(args.steps):
         if i == args.steps - 1:
             m.probe_enable([args.probe])
         step(args.warmup + i)
+        ev_step[i].record(stream)
     ev1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     gpu_ms = ev0.elapsed_time(ev1)
+    # per-step times from the events recorded after each step (the last step
+    # also carries the roofline kernel's probe events)
+    per_step = [ev0.elapsed_time(ev_step[0])] + [ev_step[i - 1].elapsed_time(ev_step[i])
+                                                 for i in range(1, args.steps)]
+    step_stats = {"median": round(float(np.median(per_step)), 3), "min": round(min(per_step), 3),
+                  "max": round(max(per_step), 3)}
     probe = m.probe_read(args.probe)
     m.probe_enable([])
     loss = m.loss()
@@ -602,6 +678,12 @@ def main():
     block = None
     if not args.no_block and args.workload == "gpt2_124m":
         block = block_measure(not args.no_cpu_baseline)
+    accum_out = None
+    if not args.no_accum and args.workload == "gpt2_124m":
+        m.close()
+        print("bench: timing the accumulation configuration (20 optimizer steps of 32 micro-batches)",
+              file=sys.stderr, flush=True)
+        accum_out = accum_measure()
 
     out = {
         "metric": "training tokens/sec on 1 MI355X at GPT-2 124M; bf16 MFMA model-FLOPs util",
@@ -626,11 +708,14 @@ def main():
         "flops_per_token_6n_12lct": flops_per_token_palm(w, m.n_params - (w["vocab_padded"] - w["vocab"]) * w["d_model"]),
         "peak_tflops": PEAK_BF16_TFLOPS,
         "gpu_event_ms_per_step": round(gpu_ms / args.steps, 3),
+        "gpu_event_ms_step_stats": step_stats,
+        "device": device_info(),
         "final_loss": round(loss, 4),
         "roofline": roofline,
         "cpu_baseline": cpu,
         "eval": eval_out,
         "block": block,
+        "accum": accum_out,
     }
     if extra:
         out["classes"] = extra
