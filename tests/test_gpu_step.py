@@ -48,6 +48,12 @@ CASES = {
     # degenerate: one-token sequences (attention over a single key, 5 rows in
     # every product, token contractions far shorter than one k-tile)
     "single_token": dict(B=5, T=1),
+    # the 124M model's block widths (12 layers, 768 wide) on 2 x 64 tokens:
+    # the grouped weight-gradient launch has the 124M step's 2,304 tiles, so
+    # its last half round (the MLP-down weight gradients of layers 8-11) takes
+    # the token contraction split in two, checked here element by element
+    "blocks124m_short": dict(n_layer=12, n_head=12, d_model=768, d_ff=3072, vocab=512, vocab_padded=512,
+                             max_seq_len=64, B=2, T=64),
 }
 
 
