@@ -33,6 +33,31 @@ DEV float hi_f(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 
 DEV bf16x8 as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8, v); }
 
+// Streaming (non-temporal) 16-byte loads and stores, for data that a kernel
+// touches once and nothing reads again soon (gigabytes that would only churn
+// the L2 and the 256 MB Infinity Cache): the optimizer's parameters, moments
+// and gradients, the logits that the cross-entropy overwrites with dlogits.
+// (The sum of squares over the gradients reads them with ordinary loads: part
+// of them is still cached from the weight-gradient launch that wrote them.)
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+DEV uint4 ld_stream(const uint4* p) {
+  const u32x4_t t = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(p));
+  return make_uint4(t.x, t.y, t.z, t.w);
+}
+DEV float4 ld_stream(const float4* p) {
+  const f32x4_t t = __builtin_nontemporal_load(reinterpret_cast<const f32x4_t*>(p));
+  return make_float4(t.x, t.y, t.z, t.w);
+}
+DEV void st_stream(uint4* p, uint4 v) {
+  const u32x4_t t = {v.x, v.y, v.z, v.w};
+  __builtin_nontemporal_store(t, reinterpret_cast<u32x4_t*>(p));
+}
+DEV void st_stream(float4* p, float4 v) {
+  const f32x4_t t = {v.x, v.y, v.z, v.w};
+  __builtin_nontemporal_store(t, reinterpret_cast<f32x4_t*>(p));
+}
+
 DEV float wave_sum(float v) {
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, WAVE);

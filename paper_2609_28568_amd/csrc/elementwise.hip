@@ -315,7 +315,7 @@ __global__ __launch_bounds__(NT) void cross_entropy_kernel(bf16_t* __restrict__ 
 #pragma unroll
   for (int i = 0; i < MAXCH; ++i) {
     const int c = min(tid + NT * i, nch - 1);
-    v[i] = *reinterpret_cast<const uint4*>(lr + c * 8);
+    v[i] = ld_stream(reinterpret_cast<const uint4*>(lr + c * 8));
   }
   // element j of chunk c counts if j < V (the padding columns carry no
   // probability)
@@ -402,8 +402,8 @@ __global__ __launch_bounds__(NT) void cross_entropy_kernel(bf16_t* __restrict__ 
         for (int e = 0; e < 8; ++e)
           if (e == (tgt & 7)) d[e] -= grad_scale;
       }
-      *reinterpret_cast<uint4*>(lr + c * 8) =
-          make_uint4(pack2(d[0], d[1]), pack2(d[2], d[3]), pack2(d[4], d[5]), pack2(d[6], d[7]));
+      st_stream(reinterpret_cast<uint4*>(lr + c * 8),
+                make_uint4(pack2(d[0], d[1]), pack2(d[2], d[3]), pack2(d[4], d[5]), pack2(d[6], d[7])));
     }
   }
   if (tid == 0) losses[pos] = mx + logf(sum) - bf2f(xt_raw);
@@ -494,10 +494,10 @@ __global__ __launch_bounds__(256) void adamw_kernel(AdamArgs a) {
   // grid size or segment split handles it.
   auto update = [&](long i, float wd) {
 #pragma clang fp contract(off)
-    float4 p = *reinterpret_cast<const float4*>(a.p + i);
-    float4 g = *reinterpret_cast<const float4*>(a.g + i);
-    float4 m = *reinterpret_cast<const float4*>(a.m + i);
-    float4 v = *reinterpret_cast<const float4*>(a.v + i);
+    float4 p = ld_stream(reinterpret_cast<const float4*>(a.p + i));
+    float4 g = ld_stream(reinterpret_cast<const float4*>(a.g + i));
+    float4 m = ld_stream(reinterpret_cast<const float4*>(a.m + i));
+    float4 v = ld_stream(reinterpret_cast<const float4*>(a.v + i));
     float pv[4] = {p.x, p.y, p.z, p.w}, gv[4] = {g.x, g.y, g.z, g.w};
     float mv[4] = {m.x, m.y, m.z, m.w}, vv[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
@@ -509,9 +509,9 @@ __global__ __launch_bounds__(256) void adamw_kernel(AdamArgs a) {
       const float upd = fmaf(wd, pv[e], mhat / (sqrtf(vhat) + a.eps));
       pv[e] = fmaf(-a.lr, upd, pv[e]);
     }
-    *reinterpret_cast<float4*>(a.p + i) = make_float4(pv[0], pv[1], pv[2], pv[3]);
-    *reinterpret_cast<float4*>(a.m + i) = make_float4(mv[0], mv[1], mv[2], mv[3]);
-    *reinterpret_cast<float4*>(a.v + i) = make_float4(vv[0], vv[1], vv[2], vv[3]);
+    st_stream(reinterpret_cast<float4*>(a.p + i), make_float4(pv[0], pv[1], pv[2], pv[3]));
+    st_stream(reinterpret_cast<float4*>(a.m + i), make_float4(mv[0], mv[1], mv[2], mv[3]));
+    st_stream(reinterpret_cast<float4*>(a.v + i), make_float4(vv[0], vv[1], vv[2], vv[3]));
     *reinterpret_cast<uint2*>(a.p_bf16 + i) = make_uint2(pack2(pv[0], pv[1]), pack2(pv[2], pv[3]));
   };
   long lo = 0;
