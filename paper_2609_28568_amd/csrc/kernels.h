@@ -265,6 +265,29 @@ hipError_t launch_qknorm_rope_bwd(const bf16_t* dpacked, const bf16_t* raw, cons
 // m = silu(g) * u over gu = [g | u] ([rows][2F]); and the gradient pair
 hipError_t launch_swiglu_fwd(const bf16_t* gu, bf16_t* m, long rows, int F, hipStream_t s);
 hipError_t launch_swiglu_bwd(const bf16_t* dm, const bf16_t* gu, bf16_t* dgu, long rows, int F, hipStream_t s);
+// Adapter products that stream a tall operand once (lora.hip): for segments
+// q < nseg and tiles t < nts of 16 columns,
+//   y[m][col[q] + tr(t) + c] = s * sum_{k < klen[q]} x[m][k0[q] + k] * w[q][(tr(t) + c) * ldw + k]
+// with tr(t) = (t / ntp) * tstride + 16 * (t % ntp), m < M, c < 16; every
+// other column of y's rows [0, ldy) is written as 0. klen multiples of 64,
+// ntp 1 or 2, nseg <= 3, nts / ntp <= 3.
+struct LoraRowArgs {
+  const bf16_t* x;
+  long ldx;
+  int M;
+  int nseg, nts, ntp, tstride;
+  int k0[3], klen[3], col[3];
+  const bf16_t* w[3];
+  long ldw;
+  float s;
+  bf16_t* y;
+  int ldy;
+};
+hipError_t launch_lora_rows(const LoraRowArgs& a, hipStream_t s);
+// Bt[l][c][k] = B[l][k][c] for l < L, c < 32, k < out (B rows of rp >= 32
+// elements, out a multiple of 64): the adapter B matrices with the
+// contraction index contiguous, for launch_lora_rows.
+hipError_t launch_lora_bt(const bf16_t* B, bf16_t* Bt, int L, int out, int rp, hipStream_t s);
 // x[r][c] *= sc for r < rows, c < cols (row stride ld)
 hipError_t launch_scale_bf16(bf16_t* x, long rows, int cols, int ld, float sc, hipStream_t s);
 

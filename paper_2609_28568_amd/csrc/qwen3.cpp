@@ -174,10 +174,11 @@ ActLayout act_layout(const Dims& d) {
 
 constexpr int DW_SPLITS = 16;   // token-contraction split of the adapter gradients
 constexpr int HEAD_SPLITS = 4;  // vocabulary-contraction split of the LM head's input gradient
-constexpr int DU_SPLITS = 8;    // contraction split of du = s dy B (a few output tiles, long contraction)
+constexpr int BT_ROWS = 32;     // rows of the transposed B copies: the largest rank
 
 struct WsLayout {
   size_t dres, dh, datt, dpacked, draw, dgu, dm, du, dsum, cosT, sinT, part, part2, sumsq, normcoef, total;
+  size_t bt[G_N];   // per adapted group: B transposed, [L][BT_ROWS][out_total] bf16
 };
 
 WsLayout ws_layout(const Dims& d) {
@@ -186,12 +187,11 @@ WsLayout ws_layout(const Dims& d) {
   // split partial slices: adapter B gradients [split][out][RP] (or the LM
   // head's input gradient [split][BTL][C]) and adapter A gradients
   // [split][n RP][in]
-  // and u or du [split][BT][n RP] (before the adapter gradients use the first area)
   size_t part = (size_t)d.BTL * d.C * HEAD_SPLITS, part2 = 0;
   for (int g = 0; g < G_N; ++g) {
     if (!(d.groups & (1 << g))) continue;
     const GroupGeom gg = group_geom(d, g);
-    part = std::max({part, (size_t)DW_SPLITS * gg.out_total * RP, (size_t)DU_SPLITS * BT * gg.n * RP});
+    part = std::max(part, (size_t)DW_SPLITS * gg.out_total * RP);
     part2 = std::max(part2, (size_t)DW_SPLITS * gg.n * RP * gg.in);
   }
   size_t o = 0;
@@ -210,6 +210,10 @@ WsLayout ws_layout(const Dims& d) {
   w.part2 = o; o += align_up(part2 * 4);
   w.sumsq = o; o += align_up((size_t)sumsq_parts() * 4);
   w.normcoef = o; o += ALIGN;
+  for (int g = 0; g < G_N; ++g) {
+    w.bt[g] = o;
+    if (d.groups & (1 << g)) o += align_up((size_t)d.L * BT_ROWS * group_geom(d, g).out_total * 2);
+  }
   w.total = o + TAIL;
   return w;
 }
@@ -330,18 +334,15 @@ hipError_t proj_fwd(qwen3_model* m, int g, int l, const bf16_t* x, const bf16_t*
     const bf16_t* wb = static_cast<const bf16_t*>(m->buf.lora_bf16) + tb->off + (size_t)l * gg.out_total * RP;
     bf16_t* u = m->ab(m->act.u[g] + l * m->act.s_u[g]);
     const int nu = gg.n * RP;
-    // u has one or two columns of output tiles: its contraction over the
-    // input width is split into fp32 slices, summed and scaled by s into u
-    int kc = 0;
-    const int su = gemm_split_plan(gg.in, DU_SPLITS, &kc);
-    float* part = m->wf(m->ws.part);
-    GemmArgs ua{};
-    ua.A = x; ua.lda = gg.in; ua.B = wa; ua.ldb = gg.in; ua.M = (int)d.BT; ua.N = nu; ua.K = gg.in;
-    ua.C = part; ua.ldc = nu; ua.splits = su; ua.k_chunk = kc; ua.split_stride = (long)d.BT * nu;
-    hipError_t e = run_gemm(m, QWEN3_K_GEMM_ADAPTER, mnk2(d.BT, gg.n * d.r, gg.in), ua, 0, 0, EPI_F32);
-    if (e != hipSuccess) return e;
-    e = m->run(QWEN3_K_OTHER, 0.0, (4.0 * su + 2.0) * d.BT * nu,
-               [&] { return launch_reduce_slices_bf16(part, su, d.BT * nu, d.s, u, m->stream); });
+    // u = s x A^T, one pass over x: the 16-row tiles of each projection's
+    // real rank rows of A, padding columns of u written as zeros
+    const int ntp = (d.r + 15) / 16;
+    LoraRowArgs ra{};
+    ra.x = x; ra.ldx = gg.in; ra.M = (int)d.BT; ra.nseg = 1; ra.nts = gg.n * ntp; ra.ntp = ntp; ra.tstride = RP;
+    ra.k0[0] = 0; ra.klen[0] = gg.in; ra.col[0] = 0; ra.w[0] = wa; ra.ldw = gg.in;
+    ra.s = d.s; ra.y = u; ra.ldy = nu;
+    hipError_t e = m->run(QWEN3_K_GEMM_ADAPTER, mnk2(d.BT, gg.n * d.r, gg.in), 0.0,
+                          [&] { return launch_lora_rows(ra, m->stream); });
     if (e != hipSuccess) return e;
     a.A2 = u; a.lda2 = nu; a.B2 = wb; a.ldb2 = RP; a.K2 = RP;
     // projection j + 1 starts at output column out[0] + ... + out[j]
@@ -376,34 +377,28 @@ hipError_t proj_bwd(qwen3_model* m, int g, int l, const bf16_t* dy, int ldy, con
     const LoraTensor* tb = m->lora_t(g, true);
     const size_t oa = ta->off + (size_t)l * gg.n * RP * gg.in, ob = tb->off + (size_t)l * gg.out_total * RP;
     const bf16_t* wa = static_cast<const bf16_t*>(m->buf.lora_bf16) + oa;
-    const bf16_t* wb = static_cast<const bf16_t*>(m->buf.lora_bf16) + ob;
     const bf16_t* u = m->ab(m->act.u[g] + l * m->act.s_u[g]);
     bf16_t* du = m->wb(m->ws.du);
     float* pb = m->wf(m->ws.part);
     float* pa = m->wf(m->ws.part2);
     hipError_t e;
-    // du_j = s dy_j B_j  ([BT, RP]; B_j read as [K = out_j][N = RP]): one
-    // column of output tiles, so the contraction over out_j is split into
-    // fp32 slices [split][BT][n RP], summed and scaled into du by one launch
-    // (every projection of the group must cut its contraction into the same
-    // number of slices, else none is split)
-    int su = gemm_split_plan(gg.out[0], DU_SPLITS, nullptr);
-    for (int j = 1; j < gg.n; ++j)
-      if (gemm_split_plan(gg.out[j], su, nullptr) != su) su = 1;
-    int col = 0;
-    for (int j = 0; j < gg.n; ++j) {
-      int kcu = 0;
-      if (gemm_split_plan(gg.out[j], su, &kcu) != su) return hipErrorInvalidValue;
-      GemmArgs q{};
-      q.A = dy + col; q.lda = ldy; q.B = wb + (size_t)col * RP; q.ldb = RP; q.M = BT; q.N = RP; q.K = gg.out[j];
-      q.C = pb + j * RP; q.ldc = nu; q.splits = su; q.k_chunk = kcu; q.split_stride = (long)BT * nu;
-      e = run_gemm(m, AD, mnk2(d.BT, d.r, gg.out[j]), q, 0, 1, EPI_F32);
+    // du_j = s dy_j B_j ([BT, RP] blocks of du), all projections in one
+    // pass over dy: segment j contracts dy's columns of projection j with the
+    // transposed copy of B_j (rows = rank, contraction index contiguous)
+    {
+      const int ntp = (d.r + 15) / 16;
+      const bf16_t* bt = m->wb(m->ws.bt[g]) + (size_t)l * BT_ROWS * gg.out_total;
+      LoraRowArgs ra{};
+      ra.x = dy; ra.ldx = ldy; ra.M = BT; ra.nseg = gg.n; ra.nts = ntp; ra.ntp = ntp; ra.tstride = RP;
+      ra.ldw = gg.out_total; ra.s = d.s; ra.y = du; ra.ldy = nu;
+      double dfl = 0.0;
+      for (int j = 0, col = 0; j < gg.n; col += gg.out[j], ++j) {
+        ra.k0[j] = col; ra.klen[j] = gg.out[j]; ra.col[j] = j * RP; ra.w[j] = bt + col;
+        dfl += mnk2(d.BT, d.r, gg.out[j]);
+      }
+      e = m->run(AD, dfl, 0.0, [&] { return launch_lora_rows(ra, m->stream); });
       if (e != hipSuccess) return e;
-      col += gg.out[j];
     }
-    e = m->run(QWEN3_K_OTHER, 0.0, (4.0 * su + 2.0) * d.BT * nu,
-               [&] { return launch_reduce_slices_bf16(pb, su, (long)BT * nu, d.s, du, m->stream); });
-    if (e != hipSuccess) return e;
     int kc = 0;
     const int splits = gemm_split_plan(BT, DW_SPLITS, &kc);
     {
@@ -649,6 +644,15 @@ gpt2_status qwen3_backward(qwen3_model* m) {
   const double rowb = 2.0 * d.BT * d.C;
   bf16_t* dres = m->wb(m->ws.dres);
   bf16_t* dh = m->wb(m->ws.dh);
+  // transposed copies of every adapted group's B (all layers), read by the
+  // du products
+  for (int g = 0; g < G_N; ++g) {
+    if (!m->has(g)) continue;
+    const int out = group_geom(d, g).out_total;
+    const bf16_t* b = static_cast<const bf16_t*>(m->buf.lora_bf16) + m->lora_t(g, true)->off;
+    TRY(m->run(QWEN3_K_OTHER, 0.0, 4.0 * d.L * BT_ROWS * out,
+               [&] { return launch_lora_bt(b, m->wb(m->ws.bt[g]), d.L, out, RP, m->stream); }));
+  }
   // LM head: dxf = dlogits embed over the loss rows, the long vocabulary
   // contraction split so that the few output tiles fill the GPU, then the
   // final RMSNorm (rows without loss get a zero gradient)

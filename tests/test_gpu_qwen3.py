@@ -24,6 +24,9 @@ CASES = {
                       lora_targets=("q", "k", "v", "gate", "up")),
     # degenerate: two-token sequences, only the second position carries loss
     "two_tokens": dict(B=32, T=2),
+    # rank above 16: two 16-row tiles per projection in the adapter products,
+    # the second one partly padding
+    "rank20": dict(lora_rank=20, lora_alpha=40.0),
 }
 
 
