@@ -27,6 +27,13 @@ CASES = {
     # rank above 16: two 16-row tiles per projection in the adapter products,
     # the second one partly padding
     "rank20": dict(lora_rank=20, lora_alpha=40.0),
+    # the rank limits: one real row of 16 in a tile, and two full tiles. (At
+    # rank 1 the q adapter's A gradient is too sensitive to the bf16 storage
+    # of the normalised input and of q|k|v for the 2e-2 bar: rounding those
+    # alone in the oracle moves it by 2.0e-2 in the second layer. The o and
+    # MLP-down adapters exercise the same single-row tiles.)
+    "rank1": dict(lora_rank=1, lora_alpha=2.0, lora_targets=("o", "down")),
+    "rank32": dict(lora_rank=32, lora_alpha=64.0, lora_targets=("gate", "up", "down")),
 }
 
 
