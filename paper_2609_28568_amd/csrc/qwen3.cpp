@@ -5,10 +5,11 @@
 // launch goes to the stream given at init; nothing here allocates device
 // memory.
 //
-// Adapters ride on the same GEMM as the base projections: u = s x A^T (the
-// down product, N = n*RP), y += u B^T (K = RP, written in place through the
-// residual epilogue); backward du = s dy B, dx += du A, dA = du^T x and
-// dB = dy^T u (contraction over the tokens, split and reduced).
+// Adapters: the down products u = s x A^T and, backward, du = s dy B run in
+// one pass over x or dy each (lora.hip, n*RP columns with the rank padding
+// written as zeros); the up products ride on the base projections' GEMMs as
+// a second contraction segment, y += u B^T and dx += du A; dA = du^T x and
+// dB = dy^T u contract over the tokens, split and reduced.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
